@@ -1,0 +1,364 @@
+"""Pins of the CPU oracle against things other than itself.
+
+* central finite differences of each block's local objective (fp64);
+* torch CPU autograd of the same network with .detach() at every cut and the
+  aggregate objective of Eq. (2) (an independent implementation);
+* torch.optim.Adam and torch's BCE-with-logits (independent library code);
+* closed forms: zero head -> l = log 2, cross with W=0,b=0 -> identity,
+  W=0,b=1 -> a_0 + a_{l-1}, Adam's first step theta - lr g/(|g|+eps);
+* the detachment invariants of Section 2.1 (exact equality) and the
+  lam-scaling of Eq. (2).
+
+A plausible slip anywhere in the oracle (dropped residual of the cross layer,
+missing ReLU mask, transposed weight, wrong loss sign or reduction, eps inside
+the square root, no bias correction, gradient leaking across a cut) fails at
+least one test here.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_18469_amd import synth
+
+F64 = np.float64
+
+
+def _tiny_mixed_cfg(inp2="x"):
+    blocks = [
+        {"input": "x", "layers": [("cross", 6, 6), ("cross", 6, 6), ("linear_relu", 6, 5), ("linear_relu", 5, 4)], "lam": 1.0},
+        {"input": inp2, "layers": [("linear_relu", 6 if inp2 == "x" else 4, 8), ("linear_relu", 8, 7)], "lam": 0.7},
+        {"input": "prev" if inp2 == "prev" else "x",
+         "layers": [("linear_relu", 7 if inp2 == "prev" else 6, 5)], "lam": 1.3},
+    ]
+    return synth.custom("f32", batch=12, in_dim=6, blocks=blocks, label_p=0.4)
+
+
+def _workload(cfg, seed=1):
+    params, batches = synth.make_workload(cfg, seed, 1)
+    x, y = batches[0]
+    return params, x.astype(F64), y.astype(F64)
+
+
+def _deepcopy(params):
+    return [{"layers": [(W.astype(F64).copy(), b.astype(F64).copy()) for (W, b) in p["layers"]],
+             "head": (p["head"][0].astype(F64).copy(), p["head"][1].astype(F64).copy())} for p in params]
+
+
+def _local_loss(cfg, params, x, y, b, a0):
+    cache = oracle.block_forward(cfg["blocks"][b], params[b], a0)
+    return cfg["blocks"][b]["lam"] * float(np.mean(oracle.bce_with_logits(cache["s"], y)))
+
+
+def _block_inputs(cfg, params, x):
+    caches = oracle.forward_all(cfg, params, x)
+    ins = []
+    for b, blk in enumerate(cfg["blocks"]):
+        ins.append(x if blk["input"] == "x" else caches[b - 1]["acts"][-1])
+    return ins
+
+
+def _grads(cfg, params, x, y):
+    caches = oracle.forward_all(cfg, params, x)
+    return [oracle.block_backward(blk, p, c, y)[1] for blk, p, c in zip(cfg["blocks"], params, caches)]
+
+
+def _leaves(tree):
+    out = []
+    for (W, b) in tree["layers"]:
+        out += [W, b]
+    out += [tree["head"][0], tree["head"][1]]
+    return out
+
+
+@pytest.mark.parametrize("inp2", ["x", "prev"])
+def test_finite_differences(inp2):
+    """Central differences of lam_b * l_b(theta_b; sg[a_0]) match the oracle's
+    gradient for every parameter of every block (fp64, rel 1e-6)."""
+    cfg = _tiny_mixed_cfg(inp2)
+    params, x, y = _workload(cfg, seed=3)
+    params = _deepcopy(params)
+    ins = _block_inputs(cfg, params, x)
+    grads = _grads(cfg, params, x, y)
+    for b in range(len(cfg["blocks"])):
+        leaves = _leaves(params[b])
+        gleaves = _leaves(grads[b])
+        for P, G in zip(leaves, gleaves):
+            flat = P.reshape(-1)
+            gflat = np.asarray(G).reshape(-1)
+            for i in range(flat.size):
+                h = 1e-6 * max(1.0, abs(flat[i]))
+                old = flat[i]
+                flat[i] = old + h
+                lp = _local_loss(cfg, params, x, y, b, ins[b])
+                flat[i] = old - h
+                lm = _local_loss(cfg, params, x, y, b, ins[b])
+                flat[i] = old
+                fd = (lp - lm) / (2 * h)
+                assert abs(fd - gflat[i]) <= 1e-6 * max(1e-3, abs(fd)) + 1e-9, (b, i, fd, gflat[i])
+
+
+def _torch_reference(cfg, params, x, y):
+    """Same network in torch autograd with .detach() at each cut and one
+    backward of L = sum lam_b l_b (Eq. 2)."""
+    tparams = []
+    for p in params:
+        layers = [(torch.tensor(W, dtype=torch.float64, requires_grad=True),
+                   torch.tensor(b, dtype=torch.float64, requires_grad=True)) for (W, b) in p["layers"]]
+        head = (torch.tensor(p["head"][0], dtype=torch.float64, requires_grad=True),
+                torch.tensor(p["head"][1], dtype=torch.float64, requires_grad=True))
+        tparams.append((layers, head))
+    xt = torch.tensor(x, dtype=torch.float64)
+    yt = torch.tensor(y, dtype=torch.float64)
+    total = 0.0
+    losses = []
+    prev = None
+    for blk, (layers, head) in zip(cfg["blocks"], tparams):
+        a0 = xt if blk["input"] == "x" else prev.detach()
+        a = a0
+        for (kind, _i, _o), (W, b) in zip(blk["layers"], layers):
+            h = torch.nn.functional.linear(a, W, b)
+            a = torch.relu(h) if kind == "linear_relu" else a0 * h + a
+        s = a @ head[0] + head[1]
+        l = torch.nn.functional.binary_cross_entropy_with_logits(s, yt)
+        losses.append(float(l.detach()))
+        total = total + blk["lam"] * l
+        prev = a
+    total.backward()
+    grads = []
+    for layers, head in tparams:
+        grads.append({"layers": [(W.grad.numpy(), b.grad.numpy()) for (W, b) in layers],
+                      "head": (head[0].grad.numpy(), head[1].grad.numpy())})
+    return losses, grads
+
+
+@pytest.mark.parametrize("inp2", ["x", "prev"])
+def test_against_torch_autograd_with_detach(inp2):
+    cfg = _tiny_mixed_cfg(inp2)
+    params, x, y = _workload(cfg, seed=5)
+    params = _deepcopy(params)
+    t_losses, t_grads = _torch_reference(cfg, params, x, y)
+    caches = oracle.forward_all(cfg, params, x)
+    for b, (blk, p, c) in enumerate(zip(cfg["blocks"], params, caches)):
+        loss, g = oracle.block_backward(blk, p, c, y)
+        assert loss == pytest.approx(t_losses[b], rel=1e-12)
+        for G, T in zip(_leaves(g), _leaves(t_grads[b])):
+            np.testing.assert_allclose(np.asarray(G).reshape(-1), np.asarray(T).reshape(-1), rtol=1e-10, atol=1e-14)
+
+
+def test_chain_gradient_excludes_downstream_path():
+    """With sg at the cut, block 1's gradient is its local gradient, not the
+    total derivative of L through block 2 (which FD of L would give)."""
+    cfg = _tiny_mixed_cfg("prev")
+    params, x, y = _workload(cfg, seed=7)
+    params = _deepcopy(params)
+    g = _grads(cfg, params, x, y)
+    W = params[0]["layers"][-1][0]
+    h = 1e-6
+    diffs = []
+    for i in np.ndindex(*W.shape):
+        old = W[i]
+        W[i] = old + h
+        lp = oracle.total_loss(cfg, params, x, y)
+        W[i] = old - h
+        lm = oracle.total_loss(cfg, params, x, y)
+        W[i] = old
+        diffs.append(abs((lp - lm) / (2 * h) - g[0]["layers"][-1][0][i]))
+    # the downstream path is real (FD of L sees it) but excluded by sg
+    assert max(diffs) > 1e-4
+
+
+def test_detachment_invariance_chain_and_shared():
+    """Perturbing a later block (chain) or any other block (shared input)
+    leaves a block's gradient bit-identical (Section 2.1)."""
+    for inp2, later in (("prev", [1, 2]), ("x", [1, 2])):
+        cfg = _tiny_mixed_cfg(inp2)
+        params, x, y = _workload(cfg, seed=11)
+        params = _deepcopy(params)
+        g0 = _grads(cfg, params, x, y)
+        rng = np.random.default_rng(0)
+        for b in later:
+            for P in _leaves(params[b]):
+                P += rng.normal(0, 0.5, size=P.shape)
+        g1 = _grads(cfg, params, x, y)
+        for A, B in zip(_leaves(g0[0]), _leaves(g1[0])):
+            assert np.array_equal(A, B)
+    # shared input: block 2 is unaffected by a change of block 1 as well
+    cfg = _tiny_mixed_cfg("x")
+    params, x, y = _workload(cfg, seed=12)
+    params = _deepcopy(params)
+    g0 = _grads(cfg, params, x, y)
+    for P in _leaves(params[0]):
+        P *= 1.5
+    g1 = _grads(cfg, params, x, y)
+    for A, B in zip(_leaves(g0[2]), _leaves(g1[2])):
+        assert np.array_equal(A, B)
+
+
+def test_lambda_scaling_exact():
+    """grad_theta_b L = lam_b grad_theta_b l_b (Eq. 2): lam=2 doubles every
+    gradient exactly."""
+    cfg = _tiny_mixed_cfg("prev")
+    for blk in cfg["blocks"]:
+        blk["lam"] = 1.0
+    params, x, y = _workload(cfg, seed=13)
+    params = _deepcopy(params)
+    g1 = _grads(cfg, params, x, y)
+    for blk in cfg["blocks"]:
+        blk["lam"] = 2.0
+    g2 = _grads(cfg, params, x, y)
+    for b in range(3):
+        for A, B in zip(_leaves(g1[b]), _leaves(g2[b])):
+            assert np.array_equal(2.0 * np.asarray(A), np.asarray(B))
+
+
+def test_lambda_zero_freezes_block():
+    cfg = _tiny_mixed_cfg("x")
+    cfg["blocks"][1]["lam"] = 0.0
+    params, x, y = _workload(cfg, seed=14)
+    m = synth.zero_state(params)
+    v = synth.zero_state(params)
+    r = oracle.step(cfg, params, m, v, 0, x, y)
+    for A, B in zip(_leaves(r["params"][1]), _leaves(_deepcopy(params)[1])):
+        assert np.array_equal(A, B)
+    for A in _leaves(r["m"][1]) + _leaves(r["v"][1]):
+        assert not np.any(A)
+
+
+def test_zero_head_closed_form():
+    """w=0, c=0: s=0, l = log 2, g_s = lam(1/2 - y)/M, body gradients are 0."""
+    cfg = _tiny_mixed_cfg("x")
+    params, x, y = _workload(cfg, seed=15)
+    params = _deepcopy(params)
+    for p in params:
+        p["head"] = (np.zeros_like(p["head"][0]), np.zeros_like(p["head"][1]))
+    caches = oracle.forward_all(cfg, params, x)
+    M = x.shape[0]
+    for blk, p, c in zip(cfg["blocks"], params, caches):
+        loss, g = oracle.block_backward(blk, p, c, y)
+        assert loss == pytest.approx(math.log(2.0), rel=1e-15)
+        gs = blk["lam"] * (0.5 - y) / M
+        np.testing.assert_allclose(g["head"][1][0], gs.sum(), rtol=1e-12, atol=1e-15)
+        np.testing.assert_allclose(g["head"][0], c["acts"][-1].T @ gs, rtol=1e-12, atol=1e-15)
+        for (dW, db) in g["layers"]:
+            assert not np.any(dW) and not np.any(db)
+
+
+def test_cross_layer_closed_forms():
+    blk = {"input": "x", "layers": [("cross", 5, 5), ("cross", 5, 5)], "lam": 1.0}
+    rng = np.random.default_rng(2)
+    x = rng.normal(size=(7, 5))
+    p = {"layers": [(np.zeros((5, 5)), np.zeros(5)), (np.zeros((5, 5)), np.zeros(5))],
+         "head": (rng.normal(size=5), np.zeros(1))}
+    c = oracle.block_forward(blk, p, x)
+    assert np.array_equal(c["acts"][1], x) and np.array_equal(c["acts"][2], x)
+    p["layers"] = [(np.zeros((5, 5)), np.ones(5)), (np.zeros((5, 5)), np.ones(5))]
+    c = oracle.block_forward(blk, p, x)
+    np.testing.assert_allclose(c["acts"][1], 2 * x)
+    np.testing.assert_allclose(c["acts"][2], 3 * x)
+    # DCNv2 cross against its elementwise definition, one row at a time
+    W = rng.normal(size=(5, 5)); b = rng.normal(size=5)
+    p["layers"] = [(W, b), (W.T.copy(), -b)]
+    c = oracle.block_forward(blk, p, x)
+    for i in range(x.shape[0]):
+        x0 = x[i]
+        x1 = np.array([x0[j] * (sum(W[j, k] * x0[k] for k in range(5)) + b[j]) + x0[j] for j in range(5)])
+        x2 = np.array([x0[j] * (sum(W[k, j] * x1[k] for k in range(5)) - b[j]) + x1[j] for j in range(5)])
+        np.testing.assert_allclose(c["acts"][1][i], x1, rtol=1e-12)
+        np.testing.assert_allclose(c["acts"][2][i], x2, rtol=1e-12)
+
+
+def test_bce_against_torch_and_extremes():
+    rng = np.random.default_rng(3)
+    s = rng.normal(0, 4, size=1000)
+    y = (rng.random(1000) < 0.3).astype(np.float64)
+    ref = torch.nn.functional.binary_cross_entropy_with_logits(
+        torch.tensor(s), torch.tensor(y), reduction="none").numpy()
+    np.testing.assert_allclose(oracle.bce_with_logits(s, y), ref, rtol=1e-13, atol=1e-15)
+    big = np.array([800.0, -800.0, 800.0, -800.0])
+    yy = np.array([1.0, 0.0, 0.0, 1.0])
+    out = oracle.bce_with_logits(big, yy)
+    assert np.all(np.isfinite(out))
+    np.testing.assert_allclose(out, [0.0, 0.0, 800.0, 800.0], atol=1e-12)
+    np.testing.assert_allclose(oracle.sigmoid(np.array([0.0, 800.0, -800.0])), [0.5, 1.0, 0.0])
+    from scipy.special import expit
+    np.testing.assert_allclose(oracle.sigmoid(s), expit(s), rtol=1e-14)
+
+
+def test_adam_against_torch_optim():
+    rng = np.random.default_rng(4)
+    theta = rng.normal(size=50)
+    m = np.zeros(50); v = np.zeros(50)
+    tt = torch.tensor(theta.copy(), requires_grad=True)
+    opt = torch.optim.Adam([tt], lr=1e-3, betas=(0.9, 0.999), eps=1e-8)
+    for t in range(1, 6):
+        g = rng.normal(size=50) * (10.0 ** rng.integers(-6, 2, size=50))
+        theta, m, v = oracle.adam_update(theta, m, v, g, t, 1e-3, 0.9, 0.999, 1e-8)
+        tt.grad = torch.tensor(g)
+        opt.step()
+        np.testing.assert_allclose(theta, tt.detach().numpy(), rtol=1e-13, atol=1e-16)
+
+
+def test_adam_first_step_closed_form():
+    rng = np.random.default_rng(6)
+    theta = rng.normal(size=20)
+    g = rng.normal(size=20)
+    g[3] = 0.0
+    t1, m1, v1 = oracle.adam_update(theta, np.zeros(20), np.zeros(20), g, 1, 1e-3, 0.9, 0.999, 1e-8)
+    np.testing.assert_allclose(t1, theta - 1e-3 * g / (np.abs(g) + 1e-8), rtol=1e-12, atol=1e-15)
+    assert t1[3] == theta[3]
+
+
+def test_step_matches_torch_training_loop():
+    """Three oracle steps equal three steps of torch autograd + torch.optim.Adam
+    on the detached network (shared-input and chain)."""
+    for inp2 in ("x", "prev"):
+        cfg = _tiny_mixed_cfg(inp2)
+        params, batches = synth.make_workload(cfg, 21, 3)
+        p = _deepcopy(params)
+        m, v = synth.zero_state(params), synth.zero_state(params)
+        tparams = [[torch.tensor(a, dtype=torch.float64, requires_grad=True) for a in _leaves(q)] for q in p]
+        opt = torch.optim.Adam([a for q in tparams for a in q], lr=1e-3)
+        t = 0
+        for (x, y) in batches:
+            r = oracle.step(cfg, p, m, v, t, x, y)
+            p, m, v, t = r["params"], r["m"], r["v"], r["t"]
+            # torch side
+            opt.zero_grad()
+            xt = torch.tensor(x, dtype=torch.float64); yt = torch.tensor(y, dtype=torch.float64)
+            total = 0.0
+            prev = None
+            for blk, q in zip(cfg["blocks"], tparams):
+                a0 = xt if blk["input"] == "x" else prev.detach()
+                a = a0
+                for li, (kind, _i, _o) in enumerate(blk["layers"]):
+                    h = torch.nn.functional.linear(a, q[2 * li], q[2 * li + 1])
+                    a = torch.relu(h) if kind == "linear_relu" else a0 * h + a
+                s = a @ q[-2] + q[-1]
+                total = total + blk["lam"] * torch.nn.functional.binary_cross_entropy_with_logits(s, yt)
+                prev = a
+            total.backward()
+            opt.step()
+        for q_np, q_t in zip(p, tparams):
+            for A, T in zip(_leaves(q_np), q_t):
+                np.testing.assert_allclose(np.asarray(A).reshape(-1), T.detach().numpy().reshape(-1), rtol=1e-9, atol=1e-12)
+
+
+def test_bf16_emulation_rounding_agrees_with_input_rounding():
+    """Two independent bf16 roundings (torch cast in the oracle, bit
+    arithmetic in the input generator) agree, and emulation stays within
+    bf16 tolerance of the exact step."""
+    rng = np.random.default_rng(8)
+    a = rng.normal(size=10000).astype(np.float32) * 10.0 ** rng.integers(-5, 5, size=10000)
+    assert np.array_equal(oracle.erase_oracle._bf16(a), synth.round_to_bf16_values(a))
+    cfg = synth.config("tiny", dtype="bf16")
+    params, batches = synth.make_workload(cfg, 0, 1)
+    x, y = batches[0]
+    m, v = synth.zero_state(params), synth.zero_state(params)
+    r0 = oracle.step(cfg, params, m, v, 0, x, y)
+    r1 = oracle.step(cfg, params, m, v, 0, x, y, emulate_bf16=True)
+    for b in range(2):
+        for A, B in zip(_leaves(r0["grads"][b]), _leaves(r1["grads"][b])):
+            assert np.linalg.norm(A - B) <= 2e-2 * np.linalg.norm(A) + 1e-12
