@@ -1,0 +1,248 @@
+#!/usr/bin/env python3
+"""Throughput of the ERASE detached-block training step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload ctr_mlp]
+
+One "step" is one call of erase_step(): for each of the 6 detached CTR
+subarchitectures (1677->512->256->128, local Linear(128->1) sigmoid-BCE head,
+batch 4096, bf16 operands with fp32 accumulation) the forward, local loss,
+weight/input gradients and Adam update.  Inputs are synthetic, seeded and
+already resident in HBM (8 batches, cycled).
+
+The headline value is samples/s of the ERASE schedule captured as a HIP graph
+(OVERLAP_GRAPH).  The same kernels are also timed in the serial order
+(SERIAL, SERIAL_GRAPH) and in the ungraphed ERASE order (OVERLAP); the
+speedups compare schedules with identical kernels.  Per-kernel durations for
+the roofline and the measured backward/forward overlap come from HIP events
+recorded by the library around each launch, on the stream of that launch.
+The CPU baseline times the float64 oracle on the host on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector/MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+METRIC = "train samples/s, 6-block CTR @1 MI355X; ERASE vs serial speedup; MFMA util %"
+KIND_SYMBOL = {"prologue": "erase_prologue", "fwd_gemm": "erase_fwd_gemm", "head_bce": "erase_head_bce",
+               "wgrad_gemm": "erase_wgrad_gemm", "dgrad_gemm": "erase_dgrad_gemm", "adam": "erase_adam"}
+
+
+def kernel_class(r, bf16=True):
+    t = "bf16" if bf16 else "f32"
+    if r["tile_m"]:
+        return f"{KIND_SYMBOL[r['kind']]}<{t},{r['tile_m']},{r['tile_n']}>"
+    return f"{KIND_SYMBOL[r['kind']]}<{t}>"
+
+
+def overlap_fraction(recs):
+    """Share of backward-stream kernel time that runs while a forward-stream
+    kernel is running (interval intersection on the device clock)."""
+    fwd = sorted((r["start_ms"], r["end_ms"]) for r in recs if r["stream"] == 0)
+    merged = []
+    for a, b in fwd:
+        if merged and a <= merged[-1][1]:
+            merged[-1][1] = max(merged[-1][1], b)
+        else:
+            merged.append([a, b])
+    tot = inter = 0.0
+    for r in recs:
+        if r["stream"] != 1:
+            continue
+        a, b = r["start_ms"], r["end_ms"]
+        tot += b - a
+        for c, d in merged:
+            lo, hi = max(a, c), min(b, d)
+            if hi > lo:
+                inter += hi - lo
+    return inter / tot if tot > 0 else 0.0
+
+
+def cpu_baseline(cfg, params, batches, budget_s):
+    """Time the float64 oracle on the host (reported baseline, not a target)."""
+    import oracle
+    from paper_2608_18469_amd import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    m = synth.zero_state(params)
+    v = synth.zero_state(params)
+    p, t = params, 0
+    steps = 0
+    t0 = time.perf_counter()
+    while True:
+        x, y = batches[steps % len(batches)]
+        r = oracle.step(cfg, p, m, v, t, x, y)
+        p, m, v, t = r["params"], r["m"], r["v"], r["t"]
+        steps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    return {"value": steps * cfg["batch"] / el, "unit": "samples/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{steps} full float64 oracle steps of {cfg['name']} (batch {cfg['batch']}, "
+                      f"{len(cfg['blocks'])} blocks) in {el:.1f} s on the host, numpy/OpenBLAS threads={threads}"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="ctr_mlp")
+    ap.add_argument("--timing-steps", type=int, default=20)
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--schedules", default="serial,overlap,serial_graph,overlap_graph")
+    ap.add_argument("--verbose", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the detached-block step is built and timed on a single MI355X; "
+              "multi-GPU runs are not part of this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2608_18469_amd import erase, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    log = (lambda *a: print(*a, file=sys.stderr, flush=True))
+
+    cfg = synth.config(args.workload)
+    bf16 = cfg["dtype"] == "bf16"
+    log(f"[bench] generating {args.workload} (batch {cfg['batch']}, {len(cfg['blocks'])} blocks)")
+    params, batches = synth.make_workload(cfg, 0, 8)
+    tr = erase.Trainer(cfg, params, keep_grads=True)
+    dev = [tr.device_batch(x, y) for (x, y) in batches]
+    losses = torch.zeros(len(cfg["blocks"]), device="cuda")
+    flops_step = synth.gemm_flops_per_step(cfg)
+    M = cfg["batch"]
+    scheds = args.schedules.split(",")
+
+    res = {}
+    for s in scheds:
+        log(f"[bench] {s}: warmup {args.warmup}")
+        for i in range(args.warmup):
+            x, y = dev[i % len(dev)]
+            tr.step(x, y, s, losses, wait_current=False)
+        tr.sync()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        host = []
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            x, y = dev[i % len(dev)]
+            evs[i][0].record(tr.sf)
+            h0 = time.perf_counter()
+            tr.step(x, y, s, losses, wait_current=False)
+            host.append(time.perf_counter() - h0)
+            evs[i][1].record(tr.sf)
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        tr.sync()
+        per = np.array([a.elapsed_time(b) for a, b in evs])  # ms per step on the device clock
+        sps = M / (per / 1e3)
+        res[s] = {"samples_per_s": M * args.steps / el, "ms_per_step": el / args.steps * 1e3,
+                  "p90_samples_per_s": float(np.percentile(sps, 90)), "median_samples_per_s": float(np.median(sps)),
+                  "host_enqueue_us": float(np.median(host) * 1e6), "elapsed_s": el}
+        log(f"[bench] {s}: {res[s]['samples_per_s']:.0f} samples/s, {res[s]['ms_per_step']:.3f} ms/step, "
+            f"enqueue {res[s]['host_enqueue_us']:.1f} us")
+
+    # per-launch kernel times (library events on each launch's own stream)
+    log(f"[bench] kernel timing: {args.timing_steps} overlap steps")
+    tr.set_timing(True)
+    recs_all = []
+    for i in range(args.timing_steps):
+        x, y = dev[i % len(dev)]
+        tr.step(x, y, "overlap", losses, wait_current=False)
+        tr.sync()
+        recs_all.append(tr.read_timing())
+    tr.set_timing(False)
+    classes = {}
+    for recs in recs_all:
+        for r in recs:
+            c = classes.setdefault(kernel_class(r, bf16), {"ms": 0.0, "n": 0, "flops": 0.0, "bytes": 0.0,
+                                                             "kind": r["kind"]})
+            c["ms"] += r["end_ms"] - r["start_ms"]
+            c["n"] += 1
+            c["flops"] += r["flops"]
+            c["bytes"] += r["bytes"]
+    nsteps = len(recs_all)
+    ovl = float(np.mean([overlap_fraction(r) for r in recs_all]))
+    dom_name, dom = max(classes.items(), key=lambda kv: kv[1]["ms"])
+    gemm_ms = sum(c["ms"] for c in classes.values() if c["kind"].endswith("gemm"))
+    gemm_flops = sum(c["flops"] for c in classes.values() if c["kind"].endswith("gemm"))
+    peak_mfma = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
+    avg_dur_s = dom["ms"] / dom["n"] / 1e3
+    if dom["kind"].endswith("gemm"):
+        achieved = dom["flops"] / dom["n"] / avg_dur_s / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": peak_mfma, "unit": "TFLOP/s"}
+    else:
+        achieved = dom["bytes"] / dom["n"] / avg_dur_s / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["kernel"] = dom_name
+    roof["avg_launch_us"] = avg_dur_s * 1e6
+    roof["launches_per_step"] = dom["n"] / nsteps
+    kernels = {k: {"avg_us": v["ms"] / v["n"] * 1e3, "launches_per_step": v["n"] / nsteps,
+                   "us_per_step": v["ms"] / nsteps * 1e3,
+                   "tflops": (v["flops"] / (v["ms"] / 1e3) / 1e12) if v["kind"].endswith("gemm") else None,
+                   "gbs": v["bytes"] / (v["ms"] / 1e3) / 1e9}
+               for k, v in sorted(classes.items(), key=lambda kv: -kv[1]["ms"])}
+
+    head = "overlap_graph" if "overlap_graph" in res else scheds[-1]
+    out = {
+        "metric": METRIC,
+        "value": res[head]["samples_per_s"],
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": res[head]["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32",
+        "data": "synthetic (seeded CTR-shaped input: 13 log1p-LogNormal dense + 26 Zipf(1.1) sum-pooled "
+                "embedding bags of dim 64; random-init weights)",
+        "config": {"workload": f"{args.workload}: 6 detached blocks 1677->512->256->128 + Linear(128->1) BCE head, "
+                               f"batch {M}, Adam" if args.workload == "ctr_mlp" else args.workload,
+                   "global_batch": M, "blocks": len(cfg["blocks"]), "schedule": head, "parallelism": "single GPU"},
+        "speedup_vs_serial": {"overlap_vs_serial": res.get("overlap", {}).get("samples_per_s", 0) /
+                              res["serial"]["samples_per_s"] if "serial" in res else None,
+                              "overlap_graph_vs_serial_graph": res.get("overlap_graph", {}).get("samples_per_s", 0) /
+                              res["serial_graph"]["samples_per_s"] if "serial_graph" in res else None,
+                              "overlap_graph_vs_serial": res[head]["samples_per_s"] / res["serial"]["samples_per_s"]
+                              if "serial" in res else None},
+        "schedules": res,
+        "mfma_util": {"gemm_kernels": gemm_flops / (gemm_ms / 1e3) / 1e12 / peak_mfma if gemm_ms else None,
+                      "whole_step": flops_step / (res[head]["ms_per_step"] / 1e3) / 1e12 / peak_mfma},
+        "bwd_fwd_overlap_fraction": ovl,
+        "roofline": roof,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] cpu baseline: oracle for ~{args.cpu_budget:.0f} s")
+        out["cpu_baseline"] = cpu_baseline(cfg, params, batches, args.cpu_budget)
+    tr.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,211 @@
+/*
+ * erase.h -- C ABI of the MI355X detached-block training step (ERASE).
+ *
+ * The operation (paper, Section 2): a network is cut into B blocks by
+ * stop-gradients, z_b = f_b(sg[z_{b-1}]; theta_b) (Eq. 1).  Every block has a
+ * local head and loss l_b; the objective is L = sum_b lambda_b l_b (Eq. 2), so
+ * the gradient of block b needs only block b's forward and local loss.  ERASE
+ * (Section 2.2) launches block b's backward as soon as its forward and loss
+ * finish, on a second stream whose events enforce the remaining dependencies,
+ * so it overlaps the forward of block b+1.  One call of erase_step() enqueues
+ * one such training step: for each block the forward, local sigmoid-BCE head
+ * and loss gradient, the weight/input gradients and an Adam update.
+ *
+ * Conventions shared by every entry point:
+ *  - Every function returns erase_status; nothing throws across the ABI.
+ *  - "device" pointers are HIP device allocations on the device that is
+ *    current when erase_init() runs; "host" pointers are ordinary memory.
+ *  - Streams are passed as `void*` holding a hipStream_t.  Both streams must
+ *    be distinct, non-null, created by the caller with default priority and
+ *    belong to the current device.  The library never destroys them.
+ *  - The caller owns all device memory (parameters, Adam moments, gradients,
+ *    workspace, inputs, labels, losses).  The library owns only the context,
+ *    its events and its HIP graphs, and never frees caller memory.  After
+ *    erase_init() it allocates no device memory.
+ *  - A context is not thread-safe; use one context per host thread.
+ *  - Arguments are validated on the host before anything is enqueued: an
+ *    invalid call returns an error and enqueues nothing.  Errors raised by
+ *    the device (HIP launch failures, a non-finite loss) surface at
+ *    erase_sync() and are sticky: every later call returns ERASE_ERR_STATE
+ *    until erase_destroy().
+ */
+#ifndef ERASE_H_
+#define ERASE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ERASE_OK = 0,
+  ERASE_ERR_INVALID_ARG = -1,  /* null pointer, bad enum, bad hyper-parameter, misaligned pointer */
+  ERASE_ERR_SHAPE = -2,        /* dimensions that do not chain or are out of range               */
+  ERASE_ERR_UNSUPPORTED = -3,  /* a well-formed request this library does not implement          */
+  ERASE_ERR_WORKSPACE = -4,    /* workspace null, misaligned (256 B) or smaller than required    */
+  ERASE_ERR_HIP = -5,          /* a HIP runtime call failed                                       */
+  ERASE_ERR_STATE = -6,        /* context already failed, or call out of order                    */
+  ERASE_ERR_NONFINITE = -7     /* a block loss was NaN or infinite                                */
+} erase_status;
+
+/* Storage type of inputs, weights used by the GEMMs and activations.
+ * ERASE_BF16: bf16 GEMM operands and stored activations/activation-gradients,
+ * fp32 accumulation; master parameters, Adam moments, gradients, logits and
+ * losses stay fp32.  ERASE_F32: everything fp32. */
+typedef enum { ERASE_F32 = 0, ERASE_BF16 = 1 } erase_dtype;
+
+/* Layer kinds of a block body (paper: f_b of Eq. 1; the CTR subarchitectures
+ * of Section 3.2 are dense MLPs, DCNv2 cross layers are the other common
+ * dense block of CTR models).
+ *   LINEAR_RELU: a_l = max(a_{l-1} W^T + b, 0),      W[out,in], b[out]
+ *   CROSS:       a_l = a_0 * (a_{l-1} W^T + b) + a_{l-1}, in == out == width
+ *                of the block input a_0; cross layers must precede every
+ *                LINEAR_RELU layer of the block. */
+typedef enum { ERASE_LAYER_LINEAR_RELU = 0, ERASE_LAYER_CROSS = 1 } erase_layer_kind;
+
+/* Local objective of a block: s = z w + c (head Linear(last->1)),
+ * l_b = mean_i [max(s_i,0) - s_i y_i + log(1 + exp(-|s_i|))]. */
+typedef enum { ERASE_LOSS_BCE = 0 } erase_loss_kind;
+
+/* Input of a block: the shared input x (independent detached
+ * subarchitectures), or sg[z_{b-1}], the previous block's output (Eq. 1). */
+typedef enum { ERASE_IN_X = 0, ERASE_IN_PREV = 1 } erase_input_src;
+
+/* Schedules of one step.  All four run the identical kernels on identical
+ * inputs and produce bit-identical results.
+ *   SERIAL:        everything on the forward stream: forward+loss of blocks
+ *                  1..B, then backward of blocks B..1, then Adam of 1..B.
+ *   OVERLAP:       ERASE early backward: forward+loss of block b on the
+ *                  forward stream, then block b's backward and Adam on the
+ *                  backward stream after an event, overlapping block b+1's
+ *                  forward; the step ends with the forward stream joined on
+ *                  the backward stream.
+ *   SERIAL_GRAPH / OVERLAP_GRAPH: the same sequences captured once into a HIP
+ *                  graph (per distinct x/labels/losses pointers) and replayed. */
+typedef enum {
+  ERASE_SCHED_SERIAL = 0,
+  ERASE_SCHED_OVERLAP = 1,
+  ERASE_SCHED_SERIAL_GRAPH = 2,
+  ERASE_SCHED_OVERLAP_GRAPH = 3
+} erase_schedule;
+
+typedef struct {
+  int32_t kind;     /* erase_layer_kind */
+  int32_t in_dim;   /* >= 1 */
+  int32_t out_dim;  /* >= 1, <= 65536 */
+} erase_layer_spec;
+
+typedef struct {
+  int32_t input_src;                /* erase_input_src; block 0 must read x */
+  int32_t n_layers;                 /* 1..16; the last layer must be LINEAR_RELU */
+  const erase_layer_spec* layers;   /* host, [n_layers] */
+  int32_t loss;                     /* erase_loss_kind */
+  float lambda;                     /* weight of l_b in Eq. 2 (finite) */
+} erase_block_spec;
+
+typedef struct {
+  int32_t n_blocks;                 /* 1..64 */
+  const erase_block_spec* blocks;   /* host, [n_blocks] */
+  int32_t batch;                    /* M, 1..2^24 */
+  int32_t in_dim;                   /* width of x, >= 1 */
+  int32_t x_ld;                     /* row pitch of x in elements, >= in_dim, multiple of 16 bytes */
+  int32_t dtype;                    /* erase_dtype */
+  float lr, beta1, beta2, eps;      /* Adam (bias-corrected, eps outside the sqrt); lr >= 0,
+                                       0 <= beta < 1, eps >= 0 */
+} erase_config;
+
+/* Per-block fp32 device buffers, each of erase_param_count() elements, in
+ * this flat order: for every layer W[out][in] (row-major) then b[out]; then
+ * the head weight w[last] and bias c[1] (torch nn.Linear order).
+ * param/m/v are read and updated in place; grad (may be NULL) receives the
+ * step's gradient of L = sum lambda_b l_b. */
+typedef struct {
+  float* param;
+  float* m;
+  float* v;
+  float* grad;
+} erase_block_buffers;
+
+/* Number of fp32 parameters of block `block`.  Host only; no HIP call. */
+erase_status erase_param_count(const erase_config* cfg, int32_t block, int64_t* count);
+
+/* Bytes of device workspace erase_init() needs for `cfg` (activations in both
+ * row- and feature-major layouts, activation gradients, GEMM copies of the
+ * weights, split-reduction partials, counters).  Host only; no HIP call. */
+erase_status erase_workspace_bytes(const erase_config* cfg, size_t* bytes);
+
+/* Validate `cfg`, carve `workspace` (device, 256-byte aligned, ws_bytes >=
+ * erase_workspace_bytes) and create the context with its events.  Enqueues on
+ * s_fwd the derivation of the GEMM weight copies from the current parameters
+ * and resets the step counter to 0; does not synchronize.  `bufs` is a host
+ * array of n_blocks entries whose device buffers must stay valid for the
+ * context's life.  The config is copied; `cfg` may be freed afterwards. */
+erase_status erase_init(const erase_config* cfg, const erase_block_buffers* bufs,
+                        void* workspace, size_t ws_bytes, void* s_fwd, void* s_bwd,
+                        void** ctx_out);
+
+/* Enqueue one training step (Section 2.2) and return without waiting.
+ *   x:      device, [batch][x_ld] of dtype, 16-byte aligned, rows' tails
+ *           beyond in_dim are ignored;
+ *   labels: device fp32 [batch], values in {0,1};
+ *   losses: device fp32 [n_blocks], receives the unweighted l_b.
+ * x, labels and losses must stay unmodified and valid until erase_sync().
+ * The step increments the device step counter before its Adam updates. */
+erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t schedule,
+                        float* losses);
+
+/* Wait for all enqueued work of the context, then report deferred errors
+ * (HIP errors, non-finite loss: ERASE_ERR_NONFINITE, sticky). */
+erase_status erase_sync(void* ctx);
+
+/* Read / overwrite the device step counter t (Adam bias correction uses t+1
+ * at the next step).  Both synchronize the forward stream.  Used for
+ * checkpoint/resume together with the caller-owned param/m/v buffers. */
+erase_status erase_get_step(void* ctx, int64_t* t);
+erase_status erase_set_step(void* ctx, int64_t t);
+
+/* Re-derive the GEMM weight copies after the caller changed `param` (e.g. a
+ * checkpoint load).  Enqueued on s_fwd. */
+erase_status erase_refresh_weights(void* ctx);
+
+/* Per-launch kernel timing, for measurement.  When enabled, non-graph
+ * schedules bracket every kernel launch with timing events (graph schedules
+ * return ERASE_ERR_UNSUPPORTED while enabled).  erase_read_timing() fills up
+ * to `cap` records of the last completed step (call after erase_sync()) and
+ * sets *n to the number of launches of that step. */
+typedef struct {
+  int32_t kind;      /* 0 prologue, 1 forward GEMM, 2 head+loss, 3 weight-grad GEMM,
+                        4 input-grad GEMM, 5 Adam */
+  int32_t block;     /* block index, -1 for the step prologue */
+  int32_t layer;     /* layer index within the block, -1 if none */
+  int32_t stream;    /* 0 forward stream, 1 backward stream */
+  float start_ms;    /* relative to the step's first event on the forward stream */
+  float end_ms;
+  int32_t tile_m;    /* GEMM workgroup tile rows (0 for non-GEMM kernels) */
+  int32_t tile_n;    /* GEMM workgroup tile columns */
+  int32_t split;     /* GEMM contraction slices (grid z) */
+  int32_t grid;      /* workgroups launched */
+  double flops;      /* algorithmic floating-point operations of the launch */
+  double bytes;      /* algorithmic HBM bytes of the launch */
+} erase_kernel_time;
+
+erase_status erase_set_timing(void* ctx, int32_t enable);
+erase_status erase_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, int32_t* n);
+
+/* Destroy the context: waits for its streams, frees events and graphs.
+ * Never frees caller memory.  NULL is accepted. */
+erase_status erase_destroy(void* ctx);
+
+/* Static description of a status code. */
+const char* erase_status_str(int32_t status);
+
+/* Last error message recorded on the context ("" if none). */
+const char* erase_last_error(void* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ERASE_H_ */

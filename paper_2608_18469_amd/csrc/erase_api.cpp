@@ -1,0 +1,994 @@
+// C-ABI entry points, host validation, workspace layout and the two-stream
+// dispatcher of the ERASE detached-block step.
+//
+// Schedules (paper, Section 2.2): conventional training runs the backward
+// after the whole forward; ERASE launches block b's backward on a second
+// stream as soon as its forward and local loss are done, with events
+// enforcing the remaining dependencies, so it overlaps block b+1's forward.
+// HIP graphs fix the launch order and remove per-launch host cost (the
+// paper's CUDA-Graph variant).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "erase.h"
+#include "internal.h"
+
+namespace {
+
+using namespace erase;
+
+constexpr int kMaxBlocks = 64;
+constexpr int kMaxLayers = 16;
+constexpr int64_t kMaxDim = 65536;
+constexpr int64_t kMaxBatch = int64_t(1) << 24;
+constexpr size_t kAlign = 256;
+constexpr int kMaxGraphs = 16;
+
+int64_t roundup(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// ---------------------------------------------------------------------------
+// validation (host only, no HIP call)
+// ---------------------------------------------------------------------------
+erase_status validate(const erase_config* c, std::string* err) {
+  auto fail = [&](erase_status s, const char* msg) {
+    if (err) *err = msg;
+    return s;
+  };
+  if (!c) return fail(ERASE_ERR_INVALID_ARG, "config is NULL");
+  if (c->dtype != ERASE_F32 && c->dtype != ERASE_BF16) return fail(ERASE_ERR_INVALID_ARG, "dtype must be F32 or BF16");
+  if (c->n_blocks < 1 || c->n_blocks > kMaxBlocks) return fail(ERASE_ERR_SHAPE, "n_blocks must be in [1, 64]");
+  if (!c->blocks) return fail(ERASE_ERR_INVALID_ARG, "blocks is NULL");
+  if (c->batch < 1 || c->batch > kMaxBatch) return fail(ERASE_ERR_SHAPE, "batch must be in [1, 2^24]");
+  if (c->in_dim < 1 || c->in_dim > kMaxDim) return fail(ERASE_ERR_SHAPE, "in_dim must be in [1, 65536]");
+  const int esz = c->dtype == ERASE_BF16 ? 2 : 4;
+  if (c->x_ld < c->in_dim || (int64_t(c->x_ld) * esz) % 16 != 0)
+    return fail(ERASE_ERR_SHAPE, "x_ld must be >= in_dim and a multiple of 16 bytes");
+  if (!(std::isfinite(c->lr) && c->lr >= 0.f)) return fail(ERASE_ERR_INVALID_ARG, "lr must be finite and >= 0");
+  if (!(c->beta1 >= 0.f && c->beta1 < 1.f && c->beta2 >= 0.f && c->beta2 < 1.f))
+    return fail(ERASE_ERR_INVALID_ARG, "betas must be in [0, 1)");
+  if (!(std::isfinite(c->eps) && c->eps >= 0.f)) return fail(ERASE_ERR_INVALID_ARG, "eps must be finite and >= 0");
+  int prev_out = -1;
+  for (int b = 0; b < c->n_blocks; ++b) {
+    const erase_block_spec& B = c->blocks[b];
+    if (B.input_src != ERASE_IN_X && B.input_src != ERASE_IN_PREV)
+      return fail(ERASE_ERR_INVALID_ARG, "input_src must be IN_X or IN_PREV");
+    if (b == 0 && B.input_src != ERASE_IN_X) return fail(ERASE_ERR_INVALID_ARG, "block 0 must read x");
+    if (B.n_layers < 1 || B.n_layers > kMaxLayers) return fail(ERASE_ERR_SHAPE, "n_layers must be in [1, 16]");
+    if (!B.layers) return fail(ERASE_ERR_INVALID_ARG, "layers is NULL");
+    if (B.loss != ERASE_LOSS_BCE) return fail(ERASE_ERR_UNSUPPORTED, "only the sigmoid-BCE local loss is implemented");
+    if (!std::isfinite(B.lambda)) return fail(ERASE_ERR_INVALID_ARG, "lambda must be finite");
+    const int width = B.input_src == ERASE_IN_X ? c->in_dim : prev_out;
+    int cur = width;
+    bool seen_linear = false;
+    for (int l = 0; l < B.n_layers; ++l) {
+      const erase_layer_spec& L = B.layers[l];
+      if (L.kind != ERASE_LAYER_LINEAR_RELU && L.kind != ERASE_LAYER_CROSS)
+        return fail(ERASE_ERR_INVALID_ARG, "layer kind must be LINEAR_RELU or CROSS");
+      if (L.in_dim < 1 || L.in_dim > kMaxDim || L.out_dim < 1 || L.out_dim > kMaxDim)
+        return fail(ERASE_ERR_SHAPE, "layer dims must be in [1, 65536]");
+      if (L.in_dim != cur) return fail(ERASE_ERR_SHAPE, "layer in_dim does not match the width feeding it");
+      if (int64_t(L.in_dim) * L.out_dim > (int64_t(1) << 31) - 1)
+        return fail(ERASE_ERR_SHAPE, "layer weight has more than 2^31-1 elements");
+      if (L.kind == ERASE_LAYER_CROSS) {
+        if (seen_linear) return fail(ERASE_ERR_UNSUPPORTED, "cross layers must precede linear layers");
+        if (L.out_dim != L.in_dim || L.in_dim != width)
+          return fail(ERASE_ERR_SHAPE, "a cross layer keeps the block input width");
+      } else {
+        seen_linear = true;
+      }
+      cur = L.out_dim;
+    }
+    if (B.layers[B.n_layers - 1].kind != ERASE_LAYER_LINEAR_RELU)
+      return fail(ERASE_ERR_UNSUPPORTED, "the last layer of a block must be LINEAR_RELU");
+    prev_out = cur;
+  }
+  return ERASE_OK;
+}
+
+// ---------------------------------------------------------------------------
+// plan: every buffer of the workspace and every launch's shape
+// ---------------------------------------------------------------------------
+struct GemmPlan {
+  int bm = 64, bn = 64, split = 1, kps = 0;
+};
+
+struct LayerRT {
+  int kind = 0, K = 0, N = 0;
+  int64_t offW = 0, offb = 0;
+  void* wsh = nullptr; int64_t ldwsh = 0;
+  void* wsht = nullptr; int64_t ldwsht = 0;
+  void* y = nullptr; int64_t ldy = 0;
+  void* yt = nullptr; int64_t ldyt = 0;
+  void* dmn = nullptr; int64_t lddmn = 0;
+  void* dnm = nullptr; int64_t lddnm = 0;
+  void* g = nullptr; int64_t ldg = 0;
+  float* part = nullptr; int64_t ldp = 0, pstride = 0;
+  float* bpart = nullptr;
+  GemmPlan fwd, wgrad, dgrad;
+};
+
+struct BlockRT {
+  int input_src = 0;
+  float lam = 1.f;
+  int L = 0;
+  LayerRT layer[kMaxLayers];
+  int64_t nparam = 0, off_w = 0, off_c = 0;
+  int nhead = 0;
+  float* pdw = nullptr;
+  float* pdc = nullptr;
+  float* ploss = nullptr;
+  AdamSeg* segs_dev = nullptr;
+  std::vector<AdamSeg> segs;
+  int64_t nchunks = 0;
+  erase_block_buffers buf{};
+};
+
+struct Plan {
+  int bf16 = 1, esz = 2, M = 0;
+  int64_t ldm = 0;
+  int64_t* t = nullptr;
+  int* status = nullptr;
+  void* xt = nullptr; int64_t ldxt = 0;
+  std::vector<BlockRT> blk;
+  size_t bytes = 0;
+};
+
+struct Carver {
+  uintptr_t base;
+  size_t off = kAlign;  // the first 256 bytes hold the step counter and status word
+  void* take(size_t n) {
+    off = (off + kAlign - 1) / kAlign * kAlign;
+    void* p = reinterpret_cast<void*>(base + off);
+    off += std::max<size_t>(n, 1);
+    return p;
+  }
+};
+
+// Workgroup tile and split of one GEMM.  Enough workgroups to cover the 256
+// CUs when the shape allows it, the largest tile that still does, and a
+// split of the contraction only for weight gradients (whose outputs are few).
+GemmPlan choose_gemm(int bf16, int64_t Mg, int64_t Ng, int64_t Kc, bool allow_split) {
+  GemmPlan p;
+  const int BK = bf16 ? 64 : 32;
+  if (!bf16) {
+    p.bm = p.bn = 64;
+    p.split = 1;
+    p.kps = (int)roundup(std::max<int64_t>(Kc, 1), BK);
+    return p;
+  }
+  const int tiles[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
+  const int64_t target = 256;
+  int best = -1;
+  for (int i = 0; i < 4; ++i) {
+    const int64_t w = cdiv(Mg, tiles[i][0]) * cdiv(Ng, tiles[i][1]);
+    if (w >= target) { best = i; break; }
+  }
+  int split = 1;
+  if (best < 0) {
+    if (allow_split) {
+      best = 0;
+      const int64_t w = cdiv(Mg, 128) * cdiv(Ng, 128);
+      while (split < 16 && w * split < target && Kc / (split * 2) >= 256) split *= 2;
+      if (w * split < target / 2) {  // still small: a smaller tile instead
+        best = 3;
+        split = 1;
+        const int64_t w2 = cdiv(Mg, 64) * cdiv(Ng, 64);
+        while (split < 16 && w2 * split < target && Kc / (split * 2) >= 256) split *= 2;
+      }
+    } else {
+      best = 3;
+    }
+  }
+  p.bm = tiles[best][0];
+  p.bn = tiles[best][1];
+  p.kps = (int)roundup(cdiv(std::max<int64_t>(Kc, 1), split), BK);
+  p.split = (int)cdiv(std::max<int64_t>(Kc, 1), p.kps);
+  return p;
+}
+
+size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
+  P->bf16 = c.dtype == ERASE_BF16;
+  P->esz = P->bf16 ? 2 : 4;
+  P->M = c.batch;
+  const int esz = P->esz;
+  const int64_t M = c.batch;
+  P->ldm = roundup(M, 64);
+  Carver cv{base};
+  P->t = reinterpret_cast<int64_t*>(base);
+  P->status = reinterpret_cast<int*>(base + 8);
+  bool any_x = false;
+  for (int b = 0; b < c.n_blocks; ++b) any_x |= c.blocks[b].input_src == ERASE_IN_X;
+  if (any_x) {
+    P->ldxt = P->ldm;
+    P->xt = cv.take(size_t(c.in_dim) * P->ldxt * esz);
+  }
+  P->blk.assign(c.n_blocks, BlockRT{});
+  for (int b = 0; b < c.n_blocks; ++b) {
+    const erase_block_spec& S = c.blocks[b];
+    BlockRT& B = P->blk[b];
+    B.input_src = S.input_src;
+    B.lam = S.lambda;
+    B.L = S.n_layers;
+    const bool next_chained = b + 1 < c.n_blocks && c.blocks[b + 1].input_src == ERASE_IN_PREV;
+    int64_t off = 0;
+    for (int l = 0; l < B.L; ++l) {
+      LayerRT& R = B.layer[l];
+      R.kind = S.layers[l].kind;
+      R.K = S.layers[l].in_dim;
+      R.N = S.layers[l].out_dim;
+      R.offW = off;
+      off += int64_t(R.K) * R.N;
+      R.offb = off;
+      off += R.N;
+      const int64_t ldK = roundup(R.K, 64), ldN = roundup(R.N, 64);
+      R.ldwsh = ldK;
+      R.wsh = cv.take(size_t(R.N) * ldK * esz);
+      if (l >= 1) {
+        R.ldwsht = ldN;
+        R.wsht = cv.take(size_t(R.K) * ldN * esz);
+      }
+      R.ldy = ldN;
+      R.y = cv.take(size_t(M) * ldN * esz);
+      if (l + 1 < B.L || next_chained) {
+        R.ldyt = P->ldm;
+        R.yt = cv.take(size_t(R.N) * P->ldm * esz);
+      }
+      R.lddnm = P->ldm;
+      R.dnm = cv.take(size_t(R.N) * P->ldm * esz);
+      if (l >= 1) {
+        R.lddmn = ldN;
+        R.dmn = cv.take(size_t(M) * ldN * esz);
+      }
+      if (R.kind == ERASE_LAYER_CROSS && l >= 1) {
+        R.ldg = ldN;
+        R.g = cv.take(size_t(M) * ldN * esz);
+      }
+      // launch shapes
+      R.fwd = choose_gemm(P->bf16, M, R.N, R.K, false);
+      R.wgrad = choose_gemm(P->bf16, R.N, R.K, M, true);
+      if (l >= 1) R.dgrad = choose_gemm(P->bf16, M, R.K, R.N, false);
+      R.ldp = ldK;
+      R.pstride = int64_t(R.N) * ldK;
+      R.part = static_cast<float*>(cv.take(size_t(R.wgrad.split) * R.pstride * 4));
+      R.bpart = static_cast<float*>(cv.take(size_t(R.wgrad.split) * R.N * 4));
+    }
+    const int NL = B.layer[B.L - 1].N;
+    B.off_w = off;
+    off += NL;
+    B.off_c = off;
+    off += 1;
+    B.nparam = off;
+    B.nhead = (int)cdiv(M, HEAD_ROWS);
+    B.pdw = static_cast<float*>(cv.take(size_t(B.nhead) * NL * 4));
+    B.pdc = static_cast<float*>(cv.take(size_t(B.nhead) * 4));
+    B.ploss = static_cast<float*>(cv.take(size_t(B.nhead) * 4));
+    const int nseg = 2 * B.L + 2;
+    B.segs_dev = static_cast<AdamSeg*>(cv.take(sizeof(AdamSeg) * nseg));
+  }
+  P->bytes = cv.off;
+  return cv.off;
+}
+
+// Adam segment tables (host copies; pointers into caller buffers/workspace).
+void build_segments(Plan* P, const erase_block_buffers* bufs) {
+  for (size_t b = 0; b < P->blk.size(); ++b) {
+    BlockRT& B = P->blk[b];
+    B.buf = bufs[b];
+    B.segs.clear();
+    int64_t chunk = 0;
+    auto add = [&](int64_t off, int rows, int cols, const float* part, int64_t pstride, int ldpart, int nsplit,
+                    void* sh, int64_t ldsh, void* sht, int64_t ldsht) {
+      AdamSeg s{};
+      s.p = B.buf.param + off;
+      s.m = B.buf.m + off;
+      s.v = B.buf.v + off;
+      s.g = B.buf.grad ? B.buf.grad + off : nullptr;
+      s.part = part;
+      s.pstride = pstride;
+      s.rows = rows;
+      s.cols = cols;
+      s.ldpart = ldpart;
+      s.nsplit = nsplit;
+      s.sh = sh;
+      s.ldsh = ldsh;
+      s.sht = sht;
+      s.ldsht = ldsht;
+      s.chunk0 = chunk;
+      chunk += cdiv(int64_t(rows) * cols, ADAM_CHUNK);
+      B.segs.push_back(s);
+    };
+    for (int l = 0; l < B.L; ++l) {
+      LayerRT& R = B.layer[l];
+      add(R.offW, R.N, R.K, R.part, R.pstride, (int)R.ldp, R.wgrad.split, R.wsh, R.ldwsh, R.wsht, R.ldwsht);
+      add(R.offb, 1, R.N, R.bpart, R.N, R.N, R.wgrad.split, nullptr, 0, nullptr, 0);
+    }
+    const int NL = B.layer[B.L - 1].N;
+    add(B.off_w, 1, NL, B.pdw, NL, NL, B.nhead, nullptr, 0, nullptr, 0);
+    add(B.off_c, 1, 1, B.pdc, 1, 1, B.nhead, nullptr, 0, nullptr, 0);
+    B.nchunks = chunk;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// context
+// ---------------------------------------------------------------------------
+struct TimedLaunch {
+  erase_kernel_time rec;
+  hipEvent_t e0, e1;
+};
+
+struct GraphEntry {
+  const void* x;
+  const float* y;
+  float* losses;
+  int sched;
+  hipGraph_t graph;
+  hipGraphExec_t exec;
+};
+
+struct Ctx {
+  erase_config cfg{};
+  std::vector<erase_block_spec> blocks;
+  std::vector<std::vector<erase_layer_spec>> layers;
+  Plan P;
+  char* ws = nullptr;
+  size_t ws_bytes = 0;
+  hipStream_t sf = nullptr, sb = nullptr;
+  int device = 0;
+  std::vector<hipEvent_t> ef, eb;
+  erase_status sticky = ERASE_OK;
+  std::string err;
+  std::vector<GraphEntry> graphs;
+  bool timing = false;
+  std::vector<hipEvent_t> tev;  // timing events pool
+  hipEvent_t tstart = nullptr;
+  std::vector<TimedLaunch> last;
+  bool last_valid = false;
+};
+
+bool hip_ok(Ctx* c, hipError_t e, const char* what) {
+  if (e == hipSuccess) return true;
+  if (c) {
+    char buf[256];
+    std::snprintf(buf, sizeof buf, "%s: %s", what, hipGetErrorString(e));
+    c->err = buf;
+    c->sticky = ERASE_ERR_HIP;
+  }
+  return false;
+}
+
+#define HIPCHK(c, call)                                  \
+  do {                                                   \
+    if (!hip_ok((c), (call), #call)) return ERASE_ERR_HIP; \
+  } while (0)
+
+// Algorithmic cost of each launch (see the measurement notes of the design).
+struct Cost {
+  double flops = 0, bytes = 0;
+  int tile_m = 0, tile_n = 0, split = 0, grid = 0;
+};
+
+Cost gemm_cost(const GemmDesc& g) {
+  Cost c;
+  c.tile_m = g.bm;
+  c.tile_n = g.bn;
+  c.split = g.split;
+  c.grid = (int)(cdiv(g.M, g.bm) * cdiv(g.N, g.bn) * g.split);
+  return c;
+}
+
+class Enqueuer {
+ public:
+  Enqueuer(Ctx* c, bool timed) : c_(c), timed_(timed) {}
+
+  template <class F>
+  erase_status run(int kind, int blk, int layer, int stream_id, hipStream_t s, Cost cost, F&& fn) {
+    TimedLaunch tl{};
+    if (timed_) {
+      if (ev_ + 2 > c_->tev.size()) {
+        c_->err = "timing event pool exhausted";
+        return ERASE_ERR_STATE;
+      }
+      tl.e0 = c_->tev[ev_++];
+      tl.e1 = c_->tev[ev_++];
+      HIPCHK(c_, hipEventRecord(tl.e0, s));
+    }
+    hipError_t e = fn();
+    if (!hip_ok(c_, e, "kernel launch")) return ERASE_ERR_HIP;
+    if (timed_) {
+      HIPCHK(c_, hipEventRecord(tl.e1, s));
+      tl.rec.kind = kind;
+      tl.rec.block = blk;
+      tl.rec.layer = layer;
+      tl.rec.stream = stream_id;
+      tl.rec.flops = cost.flops;
+      tl.rec.bytes = cost.bytes;
+      tl.rec.tile_m = cost.tile_m;
+      tl.rec.tile_n = cost.tile_n;
+      tl.rec.split = cost.split;
+      tl.rec.grid = cost.grid;
+      out_.push_back(tl);
+    }
+    return ERASE_OK;
+  }
+  std::vector<TimedLaunch>& launches() { return out_; }
+
+ private:
+  Ctx* c_;
+  bool timed_;
+  size_t ev_ = 0;
+  std::vector<TimedLaunch> out_;
+};
+
+#define RUN(...)                                   \
+  do {                                             \
+    erase_status st_ = q.run(__VA_ARGS__);         \
+    if (st_ != ERASE_OK) return st_;               \
+  } while (0)
+
+// Input of layer l of block b, row-major and feature-major.
+void layer_input(const Ctx* c, int b, int l, const void* x, const void** mn, int64_t* ldmn, const void** nm,
+                 int64_t* ldnm) {
+  const Plan& P = c->P;
+  const BlockRT& B = P.blk[b];
+  if (l > 0) {
+    *mn = B.layer[l - 1].y;
+    *ldmn = B.layer[l - 1].ldy;
+    *nm = B.layer[l - 1].yt;
+    *ldnm = B.layer[l - 1].ldyt;
+  } else if (B.input_src == ERASE_IN_X) {
+    *mn = x;
+    *ldmn = c->cfg.x_ld;
+    *nm = P.xt;
+    *ldnm = P.ldxt;
+  } else {
+    const BlockRT& A = P.blk[b - 1];
+    const LayerRT& R = A.layer[A.L - 1];
+    *mn = R.y;
+    *ldmn = R.ldy;
+    *nm = R.yt;
+    *ldnm = R.ldyt;
+  }
+}
+
+erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const float* labels, hipStream_t s, int sid) {
+  const Plan& P = c->P;
+  const BlockRT& B = P.blk[b];
+  const int M = P.M, esz = P.esz;
+  const void* x0;
+  int64_t ldx0;
+  const void* unused;
+  int64_t unused_ld;
+  layer_input(c, b, 0, x, &x0, &ldx0, &unused, &unused_ld);
+  for (int l = 0; l < B.L; ++l) {
+    const LayerRT& R = B.layer[l];
+    const void* a;
+    int64_t lda;
+    layer_input(c, b, l, x, &a, &lda, &unused, &unused_ld);
+    GemmDesc g{};
+    g.A = a;
+    g.lda = lda;
+    g.B = R.wsh;
+    g.ldb = R.ldwsh;
+    g.M = M;
+    g.N = R.N;
+    g.K = R.K;
+    g.kps = R.fwd.kps;
+    g.split = 1;
+    g.bm = R.fwd.bm;
+    g.bn = R.fwd.bn;
+    EpiParams e{};
+    e.bias = B.buf.param + R.offb;
+    e.y = R.y;
+    e.ldy = R.ldy;
+    e.yt = R.yt;
+    e.ldyt = R.ldyt;
+    const int kind = R.kind == ERASE_LAYER_CROSS ? GK_FWD_CROSS : GK_FWD_RELU;
+    if (kind == GK_FWD_CROSS) {
+      e.x0 = x0;
+      e.ldx0 = ldx0;
+      e.xl = a;
+      e.ldxl = lda;
+    }
+    Cost cost = gemm_cost(g);
+    cost.flops = 2.0 * M * R.N * R.K;
+    cost.bytes = double(esz) * (double(M) * R.K + double(R.N) * R.K + double(M) * R.N * (R.yt ? 2 : 1)) + 4.0 * R.N +
+                 (kind == GK_FWD_CROSS ? 2.0 * esz * M * R.N : 0.0);
+    const int bf = P.bf16;
+    RUN(1, b, l, sid, s, cost, [&]() { return launch_gemm(bf, kind, g, e, s); });
+  }
+  const LayerRT& Rl = B.layer[B.L - 1];
+  HeadArgs h{};
+  h.z = Rl.y;
+  h.ldz = Rl.ldy;
+  h.w = B.buf.param + B.off_w;
+  h.c = B.buf.param + B.off_c;
+  h.y = labels;
+  h.lam = B.lam;
+  h.inv_m = 1.0f / float(M);
+  h.M = M;
+  h.N = Rl.N;
+  h.dmn = Rl.dmn;
+  h.lddmn = Rl.lddmn;
+  h.dnm = Rl.dnm;
+  h.lddnm = Rl.lddnm;
+  h.pdw = B.pdw;
+  h.pdc = B.pdc;
+  h.ploss = B.ploss;
+  Cost cost;
+  cost.grid = B.nhead;
+  cost.flops = 4.0 * M * Rl.N;
+  cost.bytes = double(esz) * M * Rl.N * (1 + 1 + (Rl.dmn ? 1 : 0)) + 4.0 * M + 4.0 * Rl.N + 4.0 * B.nhead * (Rl.N + 2);
+  const int bf = P.bf16;
+  RUN(2, b, -1, sid, s, cost, [&]() { return launch_head(bf, h, s); });
+  return ERASE_OK;
+}
+
+erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStream_t s, int sid) {
+  const Plan& P = c->P;
+  const BlockRT& B = P.blk[b];
+  const int M = P.M, esz = P.esz, bf = P.bf16;
+  const void* x0;
+  int64_t ldx0;
+  const void* unused;
+  int64_t unused_ld;
+  layer_input(c, b, 0, x, &x0, &ldx0, &unused, &unused_ld);
+  for (int l = B.L - 1; l >= 0; --l) {
+    const LayerRT& R = B.layer[l];
+    const void* inmn;
+    int64_t ldinmn;
+    const void* innm;
+    int64_t ldinnm;
+    layer_input(c, b, l, x, &inmn, &ldinmn, &innm, &ldinnm);
+    {  // weight and bias gradient: dW = dH^T a_{l-1}, db = row sums of dH^T
+      GemmDesc g{};
+      g.A = R.dnm;
+      g.lda = R.lddnm;
+      g.B = innm;
+      g.ldb = ldinnm;
+      g.M = R.N;
+      g.N = R.K;
+      g.K = M;
+      g.kps = R.wgrad.kps;
+      g.split = R.wgrad.split;
+      g.bm = R.wgrad.bm;
+      g.bn = R.wgrad.bn;
+      EpiParams e{};
+      e.part = R.part;
+      e.ldp = R.ldp;
+      e.pstride = R.pstride;
+      e.bpart = R.bpart;
+      Cost cost = gemm_cost(g);
+      cost.flops = 2.0 * M * R.N * R.K;
+      cost.bytes = double(esz) * M * (double(R.N) + R.K) + 4.0 * R.wgrad.split * (double(R.N) * R.K + R.N);
+      RUN(3, b, l, sid, s, cost, [&]() { return launch_gemm(bf, GK_WGRAD, g, e, s); });
+    }
+    if (l == 0) break;  // the block input is detached: no input gradient
+    {
+      const LayerRT& Rb = B.layer[l - 1];
+      GemmDesc g{};
+      g.A = R.dmn;
+      g.lda = R.lddmn;
+      g.B = R.wsht;
+      g.ldb = R.ldwsht;
+      g.M = M;
+      g.N = R.K;
+      g.K = R.N;
+      g.kps = R.dgrad.kps;
+      g.split = 1;
+      g.bm = R.dgrad.bm;
+      g.bn = R.dgrad.bn;
+      EpiParams e{};
+      if (R.kind == ERASE_LAYER_CROSS) {
+        e.res = R.g;
+        e.ldres = R.ldg;
+      }
+      e.dmn = Rb.dmn;
+      e.lddmn = Rb.lddmn;
+      e.dnm = Rb.dnm;
+      e.lddnm = Rb.lddnm;
+      if (Rb.kind == ERASE_LAYER_CROSS) {
+        e.below_cross = 1;
+        e.x0 = x0;
+        e.ldx0 = ldx0;
+        e.gout = Rb.g;
+        e.ldgout = Rb.ldg;
+      } else {
+        e.below_cross = 0;
+        e.mask = Rb.y;
+        e.ldmask = Rb.ldy;
+      }
+      Cost cost = gemm_cost(g);
+      cost.flops = 2.0 * M * R.N * R.K;
+      const double outs = 1.0 + (Rb.dmn ? 1.0 : 0.0) + (e.gout ? 1.0 : 0.0);
+      cost.bytes = double(esz) * (double(M) * R.N + double(R.N) * R.K + double(M) * R.K * (outs + 1.0) +
+                                  (e.res ? double(M) * R.K : 0.0));
+      RUN(4, b, l, sid, s, cost, [&]() { return launch_gemm(bf, GK_DGRAD, g, e, s); });
+    }
+  }
+  return ERASE_OK;
+}
+
+erase_status enqueue_adam(Ctx* c, Enqueuer& q, int b, float* losses, hipStream_t s, int sid) {
+  const Plan& P = c->P;
+  const BlockRT& B = P.blk[b];
+  AdamArgs a{};
+  a.seg = B.segs_dev;
+  a.nseg = (int)B.segs.size();
+  a.nchunks = B.nchunks;
+  a.t = P.t;
+  a.lr = c->cfg.lr;
+  a.beta1 = c->cfg.beta1;
+  a.beta2 = c->cfg.beta2;
+  a.eps = c->cfg.eps;
+  a.ploss = B.ploss;
+  a.nloss = B.nhead;
+  a.inv_m = 1.0f / float(P.M);
+  a.loss_out = losses + b;
+  a.status = P.status;
+  Cost cost;
+  cost.grid = (int)B.nchunks;
+  for (const AdamSeg& sg : B.segs) {
+    const double n = double(sg.rows) * sg.cols;
+    cost.flops += 12.0 * n;
+    cost.bytes += n * (4.0 * sg.nsplit + 24.0 + (sg.g ? 4.0 : 0.0) + (sg.sh ? P.esz : 0) + (sg.sht ? P.esz : 0));
+  }
+  const int bf = P.bf16;
+  RUN(5, b, -1, sid, s, cost, [&]() { return launch_adam(bf, a, s); });
+  return ERASE_OK;
+}
+
+// One step's launches.  `sched` selects serial or overlapped order; graph
+// schedules call this under stream capture.
+erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* labels, int sched, float* losses) {
+  const Plan& P = c->P;
+  const bool overlap = sched == ERASE_SCHED_OVERLAP || sched == ERASE_SCHED_OVERLAP_GRAPH;
+  const int nb = (int)P.blk.size();
+  hipStream_t sf = c->sf, sb = c->sb;
+  {
+    PrologueArgs pa{};
+    pa.t = P.t;
+    pa.x = x;
+    pa.ldx = c->cfg.x_ld;
+    pa.xt = P.xt;
+    pa.ldxt = P.ldxt;
+    pa.M = P.M;
+    pa.K = c->cfg.in_dim;
+    Cost cost;
+    cost.bytes = P.xt ? 2.0 * P.esz * double(P.M) * c->cfg.in_dim : 0.0;
+    const int bf = P.bf16;
+    RUN(0, -1, -1, 0, sf, cost, [&]() { return launch_prologue(bf, pa, sf); });
+  }
+  if (overlap) {
+    for (int b = 0; b < nb; ++b) {
+      erase_status st = enqueue_forward(c, q, b, x, labels, sf, 0);
+      if (st != ERASE_OK) return st;
+      HIPCHK(c, hipEventRecord(c->ef[b], sf));
+      HIPCHK(c, hipStreamWaitEvent(sb, c->ef[b], 0));
+      st = enqueue_backward(c, q, b, x, sb, 1);
+      if (st != ERASE_OK) return st;
+      st = enqueue_adam(c, q, b, losses, sb, 1);
+      if (st != ERASE_OK) return st;
+    }
+    HIPCHK(c, hipEventRecord(c->eb[nb - 1], sb));
+    HIPCHK(c, hipStreamWaitEvent(sf, c->eb[nb - 1], 0));
+  } else {
+    for (int b = 0; b < nb; ++b) {
+      erase_status st = enqueue_forward(c, q, b, x, labels, sf, 0);
+      if (st != ERASE_OK) return st;
+    }
+    for (int b = nb - 1; b >= 0; --b) {
+      erase_status st = enqueue_backward(c, q, b, x, sf, 0);
+      if (st != ERASE_OK) return st;
+    }
+    for (int b = 0; b < nb; ++b) {
+      erase_status st = enqueue_adam(c, q, b, losses, sf, 0);
+      if (st != ERASE_OK) return st;
+    }
+  }
+  return ERASE_OK;
+}
+
+int launches_per_step(const Plan& P) {
+  int n = 1;
+  for (const BlockRT& B : P.blk) n += B.L + 1 + B.L + (B.L - 1) + 1;
+  return n;
+}
+
+erase_status refresh(Ctx* c) {
+  for (const BlockRT& B : c->P.blk) {
+    AdamArgs a{};
+    a.seg = B.segs_dev;
+    a.nseg = (int)B.segs.size();
+    a.nchunks = B.nchunks;
+    HIPCHK(c, launch_refresh(c->P.bf16, a, c->sf));
+  }
+  return ERASE_OK;
+}
+
+void destroy_graphs(Ctx* c) {
+  for (GraphEntry& g : c->graphs) {
+    if (g.exec) (void)hipGraphExecDestroy(g.exec);
+    if (g.graph) (void)hipGraphDestroy(g.graph);
+  }
+  c->graphs.clear();
+}
+
+Ctx* as_ctx(void* p) { return static_cast<Ctx*>(p); }
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+extern "C" {
+
+erase_status erase_param_count(const erase_config* cfg, int32_t block, int64_t* count) {
+  if (!count) return ERASE_ERR_INVALID_ARG;
+  erase_status st = validate(cfg, nullptr);
+  if (st != ERASE_OK) return st;
+  if (block < 0 || block >= cfg->n_blocks) return ERASE_ERR_INVALID_ARG;
+  const erase_block_spec& B = cfg->blocks[block];
+  int64_t n = 0;
+  for (int l = 0; l < B.n_layers; ++l) n += int64_t(B.layers[l].in_dim) * B.layers[l].out_dim + B.layers[l].out_dim;
+  n += B.layers[B.n_layers - 1].out_dim + 1;
+  *count = n;
+  return ERASE_OK;
+}
+
+erase_status erase_workspace_bytes(const erase_config* cfg, size_t* bytes) {
+  if (!bytes) return ERASE_ERR_INVALID_ARG;
+  erase_status st = validate(cfg, nullptr);
+  if (st != ERASE_OK) return st;
+  Plan P;
+  *bytes = build_plan(*cfg, 0, &P);
+  return ERASE_OK;
+}
+
+erase_status erase_init(const erase_config* cfg, const erase_block_buffers* bufs, void* workspace, size_t ws_bytes,
+                        void* s_fwd, void* s_bwd, void** ctx_out) {
+  if (!ctx_out) return ERASE_ERR_INVALID_ARG;
+  *ctx_out = nullptr;
+  std::string err;
+  erase_status st = validate(cfg, &err);
+  if (st != ERASE_OK) return st;
+  if (!bufs) return ERASE_ERR_INVALID_ARG;
+  for (int b = 0; b < cfg->n_blocks; ++b) {
+    if (!bufs[b].param || !bufs[b].m || !bufs[b].v) return ERASE_ERR_INVALID_ARG;
+    const uintptr_t al = reinterpret_cast<uintptr_t>(bufs[b].param) | reinterpret_cast<uintptr_t>(bufs[b].m) |
+                         reinterpret_cast<uintptr_t>(bufs[b].v) | reinterpret_cast<uintptr_t>(bufs[b].grad);
+    if (al % 4) return ERASE_ERR_INVALID_ARG;
+  }
+  if (!s_fwd || !s_bwd || s_fwd == s_bwd) return ERASE_ERR_INVALID_ARG;
+  if (!workspace || reinterpret_cast<uintptr_t>(workspace) % kAlign) return ERASE_ERR_WORKSPACE;
+  {
+    Plan probe;
+    if (ws_bytes < build_plan(*cfg, 0, &probe)) return ERASE_ERR_WORKSPACE;
+  }
+
+  Ctx* c = new Ctx();
+  c->cfg = *cfg;
+  c->blocks.assign(cfg->blocks, cfg->blocks + cfg->n_blocks);
+  c->layers.resize(cfg->n_blocks);
+  for (int b = 0; b < cfg->n_blocks; ++b) {
+    c->layers[b].assign(cfg->blocks[b].layers, cfg->blocks[b].layers + cfg->blocks[b].n_layers);
+    c->blocks[b].layers = c->layers[b].data();
+  }
+  c->cfg.blocks = c->blocks.data();
+  c->ws = static_cast<char*>(workspace);
+  c->ws_bytes = ws_bytes;
+  c->sf = static_cast<hipStream_t>(s_fwd);
+  c->sb = static_cast<hipStream_t>(s_bwd);
+  build_plan(c->cfg, reinterpret_cast<uintptr_t>(workspace), &c->P);
+  build_segments(&c->P, bufs);
+
+  auto bail = [&](erase_status s) {
+    for (hipEvent_t e : c->ef) (void)hipEventDestroy(e);
+    for (hipEvent_t e : c->eb) (void)hipEventDestroy(e);
+    delete c;
+    return s;
+  };
+  if (hipGetDevice(&c->device) != hipSuccess) return bail(ERASE_ERR_HIP);
+  for (int b = 0; b < cfg->n_blocks; ++b) {
+    hipEvent_t e1, e2;
+    if (hipEventCreateWithFlags(&e1, hipEventDisableTiming) != hipSuccess) return bail(ERASE_ERR_HIP);
+    c->ef.push_back(e1);
+    if (hipEventCreateWithFlags(&e2, hipEventDisableTiming) != hipSuccess) return bail(ERASE_ERR_HIP);
+    c->eb.push_back(e2);
+  }
+  // counters, segment tables, then the GEMM copies of the weights
+  if (hipMemsetAsync(c->ws, 0, kAlign, c->sf) != hipSuccess) return bail(ERASE_ERR_HIP);
+  for (BlockRT& B : c->P.blk) {
+    if (hipMemcpyAsync(B.segs_dev, B.segs.data(), sizeof(AdamSeg) * B.segs.size(), hipMemcpyHostToDevice, c->sf) !=
+        hipSuccess)
+      return bail(ERASE_ERR_HIP);
+  }
+  if (refresh(c) != ERASE_OK) return bail(ERASE_ERR_HIP);
+  // the host copies of the segment tables must outlive the async copies:
+  // they live in the context, which outlives the stream work it enqueued
+  *ctx_out = c;
+  return ERASE_OK;
+}
+
+erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t schedule, float* losses) {
+  Ctx* c = as_ctx(ctx);
+  if (!c) return ERASE_ERR_INVALID_ARG;
+  if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
+  if (!x || !labels || !losses) return ERASE_ERR_INVALID_ARG;
+  if (reinterpret_cast<uintptr_t>(x) % 16 || reinterpret_cast<uintptr_t>(labels) % 4 ||
+      reinterpret_cast<uintptr_t>(losses) % 4)
+    return ERASE_ERR_INVALID_ARG;
+  if (schedule < ERASE_SCHED_SERIAL || schedule > ERASE_SCHED_OVERLAP_GRAPH) return ERASE_ERR_INVALID_ARG;
+  const bool graph = schedule == ERASE_SCHED_SERIAL_GRAPH || schedule == ERASE_SCHED_OVERLAP_GRAPH;
+  if (graph && c->timing) return ERASE_ERR_UNSUPPORTED;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != c->device) {
+    c->err = "erase_step called with a different current device than erase_init";
+    return ERASE_ERR_STATE;
+  }
+  if (!graph) {
+    Enqueuer q(c, c->timing);
+    if (c->timing) HIPCHK(c, hipEventRecord(c->tstart, c->sf));
+    erase_status st = enqueue_step(c, q, x, labels, schedule, losses);
+    if (st != ERASE_OK) {
+      c->sticky = st == ERASE_ERR_HIP ? st : c->sticky;
+      return st;
+    }
+    if (c->timing) {
+      c->last = q.launches();
+      c->last_valid = true;
+    }
+    return ERASE_OK;
+  }
+  GraphEntry* ge = nullptr;
+  for (GraphEntry& g : c->graphs)
+    if (g.x == x && g.y == labels && g.losses == losses && g.sched == schedule) ge = &g;
+  if (!ge) {
+    if ((int)c->graphs.size() >= kMaxGraphs) {
+      // evict the oldest entry; its replays are ordered before anything new on sf
+      HIPCHK(c, hipStreamSynchronize(c->sf));
+      GraphEntry old = c->graphs.front();
+      if (old.exec) (void)hipGraphExecDestroy(old.exec);
+      if (old.graph) (void)hipGraphDestroy(old.graph);
+      c->graphs.erase(c->graphs.begin());
+    }
+    GraphEntry g{x, labels, losses, schedule, nullptr, nullptr};
+    HIPCHK(c, hipStreamBeginCapture(c->sf, hipStreamCaptureModeThreadLocal));
+    Enqueuer q(c, false);
+    erase_status st = enqueue_step(c, q, x, labels, schedule, losses);
+    hipGraph_t graph_h = nullptr;
+    hipError_t ee = hipStreamEndCapture(c->sf, &graph_h);
+    if (st != ERASE_OK) {
+      if (graph_h) (void)hipGraphDestroy(graph_h);
+      return st;
+    }
+    HIPCHK(c, ee);
+    g.graph = graph_h;
+    if (!hip_ok(c, hipGraphInstantiate(&g.exec, g.graph, nullptr, nullptr, 0), "hipGraphInstantiate")) {
+      (void)hipGraphDestroy(g.graph);
+      return ERASE_ERR_HIP;
+    }
+    c->graphs.push_back(g);
+    ge = &c->graphs.back();
+  }
+  HIPCHK(c, hipGraphLaunch(ge->exec, c->sf));
+  return ERASE_OK;
+}
+
+erase_status erase_sync(void* ctx) {
+  Ctx* c = as_ctx(ctx);
+  if (!c) return ERASE_ERR_INVALID_ARG;
+  if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
+  HIPCHK(c, hipStreamSynchronize(c->sf));
+  HIPCHK(c, hipStreamSynchronize(c->sb));
+  int status = 0;
+  HIPCHK(c, hipMemcpy(&status, c->P.status, sizeof(int), hipMemcpyDeviceToHost));
+  if (status != 0) {
+    c->sticky = ERASE_ERR_NONFINITE;
+    c->err = "a block loss was not finite";
+    return ERASE_ERR_NONFINITE;
+  }
+  return ERASE_OK;
+}
+
+erase_status erase_get_step(void* ctx, int64_t* t) {
+  Ctx* c = as_ctx(ctx);
+  if (!c || !t) return ERASE_ERR_INVALID_ARG;
+  if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
+  HIPCHK(c, hipStreamSynchronize(c->sf));
+  HIPCHK(c, hipMemcpy(t, c->P.t, sizeof(int64_t), hipMemcpyDeviceToHost));
+  return ERASE_OK;
+}
+
+erase_status erase_set_step(void* ctx, int64_t t) {
+  Ctx* c = as_ctx(ctx);
+  if (!c || t < 0) return ERASE_ERR_INVALID_ARG;
+  if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
+  HIPCHK(c, hipStreamSynchronize(c->sf));
+  HIPCHK(c, hipMemcpy(c->P.t, &t, sizeof(int64_t), hipMemcpyHostToDevice));
+  return ERASE_OK;
+}
+
+erase_status erase_refresh_weights(void* ctx) {
+  Ctx* c = as_ctx(ctx);
+  if (!c) return ERASE_ERR_INVALID_ARG;
+  if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
+  return refresh(c);
+}
+
+erase_status erase_set_timing(void* ctx, int32_t enable) {
+  Ctx* c = as_ctx(ctx);
+  if (!c) return ERASE_ERR_INVALID_ARG;
+  if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
+  if (enable && c->tev.empty()) {
+    const int n = 2 * launches_per_step(c->P);
+    for (int i = 0; i < n; ++i) {
+      hipEvent_t e;
+      HIPCHK(c, hipEventCreate(&e));
+      c->tev.push_back(e);
+    }
+    HIPCHK(c, hipEventCreate(&c->tstart));
+  }
+  c->timing = enable != 0;
+  c->last_valid = false;
+  return ERASE_OK;
+}
+
+erase_status erase_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, int32_t* n) {
+  Ctx* c = as_ctx(ctx);
+  if (!c || !n || (cap > 0 && !out)) return ERASE_ERR_INVALID_ARG;
+  if (!c->last_valid) return ERASE_ERR_STATE;
+  *n = (int32_t)c->last.size();
+  for (int i = 0; i < (int)c->last.size() && i < cap; ++i) {
+    TimedLaunch& t = c->last[i];
+    float a = 0.f, b = 0.f;
+    HIPCHK(c, hipEventElapsedTime(&a, c->tstart, t.e0));
+    HIPCHK(c, hipEventElapsedTime(&b, c->tstart, t.e1));
+    out[i] = t.rec;
+    out[i].start_ms = a;
+    out[i].end_ms = b;
+  }
+  return ERASE_OK;
+}
+
+erase_status erase_destroy(void* ctx) {
+  Ctx* c = as_ctx(ctx);
+  if (!c) return ERASE_OK;
+  (void)hipStreamSynchronize(c->sf);
+  (void)hipStreamSynchronize(c->sb);
+  destroy_graphs(c);
+  for (hipEvent_t e : c->ef) (void)hipEventDestroy(e);
+  for (hipEvent_t e : c->eb) (void)hipEventDestroy(e);
+  for (hipEvent_t e : c->tev) (void)hipEventDestroy(e);
+  if (c->tstart) (void)hipEventDestroy(c->tstart);
+  delete c;
+  return ERASE_OK;
+}
+
+const char* erase_status_str(int32_t s) {
+  switch (s) {
+    case ERASE_OK: return "ok";
+    case ERASE_ERR_INVALID_ARG: return "invalid argument";
+    case ERASE_ERR_SHAPE: return "invalid shape";
+    case ERASE_ERR_UNSUPPORTED: return "unsupported";
+    case ERASE_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case ERASE_ERR_HIP: return "HIP runtime error";
+    case ERASE_ERR_STATE: return "context in a failed state or call out of order";
+    case ERASE_ERR_NONFINITE: return "non-finite loss";
+    default: return "unknown status";
+  }
+}
+
+const char* erase_last_error(void* ctx) {
+  Ctx* c = as_ctx(ctx);
+  return c ? c->err.c_str() : "";
+}
+
+}  // extern "C"

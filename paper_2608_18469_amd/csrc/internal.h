@@ -1,0 +1,102 @@
+// Internal interface between the dispatcher (erase_api.cpp) and the HIP
+// kernels (kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace erase {
+
+// One GEMM launch: C[m][n] = sum_k A[m][k] * B[n][k] (both operands stored
+// with the contraction index contiguous), fp32 accumulation.  The
+// contraction range is split into `split` slices of `kps` elements; slice z
+// is handled by blockIdx.z.
+struct GemmDesc {
+  const void* A;
+  int64_t lda;
+  const void* B;
+  int64_t ldb;
+  int M, N, K;
+  int kps;
+  int split;
+  int bm, bn;  // workgroup tile
+};
+
+enum GemmKind { GK_FWD_RELU = 0, GK_FWD_CROSS = 1, GK_WGRAD = 2, GK_DGRAD = 3 };
+
+// Epilogue operands.  Which fields are read depends on the GemmKind.
+struct EpiParams {
+  // forward: y = relu(acc + bias) or x0 * (acc + bias) + xl
+  const float* bias;
+  void* y;   int64_t ldy;    // [M][ldy] row-major output
+  void* yt;  int64_t ldyt;   // [N][ldyt] feature-major copy, nullable
+  const void* x0; int64_t ldx0;  // block input (cross forward, and cross-below dgrad)
+  const void* xl; int64_t ldxl;  // layer input (cross forward residual)
+  // weight gradient: part[z][m][n], row sums of A into bpart[z][m]
+  float* part; int64_t ldp; int64_t pstride;
+  float* bpart;
+  // input gradient: g = acc (+ res); below relu: g*[mask>0]; below cross: g, g*x0
+  const void* res;  int64_t ldres;
+  const void* mask; int64_t ldmask;
+  void* gout; int64_t ldgout;
+  void* dmn;  int64_t lddmn;
+  void* dnm;  int64_t lddnm;
+  int below_cross;
+};
+
+hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s);
+
+// Step prologue: t += 1, and the feature-major copy xt[k][m] = x[m][k].
+struct PrologueArgs {
+  int64_t* t;
+  const void* x; int64_t ldx;
+  void* xt; int64_t ldxt;
+  int M, K;
+};
+hipError_t launch_prologue(int bf16, const PrologueArgs& a, hipStream_t s);
+
+// Fused local head + sigmoid-BCE + gradient at z (one workgroup per 64 rows).
+struct HeadArgs {
+  const void* z; int64_t ldz;    // [M][N] block output
+  const float* w;                // head weight [N] (fp32 master)
+  const float* c;                // head bias [1]
+  const float* y;                // labels [M]
+  float lam, inv_m;
+  int M, N;
+  void* dmn; int64_t lddmn;      // dz row-major (nullable)
+  void* dnm; int64_t lddnm;      // dz feature-major
+  float* pdw;                    // [nblk][N]
+  float* pdc;                    // [nblk]
+  float* ploss;                  // [nblk]
+};
+constexpr int HEAD_ROWS = 64;
+hipError_t launch_head(int bf16, const HeadArgs& a, hipStream_t s);
+
+// Fused split-reduction + Adam + GEMM-copy refresh for one block.  The
+// segment table lives in device memory (written once at init).
+struct AdamSeg {
+  float* p; float* m; float* v; float* g;   // flat [rows*cols] fp32 (g nullable)
+  const float* part;                        // partial sums [nsplit][rows][ldpart]
+  int64_t pstride;
+  int rows, cols, ldpart, nsplit;
+  void* sh;  int64_t ldsh;                  // GEMM copy [rows][ldsh], nullable
+  void* sht; int64_t ldsht;                 // transposed GEMM copy [cols][ldsht], nullable
+  int64_t chunk0;                           // first chunk index of this segment
+};
+struct AdamArgs {
+  const AdamSeg* seg;  // device [nseg]
+  int nseg;
+  int64_t nchunks;
+  const int64_t* t;
+  float lr, beta1, beta2, eps;
+  const float* ploss; int nloss; float inv_m;  // loss finalize (nullable ploss)
+  float* loss_out;
+  int* status;
+};
+constexpr int ADAM_CHUNK = 1024;
+hipError_t launch_adam(int bf16, const AdamArgs& a, hipStream_t s);
+
+// Weight copies only (init / refresh): same segments, no update.
+hipError_t launch_refresh(int bf16, const AdamArgs& a, hipStream_t s);
+
+}  // namespace erase

@@ -1,0 +1,152 @@
+"""Host-only checks of the C ABI: the library loads, exports every entry
+point the header declares, and validates configurations before any HIP call
+(no GPU needed: nothing here launches device work)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_18469_amd import erase, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    with open(os.path.join(ROOT, "include", "erase.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(erase_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = erase.lib()
+    names = _declared_functions()
+    assert len(names) >= 13
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(erase.SIGNATURES), set(names) ^ set(erase.SIGNATURES)
+
+
+def test_status_strings():
+    L = erase.lib()
+    for s in range(0, -8, -1):
+        assert L.erase_status_str(s) and L.erase_status_str(s) != b"unknown status"
+    assert L.erase_status_str(42) == b"unknown status"
+
+
+def _ncfg(cfg, **kw):
+    return erase.NativeConfig(cfg, **kw)
+
+
+def test_param_count_matches_generator():
+    for name in ("tiny", "ctr_mlp", "ctr_dcn", "deep_chain"):
+        cfg = synth.config(name)
+        nc = _ncfg(cfg)
+        total = sum(erase.param_count(nc, b) for b in range(len(cfg["blocks"])))
+        assert total == synth.param_count(cfg)
+    assert synth.param_count(synth.config("ctr_mlp")) == 6140934
+    assert synth.param_count(synth.config("ctr_dcn")) == 53527182
+    assert synth.param_count(synth.config("deep_chain")) == 1582092
+
+
+def test_pack_unpack_roundtrip():
+    cfg = synth.config("tiny")
+    params, _ = synth.make_workload(cfg, 0, 1)
+    for blk, p in zip(cfg["blocks"], params):
+        flat = erase.pack_block(p)
+        q = erase.unpack_block(blk, flat)
+        for (W, b), (W2, b2) in zip(p["layers"], q["layers"]):
+            assert (W == W2).all() and (b == b2).all()
+        assert (q["head"][0] == p["head"][0]).all() and (q["head"][1] == p["head"][1]).all()
+
+
+def test_workspace_bytes_positive_and_monotone_in_batch():
+    a = erase.workspace_bytes(_ncfg(synth.config("ctr_mlp", batch=1024)))
+    b = erase.workspace_bytes(_ncfg(synth.config("ctr_mlp")))
+    assert 0 < a < b
+    # full CTR-MLP: activations in two layouts, gradients, partials; well under 1 GiB
+    assert b < (1 << 30)
+
+
+def _status_ws(cfg_mut):
+    cfg = synth.config("tiny")
+    nc = _ncfg(cfg)
+    cfg_mut(nc)
+    n = ctypes.c_size_t(0)
+    return erase.lib().erase_workspace_bytes(nc.ptr(), ctypes.byref(n))
+
+
+@pytest.mark.parametrize("mut,code", [
+    (lambda nc: setattr(nc.c, "n_blocks", 0), erase.ERR_SHAPE),
+    (lambda nc: setattr(nc.c, "batch", 0), erase.ERR_SHAPE),
+    (lambda nc: setattr(nc.c, "dtype", 7), erase.ERR_INVALID_ARG),
+    (lambda nc: setattr(nc.c, "x_ld", 15), erase.ERR_SHAPE),
+    (lambda nc: setattr(nc.c, "x_ld", 18), erase.ERR_SHAPE),  # 72 bytes: not a multiple of 16
+    (lambda nc: setattr(nc.c, "lr", float("nan")), erase.ERR_INVALID_ARG),
+    (lambda nc: setattr(nc.c, "beta1", 1.0), erase.ERR_INVALID_ARG),
+    (lambda nc: setattr(nc.c, "eps", -1.0), erase.ERR_INVALID_ARG),
+    (lambda nc: setattr(nc._blocks[0], "input_src", erase.IN_PREV), erase.ERR_INVALID_ARG),
+    (lambda nc: setattr(nc._blocks[1], "input_src", 5), erase.ERR_INVALID_ARG),
+    (lambda nc: setattr(nc._blocks[0], "loss", 3), erase.ERR_UNSUPPORTED),
+    (lambda nc: setattr(nc._blocks[0], "n_layers", 0), erase.ERR_SHAPE),
+    (lambda nc: setattr(nc._blocks[0], "lam", float("inf")), erase.ERR_INVALID_ARG),
+    (lambda nc: setattr(nc._layers[0][0], "in_dim", 17), erase.ERR_SHAPE),
+    (lambda nc: setattr(nc._layers[0][1], "in_dim", 31), erase.ERR_SHAPE),
+    (lambda nc: setattr(nc._layers[0][1], "kind", 9), erase.ERR_INVALID_ARG),
+    (lambda nc: setattr(nc._layers[0][1], "kind", erase.CROSS), erase.ERR_UNSUPPORTED),
+])
+def test_validation_errors(mut, code):
+    assert _status_ws(mut) == code
+
+
+def test_cross_must_keep_width_and_precede_linear():
+    blocks = [{"input": "x", "layers": [("cross", 8, 8), ("linear_relu", 8, 4)], "lam": 1.0}]
+    nc = _ncfg(synth.custom("f32", 16, 8, blocks))
+    assert erase.workspace_bytes(nc) > 0
+    bad = [{"input": "x", "layers": [("linear_relu", 8, 8), ("cross", 8, 8), ("linear_relu", 8, 4)], "lam": 1.0}]
+    n = ctypes.c_size_t(0)
+    assert erase.lib().erase_workspace_bytes(_ncfg(synth.custom("f32", 16, 8, bad)).ptr(), ctypes.byref(n)) \
+        == erase.ERR_UNSUPPORTED
+    bad = [{"input": "x", "layers": [("cross", 8, 6), ("linear_relu", 6, 4)], "lam": 1.0}]
+    assert erase.lib().erase_workspace_bytes(_ncfg(synth.custom("f32", 16, 8, bad)).ptr(), ctypes.byref(n)) \
+        == erase.ERR_SHAPE
+    chain = [{"input": "x", "layers": [("linear_relu", 8, 6)], "lam": 1.0},
+             {"input": "prev", "layers": [("linear_relu", 7, 4)], "lam": 1.0}]
+    assert erase.lib().erase_workspace_bytes(_ncfg(synth.custom("f32", 16, 8, chain)).ptr(), ctypes.byref(n)) \
+        == erase.ERR_SHAPE
+
+
+def test_init_rejects_bad_arguments_before_any_hip_call():
+    L = erase.lib()
+    cfg = synth.config("tiny")
+    nc = _ncfg(cfg)
+    ctx = ctypes.c_void_p()
+    bufs = (erase.BlockBuffers * 2)()
+    # null buffers
+    assert L.erase_init(nc.ptr(), bufs, ctypes.c_void_p(256), 1 << 20, ctypes.c_void_p(8), ctypes.c_void_p(16),
+                        ctypes.byref(ctx)) == erase.ERR_INVALID_ARG
+    for b in range(2):
+        bufs[b] = erase.BlockBuffers(256, 512, 768, None)
+    # same stream twice
+    assert L.erase_init(nc.ptr(), bufs, ctypes.c_void_p(256), 1 << 20, ctypes.c_void_p(8), ctypes.c_void_p(8),
+                        ctypes.byref(ctx)) == erase.ERR_INVALID_ARG
+    # misaligned / null / small workspace
+    assert L.erase_init(nc.ptr(), bufs, ctypes.c_void_p(100), 1 << 20, ctypes.c_void_p(8), ctypes.c_void_p(16),
+                        ctypes.byref(ctx)) == erase.ERR_WORKSPACE
+    assert L.erase_init(nc.ptr(), bufs, None, 1 << 20, ctypes.c_void_p(8), ctypes.c_void_p(16),
+                        ctypes.byref(ctx)) == erase.ERR_WORKSPACE
+    assert L.erase_init(nc.ptr(), bufs, ctypes.c_void_p(256), 16, ctypes.c_void_p(8), ctypes.c_void_p(16),
+                        ctypes.byref(ctx)) == erase.ERR_WORKSPACE
+    assert ctx.value is None
+    # step/sync on a NULL context
+    assert L.erase_step(None, None, None, 0, None) == erase.ERR_INVALID_ARG
+    assert L.erase_sync(None) == erase.ERR_INVALID_ARG
+    assert L.erase_destroy(None) == erase.OK
+
+
+def test_gemm_flop_count_of_ctr_mlp():
+    # 26.51 MFLOP per sample: forward and weight gradient of every layer, input
+    # gradient of every layer but the first of each block
+    f = synth.gemm_flops_per_step(synth.config("ctr_mlp"))
+    assert abs(f / 4096 / 1e6 - 26.51) < 0.01

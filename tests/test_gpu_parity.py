@@ -1,0 +1,198 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Tolerances: fp32 workloads 1e-4 relative against the float64 oracle
+(norm-wise per tensor, plain relative on each loss).  bf16 workloads 2e-2
+relative against the oracle that rounds to bf16 the tensors the GPU stores in
+bf16, and against the float64 oracle within 2e-2 on losses and parameters and
+within what bf16 arithmetic itself attains on gradients and moments (see
+tests/gpu_util.check_bf16).  All schedules (serial, overlapped, and both
+captured as HIP graphs) must agree bit for bit.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from paper_2608_18469_amd import erase, synth
+from tests.gpu_util import assert_bit_identical, check_bf16, compare, run_gpu, run_oracle
+
+pytestmark = pytest.mark.gpu
+
+SCHEDS = ["serial", "overlap", "serial_graph", "overlap_graph"]
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _mixed_fp32(batch=150):
+    blocks = [
+        {"input": "x", "layers": [("cross", 100, 100), ("cross", 100, 100), ("linear_relu", 100, 70),
+                                  ("linear_relu", 70, 50)], "lam": 1.0},
+        {"input": "prev", "layers": [("linear_relu", 50, 90), ("linear_relu", 90, 33)], "lam": 0.5},
+        {"input": "x", "layers": [("linear_relu", 100, 130)], "lam": 2.0},
+    ]
+    return synth.custom("f32", batch, 100, blocks, label_p=0.3)
+
+
+def test_tiny_fp32_three_steps_vs_oracle():
+    _say("case: tiny fp32 3 steps")
+    cfg = synth.config("tiny")
+    params, batches = synth.make_workload(cfg, 0, 3)
+    _, g = run_gpu(cfg, params, batches, "overlap")
+    r = run_oracle(cfg, params, batches)
+    compare(cfg, g, r, 1e-4)
+
+
+def test_tiny_chain_fp32_vs_oracle():
+    _say("case: tiny_chain fp32 3 steps")
+    cfg = synth.config("tiny_chain")
+    params, batches = synth.make_workload(cfg, 1, 3)
+    _, g = run_gpu(cfg, params, batches, "overlap")
+    r = run_oracle(cfg, params, batches)
+    compare(cfg, g, r, 1e-4)
+
+
+@pytest.mark.parametrize("batch", [150, 1, 64, 257])
+def test_cross_chain_mixed_fp32_vs_oracle(batch):
+    """Cross layers, a chained block and ragged shapes spanning several 64x64
+    tiles, fp32."""
+    _say(f"case: mixed fp32 batch={batch}")
+    cfg = _mixed_fp32(batch)
+    params, batches = synth.make_workload(cfg, 2, 2)
+    _, g = run_gpu(cfg, params, batches, "overlap")
+    r = run_oracle(cfg, params, batches)
+    compare(cfg, g, r, 1e-4)
+
+
+def test_odd_small_dims_fp32():
+    _say("case: odd small dims fp32")
+    blocks = [{"input": "x", "layers": [("linear_relu", 3, 1)], "lam": 1.0},
+              {"input": "prev", "layers": [("linear_relu", 1, 5), ("linear_relu", 5, 2)], "lam": 1.0}]
+    cfg = synth.custom("f32", 7, 3, blocks, label_p=0.5)
+    params, batches = synth.make_workload(cfg, 4, 2)
+    _, g = run_gpu(cfg, params, batches)
+    r = run_oracle(cfg, params, batches)
+    compare(cfg, g, r, 1e-4)
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny_chain"])
+def test_schedules_bit_identical_fp32(name):
+    _say(f"case: schedules bit-identical {name}")
+    cfg = synth.config(name)
+    params, batches = synth.make_workload(cfg, 0, 3)
+    runs = [run_gpu(cfg, params, batches, s)[1] for s in SCHEDS]
+    for other in runs[1:]:
+        assert_bit_identical(runs[0], other)
+
+
+def _ctr_small(batch=1000, blocks=2):
+    cfg = synth.config("ctr_mlp", batch=batch, ctr_rows=5000)
+    cfg["blocks"] = cfg["blocks"][:blocks]
+    return cfg
+
+
+def test_ctr_mlp_bf16_small_vs_oracle():
+    """Full CTR widths (1677->512->256->128), ragged batch 1000, 2 blocks."""
+    _say("case: ctr_mlp bf16 batch=1000")
+    cfg = _ctr_small()
+    params, batches = synth.make_workload(cfg, 0, 2)
+    _, g = run_gpu(cfg, params, batches, "overlap")
+    _say("  ", check_bf16(cfg, g, params, batches))
+
+
+def test_ctr_mlp_bf16_schedules_bit_identical():
+    _say("case: ctr_mlp bf16 schedules bit-identical")
+    cfg = _ctr_small(batch=777, blocks=3)
+    params, batches = synth.make_workload(cfg, 3, 2)
+    runs = [run_gpu(cfg, params, batches, s)[1] for s in SCHEDS]
+    for other in runs[1:]:
+        assert_bit_identical(runs[0], other)
+
+
+def test_ctr_mlp_full_size_vs_oracle():
+    """The benchmarked workload itself: 6 blocks, batch 4096, bf16, 2 steps,
+    in the overlapped-graph schedule the benchmark times."""
+    _say("case: ctr_mlp full size, overlap_graph")
+    cfg = synth.config("ctr_mlp")
+    params, batches = synth.make_workload(cfg, 0, 2)
+    _, g = run_gpu(cfg, params, batches, "overlap_graph")
+    _say("  ", check_bf16(cfg, g, params, batches))
+
+
+def test_deep_chain_full_size_vs_oracle():
+    _say("case: deep_chain full size")
+    cfg = synth.config("deep_chain")
+    params, batches = synth.make_workload(cfg, 0, 2)
+    _, g = run_gpu(cfg, params, batches, "overlap")
+    _say("  ", check_bf16(cfg, g, params, batches))
+
+
+def test_dcn_bf16_small_vs_oracle():
+    _say("case: dcn bf16 small")
+    blocks = [{"input": "x", "layers": [("cross", 200, 200), ("cross", 200, 200), ("linear_relu", 200, 128),
+                                        ("linear_relu", 128, 64)], "lam": 1.0} for _ in range(2)]
+    cfg = synth.custom("bf16", 300, 200, blocks, label_p=0.1)
+    params, batches = synth.make_workload(cfg, 5, 2)
+    _, g = run_gpu(cfg, params, batches, "overlap")
+    _say("  ", check_bf16(cfg, g, params, batches))
+
+
+def test_nonfinite_input_is_reported():
+    _say("case: non-finite input")
+    cfg = synth.config("tiny")
+    params, batches = synth.make_workload(cfg, 0, 1)
+    x, y = batches[0]
+    x = x.copy()
+    x[3, 5] = np.nan
+    tr = erase.Trainer(cfg, params)
+    xd, yd = tr.device_batch(x, y)
+    tr.step(xd, yd, "overlap")
+    with pytest.raises(erase.EraseError) as ei:
+        tr.sync()
+    assert ei.value.status == erase.ERR_NONFINITE
+    with pytest.raises(erase.EraseError) as ei:  # sticky
+        tr.step(xd, yd, "overlap")
+    assert ei.value.status == erase.ERR_STATE
+
+
+def test_checkpoint_resume_bit_identical():
+    _say("case: checkpoint/resume")
+    cfg = _mixed_fp32(96)
+    params, batches = synth.make_workload(cfg, 6, 4)
+    _, full = run_gpu(cfg, params, batches, "overlap")
+    tr, first = run_gpu(cfg, params, batches[:2], "overlap")
+    p, m, v, _g = tr.state()
+    t = tr.get_step()
+    assert t == 2
+    tr.close()
+    tr2 = erase.Trainer(cfg, p, m=m, v=v, step=t)
+    _, rest = run_gpu(cfg, p, batches[2:], "overlap", trainer=tr2)
+    assert_bit_identical(full, first + rest)
+
+
+def test_repeatable_across_contexts():
+    _say("case: repeatability")
+    cfg = _ctr_small(batch=512, blocks=2)
+    params, batches = synth.make_workload(cfg, 9, 2)
+    a = run_gpu(cfg, params, batches, "overlap_graph")[1]
+    b = run_gpu(cfg, params, batches, "overlap_graph")[1]
+    assert_bit_identical(a, b)
+
+
+def test_kernel_timing_records():
+    _say("case: kernel timing")
+    cfg = _ctr_small(batch=512, blocks=2)
+    params, batches = synth.make_workload(cfg, 9, 1)
+    tr = erase.Trainer(cfg, params)
+    xd, yd = tr.device_batch(*batches[0])
+    tr.set_timing(True)
+    tr.step(xd, yd, "overlap")
+    tr.sync()
+    recs = tr.read_timing()
+    # prologue + per block: 3 fwd, head, 3 wgrad, 2 dgrad, adam
+    assert len(recs) == 1 + 2 * 10
+    assert all(r["end_ms"] >= r["start_ms"] >= 0 for r in recs)
+    assert {r["stream"] for r in recs if r["kind"] in ("wgrad_gemm", "adam")} == {1}
+    with pytest.raises(erase.EraseError):
+        tr.step(xd, yd, "overlap_graph")
