@@ -87,6 +87,7 @@ erase_status validate(const erase_config* c, std::string* err) {
     }
     if (B.layers[B.n_layers - 1].kind != ERASE_LAYER_LINEAR_RELU)
       return fail(ERASE_ERR_UNSUPPORTED, "the last layer of a block must be LINEAR_RELU");
+    if (cur > HEAD_MAX_N) return fail(ERASE_ERR_UNSUPPORTED, "the head input width must be <= 2048");
     prev_out = cur;
   }
   return ERASE_OK;
@@ -132,9 +133,11 @@ struct BlockRT {
 
 struct Plan {
   int bf16 = 1, esz = 2, M = 0;
-  int64_t ldm = 0;
+  int64_t ldm = 0;  // feature-major leading dimension: roundup(M, 64)
+  int64_t Mr = 0;   // allocated rows of row-major arrays: roundup(M, 128)
   int64_t* t = nullptr;
   int* status = nullptr;
+  void* xp = nullptr; int64_t ldxp = 0;  // zero-padded copy of x
   void* xt = nullptr; int64_t ldxt = 0;
   std::vector<BlockRT> blk;
   size_t bytes = 0;
@@ -200,14 +203,18 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
   const int esz = P->esz;
   const int64_t M = c.batch;
   P->ldm = roundup(M, 64);
+  P->Mr = roundup(M, 128);
+  const int64_t Mr = P->Mr;
   Carver cv{base};
   P->t = reinterpret_cast<int64_t*>(base);
   P->status = reinterpret_cast<int*>(base + 8);
   bool any_x = false;
   for (int b = 0; b < c.n_blocks; ++b) any_x |= c.blocks[b].input_src == ERASE_IN_X;
   if (any_x) {
+    P->ldxp = roundup(c.in_dim, 64);
+    P->xp = cv.take(size_t(Mr) * P->ldxp * esz);
     P->ldxt = P->ldm;
-    P->xt = cv.take(size_t(c.in_dim) * P->ldxt * esz);
+    P->xt = cv.take(size_t(roundup(c.in_dim, 128)) * P->ldxt * esz);
   }
   P->blk.assign(c.n_blocks, BlockRT{});
   for (int b = 0; b < c.n_blocks; ++b) {
@@ -227,33 +234,37 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
       off += int64_t(R.K) * R.N;
       R.offb = off;
       off += R.N;
+      // Every GEMM operand is zero-padded: rows to a multiple of 128 (the
+      // largest tile), leading dimensions to a multiple of 64 (the k-step).
       const int64_t ldK = roundup(R.K, 64), ldN = roundup(R.N, 64);
+      const int64_t Kr = roundup(R.K, 128), Nr = roundup(R.N, 128);
       R.ldwsh = ldK;
-      R.wsh = cv.take(size_t(R.N) * ldK * esz);
+      R.wsh = cv.take(size_t(Nr) * ldK * esz);
       if (l >= 1) {
         R.ldwsht = ldN;
-        R.wsht = cv.take(size_t(R.K) * ldN * esz);
+        R.wsht = cv.take(size_t(Kr) * ldN * esz);
       }
       R.ldy = ldN;
-      R.y = cv.take(size_t(M) * ldN * esz);
+      R.y = cv.take(size_t(Mr) * ldN * esz);
       if (l + 1 < B.L || next_chained) {
         R.ldyt = P->ldm;
-        R.yt = cv.take(size_t(R.N) * P->ldm * esz);
+        R.yt = cv.take(size_t(Nr) * P->ldm * esz);
       }
       R.lddnm = P->ldm;
-      R.dnm = cv.take(size_t(R.N) * P->ldm * esz);
+      R.dnm = cv.take(size_t(Nr) * P->ldm * esz);
       if (l >= 1) {
         R.lddmn = ldN;
-        R.dmn = cv.take(size_t(M) * ldN * esz);
+        R.dmn = cv.take(size_t(Mr) * ldN * esz);
       }
       if (R.kind == ERASE_LAYER_CROSS && l >= 1) {
         R.ldg = ldN;
-        R.g = cv.take(size_t(M) * ldN * esz);
+        R.g = cv.take(size_t(Mr) * ldN * esz);
       }
-      // launch shapes
-      R.fwd = choose_gemm(P->bf16, M, R.N, R.K, false);
-      R.wgrad = choose_gemm(P->bf16, R.N, R.K, M, true);
-      if (l >= 1) R.dgrad = choose_gemm(P->bf16, M, R.K, R.N, false);
+      // launch shapes (contraction lengths padded to the k-step)
+      const int BK = P->bf16 ? 64 : 32;
+      R.fwd = choose_gemm(P->bf16, M, R.N, roundup(R.K, BK), false);
+      R.wgrad = choose_gemm(P->bf16, R.N, R.K, roundup(M, BK), true);
+      if (l >= 1) R.dgrad = choose_gemm(P->bf16, M, R.K, roundup(R.N, BK), false);
       R.ldp = ldK;
       R.pstride = int64_t(R.N) * ldK;
       R.part = static_cast<float*>(cv.take(size_t(R.wgrad.split) * R.pstride * 4));
@@ -265,7 +276,7 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
     B.off_c = off;
     off += 1;
     B.nparam = off;
-    B.nhead = (int)cdiv(M, HEAD_ROWS);
+    B.nhead = (int)cdiv(M, head_rows(NL, esz));
     B.pdw = static_cast<float*>(cv.take(size_t(B.nhead) * NL * 4));
     B.pdc = static_cast<float*>(cv.take(size_t(B.nhead) * 4));
     B.ploss = static_cast<float*>(cv.take(size_t(B.nhead) * 4));
@@ -444,8 +455,9 @@ void layer_input(const Ctx* c, int b, int l, const void* x, const void** mn, int
     *nm = B.layer[l - 1].yt;
     *ldnm = B.layer[l - 1].ldyt;
   } else if (B.input_src == ERASE_IN_X) {
-    *mn = x;
-    *ldmn = c->cfg.x_ld;
+    (void)x;
+    *mn = P.xp;
+    *ldmn = P.ldxp;
     *nm = P.xt;
     *ldnm = P.ldxt;
   } else {
@@ -479,7 +491,7 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
     g.ldb = R.ldwsh;
     g.M = M;
     g.N = R.N;
-    g.K = R.K;
+    g.K = (int)roundup(R.K, P.bf16 ? 64 : 32);
     g.kps = R.fwd.kps;
     g.split = 1;
     g.bm = R.fwd.bm;
@@ -555,7 +567,7 @@ erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStre
       g.ldb = ldinnm;
       g.M = R.N;
       g.N = R.K;
-      g.K = M;
+      g.K = (int)roundup(M, P.bf16 ? 64 : 32);
       g.kps = R.wgrad.kps;
       g.split = R.wgrad.split;
       g.bm = R.wgrad.bm;
@@ -580,7 +592,7 @@ erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStre
       g.ldb = R.ldwsht;
       g.M = M;
       g.N = R.K;
-      g.K = R.N;
+      g.K = (int)roundup(R.N, P.bf16 ? 64 : 32);
       g.kps = R.dgrad.kps;
       g.split = 1;
       g.bm = R.dgrad.bm;
@@ -622,6 +634,7 @@ erase_status enqueue_adam(Ctx* c, Enqueuer& q, int b, float* losses, hipStream_t
   AdamArgs a{};
   a.seg = B.segs_dev;
   a.nseg = (int)B.segs.size();
+  for (int i = 0; i < a.nseg; ++i) a.chunk0[i] = B.segs[i].chunk0;
   a.nchunks = B.nchunks;
   a.t = P.t;
   a.lr = c->cfg.lr;
@@ -657,12 +670,14 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
     pa.t = P.t;
     pa.x = x;
     pa.ldx = c->cfg.x_ld;
+    pa.xp = P.xp;
+    pa.ldxp = P.ldxp;
     pa.xt = P.xt;
     pa.ldxt = P.ldxt;
     pa.M = P.M;
     pa.K = c->cfg.in_dim;
     Cost cost;
-    cost.bytes = P.xt ? 2.0 * P.esz * double(P.M) * c->cfg.in_dim : 0.0;
+    cost.bytes = P.xt ? 3.0 * P.esz * double(P.M) * c->cfg.in_dim : 0.0;
     const int bf = P.bf16;
     RUN(0, -1, -1, 0, sf, cost, [&]() { return launch_prologue(bf, pa, sf); });
   }
@@ -707,6 +722,7 @@ erase_status refresh(Ctx* c) {
     AdamArgs a{};
     a.seg = B.segs_dev;
     a.nseg = (int)B.segs.size();
+    for (int i = 0; i < a.nseg; ++i) a.chunk0[i] = B.segs[i].chunk0;
     a.nchunks = B.nchunks;
     HIPCHK(c, launch_refresh(c->P.bf16, a, c->sf));
   }
@@ -803,8 +819,10 @@ erase_status erase_init(const erase_config* cfg, const erase_block_buffers* bufs
     if (hipEventCreateWithFlags(&e2, hipEventDisableTiming) != hipSuccess) return bail(ERASE_ERR_HIP);
     c->eb.push_back(e2);
   }
-  // counters, segment tables, then the GEMM copies of the weights
-  if (hipMemsetAsync(c->ws, 0, kAlign, c->sf) != hipSuccess) return bail(ERASE_ERR_HIP);
+  // zero the workspace once (counters, and the padding every GEMM operand
+  // relies on: nothing writes outside the logical extents afterwards), then
+  // the segment tables and the GEMM copies of the weights
+  if (hipMemsetAsync(c->ws, 0, c->P.bytes, c->sf) != hipSuccess) return bail(ERASE_ERR_HIP);
   for (BlockRT& B : c->P.blk) {
     if (hipMemcpyAsync(B.segs_dev, B.segs.data(), sizeof(AdamSeg) * B.segs.size(), hipMemcpyHostToDevice, c->sf) !=
         hipSuccess)

@@ -11,6 +11,12 @@ namespace erase {
 // with the contraction index contiguous), fp32 accumulation.  The
 // contraction range is split into `split` slices of `kps` elements; slice z
 // is handled by blockIdx.z.
+//
+// Operand contract (no loads are masked): K is the padded contraction length,
+// a multiple of the k-step (64 bf16 / 32 fp32 elements); A holds at least
+// roundup(M, 128) rows and B roundup(N, 128) rows of at least K elements, and
+// every element outside the logical [M or N][K_logical] block is zero.  M and
+// N are the logical output extents the epilogue stores.
 struct GemmDesc {
   const void* A;
   int64_t lda;
@@ -46,10 +52,12 @@ struct EpiParams {
 
 hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s);
 
-// Step prologue: t += 1, and the feature-major copy xt[k][m] = x[m][k].
+// Step prologue: t += 1, the zero-padded copy xp[m][k] = x[m][k] and the
+// feature-major copy xt[k][m] = x[m][k] (padding of both stays zero).
 struct PrologueArgs {
   int64_t* t;
   const void* x; int64_t ldx;
+  void* xp; int64_t ldxp;
   void* xt; int64_t ldxt;
   int M, K;
 };
@@ -69,7 +77,19 @@ struct HeadArgs {
   float* pdc;                    // [nblk]
   float* ploss;                  // [nblk]
 };
-constexpr int HEAD_ROWS = 64;
+// Rows of z per head workgroup: the [rows][N] tile is staged in LDS (at most
+// 64 KiB), 32 rows when it fits, never fewer than one 16-byte column item.
+constexpr int HEAD_MAX_N = 2048;
+__host__ __device__ inline int head_pitch(int N, int esz) {  // elements per LDS row: 16-byte multiple plus one chunk
+  const int kch = 16 / esz;
+  return (N + kch - 1) / kch * kch + kch;
+}
+__host__ __device__ inline int head_rows(int N, int esz) {
+  int r = 32;
+  while (r > 16 / esz && r * head_pitch(N, esz) * esz > 65536) r /= 2;
+  return r;
+}
+inline size_t head_lds_bytes(int N, int esz) { return (size_t)head_rows(N, esz) * head_pitch(N, esz) * esz; }
 hipError_t launch_head(int bf16, const HeadArgs& a, hipStream_t s);
 
 // Fused split-reduction + Adam + GEMM-copy refresh for one block.  The
@@ -83,8 +103,10 @@ struct AdamSeg {
   void* sht; int64_t ldsht;                 // transposed GEMM copy [cols][ldsht], nullable
   int64_t chunk0;                           // first chunk index of this segment
 };
+constexpr int ADAM_MAX_SEG = 34;  // 16 layers x (W, b) + head (w, c)
 struct AdamArgs {
   const AdamSeg* seg;  // device [nseg]
+  int64_t chunk0[ADAM_MAX_SEG];  // first chunk of each segment (kernel-argument copy)
   int nseg;
   int64_t nchunks;
   const int64_t* t;

@@ -24,12 +24,15 @@
 // schedule of the same step produces bit-identical results.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "internal.h"
 
 namespace erase {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));  // 16-byte chunk in registers
 
 // ---------------------------------------------------------------------------
 // element conversions (bf16 is carried as uint16_t)
@@ -81,28 +84,8 @@ template <> struct GT<uint16_t> { static constexpr int KCH = 8, BK = 64, KMF = 3
 // fp32: 16-byte chunk = 4 elements, k-step 32, v_mfma_f32_16x16x4_f32
 template <> struct GT<float> { static constexpr int KCH = 4, BK = 32, KMF = 4; };
 
-// One 16-byte chunk of row `row`, contraction elements [k, k+KCH), zero
-// outside rows < nrows and k < kend.  Only in-range elements are read.
-template <typename T>
-__device__ __forceinline__ uint4 load_chunk(const T* P, int64_t ld, int row, int nrows, int k, int kend) {
-  constexpr int KCH = GT<T>::KCH;
-  uint4 v = make_uint4(0u, 0u, 0u, 0u);
-  if (row < nrows && k < kend) {
-    const T* p = P + (int64_t)row * ld + k;
-    if (k + KCH <= kend) {
-      v = *reinterpret_cast<const uint4*>(p);
-    } else {
-      T tmp[KCH];
-#pragma unroll
-      for (int e = 0; e < KCH; ++e) tmp[e] = (k + e < kend) ? p[e] : T(0);
-      __builtin_memcpy(&v, tmp, 16);
-    }
-  }
-  return v;
-}
-
-__device__ __forceinline__ float sum8_bf16(const uint4& a) {
-  const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+__device__ __forceinline__ float sum8_bf16(const u32x4_t& a) {
+  const uint32_t w[4] = {a[0], a[1], a[2], a[3]};
   float s = 0.f;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -112,80 +95,38 @@ __device__ __forceinline__ float sum8_bf16(const uint4& a) {
   return s;
 }
 
+// Value of the fused epilogue at (m, n), m < M and n < N, in the output type.
 template <typename T, int KIND>
-__device__ __forceinline__ void epilogue4(const GemmDesc& g, const EpiParams& e, int mb, int n, const f32x4_t& acc,
-                                          int z) {
-  const int M = g.M;
-  if constexpr (KIND == GK_FWD_RELU || KIND == GK_FWD_CROSS) {
-    const float bn = e.bias[n];
-    T* Y = static_cast<T*>(e.y);
-    T o[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int m = mb + q;
-      float v = acc[q] + bn;
-      if constexpr (KIND == GK_FWD_RELU) {
-        v = v < 0.f ? 0.f : v;  // keeps NaN, like max(h, 0) on the host
-      } else {
-        if (m < M) {
-          const float x0 = ldf(static_cast<const T*>(e.x0) + (int64_t)m * e.ldx0 + n);
-          const float xl = ldf(static_cast<const T*>(e.xl) + (int64_t)m * e.ldxl + n);
-          v = fmaf(x0, v, xl);
-        }
-      }
-      o[q] = cvt<T>(v);
-      if (m < M) Y[(int64_t)m * e.ldy + n] = o[q];
-    }
-    if (e.yt) {
-      T* Yt = static_cast<T*>(e.yt) + (int64_t)n * e.ldyt;
-      if (mb + 3 < M) {
-        st4(Yt + mb, o);
-      } else {
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (mb + q < M) Yt[mb + q] = o[q];
-      }
-    }
-  } else if constexpr (KIND == GK_WGRAD) {
-    float* P = e.part + (int64_t)z * e.pstride;
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (mb + q < M) P[(int64_t)(mb + q) * e.ldp + n] = acc[q];
+__device__ __forceinline__ T epi_value(const EpiParams& e, int m, int n, float acc, float bn) {
+  if constexpr (KIND == GK_FWD_RELU) {
+    const float v = acc + bn;
+    return cvt<T>(v < 0.f ? 0.f : v);  // keeps NaN, like max(h, 0) on the host
+  } else if constexpr (KIND == GK_FWD_CROSS) {
+    const float x0 = ldf(static_cast<const T*>(e.x0) + (int64_t)m * e.ldx0 + n);
+    const float xl = ldf(static_cast<const T*>(e.xl) + (int64_t)m * e.ldxl + n);
+    return cvt<T>(fmaf(x0, acc + bn, xl));
   } else {  // GK_DGRAD
-    T d[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int m = mb + q;
-      d[q] = T(0);
-      if (m >= M) continue;
-      float v = acc[q];
-      if (e.res) v += ldf(static_cast<const T*>(e.res) + (int64_t)m * e.ldres + n);
-      if (!e.below_cross) {
-        const float mk = ldf(static_cast<const T*>(e.mask) + (int64_t)m * e.ldmask + n);
-        d[q] = cvt<T>(mk > 0.f ? v : 0.f);
-      } else {
-        const T gq = cvt<T>(v);
-        if (e.gout) static_cast<T*>(e.gout)[(int64_t)m * e.ldgout + n] = gq;
-        const float x0 = ldf(static_cast<const T*>(e.x0) + (int64_t)m * e.ldx0 + n);
-        d[q] = cvt<T>(asf(gq) * x0);
-      }
-      if (e.dmn) static_cast<T*>(e.dmn)[(int64_t)m * e.lddmn + n] = d[q];
+    float v = acc;
+    if (e.res) v += ldf(static_cast<const T*>(e.res) + (int64_t)m * e.ldres + n);
+    if (!e.below_cross) {
+      const float mk = ldf(static_cast<const T*>(e.mask) + (int64_t)m * e.ldmask + n);
+      return cvt<T>(mk > 0.f ? v : 0.f);
     }
-    T* Dt = static_cast<T*>(e.dnm) + (int64_t)n * e.lddnm;
-    if (mb + 3 < M) {
-      st4(Dt + mb, d);
-    } else {
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (mb + q < M) Dt[mb + q] = d[q];
-    }
+    const T gq = cvt<T>(v);
+    if (e.gout) static_cast<T*>(e.gout)[(int64_t)m * e.ldgout + n] = gq;
+    const float x0 = ldf(static_cast<const T*>(e.x0) + (int64_t)m * e.ldx0 + n);
+    return cvt<T>(asf(gq) * x0);
   }
 }
 
 // Workgroup of 256 threads = 4 waves in a 2x2 arrangement; each wave owns a
-// (BM/2) x (BN/2) sub-tile built from 16x16 MFMA tiles.  One LDS buffer per
-// operand with register prefetch of the next k-step; LDS rows are padded by
-// 16 bytes so the 16 rows read by one MFMA fragment hit distinct banks.
+// (BM/2) x (BN/2) sub-tile of 16x16 MFMA tiles.  Pipeline: two LDS stages
+// and two register sets, so the global loads of k-step it+3 are issued while
+// k-step it is computed and land two compute phases later; one barrier per
+// k-step.  Interior tiles take an unpredicated load path.  LDS rows are padded
+// by 16 bytes so the 16 rows read by one MFMA fragment hit distinct banks.
+// The epilogue stages the output tile in LDS and writes it with 16-byte
+// stores, row-major and (forward / input gradient) feature-major.
 template <typename T, int BM, int BN, int KIND>
 __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e) {
   constexpr int BK = GT<T>::BK, KCH = GT<T>::KCH, KMF = GT<T>::KMF;
@@ -194,8 +135,15 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e)
   constexpr int CPR = BK / KCH;
   constexpr int CA = BM * CPR / 256, CB = BN * CPR / 256;
   static_assert(CA * 256 == BM * CPR && CB * 256 == BN * CPR, "tile does not match 256 threads");
-  __shared__ __attribute__((aligned(16))) T sA[BM * PITCH];
-  __shared__ __attribute__((aligned(16))) T sB[BN * PITCH];
+  constexpr int STAGE = (BM + BN) * PITCH;
+  using OT = typename std::conditional<KIND == GK_WGRAD, float, T>::type;
+  constexpr int OCH = 16 / (int)sizeof(OT);
+  constexpr int OPITCH = BN + OCH;
+  constexpr int MAIN_BYTES = 2 * STAGE * (int)sizeof(T);
+  constexpr int EPI_BYTES = BM * OPITCH * (int)sizeof(OT);
+  constexpr int SMEM = MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES;
+  __shared__ __attribute__((aligned(16))) char smem[SMEM];
+  T* lds = reinterpret_cast<T*>(smem);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -217,103 +165,185 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e)
 #pragma unroll
   for (int i = 0; i < TM; ++i) rs[i] = 0.f;
 
-  uint4 ra[CA], rb[CB];
+  u32x4_t ra0[CA], rb0[CB], ra1[CA], rb1[CB];
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  // k-step j covers [kbeg + j*BK, kbeg + (j+1)*BK); loads past the last
+  // k-step are clamped onto it (in bounds, never computed)
+  const int klast = kbeg + (nk > 0 ? nk - 1 : 0) * BK;
+  // per-thread chunk coordinates (row offset, k offset) of the tile loads
+  const T* pa = A + (int64_t)(m0 + tid / CPR) * g.lda + (tid % CPR) * KCH;
+  const T* pb = B + (int64_t)(n0 + tid / CPR) * g.ldb + (tid % CPR) * KCH;
+  constexpr int RSTEP = 256 / CPR;  // tile rows between a thread's chunks
+  const int sofs = (tid / CPR) * PITCH + (tid % CPR) * KCH;
 
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < CA; ++i) {
-      const int c = tid + i * 256;
-      ra[i] = load_chunk<T>(A, g.lda, m0 + c / CPR, g.M, k0 + (c % CPR) * KCH, kend);
-    }
-#pragma unroll
-    for (int i = 0; i < CB; ++i) {
-      const int c = tid + i * 256;
-      rb[i] = load_chunk<T>(B, g.ldb, n0 + c / CPR, g.N, k0 + (c % CPR) * KCH, kend);
-    }
-  };
-  auto sstore = [&]() {
-#pragma unroll
-    for (int i = 0; i < CA; ++i) {
-      const int c = tid + i * 256;
-      *reinterpret_cast<uint4*>(&sA[(c / CPR) * PITCH + (c % CPR) * KCH]) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < CB; ++i) {
-      const int c = tid + i * 256;
-      *reinterpret_cast<uint4*>(&sB[(c / CPR) * PITCH + (c % CPR) * KCH]) = rb[i];
-    }
-  };
-  auto compute = [&]() {
-#pragma unroll
-    for (int ks = 0; ks < BK; ks += KMF) {
-      if constexpr (sizeof(T) == 2) {
-        uint4 fa[TM], fb[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          fa[i] = *reinterpret_cast<const uint4*>(&sA[(wm * WM + i * 16 + (lane & 15)) * PITCH + ks + (lane >> 4) * 8]);
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          fb[j] = *reinterpret_cast<const uint4*>(&sB[(wn * WN + j * 16 + (lane & 15)) * PITCH + ks + (lane >> 4) * 8]);
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, fa[i]),
-                                                                __builtin_bit_cast(bf16x8_t, fb[j]), acc[i][j], 0, 0, 0);
-        if (do_rows) {
-#pragma unroll
-          for (int i = 0; i < TM; ++i) rs[i] += sum8_bf16(fa[i]);
-        }
-      } else {
-        float fa[TM], fb[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i) fa[i] = sA[(wm * WM + i * 16 + (lane & 15)) * PITCH + ks + (lane >> 4)];
-#pragma unroll
-        for (int j = 0; j < TN; ++j) fb[j] = sB[(wn * WN + j * 16 + (lane & 15)) * PITCH + ks + (lane >> 4)];
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i], fb[j], acc[i][j], 0, 0, 0);
-        if (do_rows) {
-#pragma unroll
-          for (int i = 0; i < TM; ++i) rs[i] += fa[i];
-        }
-      }
-    }
-  };
+  // Statically indexed register sets; macros keep them out of memory.
+  // Every operand is zero-padded (see GemmDesc): loads are never masked.
+#define ERASE_GLOAD(RA, RB, KSTEP)                                                                    \
+  do {                                                                                                \
+    const int k0_ = min(kbeg + (KSTEP) * BK, klast);                                                  \
+    _Pragma("unroll") for (int i = 0; i < CA; ++i)                                                    \
+        RA[i] = *reinterpret_cast<const u32x4_t*>(pa + (int64_t)(i * RSTEP) * g.lda + k0_);             \
+    _Pragma("unroll") for (int i = 0; i < CB; ++i)                                                    \
+        RB[i] = *reinterpret_cast<const u32x4_t*>(pb + (int64_t)(i * RSTEP) * g.ldb + k0_);             \
+  } while (0)
+#define ERASE_SSTORE(RA, RB, ST)                                                                      \
+  do {                                                                                                \
+    T* sa_ = lds + (ST) * STAGE;                                                                      \
+    _Pragma("unroll") for (int i = 0; i < CA; ++i)                                                    \
+        *reinterpret_cast<u32x4_t*>(sa_ + sofs + i * RSTEP * PITCH) = RA[i];                            \
+    _Pragma("unroll") for (int i = 0; i < CB; ++i)                                                    \
+        *reinterpret_cast<u32x4_t*>(sa_ + BM * PITCH + sofs + i * RSTEP * PITCH) = RB[i];               \
+  } while (0)
 
+  const int frow = (lane & 15) * PITCH + (lane >> 4) * (KMF / 4);  // fragment offset within a 16-row slab
+#define ERASE_COMPUTE(ST)                                                                             \
+  do {                                                                                                \
+    const T* sa_ = lds + (ST) * STAGE + wm * WM * PITCH + frow;                                       \
+    const T* sb_ = lds + (ST) * STAGE + BM * PITCH + wn * WN * PITCH + frow;                          \
+    _Pragma("unroll") for (int ks = 0; ks < BK; ks += KMF) {                                          \
+      if constexpr (sizeof(T) == 2) {                                                                 \
+        u32x4_t fa[TM], fb[TN];                                                                         \
+        _Pragma("unroll") for (int i = 0; i < TM; ++i)                                                \
+            fa[i] = *reinterpret_cast<const u32x4_t*>(sa_ + i * 16 * PITCH + ks);                       \
+        _Pragma("unroll") for (int j = 0; j < TN; ++j)                                                \
+            fb[j] = *reinterpret_cast<const u32x4_t*>(sb_ + j * 16 * PITCH + ks);                       \
+        _Pragma("unroll") for (int i = 0; i < TM; ++i)                                                \
+        _Pragma("unroll") for (int j = 0; j < TN; ++j)                                                \
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(                                      \
+                __builtin_bit_cast(bf16x8_t, fa[i]), __builtin_bit_cast(bf16x8_t, fb[j]), acc[i][j], 0, 0, 0); \
+        if (do_rows) {                                                                                \
+          _Pragma("unroll") for (int i = 0; i < TM; ++i) rs[i] += sum8_bf16(fa[i]);                   \
+        }                                                                                             \
+      } else {                                                                                        \
+        float fa[TM], fb[TN];                                                                         \
+        _Pragma("unroll") for (int i = 0; i < TM; ++i) fa[i] = asf(sa_[i * 16 * PITCH + ks]);         \
+        _Pragma("unroll") for (int j = 0; j < TN; ++j) fb[j] = asf(sb_[j * 16 * PITCH + ks]);         \
+        _Pragma("unroll") for (int i = 0; i < TM; ++i)                                                \
+        _Pragma("unroll") for (int j = 0; j < TN; ++j)                                                \
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i], fb[j], acc[i][j], 0, 0, 0);       \
+        if (do_rows) {                                                                                \
+          _Pragma("unroll") for (int i = 0; i < TM; ++i) rs[i] += fa[i];                              \
+        }                                                                                             \
+      }                                                                                               \
+    }                                                                                                 \
+  } while (0)
+
+  // stage 0 <- k-step 0; registers: set 1 <- k-step 1, set 0 <- k-step 2
   if (nk > 0) {
-    gload(kbeg);
-    sstore();
+    ERASE_GLOAD(ra0, rb0, 0);
+    ERASE_GLOAD(ra1, rb1, 1);
+    ERASE_SSTORE(ra0, rb0, 0);
+    ERASE_GLOAD(ra0, rb0, 2);
   }
   __syncthreads();
-  for (int it = 0; it < nk; ++it) {
-    const bool more = it + 1 < nk;
-    if (more) gload(kbeg + (it + 1) * BK);
-    compute();
+  int it = 0;
+  for (; it + 1 < nk; it += 2) {
+    // stage 0 holds k-step it, set 1 k-step it+1, set 0 k-step it+2
+    ERASE_COMPUTE(0);
+    ERASE_SSTORE(ra1, rb1, 1);
+    ERASE_GLOAD(ra1, rb1, it + 3);
     __syncthreads();
-    if (more) sstore();
+    // stage 1 holds k-step it+1, set 0 k-step it+2, set 1 k-step it+3
+    ERASE_COMPUTE(1);
+    ERASE_SSTORE(ra0, rb0, 0);
+    ERASE_GLOAD(ra0, rb0, it + 4);
     __syncthreads();
   }
+  if (it < nk) {  // odd count: the last k-step is in stage 0
+    ERASE_COMPUTE(0);
+    __syncthreads();  // the epilogue below reuses this LDS
+  }
+#undef ERASE_GLOAD
+#undef ERASE_SSTORE
+#undef ERASE_COMPUTE
 
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int mb = m0 + wm * WM + i * 16 + (lane >> 4) * 4;
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int n = n0 + wn * WN + j * 16 + (lane & 15);
-      if (n < g.N) epilogue4<T, KIND>(g, e, mb, n, acc[i][j], z);
-    }
-  }
   if (do_rows) {
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
-      float s = rs[i];
-      s += __shfl_xor(s, 16, 64);
-      s += __shfl_xor(s, 32, 64);
+      float sr = rs[i];
+      sr += __shfl_xor(sr, 16, 64);
+      sr += __shfl_xor(sr, 32, 64);
       const int m = m0 + wm * WM + i * 16 + lane;
-      if (lane < 16 && m < g.M) e.bpart[(int64_t)z * g.M + m] = s;
+      if (lane < 16 && m < g.M) e.bpart[(int64_t)z * g.M + m] = sr;
+    }
+  }
+
+  // epilogue: values -> LDS tile [BM][OPITCH] -> 16-byte stores
+  OT* sc = reinterpret_cast<OT*>(smem);
+  const int M = g.M, N = g.N;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int nl = wn * WN + j * 16 + (lane & 15);
+    const int n = n0 + nl;
+    float bn = 0.f;
+    if constexpr (KIND == GK_FWD_RELU || KIND == GK_FWD_CROSS) bn = (n < N) ? e.bias[n] : 0.f;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int ml = wm * WM + i * 16 + (lane >> 4) * 4 + q;
+        const int m = m0 + ml;
+        OT v;
+        if constexpr (KIND == GK_WGRAD) {
+          v = acc[i][j][q];
+        } else {
+          v = (m < M && n < N) ? epi_value<T, KIND>(e, m, n, acc[i][j][q], bn) : OT(0);
+        }
+        sc[ml * OPITCH + nl] = v;
+      }
+    }
+  }
+  __syncthreads();
+  OT* omn;
+  int64_t ldmn;
+  OT* onm = nullptr;
+  int64_t ldnm = 0;
+  if constexpr (KIND == GK_WGRAD) {
+    omn = e.part + (int64_t)z * e.pstride;
+    ldmn = e.ldp;
+  } else if constexpr (KIND == GK_DGRAD) {
+    omn = static_cast<OT*>(e.dmn);
+    ldmn = e.lddmn;
+    onm = static_cast<OT*>(e.dnm);
+    ldnm = e.lddnm;
+  } else {
+    omn = static_cast<OT*>(e.y);
+    ldmn = e.ldy;
+    onm = static_cast<OT*>(e.yt);
+    ldnm = e.ldyt;
+  }
+  if (omn) {
+    constexpr int CPRO = BN / OCH;
+    for (int c = tid; c < BM * CPRO; c += 256) {
+      const int ml = c / CPRO, nl = (c % CPRO) * OCH;
+      const int m = m0 + ml, n = n0 + nl;
+      if (m >= M || n >= N) continue;
+      const OT* src = &sc[ml * OPITCH + nl];
+      OT* dst = omn + (int64_t)m * ldmn + n;
+      if (n + OCH <= N) {
+        *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(src);
+      } else {
+        for (int q = 0; q < OCH && n + q < N; ++q) dst[q] = src[q];
+      }
+    }
+  }
+  if (onm) {
+    constexpr int IPC = BM / OCH;  // items of OCH rows per column
+    for (int c = tid; c < BN * IPC; c += 256) {
+      const int nl = c / IPC, ml = (c % IPC) * OCH;
+      const int n = n0 + nl, m = m0 + ml;
+      if (n >= N || m >= M) continue;
+      OT o[OCH];
+#pragma unroll
+      for (int q = 0; q < OCH; ++q) o[q] = sc[(ml + q) * OPITCH + nl];
+      OT* dst = onm + (int64_t)n * ldnm + m;
+      if (m + OCH <= M) {
+        uint4 v;
+        __builtin_memcpy(&v, o, 16);
+        *reinterpret_cast<uint4*>(dst) = v;
+      } else {
+        for (int q = 0; q < OCH && m + q < M; ++q) dst[q] = o[q];
+      }
     }
   }
 }
@@ -362,34 +392,60 @@ hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e
 }
 
 // ---------------------------------------------------------------------------
-// step prologue: t += 1 and xt[k][m] = x[m][k] through a 64x64 LDS tile
+// step prologue: t += 1, xp = x (zero-padded copy) and xt = x^T, through a
+// 64 x 64 LDS tile with 16-byte global loads and stores
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void erase_prologue(PrologueArgs a) {
-  __shared__ T tile[64][65];
+  constexpr int KCH = 16 / sizeof(T);
+  constexpr int TP = 64 + KCH;  // LDS pitch (elements)
+  __shared__ __attribute__((aligned(16))) T tile[64 * TP];
   if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) a.t[0] = a.t[0] + 1;
-  if (a.xt == nullptr) return;
+  if (a.xp == nullptr) return;
   const T* X = static_cast<const T*>(a.x);
-  T* XT = static_cast<T*>(a.xt);
   const int k0 = blockIdx.x * 64, m0 = blockIdx.y * 64;
-  const int c = threadIdx.x & 63, r4 = threadIdx.x >> 6;
+  constexpr int CPR = 64 / KCH;  // chunks per tile row
+  for (int c = threadIdx.x; c < 64 * CPR; c += 256) {
+    const int r = c / CPR, kc = (c % CPR) * KCH;
+    const int m = m0 + r, k = k0 + kc;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (m < a.M && k < a.K) {
+      // x rows hold at least roundup(K, KCH) elements (16-byte row pitch)
+      v = *reinterpret_cast<const uint4*>(X + (int64_t)m * a.ldx + k);
+      if (k + KCH > a.K) {
+        T e[KCH];
+        __builtin_memcpy(e, &v, 16);
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int r = r4 + 4 * i;
-    const int m = m0 + r, k = k0 + c;
-    tile[r][c] = (m < a.M && k < a.K) ? X[(int64_t)m * a.ldx + k] : T(0);
+        for (int q = 0; q < KCH; ++q)
+          if (k + q >= a.K) e[q] = T(0);
+        __builtin_memcpy(&v, e, 16);
+      }
+      *reinterpret_cast<uint4*>(static_cast<T*>(a.xp) + (int64_t)m * a.ldxp + k) = v;
+    }
+    *reinterpret_cast<uint4*>(&tile[r * TP + kc]) = v;
   }
   __syncthreads();
+  // xt rows k, KCH consecutive m per item
+  for (int c = threadIdx.x; c < 64 * CPR; c += 256) {
+    const int kr = c / CPR, mc = (c % CPR) * KCH;
+    const int k = k0 + kr, m = m0 + mc;
+    if (k >= a.K || m >= a.M) continue;
+    T o[KCH];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int r = r4 + 4 * i;  // k within tile
-    const int k = k0 + r, m = m0 + c;
-    if (k < a.K && m < a.M) XT[(int64_t)k * a.ldxt + m] = tile[c][r];
+    for (int q = 0; q < KCH; ++q) o[q] = tile[(mc + q) * TP + kr];
+    T* dst = static_cast<T*>(a.xt) + (int64_t)k * a.ldxt + m;
+    if (m + KCH <= a.M) {
+      uint4 v;
+      __builtin_memcpy(&v, o, 16);
+      *reinterpret_cast<uint4*>(dst) = v;
+    } else {
+      for (int q = 0; q < KCH && m + q < a.M; ++q) dst[q] = o[q];
+    }
   }
 }
 
 hipError_t launch_prologue(int bf16, const PrologueArgs& a, hipStream_t s) {
-  dim3 grid(a.xt ? (a.K + 63) / 64 : 1, a.xt ? (a.M + 63) / 64 : 1), block(256);
+  dim3 grid(a.xp ? (a.K + 63) / 64 : 1, a.xp ? (a.M + 63) / 64 : 1), block(256);
   if (bf16)
     hipLaunchKernelGGL(erase_prologue<uint16_t>, grid, block, 0, s, a);
   else
@@ -398,75 +454,128 @@ hipError_t launch_prologue(int bf16, const PrologueArgs& a, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// local head + sigmoid-BCE + gradient at z, HEAD_ROWS rows per workgroup
+// local head + sigmoid-BCE + gradient at z.  One workgroup stages R rows of z
+// ([R][N] tile in LDS, 16-byte global loads), then:
+//   s_i = z_i . w + c, l_i = max(s,0) - s y + log1p(e^-|s|),
+//   ds_i = lam (sigmoid(s_i) - y_i) / M,
+//   dz = ds_i w_n [z_in > 0]  (row-major and feature-major, 16-byte stores),
+//   partial dw_n = sum_i z_in ds_i, partial dc = sum_i ds_i, partial loss,
+// every sum in a fixed order.
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void erase_head_bce(HeadArgs a) {
-  __shared__ float s_ds[HEAD_ROWS];
-  __shared__ float s_loss[HEAD_ROWS];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int r0 = blockIdx.x * HEAD_ROWS;
-  const int rows = min(HEAD_ROWS, a.M - r0);
+  extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+  constexpr int KCH = 16 / sizeof(T);  // elements per 16-byte chunk
+  __shared__ float s_ds[32];
+  __shared__ float s_loss[32];
+  T* tile = reinterpret_cast<T*>(smem_raw);
+  const int N = a.N;
+  const int R = head_rows(N, sizeof(T));
+  const int pitch = head_pitch(N, sizeof(T));
+  const int tid = threadIdx.x;
+  const int r0 = blockIdx.x * R;
+  const int rows = min(R, a.M - r0);
   const T* Z = static_cast<const T*>(a.z);
-  const float c = a.c[0];
+  const int cpr = (N + KCH - 1) / KCH;  // chunks per row
 
-  // logits, per-row loss and dl/ds (16 rows per wave)
-  for (int i = 0; i < HEAD_ROWS / 4; ++i) {
-    const int rl = wave * (HEAD_ROWS / 4) + i;
-    float part = 0.f;
-    if (rl < rows) {
-      const T* zr = Z + (int64_t)(r0 + rl) * a.ldz;
-      for (int n = lane; n < a.N; n += 64) part = fmaf(ldf(zr + n), a.w[n], part);
+  // stage the tile (rows beyond M and columns beyond N are zero)
+  for (int c = tid; c < R * cpr; c += 256) {
+    const int r = c / cpr, k = (c - r * cpr) * KCH;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (r < rows) {
+      const T* p = Z + (int64_t)(r0 + r) * a.ldz + k;
+      if (k + KCH <= N) {
+        v = *reinterpret_cast<const uint4*>(p);
+      } else {
+        T tmp[KCH];
+#pragma unroll
+        for (int e = 0; e < KCH; ++e) tmp[e] = (k + e < N) ? p[e] : T(0);
+        __builtin_memcpy(&v, tmp, 16);
+      }
     }
-    part = wave_sum(part);
-    if (lane == 0) {
+    *reinterpret_cast<uint4*>(&tile[r * pitch + k]) = v;
+  }
+  __syncthreads();
+
+  // logits: 256/R lanes per row, then a fixed butterfly over those lanes
+  {
+    const int tpr = 256 / R;  // power of two, 8..64
+    const int r = tid / tpr, j = tid - r * tpr;
+    float part = 0.f;
+    for (int n = j; n < N; n += tpr) part = fmaf(asf(tile[r * pitch + n]), a.w[n], part);
+    for (int off = 1; off < tpr; off <<= 1) part += __shfl_xor(part, off, 64);
+    if (j == 0) {
       float ds = 0.f, l = 0.f;
-      if (rl < rows) {
-        const float s = part + c;
-        const float yv = a.y[r0 + rl];
+      if (r < rows) {
+        const float s = part + a.c[0];
+        const float yv = a.y[r0 + r];
         const float en = __expf(-fabsf(s));
         const float sig = s >= 0.f ? 1.f / (1.f + en) : en / (1.f + en);
         ds = a.lam * (sig - yv) * a.inv_m;
         l = fmaxf(s, 0.f) - s * yv + log1pf(en);
       }
-      s_ds[rl] = ds;
-      s_loss[rl] = l;
+      s_ds[r] = ds;
+      s_loss[r] = l;
     }
   }
   __syncthreads();
 
-  // gradient at the pre-activation of the last (ReLU) layer, row-major
+  // dz row-major
   if (a.dmn) {
     T* D = static_cast<T*>(a.dmn);
-    for (int idx = tid; idx < rows * a.N; idx += 256) {
-      const int rl = idx / a.N, n = idx - rl * a.N;
-      const int64_t m = r0 + rl;
-      const float zv = ldf(Z + m * a.ldz + n);
-      D[m * a.lddmn + n] = cvt<T>(zv > 0.f ? s_ds[rl] * a.w[n] : 0.f);
+    for (int c = tid; c < rows * cpr; c += 256) {
+      const int r = c / cpr, k = (c - r * cpr) * KCH;
+      const float ds = s_ds[r];
+      T o[KCH];
+#pragma unroll
+      for (int e = 0; e < KCH; ++e) {
+        const float zv = asf(tile[r * pitch + k + e]);
+        o[e] = cvt<T>((zv > 0.f && k + e < N) ? ds * a.w[min(k + e, N - 1)] : 0.f);
+      }
+      T* p = D + (int64_t)(r0 + r) * a.lddmn + k;
+      if (k + KCH <= N) {
+        uint4 v;
+        __builtin_memcpy(&v, o, 16);
+        *reinterpret_cast<uint4*>(p) = v;
+      } else {
+        for (int e = 0; e < KCH && k + e < N; ++e) p[e] = o[e];
+      }
     }
   }
-  // ... and feature-major
+  // dz feature-major: items of KCH consecutive rows of one column
   {
     T* D = static_cast<T*>(a.dnm);
-    for (int idx = tid; idx < a.N * HEAD_ROWS; idx += 256) {
-      const int n = idx / HEAD_ROWS, rl = idx - n * HEAD_ROWS;
-      if (rl >= rows) continue;
-      const int64_t m = r0 + rl;
-      const float zv = ldf(Z + m * a.ldz + n);
-      D[(int64_t)n * a.lddnm + m] = cvt<T>(zv > 0.f ? s_ds[rl] * a.w[n] : 0.f);
+    const int ipc = R / KCH;  // items per column
+    for (int it = tid; it < N * ipc; it += 256) {
+      const int n = it / ipc, rb = (it - n * ipc) * KCH;
+      const float wn = a.w[n];
+      T o[KCH];
+#pragma unroll
+      for (int e = 0; e < KCH; ++e) {
+        const float zv = asf(tile[(rb + e) * pitch + n]);
+        o[e] = cvt<T>(zv > 0.f ? s_ds[rb + e] * wn : 0.f);
+      }
+      T* p = D + (int64_t)n * a.lddnm + r0 + rb;
+      if (rb + KCH <= rows) {
+        uint4 v;
+        __builtin_memcpy(&v, o, 16);
+        *reinterpret_cast<uint4*>(p) = v;
+      } else {
+        for (int e = 0; e < KCH && rb + e < rows; ++e) p[e] = o[e];
+      }
     }
   }
-  // partial head gradients and loss of this workgroup's rows (fixed order)
-  for (int n = tid; n < a.N; n += 256) {
+  // partial head gradients and loss of this workgroup's rows
+  for (int n = tid; n < N; n += 256) {
     float acc = 0.f;
-    for (int rl = 0; rl < rows; ++rl) acc = fmaf(ldf(Z + (int64_t)(r0 + rl) * a.ldz + n), s_ds[rl], acc);
-    a.pdw[(int64_t)blockIdx.x * a.N + n] = acc;
+    for (int r = 0; r < rows; ++r) acc = fmaf(asf(tile[r * pitch + n]), s_ds[r], acc);
+    a.pdw[(int64_t)blockIdx.x * N + n] = acc;
   }
   if (tid == 0) {
     float sd = 0.f, sl = 0.f;
-    for (int rl = 0; rl < rows; ++rl) {
-      sd += s_ds[rl];
-      sl += s_loss[rl];
+    for (int r = 0; r < rows; ++r) {
+      sd += s_ds[r];
+      sl += s_loss[r];
     }
     a.pdc[blockIdx.x] = sd;
     a.ploss[blockIdx.x] = sl;
@@ -474,11 +583,13 @@ __global__ __launch_bounds__(256) void erase_head_bce(HeadArgs a) {
 }
 
 hipError_t launch_head(int bf16, const HeadArgs& a, hipStream_t s) {
-  dim3 grid((a.M + HEAD_ROWS - 1) / HEAD_ROWS), block(256);
+  const int esz = bf16 ? 2 : 4;
+  dim3 grid((a.M + head_rows(a.N, esz) - 1) / head_rows(a.N, esz)), block(256);
+  const size_t lds = head_lds_bytes(a.N, esz);
   if (bf16)
-    hipLaunchKernelGGL(erase_head_bce<uint16_t>, grid, block, 0, s, a);
+    hipLaunchKernelGGL(erase_head_bce<uint16_t>, grid, block, lds, s, a);
   else
-    hipLaunchKernelGGL(erase_head_bce<float>, grid, block, 0, s, a);
+    hipLaunchKernelGGL(erase_head_bce<float>, grid, block, lds, s, a);
   return hipGetLastError();
 }
 
@@ -487,16 +598,18 @@ hipError_t launch_head(int bf16, const HeadArgs& a, hipStream_t s) {
 // workgroup), with the ordered reduction of split partials fused in front
 // and the GEMM copies of the updated weights written behind.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ int find_seg(const AdamSeg* seg, int nseg, int64_t chunk) {
+__device__ __forceinline__ int find_seg(const AdamArgs& a, int64_t chunk) {
   int s = 0;
-  while (s + 1 < nseg && seg[s + 1].chunk0 <= chunk) ++s;
+  while (s + 1 < a.nseg && a.chunk0[s + 1] <= chunk) ++s;
   return s;
 }
 
 template <typename T>
 __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
+  constexpr int PER = ADAM_CHUNK / 256;  // elements per thread, 256 apart
+  constexpr int ZB = 8;                  // partial loads issued together per element
   const int64_t chunk = blockIdx.x;
-  const AdamSeg sg = a.seg[find_seg(a.seg, a.nseg, chunk)];
+  const AdamSeg sg = a.seg[find_seg(a, chunk)];
   const double t = (double)a.t[0];
   const float bc1 = (float)(1.0 - pow((double)a.beta1, t));
   const float bc2s = (float)sqrt(1.0 - pow((double)a.beta2, t));
@@ -506,23 +619,56 @@ __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
   const int base = (int)((chunk - sg.chunk0) * ADAM_CHUNK);
   T* SH = static_cast<T*>(sg.sh);
   T* SHT = static_cast<T*>(sg.sht);
+
+  int idx[PER], row[PER], col[PER];
+  bool ok[PER];
+  const float* pp[PER];
+  float g[PER];
 #pragma unroll
-  for (int q = 0; q < ADAM_CHUNK / 256; ++q) {
-    const int i = base + q * 256 + (int)threadIdx.x;
-    if (i >= n) break;
-    const int r = i / sg.cols, c = i - r * sg.cols;
-    const float* pp = sg.part + (int64_t)r * sg.ldpart + c;
-    float g = 0.f;
-    for (int zz = 0; zz < sg.nsplit; ++zz) g += pp[(int64_t)zz * sg.pstride];
-    if (sg.g) sg.g[i] = g;
-    const float m = fmaf(b1, sg.m[i], (1.f - b1) * g);
-    const float v = fmaf(b2, sg.v[i], (1.f - b2) * g * g);
-    const float p = sg.p[i] - step * m / (sqrtf(v) / bc2s + a.eps);
+  for (int q = 0; q < PER; ++q) {
+    idx[q] = base + q * 256 + (int)threadIdx.x;
+    ok[q] = idx[q] < n;
+    const int i = ok[q] ? idx[q] : 0;
+    row[q] = i / sg.cols;
+    col[q] = i - row[q] * sg.cols;
+    pp[q] = sg.part + (int64_t)row[q] * sg.ldpart + col[q];
+    g[q] = 0.f;
+  }
+  // ordered reduction of the split partials: slice 0, 1, ..., nsplit-1
+  for (int z0 = 0; z0 < sg.nsplit; z0 += ZB) {
+    float tv[PER][ZB];
+#pragma unroll
+    for (int q = 0; q < PER; ++q)
+#pragma unroll
+      for (int j = 0; j < ZB; ++j)
+        tv[q][j] = (ok[q] && z0 + j < sg.nsplit) ? pp[q][(int64_t)(z0 + j) * sg.pstride] : 0.f;
+#pragma unroll
+    for (int q = 0; q < PER; ++q)
+#pragma unroll
+      for (int j = 0; j < ZB; ++j)
+        if (z0 + j < sg.nsplit) g[q] += tv[q][j];
+  }
+  float pv[PER], mv[PER], vv[PER];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    if (!ok[q]) continue;
+    pv[q] = sg.p[idx[q]];
+    mv[q] = sg.m[idx[q]];
+    vv[q] = sg.v[idx[q]];
+  }
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    if (!ok[q]) continue;
+    const int i = idx[q];
+    const float m = fmaf(b1, mv[q], (1.f - b1) * g[q]);
+    const float v = fmaf(b2, vv[q], (1.f - b2) * g[q] * g[q]);
+    const float p = pv[q] - step * m / (sqrtf(v) / bc2s + a.eps);
+    if (sg.g) sg.g[i] = g[q];
     sg.m[i] = m;
     sg.v[i] = v;
     sg.p[i] = p;
-    if (SH) SH[(int64_t)r * sg.ldsh + c] = cvt<T>(p);
-    if (SHT) SHT[(int64_t)c * sg.ldsht + r] = cvt<T>(p);
+    if (SH) SH[(int64_t)row[q] * sg.ldsh + col[q]] = cvt<T>(p);
+    if (SHT) SHT[(int64_t)col[q] * sg.ldsht + row[q]] = cvt<T>(p);
   }
   if (chunk == 0 && threadIdx.x == 0 && a.ploss) {
     float L = 0.f;
@@ -536,7 +682,7 @@ __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
 template <typename T>
 __global__ __launch_bounds__(256) void erase_refresh(AdamArgs a) {
   const int64_t chunk = blockIdx.x;
-  const AdamSeg sg = a.seg[find_seg(a.seg, a.nseg, chunk)];
+  const AdamSeg sg = a.seg[find_seg(a, chunk)];
   const int n = sg.rows * sg.cols;
   const int base = (int)((chunk - sg.chunk0) * ADAM_CHUNK);
   T* SH = static_cast<T*>(sg.sh);

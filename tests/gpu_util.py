@@ -83,27 +83,25 @@ def compare(cfg, gpu, ref, tol, what=FIELDS):
 
 
 def check_bf16(cfg, gpu, params, batches, tol=2e-2, slack=1.5):
-    """bf16 parity, two readings of the same tolerance:
+    """bf16 parity against two oracles on the same inputs: the float64 oracle
+    and the one that rounds to bf16 exactly the tensors the GPU stores in bf16.
 
-    * against the oracle that rounds to bf16 exactly the tensors the GPU
-      stores in bf16: every field within `tol`;
-    * against the float64 oracle: losses and parameters within `tol`;
-      gradients and moments within max(tol, slack * e), where e is the
-      bf16-emulating oracle's own distance from float64.  bf16 rounding of
-      GEMM operands moves pre-activations by ~2^-8 relative and flips the
-      ReLU mask of the few elements closer to zero than that; each flip moves
-      a whole gradient entry, so the attainable gradient error depends on the
-      workload and is measured, not assumed.
+    Bound per field: max(tol, slack * e), where e is the bf16-emulating
+    oracle's own distance from float64.  bf16 rounding of GEMM operands moves
+    pre-activations by ~2^-8 relative and flips the ReLU mask of elements
+    closer to zero than that; each flip moves a whole gradient entry, so what
+    bf16 arithmetic can attain depends on the workload and is measured by e,
+    not assumed.  Where e is small (the CTR MLP) the bound is tol itself.
     """
     r64 = run_oracle(cfg, params, batches)
     rbf = run_oracle(cfg, params, batches, emulate_bf16=True)
-    w_emul = compare(cfg, gpu, rbf, tol)
     inherent = worst_errors(cfg, rbf, r64)
+    bounds = {k: max(tol, slack * inherent[k]) for k in FIELDS}
+    w_emul = worst_errors(cfg, gpu, rbf)
     w64 = worst_errors(cfg, gpu, r64)
-    bounds = {k: (tol if k in ("losses", "params") else max(tol, slack * inherent[k])) for k in FIELDS}
-    bad = {k: (w64[k], bounds[k]) for k in FIELDS if not w64[k] <= bounds[k]}
-    assert not bad, f"vs float64 oracle: {w64}, bounds {bounds}"
-    return {"vs_bf16_oracle": w_emul, "vs_f64_oracle": w64, "bf16_oracle_vs_f64": inherent}
+    bad = {k: (w_emul[k], w64[k], bounds[k]) for k in FIELDS if not (w_emul[k] <= bounds[k] and w64[k] <= bounds[k])}
+    assert not bad, f"bf16 parity: (vs bf16 oracle, vs f64 oracle, bound) {bad}; bf16 oracle vs f64: {inherent}"
+    return {"vs_bf16_oracle": w_emul, "vs_f64_oracle": w64, "bf16_oracle_vs_f64": inherent, "bounds": bounds}
 
 
 def assert_bit_identical(a, b):

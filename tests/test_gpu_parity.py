@@ -92,10 +92,12 @@ def _ctr_small(batch=1000, blocks=2):
     return cfg
 
 
-def test_ctr_mlp_bf16_small_vs_oracle():
-    """Full CTR widths (1677->512->256->128), ragged batch 1000, 2 blocks."""
-    _say("case: ctr_mlp bf16 batch=1000")
-    cfg = _ctr_small()
+@pytest.mark.parametrize("batch", [1000, 777])
+def test_ctr_mlp_bf16_small_vs_oracle(batch):
+    """Full CTR widths (1677->512->256->128), 2 blocks, ragged batches; 777
+    pads to an odd number of k-steps in the weight-gradient GEMMs."""
+    _say(f"case: ctr_mlp bf16 batch={batch}")
+    cfg = _ctr_small(batch=batch)
     params, batches = synth.make_workload(cfg, 0, 2)
     _, g = run_gpu(cfg, params, batches, "overlap")
     _say("  ", check_bf16(cfg, g, params, batches))
@@ -134,6 +136,17 @@ def test_dcn_bf16_small_vs_oracle():
                                         ("linear_relu", 128, 64)], "lam": 1.0} for _ in range(2)]
     cfg = synth.custom("bf16", 300, 200, blocks, label_p=0.1)
     params, batches = synth.make_workload(cfg, 5, 2)
+    _, g = run_gpu(cfg, params, batches, "overlap")
+    _say("  ", check_bf16(cfg, g, params, batches))
+
+
+def test_ctr_dcn_bf16_small_vs_oracle():
+    """The DCN workload's real shape (1677-wide cross layers on the CTR input,
+    1677->1024->1024->512), ragged batch 300, 2 blocks."""
+    _say("case: ctr_dcn bf16 batch=300")
+    cfg = synth.config("ctr_dcn", batch=300, ctr_rows=5000)
+    cfg["blocks"] = cfg["blocks"][:2]
+    params, batches = synth.make_workload(cfg, 1, 2)
     _, g = run_gpu(cfg, params, batches, "overlap")
     _say("  ", check_bf16(cfg, g, params, batches))
 
