@@ -35,7 +35,8 @@ PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector/MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 METRIC = "train samples/s, 6-block CTR @1 MI355X; ERASE vs serial speedup; MFMA util %"
 KIND_SYMBOL = {"prologue": "erase_prologue", "fwd_gemm": "erase_fwd_gemm", "head_bce": "erase_head_bce",
-               "wgrad_gemm": "erase_wgrad_gemm", "dgrad_gemm": "erase_dgrad_gemm", "adam": "erase_adam"}
+               "wgrad_gemm": "erase_wgrad_gemm", "dgrad_gemm": "erase_dgrad_gemm", "adam": "erase_adam",
+               "bwd_gemm": "erase_bwd_gemm"}
 
 
 def kernel_class(r, bf16=True):

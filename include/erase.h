@@ -177,7 +177,8 @@ erase_status erase_refresh_weights(void* ctx);
  * sets *n to the number of launches of that step. */
 typedef struct {
   int32_t kind;      /* 0 prologue, 1 forward GEMM, 2 head+loss, 3 weight-grad GEMM,
-                        4 input-grad GEMM, 5 Adam */
+                        4 input-grad GEMM, 5 Adam, 6 input- and weight-grad GEMMs of one
+                        layer in one launch */
   int32_t block;     /* block index, -1 for the step prologue */
   int32_t layer;     /* layer index within the block, -1 if none */
   int32_t stream;    /* 0 forward stream, 1 backward stream */

@@ -113,6 +113,7 @@ struct LayerRT {
   float* part = nullptr; int64_t ldp = 0, pstride = 0;
   float* bpart = nullptr;
   GemmPlan fwd, wgrad, dgrad;
+  bool grouped = false;  // input- and weight-gradient GEMMs share one launch
 };
 
 struct BlockRT {
@@ -160,40 +161,33 @@ struct Carver {
 GemmPlan choose_gemm(int bf16, int64_t Mg, int64_t Ng, int64_t Kc, bool allow_split) {
   GemmPlan p;
   const int BK = bf16 ? 64 : 32;
-  if (!bf16) {
-    p.bm = p.bn = 64;
-    p.split = 1;
-    p.kps = (int)roundup(std::max<int64_t>(Kc, 1), BK);
+  auto finish = [&](int bm, int bn, int split) {
+    p.bm = bm;
+    p.bn = bn;
+    p.kps = (int)roundup(cdiv(std::max<int64_t>(Kc, 1), split), BK);
+    p.split = (int)cdiv(std::max<int64_t>(Kc, 1), p.kps);
     return p;
-  }
+  };
+  if (!bf16) return finish(64, 64, 1);
+  // At least `target` workgroups (1.5 per CU) so the launch covers the
+  // chip; the largest tile that reaches it (fewer LDS bytes per MFMA).  A
+  // long contraction keeps the 128x128 tile and splits instead; otherwise a
+  // short one falls back to 64x64, split only for weight gradients.
+  const int64_t target = 384;
   const int tiles[4][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}};
-  const int64_t target = 256;
-  int best = -1;
-  for (int i = 0; i < 4; ++i) {
-    const int64_t w = cdiv(Mg, tiles[i][0]) * cdiv(Ng, tiles[i][1]);
-    if (w >= target) { best = i; break; }
+  for (int i = 0; i < 4; ++i)
+    if (cdiv(Mg, tiles[i][0]) * cdiv(Ng, tiles[i][1]) >= target) return finish(tiles[i][0], tiles[i][1], 1);
+  if (allow_split) {
+    const int64_t w128 = cdiv(Mg, 128) * cdiv(Ng, 128);
+    int s = 1;
+    while (s < 16 && w128 * s < target && Kc / (s * 2) >= 2048) s *= 2;
+    if (w128 * s >= target) return finish(128, 128, s);
+    const int64_t w64 = cdiv(Mg, 64) * cdiv(Ng, 64);
+    s = 1;
+    while (s < 16 && w64 * s < target && Kc / (s * 2) >= 256) s *= 2;
+    return finish(64, 64, s);
   }
-  int split = 1;
-  if (best < 0) {
-    if (allow_split) {
-      best = 0;
-      const int64_t w = cdiv(Mg, 128) * cdiv(Ng, 128);
-      while (split < 16 && w * split < target && Kc / (split * 2) >= 256) split *= 2;
-      if (w * split < target / 2) {  // still small: a smaller tile instead
-        best = 3;
-        split = 1;
-        const int64_t w2 = cdiv(Mg, 64) * cdiv(Ng, 64);
-        while (split < 16 && w2 * split < target && Kc / (split * 2) >= 256) split *= 2;
-      }
-    } else {
-      best = 3;
-    }
-  }
-  p.bm = tiles[best][0];
-  p.bn = tiles[best][1];
-  p.kps = (int)roundup(cdiv(std::max<int64_t>(Kc, 1), split), BK);
-  p.split = (int)cdiv(std::max<int64_t>(Kc, 1), p.kps);
-  return p;
+  return finish(64, 64, 1);
 }
 
 size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
@@ -264,7 +258,22 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
       const int BK = P->bf16 ? 64 : 32;
       R.fwd = choose_gemm(P->bf16, M, R.N, roundup(R.K, BK), false);
       R.wgrad = choose_gemm(P->bf16, R.N, R.K, roundup(M, BK), true);
-      if (l >= 1) R.dgrad = choose_gemm(P->bf16, M, R.K, roundup(R.N, BK), false);
+      if (l >= 1) {
+        R.dgrad = choose_gemm(P->bf16, M, R.K, roundup(R.N, BK), false);
+        // one launch for both backward GEMMs when they can share a tile
+        if (R.dgrad.bm != R.wgrad.bm || R.dgrad.bn != R.wgrad.bn) {
+          GemmPlan d64 = choose_gemm(P->bf16, 1, 1, roundup(R.N, BK), false);  // 64x64, split 1
+          GemmPlan w64 = d64;
+          const int64_t w = cdiv(R.N, 64) * cdiv(R.K, 64);
+          int sp = 1;
+          while (sp < 16 && w * sp < 384 && roundup(M, BK) / (sp * 2) >= 256) sp *= 2;
+          w64.kps = (int)roundup(cdiv(roundup(M, BK), sp), BK);
+          w64.split = (int)cdiv(roundup(M, BK), w64.kps);
+          R.dgrad = d64;
+          R.wgrad = w64;
+        }
+        R.grouped = (R.dgrad.bm == 64 && R.dgrad.bn == 64) || (R.dgrad.bm == 128 && R.dgrad.bn == 128);
+      }
       R.ldp = ldK;
       R.pstride = int64_t(R.N) * ldK;
       R.part = static_cast<float*>(cv.take(size_t(R.wgrad.split) * R.pstride * 4));
@@ -543,6 +552,11 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
   return ERASE_OK;
 }
 
+// Backward GEMMs of block b, last layer first.  Per layer l: the weight and
+// bias gradient dW = dH^T a_{l-1}, db = row sums of dH^T, and (l > 0) the
+// input gradient of the layer below; the block input is detached (Eq. 1), so
+// layer 0 has no input gradient.  When both GEMMs of a layer share a tile
+// they go out as one launch.
 erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStream_t s, int sid) {
   const Plan& P = c->P;
   const BlockRT& B = P.blk[b];
@@ -559,70 +573,78 @@ erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStre
     const void* innm;
     int64_t ldinnm;
     layer_input(c, b, l, x, &inmn, &ldinmn, &innm, &ldinnm);
-    {  // weight and bias gradient: dW = dH^T a_{l-1}, db = row sums of dH^T
-      GemmDesc g{};
-      g.A = R.dnm;
-      g.lda = R.lddnm;
-      g.B = innm;
-      g.ldb = ldinnm;
-      g.M = R.N;
-      g.N = R.K;
-      g.K = (int)roundup(M, P.bf16 ? 64 : 32);
-      g.kps = R.wgrad.kps;
-      g.split = R.wgrad.split;
-      g.bm = R.wgrad.bm;
-      g.bn = R.wgrad.bn;
-      EpiParams e{};
-      e.part = R.part;
-      e.ldp = R.ldp;
-      e.pstride = R.pstride;
-      e.bpart = R.bpart;
-      Cost cost = gemm_cost(g);
-      cost.flops = 2.0 * M * R.N * R.K;
-      cost.bytes = double(esz) * M * (double(R.N) + R.K) + 4.0 * R.wgrad.split * (double(R.N) * R.K + R.N);
-      RUN(3, b, l, sid, s, cost, [&]() { return launch_gemm(bf, GK_WGRAD, g, e, s); });
+    GemmDesc gw{};
+    gw.A = R.dnm;
+    gw.lda = R.lddnm;
+    gw.B = innm;
+    gw.ldb = ldinnm;
+    gw.M = R.N;
+    gw.N = R.K;
+    gw.K = (int)roundup(M, P.bf16 ? 64 : 32);
+    gw.kps = R.wgrad.kps;
+    gw.split = R.wgrad.split;
+    gw.bm = R.wgrad.bm;
+    gw.bn = R.wgrad.bn;
+    EpiParams ew{};
+    ew.part = R.part;
+    ew.ldp = R.ldp;
+    ew.pstride = R.pstride;
+    ew.bpart = R.bpart;
+    Cost cw = gemm_cost(gw);
+    cw.flops = 2.0 * M * R.N * R.K;
+    cw.bytes = double(esz) * M * (double(R.N) + R.K) + 4.0 * R.wgrad.split * (double(R.N) * R.K + R.N);
+    if (l == 0) {
+      RUN(3, b, l, sid, s, cw, [&]() { return launch_gemm(bf, GK_WGRAD, gw, ew, s); });
+      break;
     }
-    if (l == 0) break;  // the block input is detached: no input gradient
-    {
-      const LayerRT& Rb = B.layer[l - 1];
-      GemmDesc g{};
-      g.A = R.dmn;
-      g.lda = R.lddmn;
-      g.B = R.wsht;
-      g.ldb = R.ldwsht;
-      g.M = M;
-      g.N = R.K;
-      g.K = (int)roundup(R.N, P.bf16 ? 64 : 32);
-      g.kps = R.dgrad.kps;
-      g.split = 1;
-      g.bm = R.dgrad.bm;
-      g.bn = R.dgrad.bn;
-      EpiParams e{};
-      if (R.kind == ERASE_LAYER_CROSS) {
-        e.res = R.g;
-        e.ldres = R.ldg;
-      }
-      e.dmn = Rb.dmn;
-      e.lddmn = Rb.lddmn;
-      e.dnm = Rb.dnm;
-      e.lddnm = Rb.lddnm;
-      if (Rb.kind == ERASE_LAYER_CROSS) {
-        e.below_cross = 1;
-        e.x0 = x0;
-        e.ldx0 = ldx0;
-        e.gout = Rb.g;
-        e.ldgout = Rb.ldg;
-      } else {
-        e.below_cross = 0;
-        e.mask = Rb.y;
-        e.ldmask = Rb.ldy;
-      }
-      Cost cost = gemm_cost(g);
-      cost.flops = 2.0 * M * R.N * R.K;
-      const double outs = 1.0 + (Rb.dmn ? 1.0 : 0.0) + (e.gout ? 1.0 : 0.0);
-      cost.bytes = double(esz) * (double(M) * R.N + double(R.N) * R.K + double(M) * R.K * (outs + 1.0) +
-                                  (e.res ? double(M) * R.K : 0.0));
-      RUN(4, b, l, sid, s, cost, [&]() { return launch_gemm(bf, GK_DGRAD, g, e, s); });
+    const LayerRT& Rb = B.layer[l - 1];
+    GemmDesc gd{};
+    gd.A = R.dmn;
+    gd.lda = R.lddmn;
+    gd.B = R.wsht;
+    gd.ldb = R.ldwsht;
+    gd.M = M;
+    gd.N = R.K;
+    gd.K = (int)roundup(R.N, P.bf16 ? 64 : 32);
+    gd.kps = R.dgrad.kps;
+    gd.split = 1;
+    gd.bm = R.dgrad.bm;
+    gd.bn = R.dgrad.bn;
+    EpiParams ed{};
+    if (R.kind == ERASE_LAYER_CROSS) {
+      ed.res = R.g;
+      ed.ldres = R.ldg;
+    }
+    ed.dmn = Rb.dmn;
+    ed.lddmn = Rb.lddmn;
+    ed.dnm = Rb.dnm;
+    ed.lddnm = Rb.lddnm;
+    if (Rb.kind == ERASE_LAYER_CROSS) {
+      ed.below_cross = 1;
+      ed.x0 = x0;
+      ed.ldx0 = ldx0;
+      ed.gout = Rb.g;
+      ed.ldgout = Rb.ldg;
+    } else {
+      ed.below_cross = 0;
+      ed.mask = Rb.y;
+      ed.ldmask = Rb.ldy;
+    }
+    Cost cd = gemm_cost(gd);
+    cd.flops = 2.0 * M * R.N * R.K;
+    const double outs = 1.0 + (Rb.dmn ? 1.0 : 0.0) + (ed.gout ? 1.0 : 0.0);
+    cd.bytes = double(esz) * (double(M) * R.N + double(R.N) * R.K + double(M) * R.K * (outs + 1.0) +
+                              (ed.res ? double(M) * R.K : 0.0));
+    if (R.grouped) {
+      Cost cg = cd;
+      cg.flops += cw.flops;
+      cg.bytes += cw.bytes;
+      cg.grid += cw.grid;
+      cg.split = cw.split;
+      RUN(6, b, l, sid, s, cg, [&]() { return launch_bwd_gemm(bf, gd, ed, gw, ew, s); });
+    } else {
+      RUN(3, b, l, sid, s, cw, [&]() { return launch_gemm(bf, GK_WGRAD, gw, ew, s); });
+      RUN(4, b, l, sid, s, cd, [&]() { return launch_gemm(bf, GK_DGRAD, gd, ed, s); });
     }
   }
   return ERASE_OK;
@@ -636,8 +658,7 @@ erase_status enqueue_adam(Ctx* c, Enqueuer& q, int b, float* losses, hipStream_t
   a.nseg = (int)B.segs.size();
   for (int i = 0; i < a.nseg; ++i) a.chunk0[i] = B.segs[i].chunk0;
   a.nchunks = B.nchunks;
-  a.t = P.t;
-  a.lr = c->cfg.lr;
+  a.hyper = reinterpret_cast<const float*>(P.t + 2);
   a.beta1 = c->cfg.beta1;
   a.beta2 = c->cfg.beta2;
   a.eps = c->cfg.eps;
@@ -668,6 +689,9 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
   {
     PrologueArgs pa{};
     pa.t = P.t;
+    pa.lr = c->cfg.lr;
+    pa.beta1 = c->cfg.beta1;
+    pa.beta2 = c->cfg.beta2;
     pa.x = x;
     pa.ldx = c->cfg.x_ld;
     pa.xp = P.xp;
@@ -712,8 +736,11 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
 }
 
 int launches_per_step(const Plan& P) {
-  int n = 1;
-  for (const BlockRT& B : P.blk) n += B.L + 1 + B.L + (B.L - 1) + 1;
+  int n = 1;  // prologue
+  for (const BlockRT& B : P.blk) {
+    n += B.L + 1 + 1 + 1;  // forward GEMMs, head, first layer's weight gradient, Adam
+    for (int l = 1; l < B.L; ++l) n += B.layer[l].grouped ? 1 : 2;
+  }
   return n;
 }
 

@@ -51,11 +51,20 @@ struct EpiParams {
 };
 
 hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s);
+// Input-gradient (gd, split 1) and weight-gradient (gw) GEMMs of one layer in
+// one launch; both must use the same tile, 64x64 or 128x128.
+hipError_t launch_bwd_gemm(int bf16, const GemmDesc& gd, const EpiParams& ed, const GemmDesc& gw, const EpiParams& ew,
+                           hipStream_t s);
 
 // Step prologue: t += 1, the zero-padded copy xp[m][k] = x[m][k] and the
 // feature-major copy xt[k][m] = x[m][k] (padding of both stays zero).
+// Workspace header (first 256 bytes): step counter t (int64 at 0), status
+// word (int32 at 8), and the Adam step factors of the current step written
+// by the prologue: lr / (1 - beta1^t) (float at 16), sqrt(1 - beta2^t)
+// (float at 20).
 struct PrologueArgs {
   int64_t* t;
+  float lr, beta1, beta2;
   const void* x; int64_t ldx;
   void* xp; int64_t ldxp;
   void* xt; int64_t ldxt;
@@ -109,8 +118,8 @@ struct AdamArgs {
   int64_t chunk0[ADAM_MAX_SEG];  // first chunk of each segment (kernel-argument copy)
   int nseg;
   int64_t nchunks;
-  const int64_t* t;
-  float lr, beta1, beta2, eps;
+  const float* hyper;  // [step factor, sqrt bias correction 2] of this step (workspace header)
+  float beta1, beta2, eps;
   const float* ploss; int nloss; float inv_m;  // loss finalize (nullable ploss)
   float* loss_out;
   int* status;

@@ -128,7 +128,17 @@ __device__ __forceinline__ T epi_value(const EpiParams& e, int m, int n, float a
 // The epilogue stages the output tile in LDS and writes it with 16-byte
 // stores, row-major and (forward / input gradient) feature-major.
 template <typename T, int BM, int BN, int KIND>
-__device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e) {
+struct GemmSmem {
+  static constexpr int BK = GT<T>::BK, KCH = GT<T>::KCH, PITCH = BK + KCH;
+  using OT = typename std::conditional<KIND == GK_WGRAD, float, T>::type;
+  static constexpr int MAIN = 2 * (BM + BN) * PITCH * (int)sizeof(T);
+  static constexpr int EPI = BM * (BN + 16 / (int)sizeof(OT)) * (int)sizeof(OT);
+  static constexpr int BYTES = MAIN > EPI ? MAIN : EPI;
+};
+
+template <typename T, int BM, int BN, int KIND>
+__device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e, int bx, int by, int bz,
+                                          char* smem) {
   constexpr int BK = GT<T>::BK, KCH = GT<T>::KCH, KMF = GT<T>::KMF;
   constexpr int PITCH = BK + KCH;
   constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 16, TN = WN / 16;
@@ -139,16 +149,12 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e)
   using OT = typename std::conditional<KIND == GK_WGRAD, float, T>::type;
   constexpr int OCH = 16 / (int)sizeof(OT);
   constexpr int OPITCH = BN + OCH;
-  constexpr int MAIN_BYTES = 2 * STAGE * (int)sizeof(T);
-  constexpr int EPI_BYTES = BM * OPITCH * (int)sizeof(OT);
-  constexpr int SMEM = MAIN_BYTES > EPI_BYTES ? MAIN_BYTES : EPI_BYTES;
-  __shared__ __attribute__((aligned(16))) char smem[SMEM];
   T* lds = reinterpret_cast<T*>(smem);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
-  const int z = blockIdx.z;
+  const int m0 = bx * BM, n0 = by * BN;
+  const int z = bz;
   const int kbeg = z * g.kps;
   const int kend = min(g.K, kbeg + g.kps);
   const T* A = static_cast<const T*>(g.A);
@@ -160,7 +166,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e)
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  const bool do_rows = (KIND == GK_WGRAD) && e.bpart != nullptr && blockIdx.y == 0 && wn == 0;
+  const bool do_rows = (KIND == GK_WGRAD) && e.bpart != nullptr && by == 0 && wn == 0;
   float rs[TM];
 #pragma unroll
   for (int i = 0; i < TM; ++i) rs[i] = 0.f;
@@ -348,21 +354,34 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e)
   }
 }
 
+#define ERASE_GEMM_KERNEL(NAME, KIND)                                                    \
+  template <typename T, int BM, int BN>                                                  \
+  __global__ __launch_bounds__(256) void NAME(GemmDesc g, EpiParams e) {                 \
+    __shared__ __attribute__((aligned(16))) char smem[GemmSmem<T, BM, BN, KIND>::BYTES]; \
+    gemm_body<T, BM, BN, KIND>(g, e, blockIdx.x, blockIdx.y, blockIdx.z, smem);          \
+  }
+ERASE_GEMM_KERNEL(erase_fwd_gemm, GK_FWD_RELU)
+ERASE_GEMM_KERNEL(erase_fwd_cross_gemm, GK_FWD_CROSS)
+ERASE_GEMM_KERNEL(erase_wgrad_gemm, GK_WGRAD)
+ERASE_GEMM_KERNEL(erase_dgrad_gemm, GK_DGRAD)
+#undef ERASE_GEMM_KERNEL
+
+// One launch for both backward GEMMs of a layer (they read the same
+// activation gradient and are independent): workgroups [0, nd) compute the
+// input-gradient tiles, the rest the weight-gradient tiles and slices.
 template <typename T, int BM, int BN>
-__global__ __launch_bounds__(256) void erase_fwd_gemm(GemmDesc g, EpiParams e) {
-  gemm_body<T, BM, BN, GK_FWD_RELU>(g, e);
-}
-template <typename T, int BM, int BN>
-__global__ __launch_bounds__(256) void erase_fwd_cross_gemm(GemmDesc g, EpiParams e) {
-  gemm_body<T, BM, BN, GK_FWD_CROSS>(g, e);
-}
-template <typename T, int BM, int BN>
-__global__ __launch_bounds__(256) void erase_wgrad_gemm(GemmDesc g, EpiParams e) {
-  gemm_body<T, BM, BN, GK_WGRAD>(g, e);
-}
-template <typename T, int BM, int BN>
-__global__ __launch_bounds__(256) void erase_dgrad_gemm(GemmDesc g, EpiParams e) {
-  gemm_body<T, BM, BN, GK_DGRAD>(g, e);
+__global__ __launch_bounds__(256) void erase_bwd_gemm(GemmDesc gd, EpiParams ed, GemmDesc gw, EpiParams ew, int nd) {
+  constexpr int SD = GemmSmem<T, BM, BN, GK_DGRAD>::BYTES, SW = GemmSmem<T, BM, BN, GK_WGRAD>::BYTES;
+  __shared__ __attribute__((aligned(16))) char smem[SD > SW ? SD : SW];
+  const int b = blockIdx.x;
+  if (b < nd) {
+    const int gx = (gd.M + BM - 1) / BM;
+    gemm_body<T, BM, BN, GK_DGRAD>(gd, ed, b % gx, b / gx, 0, smem);
+  } else {
+    const int i = b - nd;
+    const int gx = (gw.M + BM - 1) / BM, gy = (gw.N + BN - 1) / BN;
+    gemm_body<T, BM, BN, GK_WGRAD>(gw, ew, i % gx, (i / gx) % gy, i / (gx * gy), smem);
+  }
 }
 
 template <typename T, int BM, int BN>
@@ -376,6 +395,27 @@ static hipError_t launch_gemm_t(int kind, const GemmDesc& g, const EpiParams& e,
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+template <typename T, int BM, int BN>
+static hipError_t launch_bwd_t(const GemmDesc& gd, const EpiParams& ed, const GemmDesc& gw, const EpiParams& ew,
+                               hipStream_t s) {
+  const int nd = ((gd.M + BM - 1) / BM) * ((gd.N + BN - 1) / BN);
+  const int nw = ((gw.M + BM - 1) / BM) * ((gw.N + BN - 1) / BN) * gw.split;
+  hipLaunchKernelGGL((erase_bwd_gemm<T, BM, BN>), dim3(nd + nw), dim3(256), 0, s, gd, ed, gw, ew, nd);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_gemm(int bf16, const GemmDesc& gd, const EpiParams& ed, const GemmDesc& gw, const EpiParams& ew,
+                           hipStream_t s) {
+  if (gd.bm != gw.bm || gd.bn != gw.bn || gd.split != 1 || gw.split <= 0) return hipErrorInvalidValue;
+  if (bf16) {
+    if (gd.bm == 128 && gd.bn == 128) return launch_bwd_t<uint16_t, 128, 128>(gd, ed, gw, ew, s);
+    if (gd.bm == 64 && gd.bn == 64) return launch_bwd_t<uint16_t, 64, 64>(gd, ed, gw, ew, s);
+  } else {
+    if (gd.bm == 64 && gd.bn == 64) return launch_bwd_t<float, 64, 64>(gd, ed, gw, ew, s);
+  }
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s) {
@@ -400,7 +440,13 @@ __global__ __launch_bounds__(256) void erase_prologue(PrologueArgs a) {
   constexpr int KCH = 16 / sizeof(T);
   constexpr int TP = 64 + KCH;  // LDS pitch (elements)
   __shared__ __attribute__((aligned(16))) T tile[64 * TP];
-  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) a.t[0] = a.t[0] + 1;
+  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
+    const int64_t t = a.t[0] + 1;
+    a.t[0] = t;
+    float* hyper = reinterpret_cast<float*>(a.t + 2);
+    hyper[0] = (float)((double)a.lr / (1.0 - pow((double)a.beta1, (double)t)));
+    hyper[1] = (float)sqrt(1.0 - pow((double)a.beta2, (double)t));
+  }
   if (a.xp == nullptr) return;
   const T* X = static_cast<const T*>(a.x);
   const int k0 = blockIdx.x * 64, m0 = blockIdx.y * 64;
@@ -468,6 +514,7 @@ __global__ __launch_bounds__(256) void erase_head_bce(HeadArgs a) {
   constexpr int KCH = 16 / sizeof(T);  // elements per 16-byte chunk
   __shared__ float s_ds[32];
   __shared__ float s_loss[32];
+  __shared__ float s_w[HEAD_MAX_N];
   T* tile = reinterpret_cast<T*>(smem_raw);
   const int N = a.N;
   const int R = head_rows(N, sizeof(T));
@@ -478,6 +525,7 @@ __global__ __launch_bounds__(256) void erase_head_bce(HeadArgs a) {
   const T* Z = static_cast<const T*>(a.z);
   const int cpr = (N + KCH - 1) / KCH;  // chunks per row
 
+  for (int n = tid; n < N; n += 256) s_w[n] = a.w[n];
   // stage the tile (rows beyond M and columns beyond N are zero)
   for (int c = tid; c < R * cpr; c += 256) {
     const int r = c / cpr, k = (c - r * cpr) * KCH;
@@ -502,7 +550,7 @@ __global__ __launch_bounds__(256) void erase_head_bce(HeadArgs a) {
     const int tpr = 256 / R;  // power of two, 8..64
     const int r = tid / tpr, j = tid - r * tpr;
     float part = 0.f;
-    for (int n = j; n < N; n += tpr) part = fmaf(asf(tile[r * pitch + n]), a.w[n], part);
+    for (int n = j; n < N; n += tpr) part = fmaf(asf(tile[r * pitch + n]), s_w[n], part);
     for (int off = 1; off < tpr; off <<= 1) part += __shfl_xor(part, off, 64);
     if (j == 0) {
       float ds = 0.f, l = 0.f;
@@ -530,7 +578,7 @@ __global__ __launch_bounds__(256) void erase_head_bce(HeadArgs a) {
 #pragma unroll
       for (int e = 0; e < KCH; ++e) {
         const float zv = asf(tile[r * pitch + k + e]);
-        o[e] = cvt<T>((zv > 0.f && k + e < N) ? ds * a.w[min(k + e, N - 1)] : 0.f);
+        o[e] = cvt<T>((zv > 0.f && k + e < N) ? ds * s_w[min(k + e, N - 1)] : 0.f);
       }
       T* p = D + (int64_t)(r0 + r) * a.lddmn + k;
       if (k + KCH <= N) {
@@ -548,7 +596,7 @@ __global__ __launch_bounds__(256) void erase_head_bce(HeadArgs a) {
     const int ipc = R / KCH;  // items per column
     for (int it = tid; it < N * ipc; it += 256) {
       const int n = it / ipc, rb = (it - n * ipc) * KCH;
-      const float wn = a.w[n];
+      const float wn = s_w[n];
       T o[KCH];
 #pragma unroll
       for (int e = 0; e < KCH; ++e) {
@@ -610,10 +658,8 @@ __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
   constexpr int ZB = 8;                  // partial loads issued together per element
   const int64_t chunk = blockIdx.x;
   const AdamSeg sg = a.seg[find_seg(a, chunk)];
-  const double t = (double)a.t[0];
-  const float bc1 = (float)(1.0 - pow((double)a.beta1, t));
-  const float bc2s = (float)sqrt(1.0 - pow((double)a.beta2, t));
-  const float step = a.lr / bc1;
+  const float step = a.hyper[0];  // lr / (1 - beta1^t)
+  const float bc2s = a.hyper[1];  // sqrt(1 - beta2^t)
   const float b1 = a.beta1, b2 = a.beta2;
   const int n = sg.rows * sg.cols;
   const int base = (int)((chunk - sg.chunk0) * ADAM_CHUNK);
@@ -623,7 +669,7 @@ __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
   int idx[PER], row[PER], col[PER];
   bool ok[PER];
   const float* pp[PER];
-  float g[PER];
+  float g[PER], pv[PER], mv[PER], vv[PER];
 #pragma unroll
   for (int q = 0; q < PER; ++q) {
     idx[q] = base + q * 256 + (int)threadIdx.x;
@@ -633,6 +679,10 @@ __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
     col[q] = i - row[q] * sg.cols;
     pp[q] = sg.part + (int64_t)row[q] * sg.ldpart + col[q];
     g[q] = 0.f;
+    // state loads first: independent of the reduction, one memory round trip
+    pv[q] = ok[q] ? sg.p[i] : 0.f;
+    mv[q] = ok[q] ? sg.m[i] : 0.f;
+    vv[q] = ok[q] ? sg.v[i] : 0.f;
   }
   // ordered reduction of the split partials: slice 0, 1, ..., nsplit-1
   for (int z0 = 0; z0 < sg.nsplit; z0 += ZB) {
@@ -647,14 +697,6 @@ __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
 #pragma unroll
       for (int j = 0; j < ZB; ++j)
         if (z0 + j < sg.nsplit) g[q] += tv[q][j];
-  }
-  float pv[PER], mv[PER], vv[PER];
-#pragma unroll
-  for (int q = 0; q < PER; ++q) {
-    if (!ok[q]) continue;
-    pv[q] = sg.p[idx[q]];
-    mv[q] = sg.m[idx[q]];
-    vv[q] = sg.v[idx[q]];
   }
 #pragma unroll
   for (int q = 0; q < PER; ++q) {
