@@ -9,10 +9,10 @@ batch 4096, bf16 operands with fp32 accumulation) the forward, local loss,
 weight/input gradients and Adam update.  Inputs are synthetic, seeded and
 already resident in HBM (8 batches, cycled).
 
-The headline value is samples/s of the ERASE schedule captured as a HIP graph
-(OVERLAP_GRAPH).  The same kernels are also timed in the serial order
-(SERIAL, SERIAL_GRAPH) and in the ungraphed ERASE order (OVERLAP); the
-speedups compare schedules with identical kernels.  Per-kernel durations for
+The headline value is samples/s of the faster ERASE schedule (OVERLAP, or
+OVERLAP_GRAPH captured as a HIP graph; the config names it).  The same kernels
+are also timed in the serial order (SERIAL, SERIAL_GRAPH); the speedups
+compare schedules with identical kernels.  Per-kernel durations for
 the roofline and the measured backward/forward overlap come from HIP events
 recorded by the library around each launch, on the stream of that launch.
 The CPU baseline times the float64 oracle on the host on a bounded sample.
@@ -164,16 +164,28 @@ def main():
         log(f"[bench] {s}: {res[s]['samples_per_s']:.0f} samples/s, {res[s]['ms_per_step']:.3f} ms/step, "
             f"enqueue {res[s]['host_enqueue_us']:.1f} us")
 
-    # per-launch kernel times (library events on each launch's own stream)
-    log(f"[bench] kernel timing: {args.timing_steps} overlap steps")
-    tr.set_timing(True)
-    recs_all = []
-    for i in range(args.timing_steps):
-        x, y = dev[i % len(dev)]
-        tr.step(x, y, "overlap", losses, wait_current=False)
-        tr.sync()
-        recs_all.append(tr.read_timing())
-    tr.set_timing(False)
+    # Per-launch kernel times from HIP events the library records around each
+    # launch on that launch's own stream: a SERIAL pass (each kernel alone on
+    # the device: the kernel table and the roofline) and an OVERLAP pass (the
+    # measured backward/forward overlap).
+    def timed(sched, n):
+        tr.set_timing(True)
+        out = []
+        for i in range(n):
+            x, y = dev[i % len(dev)]
+            tr.step(x, y, sched, losses, wait_current=False)
+            tr.sync()
+            out.append(tr.read_timing())
+        tr.set_timing(False)
+        return out
+
+    log(f"[bench] kernel timing: {args.timing_steps} serial + {args.timing_steps} overlap steps")
+    recs_all = timed("serial", args.timing_steps)
+    recs_ovl = timed("overlap", args.timing_steps)
+    # an empty event pair per step (reported only: kernel events are stamped by the kernel dispatch)
+    ev_cost_ms = float(np.median([r[0]["end_ms"] - r[0]["start_ms"] for r in recs_all]))
+    recs_all = [r[1:] for r in recs_all]
+    recs_ovl = [r[1:] for r in recs_ovl]
     classes = {}
     for recs in recs_all:
         for r in recs:
@@ -184,7 +196,7 @@ def main():
             c["flops"] += r["flops"]
             c["bytes"] += r["bytes"]
     nsteps = len(recs_all)
-    ovl = float(np.mean([overlap_fraction(r) for r in recs_all]))
+    ovl = float(np.mean([overlap_fraction(r) for r in recs_ovl]))
     dom_name, dom = max(classes.items(), key=lambda kv: kv[1]["ms"])
     gemm_ms = sum(c["ms"] for c in classes.values() if c["kind"].endswith("gemm"))
     gemm_flops = sum(c["flops"] for c in classes.values() if c["kind"].endswith("gemm"))
@@ -207,7 +219,9 @@ def main():
                    "gbs": v["bytes"] / (v["ms"] / 1e3) / 1e9}
                for k, v in sorted(classes.items(), key=lambda kv: -kv[1]["ms"])}
 
-    head = "overlap_graph" if "overlap_graph" in res else scheds[-1]
+    # headline: the faster of the two ERASE schedules (named in the config)
+    erase_scheds = [k for k in ("overlap", "overlap_graph") if k in res]
+    head = max(erase_scheds, key=lambda k: res[k]["samples_per_s"]) if erase_scheds else scheds[-1]
     out = {
         "metric": METRIC,
         "value": res[head]["samples_per_s"],
@@ -225,16 +239,22 @@ def main():
         "config": {"workload": f"{args.workload}: 6 detached blocks 1677->512->256->128 + Linear(128->1) BCE head, "
                                f"batch {M}, Adam" if args.workload == "ctr_mlp" else args.workload,
                    "global_batch": M, "blocks": len(cfg["blocks"]), "schedule": head, "parallelism": "single GPU"},
-        "speedup_vs_serial": {"overlap_vs_serial": res.get("overlap", {}).get("samples_per_s", 0) /
-                              res["serial"]["samples_per_s"] if "serial" in res else None,
-                              "overlap_graph_vs_serial_graph": res.get("overlap_graph", {}).get("samples_per_s", 0) /
-                              res["serial_graph"]["samples_per_s"] if "serial_graph" in res else None,
-                              "overlap_graph_vs_serial": res[head]["samples_per_s"] / res["serial"]["samples_per_s"]
-                              if "serial" in res else None},
+        "speedup_vs_serial": {
+            "overlap_vs_serial": (res["overlap"]["samples_per_s"] / res["serial"]["samples_per_s"]
+                                  if "overlap" in res and "serial" in res else None),
+            "overlap_graph_vs_serial_graph": (res["overlap_graph"]["samples_per_s"] /
+                                              res["serial_graph"]["samples_per_s"]
+                                              if "overlap_graph" in res and "serial_graph" in res else None),
+            "headline_vs_best_serial": (res[head]["samples_per_s"] /
+                                        max(res[k]["samples_per_s"] for k in ("serial", "serial_graph") if k in res)
+                                        if any(k in res for k in ("serial", "serial_graph")) else None)},
         "schedules": res,
         "mfma_util": {"gemm_kernels": gemm_flops / (gemm_ms / 1e3) / 1e12 / peak_mfma if gemm_ms else None,
                       "whole_step": flops_step / (res[head]["ms_per_step"] / 1e3) / 1e12 / peak_mfma},
         "bwd_fwd_overlap_fraction": ovl,
+        "kernel_timing": "per-kernel figures from a SERIAL pass (kernels alone), HIP events stamped at each "
+                         "kernel's own start and end; overlap fraction from an OVERLAP pass",
+        "event_pair_cost_us": ev_cost_ms * 1e3,
         "roofline": roof,
         "kernels": kernels,
     }

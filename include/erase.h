@@ -171,14 +171,16 @@ erase_status erase_set_step(void* ctx, int64_t t);
 erase_status erase_refresh_weights(void* ctx);
 
 /* Per-launch kernel timing, for measurement.  When enabled, non-graph
- * schedules bracket every kernel launch with timing events (graph schedules
- * return ERASE_ERR_UNSUPPORTED while enabled).  erase_read_timing() fills up
- * to `cap` records of the last completed step (call after erase_sync()) and
- * sets *n to the number of launches of that step. */
+ * schedules bracket every kernel launch with timing events on the launch's
+ * own stream (graph schedules return ERASE_ERR_UNSUPPORTED while enabled).
+ * erase_read_timing() fills up to `cap` records of the last completed step
+ * (call after erase_sync()) and sets *n to the number of records: record 0
+ * is an empty event pair on the forward stream (kind 7; its length is the
+ * cost of the timing itself), then one record per launch in enqueue order. */
 typedef struct {
   int32_t kind;      /* 0 prologue, 1 forward GEMM, 2 head+loss, 3 weight-grad GEMM,
                         4 input-grad GEMM, 5 Adam, 6 input- and weight-grad GEMMs of one
-                        layer in one launch */
+                        layer in one launch, 7 empty interval (no kernel) */
   int32_t block;     /* block index, -1 for the step prologue */
   int32_t layer;     /* layer index within the block, -1 if none */
   int32_t stream;    /* 0 forward stream, 1 backward stream */

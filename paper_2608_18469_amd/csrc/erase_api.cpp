@@ -369,6 +369,7 @@ struct Ctx {
   bool timing = false;
   std::vector<hipEvent_t> tev;  // timing events pool
   hipEvent_t tstart = nullptr;
+  hipEvent_t tnull0 = nullptr, tnull1 = nullptr;  // empty interval: event overhead
   std::vector<TimedLaunch> last;
   bool last_valid = false;
 };
@@ -411,6 +412,7 @@ class Enqueuer {
   template <class F>
   erase_status run(int kind, int blk, int layer, int stream_id, hipStream_t s, Cost cost, F&& fn) {
     TimedLaunch tl{};
+    LaunchEv lev;
     if (timed_) {
       if (ev_ + 2 > c_->tev.size()) {
         c_->err = "timing event pool exhausted";
@@ -418,12 +420,13 @@ class Enqueuer {
       }
       tl.e0 = c_->tev[ev_++];
       tl.e1 = c_->tev[ev_++];
-      HIPCHK(c_, hipEventRecord(tl.e0, s));
+      lev.e0 = tl.e0;  // stamped at the kernel's own start and end
+      lev.e1 = tl.e1;
     }
-    hipError_t e = fn();
+    (void)s;
+    hipError_t e = fn(lev);
     if (!hip_ok(c_, e, "kernel launch")) return ERASE_ERR_HIP;
     if (timed_) {
-      HIPCHK(c_, hipEventRecord(tl.e1, s));
       tl.rec.kind = kind;
       tl.rec.block = blk;
       tl.rec.layer = layer;
@@ -523,7 +526,7 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
     cost.bytes = double(esz) * (double(M) * R.K + double(R.N) * R.K + double(M) * R.N * (R.yt ? 2 : 1)) + 4.0 * R.N +
                  (kind == GK_FWD_CROSS ? 2.0 * esz * M * R.N : 0.0);
     const int bf = P.bf16;
-    RUN(1, b, l, sid, s, cost, [&]() { return launch_gemm(bf, kind, g, e, s); });
+    RUN(1, b, l, sid, s, cost, [&](const LaunchEv& ev) { return launch_gemm(bf, kind, g, e, s, ev); });
   }
   const LayerRT& Rl = B.layer[B.L - 1];
   HeadArgs h{};
@@ -548,7 +551,7 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
   cost.flops = 4.0 * M * Rl.N;
   cost.bytes = double(esz) * M * Rl.N * (1 + 1 + (Rl.dmn ? 1 : 0)) + 4.0 * M + 4.0 * Rl.N + 4.0 * B.nhead * (Rl.N + 2);
   const int bf = P.bf16;
-  RUN(2, b, -1, sid, s, cost, [&]() { return launch_head(bf, h, s); });
+  RUN(2, b, -1, sid, s, cost, [&](const LaunchEv& ev) { return launch_head(bf, h, s, ev); });
   return ERASE_OK;
 }
 
@@ -594,7 +597,7 @@ erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStre
     cw.flops = 2.0 * M * R.N * R.K;
     cw.bytes = double(esz) * M * (double(R.N) + R.K) + 4.0 * R.wgrad.split * (double(R.N) * R.K + R.N);
     if (l == 0) {
-      RUN(3, b, l, sid, s, cw, [&]() { return launch_gemm(bf, GK_WGRAD, gw, ew, s); });
+      RUN(3, b, l, sid, s, cw, [&](const LaunchEv& ev) { return launch_gemm(bf, GK_WGRAD, gw, ew, s, ev); });
       break;
     }
     const LayerRT& Rb = B.layer[l - 1];
@@ -641,10 +644,10 @@ erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStre
       cg.bytes += cw.bytes;
       cg.grid += cw.grid;
       cg.split = cw.split;
-      RUN(6, b, l, sid, s, cg, [&]() { return launch_bwd_gemm(bf, gd, ed, gw, ew, s); });
+      RUN(6, b, l, sid, s, cg, [&](const LaunchEv& ev) { return launch_bwd_gemm(bf, gd, ed, gw, ew, s, ev); });
     } else {
-      RUN(3, b, l, sid, s, cw, [&]() { return launch_gemm(bf, GK_WGRAD, gw, ew, s); });
-      RUN(4, b, l, sid, s, cd, [&]() { return launch_gemm(bf, GK_DGRAD, gd, ed, s); });
+      RUN(3, b, l, sid, s, cw, [&](const LaunchEv& ev) { return launch_gemm(bf, GK_WGRAD, gw, ew, s, ev); });
+      RUN(4, b, l, sid, s, cd, [&](const LaunchEv& ev) { return launch_gemm(bf, GK_DGRAD, gd, ed, s, ev); });
     }
   }
   return ERASE_OK;
@@ -675,7 +678,7 @@ erase_status enqueue_adam(Ctx* c, Enqueuer& q, int b, float* losses, hipStream_t
     cost.bytes += n * (4.0 * sg.nsplit + 24.0 + (sg.g ? 4.0 : 0.0) + (sg.sh ? P.esz : 0) + (sg.sht ? P.esz : 0));
   }
   const int bf = P.bf16;
-  RUN(5, b, -1, sid, s, cost, [&]() { return launch_adam(bf, a, s); });
+  RUN(5, b, -1, sid, s, cost, [&](const LaunchEv& ev) { return launch_adam(bf, a, s, ev); });
   return ERASE_OK;
 }
 
@@ -703,7 +706,7 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
     Cost cost;
     cost.bytes = P.xt ? 3.0 * P.esz * double(P.M) * c->cfg.in_dim : 0.0;
     const int bf = P.bf16;
-    RUN(0, -1, -1, 0, sf, cost, [&]() { return launch_prologue(bf, pa, sf); });
+    RUN(0, -1, -1, 0, sf, cost, [&](const LaunchEv& ev) { return launch_prologue(bf, pa, sf, ev); });
   }
   if (overlap) {
     for (int b = 0; b < nb; ++b) {
@@ -880,7 +883,11 @@ erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t s
   }
   if (!graph) {
     Enqueuer q(c, c->timing);
-    if (c->timing) HIPCHK(c, hipEventRecord(c->tstart, c->sf));
+    if (c->timing) {
+      HIPCHK(c, hipEventRecord(c->tstart, c->sf));
+      HIPCHK(c, hipEventRecord(c->tnull0, c->sf));
+      HIPCHK(c, hipEventRecord(c->tnull1, c->sf));
+    }
     erase_status st = enqueue_step(c, q, x, labels, schedule, losses);
     if (st != ERASE_OK) {
       c->sticky = st == ERASE_ERR_HIP ? st : c->sticky;
@@ -980,6 +987,8 @@ erase_status erase_set_timing(void* ctx, int32_t enable) {
       c->tev.push_back(e);
     }
     HIPCHK(c, hipEventCreate(&c->tstart));
+    HIPCHK(c, hipEventCreate(&c->tnull0));
+    HIPCHK(c, hipEventCreate(&c->tnull1));
   }
   c->timing = enable != 0;
   c->last_valid = false;
@@ -990,15 +999,27 @@ erase_status erase_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, i
   Ctx* c = as_ctx(ctx);
   if (!c || !n || (cap > 0 && !out)) return ERASE_ERR_INVALID_ARG;
   if (!c->last_valid) return ERASE_ERR_STATE;
-  *n = (int32_t)c->last.size();
-  for (int i = 0; i < (int)c->last.size() && i < cap; ++i) {
+  *n = (int32_t)c->last.size() + 1;
+  if (cap > 0) {  // record 0: the empty interval (kind 7), i.e. the cost of an event pair
+    float a = 0.f, b = 0.f;
+    HIPCHK(c, hipEventElapsedTime(&a, c->tstart, c->tnull0));
+    HIPCHK(c, hipEventElapsedTime(&b, c->tstart, c->tnull1));
+    erase_kernel_time r{};
+    r.kind = 7;
+    r.block = -1;
+    r.layer = -1;
+    r.start_ms = a;
+    r.end_ms = b;
+    out[0] = r;
+  }
+  for (int i = 0; i < (int)c->last.size() && i + 1 < cap; ++i) {
     TimedLaunch& t = c->last[i];
     float a = 0.f, b = 0.f;
     HIPCHK(c, hipEventElapsedTime(&a, c->tstart, t.e0));
     HIPCHK(c, hipEventElapsedTime(&b, c->tstart, t.e1));
-    out[i] = t.rec;
-    out[i].start_ms = a;
-    out[i].end_ms = b;
+    out[i + 1] = t.rec;
+    out[i + 1].start_ms = a;
+    out[i + 1].end_ms = b;
   }
   return ERASE_OK;
 }
@@ -1013,6 +1034,8 @@ erase_status erase_destroy(void* ctx) {
   for (hipEvent_t e : c->eb) (void)hipEventDestroy(e);
   for (hipEvent_t e : c->tev) (void)hipEventDestroy(e);
   if (c->tstart) (void)hipEventDestroy(c->tstart);
+  if (c->tnull0) (void)hipEventDestroy(c->tnull0);
+  if (c->tnull1) (void)hipEventDestroy(c->tnull1);
   delete c;
   return ERASE_OK;
 }

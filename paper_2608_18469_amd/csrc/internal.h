@@ -30,6 +30,13 @@ struct GemmDesc {
 
 enum GemmKind { GK_FWD_RELU = 0, GK_FWD_CROSS = 1, GK_WGRAD = 2, GK_DGRAD = 3 };
 
+// Optional timing events of one launch: when set, the kernel is dispatched
+// with hipExtLaunchKernelGGL, which stamps e0/e1 at the kernel's own start
+// and end on the device.
+struct LaunchEv {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+};
+
 // Epilogue operands.  Which fields are read depends on the GemmKind.
 struct EpiParams {
   // forward: y = relu(acc + bias) or x0 * (acc + bias) + xl
@@ -50,11 +57,12 @@ struct EpiParams {
   int below_cross;
 };
 
-hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s);
+hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s,
+                       const LaunchEv& ev = {});
 // Input-gradient (gd, split 1) and weight-gradient (gw) GEMMs of one layer in
 // one launch; both must use the same tile, 64x64 or 128x128.
 hipError_t launch_bwd_gemm(int bf16, const GemmDesc& gd, const EpiParams& ed, const GemmDesc& gw, const EpiParams& ew,
-                           hipStream_t s);
+                           hipStream_t s, const LaunchEv& ev = {});
 
 // Step prologue: t += 1, the zero-padded copy xp[m][k] = x[m][k] and the
 // feature-major copy xt[k][m] = x[m][k] (padding of both stays zero).
@@ -70,7 +78,7 @@ struct PrologueArgs {
   void* xt; int64_t ldxt;
   int M, K;
 };
-hipError_t launch_prologue(int bf16, const PrologueArgs& a, hipStream_t s);
+hipError_t launch_prologue(int bf16, const PrologueArgs& a, hipStream_t s, const LaunchEv& ev = {});
 
 // Fused local head + sigmoid-BCE + gradient at z (one workgroup per 64 rows).
 struct HeadArgs {
@@ -99,7 +107,7 @@ __host__ __device__ inline int head_rows(int N, int esz) {
   return r;
 }
 inline size_t head_lds_bytes(int N, int esz) { return (size_t)head_rows(N, esz) * head_pitch(N, esz) * esz; }
-hipError_t launch_head(int bf16, const HeadArgs& a, hipStream_t s);
+hipError_t launch_head(int bf16, const HeadArgs& a, hipStream_t s, const LaunchEv& ev = {});
 
 // Fused split-reduction + Adam + GEMM-copy refresh for one block.  The
 // segment table lives in device memory (written once at init).
@@ -125,7 +133,7 @@ struct AdamArgs {
   int* status;
 };
 constexpr int ADAM_CHUNK = 1024;
-hipError_t launch_adam(int bf16, const AdamArgs& a, hipStream_t s);
+hipError_t launch_adam(int bf16, const AdamArgs& a, hipStream_t s, const LaunchEv& ev = {});
 
 // Weight copies only (init / refresh): same segments, no update.
 hipError_t launch_refresh(int bf16, const AdamArgs& a, hipStream_t s);

@@ -22,6 +22,7 @@
 //
 // No float atomics anywhere: every reduction has a fixed order, so every
 // schedule of the same step produces bit-identical results.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
@@ -29,6 +30,14 @@
 #include "internal.h"
 
 namespace erase {
+
+#define ERASE_LAUNCH(KERNEL, GRID, BLOCK, SHMEM, STREAM, EV, ...)                                   \
+  do {                                                                                             \
+    if ((EV).e0)                                                                                   \
+      hipExtLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, (EV).e0, (EV).e1, 0, __VA_ARGS__); \
+    else                                                                                           \
+      hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, __VA_ARGS__);                        \
+  } while (0)
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
@@ -67,6 +76,13 @@ __device__ __forceinline__ void st4(uint16_t* p, const uint16_t v[4]) {
 }
 __device__ __forceinline__ void st4(float* p, const float v[4]) {
   *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+}
+
+// Pointers read from device memory (not kernel arguments) are generic to the
+// compiler; this marks them global so loads and stores use the global path.
+template <typename T>
+__device__ __forceinline__ __attribute__((address_space(1))) T* gmem(T* p) {
+  return (__attribute__((address_space(1))) T*)p;
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
@@ -385,13 +401,13 @@ __global__ __launch_bounds__(256) void erase_bwd_gemm(GemmDesc gd, EpiParams ed,
 }
 
 template <typename T, int BM, int BN>
-static hipError_t launch_gemm_t(int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s) {
+static hipError_t launch_gemm_t(int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s, const LaunchEv& ev) {
   dim3 grid((g.M + BM - 1) / BM, (g.N + BN - 1) / BN, g.split), block(256);
   switch (kind) {
-    case GK_FWD_RELU: hipLaunchKernelGGL((erase_fwd_gemm<T, BM, BN>), grid, block, 0, s, g, e); break;
-    case GK_FWD_CROSS: hipLaunchKernelGGL((erase_fwd_cross_gemm<T, BM, BN>), grid, block, 0, s, g, e); break;
-    case GK_WGRAD: hipLaunchKernelGGL((erase_wgrad_gemm<T, BM, BN>), grid, block, 0, s, g, e); break;
-    case GK_DGRAD: hipLaunchKernelGGL((erase_dgrad_gemm<T, BM, BN>), grid, block, 0, s, g, e); break;
+    case GK_FWD_RELU: ERASE_LAUNCH((erase_fwd_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;
+    case GK_FWD_CROSS: ERASE_LAUNCH((erase_fwd_cross_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;
+    case GK_WGRAD: ERASE_LAUNCH((erase_wgrad_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;
+    case GK_DGRAD: ERASE_LAUNCH((erase_dgrad_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -399,34 +415,34 @@ static hipError_t launch_gemm_t(int kind, const GemmDesc& g, const EpiParams& e,
 
 template <typename T, int BM, int BN>
 static hipError_t launch_bwd_t(const GemmDesc& gd, const EpiParams& ed, const GemmDesc& gw, const EpiParams& ew,
-                               hipStream_t s) {
+                               hipStream_t s, const LaunchEv& ev) {
   const int nd = ((gd.M + BM - 1) / BM) * ((gd.N + BN - 1) / BN);
   const int nw = ((gw.M + BM - 1) / BM) * ((gw.N + BN - 1) / BN) * gw.split;
-  hipLaunchKernelGGL((erase_bwd_gemm<T, BM, BN>), dim3(nd + nw), dim3(256), 0, s, gd, ed, gw, ew, nd);
+  ERASE_LAUNCH((erase_bwd_gemm<T, BM, BN>), dim3(nd + nw), dim3(256), 0, s, ev, gd, ed, gw, ew, nd);
   return hipGetLastError();
 }
 
 hipError_t launch_bwd_gemm(int bf16, const GemmDesc& gd, const EpiParams& ed, const GemmDesc& gw, const EpiParams& ew,
-                           hipStream_t s) {
+                           hipStream_t s, const LaunchEv& ev) {
   if (gd.bm != gw.bm || gd.bn != gw.bn || gd.split != 1 || gw.split <= 0) return hipErrorInvalidValue;
   if (bf16) {
-    if (gd.bm == 128 && gd.bn == 128) return launch_bwd_t<uint16_t, 128, 128>(gd, ed, gw, ew, s);
-    if (gd.bm == 64 && gd.bn == 64) return launch_bwd_t<uint16_t, 64, 64>(gd, ed, gw, ew, s);
+    if (gd.bm == 128 && gd.bn == 128) return launch_bwd_t<uint16_t, 128, 128>(gd, ed, gw, ew, s, ev);
+    if (gd.bm == 64 && gd.bn == 64) return launch_bwd_t<uint16_t, 64, 64>(gd, ed, gw, ew, s, ev);
   } else {
-    if (gd.bm == 64 && gd.bn == 64) return launch_bwd_t<float, 64, 64>(gd, ed, gw, ew, s);
+    if (gd.bm == 64 && gd.bn == 64) return launch_bwd_t<float, 64, 64>(gd, ed, gw, ew, s, ev);
   }
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s) {
+hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s, const LaunchEv& ev) {
   if (g.M <= 0 || g.N <= 0 || g.split <= 0) return hipErrorInvalidValue;
   if (bf16) {
-    if (g.bm == 128 && g.bn == 128) return launch_gemm_t<uint16_t, 128, 128>(kind, g, e, s);
-    if (g.bm == 128 && g.bn == 64) return launch_gemm_t<uint16_t, 128, 64>(kind, g, e, s);
-    if (g.bm == 64 && g.bn == 128) return launch_gemm_t<uint16_t, 64, 128>(kind, g, e, s);
-    if (g.bm == 64 && g.bn == 64) return launch_gemm_t<uint16_t, 64, 64>(kind, g, e, s);
+    if (g.bm == 128 && g.bn == 128) return launch_gemm_t<uint16_t, 128, 128>(kind, g, e, s, ev);
+    if (g.bm == 128 && g.bn == 64) return launch_gemm_t<uint16_t, 128, 64>(kind, g, e, s, ev);
+    if (g.bm == 64 && g.bn == 128) return launch_gemm_t<uint16_t, 64, 128>(kind, g, e, s, ev);
+    if (g.bm == 64 && g.bn == 64) return launch_gemm_t<uint16_t, 64, 64>(kind, g, e, s, ev);
   } else {
-    if (g.bm == 64 && g.bn == 64) return launch_gemm_t<float, 64, 64>(kind, g, e, s);
+    if (g.bm == 64 && g.bn == 64) return launch_gemm_t<float, 64, 64>(kind, g, e, s, ev);
   }
   return hipErrorInvalidValue;
 }
@@ -490,12 +506,12 @@ __global__ __launch_bounds__(256) void erase_prologue(PrologueArgs a) {
   }
 }
 
-hipError_t launch_prologue(int bf16, const PrologueArgs& a, hipStream_t s) {
+hipError_t launch_prologue(int bf16, const PrologueArgs& a, hipStream_t s, const LaunchEv& ev) {
   dim3 grid(a.xp ? (a.K + 63) / 64 : 1, a.xp ? (a.M + 63) / 64 : 1), block(256);
   if (bf16)
-    hipLaunchKernelGGL(erase_prologue<uint16_t>, grid, block, 0, s, a);
+    ERASE_LAUNCH(erase_prologue<uint16_t>, grid, block, 0, s, ev, a);
   else
-    hipLaunchKernelGGL(erase_prologue<float>, grid, block, 0, s, a);
+    ERASE_LAUNCH(erase_prologue<float>, grid, block, 0, s, ev, a);
   return hipGetLastError();
 }
 
@@ -630,14 +646,14 @@ __global__ __launch_bounds__(256) void erase_head_bce(HeadArgs a) {
   }
 }
 
-hipError_t launch_head(int bf16, const HeadArgs& a, hipStream_t s) {
+hipError_t launch_head(int bf16, const HeadArgs& a, hipStream_t s, const LaunchEv& ev) {
   const int esz = bf16 ? 2 : 4;
   dim3 grid((a.M + head_rows(a.N, esz) - 1) / head_rows(a.N, esz)), block(256);
   const size_t lds = head_lds_bytes(a.N, esz);
   if (bf16)
-    hipLaunchKernelGGL(erase_head_bce<uint16_t>, grid, block, lds, s, a);
+    ERASE_LAUNCH(erase_head_bce<uint16_t>, grid, block, (uint32_t)lds, s, ev, a);
   else
-    hipLaunchKernelGGL(erase_head_bce<float>, grid, block, lds, s, a);
+    ERASE_LAUNCH(erase_head_bce<float>, grid, block, (uint32_t)lds, s, ev, a);
   return hipGetLastError();
 }
 
@@ -663,35 +679,39 @@ __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
   const float b1 = a.beta1, b2 = a.beta2;
   const int n = sg.rows * sg.cols;
   const int base = (int)((chunk - sg.chunk0) * ADAM_CHUNK);
-  T* SH = static_cast<T*>(sg.sh);
-  T* SHT = static_cast<T*>(sg.sht);
+  auto P = gmem(sg.p);
+  auto Mo = gmem(sg.m);
+  auto V = gmem(sg.v);
+  auto PART = gmem(sg.part);
 
   int idx[PER], row[PER], col[PER];
   bool ok[PER];
-  const float* pp[PER];
+  int64_t po[PER];
   float g[PER], pv[PER], mv[PER], vv[PER];
 #pragma unroll
   for (int q = 0; q < PER; ++q) {
     idx[q] = base + q * 256 + (int)threadIdx.x;
     ok[q] = idx[q] < n;
-    const int i = ok[q] ? idx[q] : 0;
+    const int i = ok[q] ? idx[q] : base;  // clamped: always a valid element
+    idx[q] = i;
     row[q] = i / sg.cols;
     col[q] = i - row[q] * sg.cols;
-    pp[q] = sg.part + (int64_t)row[q] * sg.ldpart + col[q];
+    po[q] = (int64_t)row[q] * sg.ldpart + col[q];
     g[q] = 0.f;
     // state loads first: independent of the reduction, one memory round trip
-    pv[q] = ok[q] ? sg.p[i] : 0.f;
-    mv[q] = ok[q] ? sg.m[i] : 0.f;
-    vv[q] = ok[q] ? sg.v[i] : 0.f;
+    pv[q] = P[i];
+    mv[q] = Mo[i];
+    vv[q] = V[i];
   }
   // ordered reduction of the split partials: slice 0, 1, ..., nsplit-1
   for (int z0 = 0; z0 < sg.nsplit; z0 += ZB) {
     float tv[PER][ZB];
 #pragma unroll
-    for (int q = 0; q < PER; ++q)
+    for (int j = 0; j < ZB; ++j) {
+      const int64_t zo = (int64_t)min(z0 + j, sg.nsplit - 1) * sg.pstride;
 #pragma unroll
-      for (int j = 0; j < ZB; ++j)
-        tv[q][j] = (ok[q] && z0 + j < sg.nsplit) ? pp[q][(int64_t)(z0 + j) * sg.pstride] : 0.f;
+      for (int q = 0; q < PER; ++q) tv[q][j] = PART[po[q] + zo];
+    }
 #pragma unroll
     for (int q = 0; q < PER; ++q)
 #pragma unroll
@@ -705,12 +725,12 @@ __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
     const float m = fmaf(b1, mv[q], (1.f - b1) * g[q]);
     const float v = fmaf(b2, vv[q], (1.f - b2) * g[q] * g[q]);
     const float p = pv[q] - step * m / (sqrtf(v) / bc2s + a.eps);
-    if (sg.g) sg.g[i] = g[q];
-    sg.m[i] = m;
-    sg.v[i] = v;
-    sg.p[i] = p;
-    if (SH) SH[(int64_t)row[q] * sg.ldsh + col[q]] = cvt<T>(p);
-    if (SHT) SHT[(int64_t)col[q] * sg.ldsht + row[q]] = cvt<T>(p);
+    if (sg.g) gmem(sg.g)[i] = g[q];
+    Mo[i] = m;
+    V[i] = v;
+    P[i] = p;
+    if (sg.sh) gmem(static_cast<T*>(sg.sh))[(int64_t)row[q] * sg.ldsh + col[q]] = cvt<T>(p);
+    if (sg.sht) gmem(static_cast<T*>(sg.sht))[(int64_t)col[q] * sg.ldsht + row[q]] = cvt<T>(p);
   }
   if (chunk == 0 && threadIdx.x == 0 && a.ploss) {
     float L = 0.f;
@@ -733,18 +753,18 @@ __global__ __launch_bounds__(256) void erase_refresh(AdamArgs a) {
     const int i = base + q * 256 + (int)threadIdx.x;
     if (i >= n) break;
     const int r = i / sg.cols, c = i - r * sg.cols;
-    const float p = sg.p[i];
-    if (SH) SH[(int64_t)r * sg.ldsh + c] = cvt<T>(p);
-    if (SHT) SHT[(int64_t)c * sg.ldsht + r] = cvt<T>(p);
+    const float p = gmem(sg.p)[i];
+    if (SH) gmem(SH)[(int64_t)r * sg.ldsh + c] = cvt<T>(p);
+    if (SHT) gmem(SHT)[(int64_t)c * sg.ldsht + r] = cvt<T>(p);
   }
 }
 
-hipError_t launch_adam(int bf16, const AdamArgs& a, hipStream_t s) {
+hipError_t launch_adam(int bf16, const AdamArgs& a, hipStream_t s, const LaunchEv& ev) {
   dim3 grid((unsigned)a.nchunks), block(256);
   if (bf16)
-    hipLaunchKernelGGL(erase_adam<uint16_t>, grid, block, 0, s, a);
+    ERASE_LAUNCH(erase_adam<uint16_t>, grid, block, 0, s, ev, a);
   else
-    hipLaunchKernelGGL(erase_adam<float>, grid, block, 0, s, a);
+    ERASE_LAUNCH(erase_adam<float>, grid, block, 0, s, ev, a);
   return hipGetLastError();
 }
 

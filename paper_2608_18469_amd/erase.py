@@ -26,7 +26,7 @@ IN_X, IN_PREV = 0, 1
 SERIAL, OVERLAP, SERIAL_GRAPH, OVERLAP_GRAPH = 0, 1, 2, 3
 SCHEDULES = {"serial": SERIAL, "overlap": OVERLAP, "serial_graph": SERIAL_GRAPH, "overlap_graph": OVERLAP_GRAPH}
 KERNEL_KINDS = {0: "prologue", 1: "fwd_gemm", 2: "head_bce", 3: "wgrad_gemm", 4: "dgrad_gemm", 5: "adam",
-                6: "bwd_gemm"}
+                6: "bwd_gemm", 7: "empty"}
 
 
 class LayerSpec(ctypes.Structure):
