@@ -107,6 +107,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--schedules", default="serial,overlap,serial_graph,overlap_graph")
     ap.add_argument("--verbose", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after the run, copy a buffer of this many MiB once (a plain copy kernel of known size "
+                         "for scaling hardware byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -262,6 +265,14 @@ def main():
         log(f"[bench] cpu baseline: oracle for ~{args.cpu_budget:.0f} s")
         out["cpu_baseline"] = cpu_baseline(cfg, params, batches, args.cpu_budget)
     tr.close()
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["calib_copy_bytes"] = 2 * n * 4
     print(json.dumps(out), flush=True)
 
 

@@ -321,7 +321,8 @@ void build_segments(Plan* P, const erase_block_buffers* bufs) {
       s.sht = sht;
       s.ldsht = ldsht;
       s.chunk0 = chunk;
-      chunk += cdiv(int64_t(rows) * cols, ADAM_CHUNK);
+      s.tcols = (int)cdiv(cols, ADAM_TC);
+      chunk += cdiv(rows, ADAM_TR) * s.tcols;
       B.segs.push_back(s);
     };
     for (int l = 0; l < B.L; ++l) {

@@ -110,7 +110,10 @@ inline size_t head_lds_bytes(int N, int esz) { return (size_t)head_rows(N, esz) 
 hipError_t launch_head(int bf16, const HeadArgs& a, hipStream_t s, const LaunchEv& ev = {});
 
 // Fused split-reduction + Adam + GEMM-copy refresh for one block.  The
-// segment table lives in device memory (written once at init).
+// segment table lives in device memory (written once at init).  A segment
+// is a [rows][cols] parameter matrix (a vector is one row) processed in
+// tiles of ADAM_TR rows x ADAM_TC columns, one workgroup per tile.
+constexpr int ADAM_TR = 8, ADAM_TC = 256;
 struct AdamSeg {
   float* p; float* m; float* v; float* g;   // flat [rows*cols] fp32 (g nullable)
   const float* part;                        // partial sums [nsplit][rows][ldpart]
@@ -118,7 +121,8 @@ struct AdamSeg {
   int rows, cols, ldpart, nsplit;
   void* sh;  int64_t ldsh;                  // GEMM copy [rows][ldsh], nullable
   void* sht; int64_t ldsht;                 // transposed GEMM copy [cols][ldsht], nullable
-  int64_t chunk0;                           // first chunk index of this segment
+  int64_t chunk0;                           // first tile index of this segment
+  int tcols;                                // tiles per row of tiles: ceil(cols / ADAM_TC)
 };
 constexpr int ADAM_MAX_SEG = 34;  // 16 layers x (W, b) + head (w, c)
 struct AdamArgs {
@@ -132,7 +136,6 @@ struct AdamArgs {
   float* loss_out;
   int* status;
 };
-constexpr int ADAM_CHUNK = 1024;
 hipError_t launch_adam(int bf16, const AdamArgs& a, hipStream_t s, const LaunchEv& ev = {});
 
 // Weight copies only (init / refresh): same segments, no update.

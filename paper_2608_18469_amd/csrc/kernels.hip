@@ -658,9 +658,9 @@ hipError_t launch_head(int bf16, const HeadArgs& a, hipStream_t s, const LaunchE
 }
 
 // ---------------------------------------------------------------------------
-// Adam over all parameter segments of one block (ADAM_CHUNK elements per
-// workgroup), with the ordered reduction of split partials fused in front
-// and the GEMM copies of the updated weights written behind.
+// Adam over all parameter segments of one block (one ADAM_TR x ADAM_TC tile
+// per workgroup), with the ordered reduction of split partials fused in
+// front and the GEMM copies of the updated weights written behind.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int find_seg(const AdamArgs& a, int64_t chunk) {
   int s = 0;
@@ -668,76 +668,113 @@ __device__ __forceinline__ int find_seg(const AdamArgs& a, int64_t chunk) {
   return s;
 }
 
+// Thread = one column of an ADAM_TR-row tile: rows are read and written
+// coalesced across the workgroup, and the transposed GEMM copy gets the
+// tile's ADAM_TR consecutive values of one column as 16-byte stores.
 template <typename T>
 __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
-  constexpr int PER = ADAM_CHUNK / 256;  // elements per thread, 256 apart
-  constexpr int ZB = 8;                  // partial loads issued together per element
+  constexpr int TR = ADAM_TR;
   const int64_t chunk = blockIdx.x;
   const AdamSeg sg = a.seg[find_seg(a, chunk)];
   const float step = a.hyper[0];  // lr / (1 - beta1^t)
   const float bc2s = a.hyper[1];  // sqrt(1 - beta2^t)
   const float b1 = a.beta1, b2 = a.beta2;
-  const int n = sg.rows * sg.cols;
-  const int base = (int)((chunk - sg.chunk0) * ADAM_CHUNK);
+  const int tile = (int)(chunk - sg.chunk0);
+  const int r0 = (tile / sg.tcols) * TR;
+  const int c = (tile % sg.tcols) * ADAM_TC + (int)threadIdx.x;
+  const bool colok = c < sg.cols;
+  const int cc = colok ? c : 0;  // clamped: loads stay in bounds
   auto P = gmem(sg.p);
   auto Mo = gmem(sg.m);
   auto V = gmem(sg.v);
   auto PART = gmem(sg.part);
 
-  int idx[PER], row[PER], col[PER];
-  bool ok[PER];
-  int64_t po[PER];
-  float g[PER], pv[PER], mv[PER], vv[PER];
+  bool ok[TR];
+  int64_t fi[TR], po[TR];
+  float g[TR], pv[TR], mv[TR], vv[TR];
 #pragma unroll
-  for (int q = 0; q < PER; ++q) {
-    idx[q] = base + q * 256 + (int)threadIdx.x;
-    ok[q] = idx[q] < n;
-    const int i = ok[q] ? idx[q] : base;  // clamped: always a valid element
-    idx[q] = i;
-    row[q] = i / sg.cols;
-    col[q] = i - row[q] * sg.cols;
-    po[q] = (int64_t)row[q] * sg.ldpart + col[q];
+  for (int q = 0; q < TR; ++q) {
+    const int r = r0 + q;
+    ok[q] = colok && r < sg.rows;
+    const int rr = r < sg.rows ? r : 0;
+    fi[q] = (int64_t)rr * sg.cols + cc;
+    po[q] = (int64_t)rr * sg.ldpart + cc;
     g[q] = 0.f;
-    // state loads first: independent of the reduction, one memory round trip
-    pv[q] = P[i];
-    mv[q] = Mo[i];
-    vv[q] = V[i];
+    pv[q] = P[fi[q]];
+    mv[q] = Mo[fi[q]];
+    vv[q] = V[fi[q]];
   }
   // ordered reduction of the split partials: slice 0, 1, ..., nsplit-1
-  for (int z0 = 0; z0 < sg.nsplit; z0 += ZB) {
-    float tv[PER][ZB];
+  if (sg.rows == 1) {
+    // a vector (bias or head parameter): one element per thread, possibly
+    // many partials (one per head workgroup): 32 loads in flight per batch
+    constexpr int ZV = 32;
+    for (int z0 = 0; z0 < sg.nsplit; z0 += ZV) {
+      float tv[ZV];
 #pragma unroll
-    for (int j = 0; j < ZB; ++j) {
-      const int64_t zo = (int64_t)min(z0 + j, sg.nsplit - 1) * sg.pstride;
+      for (int j = 0; j < ZV; ++j) tv[j] = (z0 + j < sg.nsplit) ? PART[po[0] + (int64_t)(z0 + j) * sg.pstride] : 0.f;
 #pragma unroll
-      for (int q = 0; q < PER; ++q) tv[q][j] = PART[po[q] + zo];
+      for (int j = 0; j < ZV; ++j)
+        if (z0 + j < sg.nsplit) g[0] += tv[j];
     }
+  } else {
+    // slice-outer, four slices in flight: TR*4 independent loads, added in
+    // slice order
+    constexpr int ZS = 4;
+    for (int z0 = 0; z0 < sg.nsplit; z0 += ZS) {
+      float tv[ZS][TR];
 #pragma unroll
-    for (int q = 0; q < PER; ++q)
+      for (int j = 0; j < ZS; ++j) {
+        const int64_t zo = (int64_t)min(z0 + j, sg.nsplit - 1) * sg.pstride;
 #pragma unroll
-      for (int j = 0; j < ZB; ++j)
-        if (z0 + j < sg.nsplit) g[q] += tv[q][j];
+        for (int q = 0; q < TR; ++q) tv[j][q] = PART[zo + po[q]];
+      }
+#pragma unroll
+      for (int j = 0; j < ZS; ++j)
+        if (z0 + j < sg.nsplit) {
+#pragma unroll
+          for (int q = 0; q < TR; ++q) g[q] += tv[j][q];
+        }
+    }
   }
+  T o[TR];
 #pragma unroll
-  for (int q = 0; q < PER; ++q) {
-    if (!ok[q]) continue;
-    const int i = idx[q];
+  for (int q = 0; q < TR; ++q) {
     const float m = fmaf(b1, mv[q], (1.f - b1) * g[q]);
     const float v = fmaf(b2, vv[q], (1.f - b2) * g[q] * g[q]);
     const float p = pv[q] - step * m / (sqrtf(v) / bc2s + a.eps);
-    if (sg.g) gmem(sg.g)[i] = g[q];
-    Mo[i] = m;
-    V[i] = v;
-    P[i] = p;
-    if (sg.sh) gmem(static_cast<T*>(sg.sh))[(int64_t)row[q] * sg.ldsh + col[q]] = cvt<T>(p);
-    if (sg.sht) gmem(static_cast<T*>(sg.sht))[(int64_t)col[q] * sg.ldsht + row[q]] = cvt<T>(p);
+    o[q] = cvt<T>(p);
+    if (!ok[q]) continue;
+    if (sg.g) gmem(sg.g)[fi[q]] = g[q];
+    Mo[fi[q]] = m;
+    V[fi[q]] = v;
+    P[fi[q]] = p;
+    if (sg.sh) gmem(static_cast<T*>(sg.sh))[(int64_t)(r0 + q) * sg.ldsh + c] = o[q];
   }
-  if (chunk == 0 && threadIdx.x == 0 && a.ploss) {
+  if (sg.sht && colok) {
+    auto D = gmem(static_cast<T*>(sg.sht)) + (int64_t)c * sg.ldsht + r0;
+    if (r0 + TR <= sg.rows) {  // TR consecutive values, 16-byte aligned (ldsht and r0 are multiples of 8)
+      constexpr int NV = TR * (int)sizeof(T) / 16;
+#pragma unroll
+      for (int w = 0; w < NV; ++w) {
+        u32x4_t v;
+        __builtin_memcpy(&v, &o[w * (16 / (int)sizeof(T))], 16);
+        *reinterpret_cast<__attribute__((address_space(1))) u32x4_t*>(D + w * (16 / (int)sizeof(T))) = v;
+      }
+    } else {
+      for (int q = 0; q < TR && r0 + q < sg.rows; ++q) D[q] = o[q];
+    }
+  }
+  if (chunk == 0 && threadIdx.x < 64 && a.ploss) {
+    // block loss: lane l sums partials l, l+64, ... in order, then a fixed
+    // butterfly across the wave
     float L = 0.f;
-    for (int i = 0; i < a.nloss; ++i) L += a.ploss[i];
-    L *= a.inv_m;
-    a.loss_out[0] = L;
-    if (!(fabsf(L) <= 3.4e38f)) a.status[0] = 1;
+    for (int i = (int)threadIdx.x; i < a.nloss; i += 64) L += a.ploss[i];
+    L = wave_sum(L) * a.inv_m;
+    if (threadIdx.x == 0) {
+      a.loss_out[0] = L;
+      if (!(fabsf(L) <= 3.4e38f)) a.status[0] = 1;
+    }
   }
 }
 
@@ -745,17 +782,15 @@ template <typename T>
 __global__ __launch_bounds__(256) void erase_refresh(AdamArgs a) {
   const int64_t chunk = blockIdx.x;
   const AdamSeg sg = a.seg[find_seg(a, chunk)];
-  const int n = sg.rows * sg.cols;
-  const int base = (int)((chunk - sg.chunk0) * ADAM_CHUNK);
-  T* SH = static_cast<T*>(sg.sh);
-  T* SHT = static_cast<T*>(sg.sht);
-  for (int q = 0; q < ADAM_CHUNK / 256; ++q) {
-    const int i = base + q * 256 + (int)threadIdx.x;
-    if (i >= n) break;
-    const int r = i / sg.cols, c = i - r * sg.cols;
-    const float p = gmem(sg.p)[i];
-    if (SH) gmem(SH)[(int64_t)r * sg.ldsh + c] = cvt<T>(p);
-    if (SHT) gmem(SHT)[(int64_t)c * sg.ldsht + r] = cvt<T>(p);
+  const int tile = (int)(chunk - sg.chunk0);
+  const int r0 = (tile / sg.tcols) * ADAM_TR;
+  const int c = (tile % sg.tcols) * ADAM_TC + (int)threadIdx.x;
+  if (c >= sg.cols) return;
+  for (int q = 0; q < ADAM_TR && r0 + q < sg.rows; ++q) {
+    const int r = r0 + q;
+    const float p = gmem(sg.p)[(int64_t)r * sg.cols + c];
+    if (sg.sh) gmem(static_cast<T*>(sg.sh))[(int64_t)r * sg.ldsh + c] = cvt<T>(p);
+    if (sg.sht) gmem(static_cast<T*>(sg.sht))[(int64_t)c * sg.ldsht + r] = cvt<T>(p);
   }
 }
 

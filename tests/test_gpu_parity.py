@@ -151,6 +151,22 @@ def test_ctr_dcn_bf16_small_vs_oracle():
     _say("  ", check_bf16(cfg, g, params, batches))
 
 
+def test_ctr_dcn_full_size_vs_oracle():
+    """The DCN workload at full size (6 blocks, batch 16384, 1677-wide cross
+    layers) in the overlapped schedule; blocks 0 and 5 are checked against the
+    oracle (blocks read the shared input and are independent, so the oracle
+    runs on just those two)."""
+    _say("case: ctr_dcn full size, blocks 0 and 5 checked")
+    cfg = synth.config("ctr_dcn")
+    params, batches = synth.make_workload(cfg, 0, 1)
+    _, g = run_gpu(cfg, params, batches, "overlap")
+    sel = [0, 5]
+    sub = dict(cfg)
+    sub["blocks"] = [cfg["blocks"][i] for i in sel]
+    gsub = [{k: (v[sel] if k == "losses" else [v[i] for i in sel]) for k, v in rec.items()} for rec in g]
+    _say("  ", check_bf16(sub, gsub, [params[i] for i in sel], batches))
+
+
 def test_nonfinite_input_is_reported():
     _say("case: non-finite input")
     cfg = synth.config("tiny")
