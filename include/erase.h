@@ -15,7 +15,7 @@
  *  - Every function returns erase_status; nothing throws across the ABI.
  *  - "device" pointers are HIP device allocations on the device that is
  *    current when erase_init() runs; "host" pointers are ordinary memory.
- *  - Streams are passed as `void*` holding a hipStream_t.  Both streams must
+ *  - Streams are passed as `void*` holding a hipStream_t.  All streams must
  *    be distinct, non-null, created by the caller with default priority and
  *    belong to the current device.  The library never destroys them.
  *  - The caller owns all device memory (parameters, Adam moments, gradients,
@@ -73,7 +73,7 @@ typedef enum { ERASE_LOSS_BCE = 0 } erase_loss_kind;
  * subarchitectures), or sg[z_{b-1}], the previous block's output (Eq. 1). */
 typedef enum { ERASE_IN_X = 0, ERASE_IN_PREV = 1 } erase_input_src;
 
-/* Schedules of one step.  All four run the identical kernels on identical
+/* Schedules of one step.  All of them run the identical kernels on identical
  * inputs and produce bit-identical results.
  *   SERIAL:        everything on the forward stream: forward+loss of blocks
  *                  1..B, then backward of blocks B..1, then Adam of 1..B.
@@ -83,12 +83,22 @@ typedef enum { ERASE_IN_X = 0, ERASE_IN_PREV = 1 } erase_input_src;
  *                  forward; the step ends with the forward stream joined on
  *                  the backward stream.
  *   SERIAL_GRAPH / OVERLAP_GRAPH: the same sequences captured once into a HIP
- *                  graph (per distinct x/labels/losses pointers) and replayed. */
+ *                  graph (per distinct x/labels/losses pointers and step
+ *                  parity) and replayed.
+ *   PIPELINE:      the OVERLAP order without the end-of-step join: block
+ *                  b's next forward waits only for its own previous backward
+ *                  (and, in a chain, for block b+1's), so one step's last
+ *                  backwards overlap the next step's first forwards.  Work
+ *                  enqueued on the forward stream after a PIPELINE step is
+ *                  not ordered after that step's backward; call erase_sync()
+ *                  before reading parameters.  Any other schedule, and
+ *                  erase_sync(), joins the outstanding backward first. */
 typedef enum {
   ERASE_SCHED_SERIAL = 0,
   ERASE_SCHED_OVERLAP = 1,
   ERASE_SCHED_SERIAL_GRAPH = 2,
-  ERASE_SCHED_OVERLAP_GRAPH = 3
+  ERASE_SCHED_OVERLAP_GRAPH = 3,
+  ERASE_SCHED_PIPELINE = 4
 } erase_schedule;
 
 typedef struct {
@@ -146,6 +156,15 @@ erase_status erase_init(const erase_config* cfg, const erase_block_buffers* bufs
                         void* workspace, size_t ws_bytes, void* s_fwd, void* s_bwd,
                         void** ctx_out);
 
+/* erase_init() with `n_bwd` backward streams (1..8, distinct, none equal to
+ * s_fwd; `s_bwd` is a host array).  In the overlapped schedules block b's
+ * backward and Adam run on s_bwd[b % n_bwd], so the backwards of different
+ * blocks may also overlap one another (the paper's CTR model used four side
+ * streams, Section 3.2).  erase_init() is this call with n_bwd = 1. */
+erase_status erase_init_streams(const erase_config* cfg, const erase_block_buffers* bufs,
+                                void* workspace, size_t ws_bytes, void* s_fwd, void* const* s_bwd,
+                                int32_t n_bwd, void** ctx_out);
+
 /* Enqueue one training step (Section 2.2) and return without waiting.
  *   x:      device, [batch][x_ld] of dtype, 16-byte aligned, rows' tails
  *           beyond in_dim are ignored;
@@ -183,7 +202,7 @@ typedef struct {
                         layer in one launch, 7 empty interval (no kernel) */
   int32_t block;     /* block index, -1 for the step prologue */
   int32_t layer;     /* layer index within the block, -1 if none */
-  int32_t stream;    /* 0 forward stream, 1 backward stream */
+  int32_t stream;    /* 0 forward stream, 1 + k backward stream k */
   float start_ms;    /* relative to the step's first event on the forward stream */
   float end_ms;
   int32_t tile_m;    /* GEMM workgroup tile rows (0 for non-GEMM kernels) */

@@ -29,6 +29,7 @@ constexpr int64_t kMaxDim = 65536;
 constexpr int64_t kMaxBatch = int64_t(1) << 24;
 constexpr size_t kAlign = 256;
 constexpr int kMaxGraphs = 16;
+constexpr int kMaxBwdStreams = 8;
 
 int64_t roundup(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -138,8 +139,10 @@ struct Plan {
   int64_t Mr = 0;   // allocated rows of row-major arrays: roundup(M, 128)
   int64_t* t = nullptr;
   int* status = nullptr;
-  void* xp = nullptr; int64_t ldxp = 0;  // zero-padded copy of x
-  void* xt = nullptr; int64_t ldxt = 0;
+  // zero-padded and feature-major copies of x, one pair per step parity so a
+  // step's prologue never overwrites what the previous step's backward reads
+  void* xp[2] = {nullptr, nullptr}; int64_t ldxp = 0;
+  void* xt[2] = {nullptr, nullptr}; int64_t ldxt = 0;
   std::vector<BlockRT> blk;
   size_t bytes = 0;
 };
@@ -206,9 +209,11 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
   for (int b = 0; b < c.n_blocks; ++b) any_x |= c.blocks[b].input_src == ERASE_IN_X;
   if (any_x) {
     P->ldxp = roundup(c.in_dim, 64);
-    P->xp = cv.take(size_t(Mr) * P->ldxp * esz);
     P->ldxt = P->ldm;
-    P->xt = cv.take(size_t(roundup(c.in_dim, 128)) * P->ldxt * esz);
+    for (int q = 0; q < 2; ++q) {
+      P->xp[q] = cv.take(size_t(Mr) * P->ldxp * esz);
+      P->xt[q] = cv.take(size_t(roundup(c.in_dim, 128)) * P->ldxt * esz);
+    }
   }
   P->blk.assign(c.n_blocks, BlockRT{});
   for (int b = 0; b < c.n_blocks; ++b) {
@@ -350,6 +355,7 @@ struct GraphEntry {
   const float* y;
   float* losses;
   int sched;
+  int par;
   hipGraph_t graph;
   hipGraphExec_t exec;
 };
@@ -361,7 +367,8 @@ struct Ctx {
   Plan P;
   char* ws = nullptr;
   size_t ws_bytes = 0;
-  hipStream_t sf = nullptr, sb = nullptr;
+  hipStream_t sf = nullptr;
+  std::vector<hipStream_t> sbs;  // backward streams; block b uses sbs[b % size]
   int device = 0;
   std::vector<hipEvent_t> ef, eb;
   erase_status sticky = ERASE_OK;
@@ -373,6 +380,9 @@ struct Ctx {
   hipEvent_t tnull0 = nullptr, tnull1 = nullptr;  // empty interval: event overhead
   std::vector<TimedLaunch> last;
   bool last_valid = false;
+  int64_t hstep = 0;     // host copy of the step counter (steps enqueued)
+  int par = 0;           // parity of the step being enqueued
+  bool pending = false;  // a PIPELINE step left backward work unjoined
 };
 
 bool hip_ok(Ctx* c, hipError_t e, const char* what) {
@@ -469,9 +479,9 @@ void layer_input(const Ctx* c, int b, int l, const void* x, const void** mn, int
     *ldnm = B.layer[l - 1].ldyt;
   } else if (B.input_src == ERASE_IN_X) {
     (void)x;
-    *mn = P.xp;
+    *mn = P.xp[c->par];
     *ldmn = P.ldxp;
-    *nm = P.xt;
+    *nm = P.xt[c->par];
     *ldnm = P.ldxt;
   } else {
     const BlockRT& A = P.blk[b - 1];
@@ -662,7 +672,7 @@ erase_status enqueue_adam(Ctx* c, Enqueuer& q, int b, float* losses, hipStream_t
   a.nseg = (int)B.segs.size();
   for (int i = 0; i < a.nseg; ++i) a.chunk0[i] = B.segs[i].chunk0;
   a.nchunks = B.nchunks;
-  a.hyper = reinterpret_cast<const float*>(P.t + 2);
+  a.hyper = reinterpret_cast<const float*>(P.t + 2) + 2 * c->par;
   a.beta1 = c->cfg.beta1;
   a.beta2 = c->cfg.beta2;
   a.eps = c->cfg.eps;
@@ -687,9 +697,11 @@ erase_status enqueue_adam(Ctx* c, Enqueuer& q, int b, float* losses, hipStream_t
 // schedules call this under stream capture.
 erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* labels, int sched, float* losses) {
   const Plan& P = c->P;
-  const bool overlap = sched == ERASE_SCHED_OVERLAP || sched == ERASE_SCHED_OVERLAP_GRAPH;
+  const bool pipeline = sched == ERASE_SCHED_PIPELINE;
+  const bool overlap = sched == ERASE_SCHED_OVERLAP || sched == ERASE_SCHED_OVERLAP_GRAPH || pipeline;
   const int nb = (int)P.blk.size();
-  hipStream_t sf = c->sf, sb = c->sb;
+  const int ns = (int)c->sbs.size();
+  hipStream_t sf = c->sf;
   {
     PrologueArgs pa{};
     pa.t = P.t;
@@ -698,30 +710,44 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
     pa.beta2 = c->cfg.beta2;
     pa.x = x;
     pa.ldx = c->cfg.x_ld;
-    pa.xp = P.xp;
+    pa.hyper = reinterpret_cast<float*>(P.t + 2) + 2 * c->par;
+    pa.xp = P.xp[c->par];
     pa.ldxp = P.ldxp;
-    pa.xt = P.xt;
+    pa.xt = P.xt[c->par];
     pa.ldxt = P.ldxt;
     pa.M = P.M;
     pa.K = c->cfg.in_dim;
     Cost cost;
-    cost.bytes = P.xt ? 3.0 * P.esz * double(P.M) * c->cfg.in_dim : 0.0;
+    cost.bytes = P.xt[0] ? 3.0 * P.esz * double(P.M) * c->cfg.in_dim : 0.0;
     const int bf = P.bf16;
     RUN(0, -1, -1, 0, sf, cost, [&](const LaunchEv& ev) { return launch_prologue(bf, pa, sf, ev); });
   }
   if (overlap) {
+    // ERASE: block b's backward and Adam go to backward stream b % ns as soon
+    // as its forward and local loss are enqueued; the step ends with the
+    // forward stream joined on every backward stream used.
     for (int b = 0; b < nb; ++b) {
+      const int k = b % ns;
+      hipStream_t sb = c->sbs[k];
+      if (pipeline && c->pending) {
+        // no end-of-step join: block b's forward waits only for the previous
+        // step's backward of block b (its weights, its activation buffers)
+        // and, in a chain, of block b+1 (which reads block b's output)
+        HIPCHK(c, hipStreamWaitEvent(sf, c->eb[b], 0));
+        if (b + 1 < nb && P.blk[b + 1].input_src == ERASE_IN_PREV) HIPCHK(c, hipStreamWaitEvent(sf, c->eb[b + 1], 0));
+      }
       erase_status st = enqueue_forward(c, q, b, x, labels, sf, 0);
       if (st != ERASE_OK) return st;
       HIPCHK(c, hipEventRecord(c->ef[b], sf));
       HIPCHK(c, hipStreamWaitEvent(sb, c->ef[b], 0));
-      st = enqueue_backward(c, q, b, x, sb, 1);
+      st = enqueue_backward(c, q, b, x, sb, 1 + k);
       if (st != ERASE_OK) return st;
-      st = enqueue_adam(c, q, b, losses, sb, 1);
+      st = enqueue_adam(c, q, b, losses, sb, 1 + k);
       if (st != ERASE_OK) return st;
+      HIPCHK(c, hipEventRecord(c->eb[b], sb));
     }
-    HIPCHK(c, hipEventRecord(c->eb[nb - 1], sb));
-    HIPCHK(c, hipStreamWaitEvent(sf, c->eb[nb - 1], 0));
+    if (!pipeline)
+      for (int b = std::max(0, nb - ns); b < nb; ++b) HIPCHK(c, hipStreamWaitEvent(sf, c->eb[b], 0));
   } else {
     for (int b = 0; b < nb; ++b) {
       erase_status st = enqueue_forward(c, q, b, x, labels, sf, 0);
@@ -746,6 +772,15 @@ int launches_per_step(const Plan& P) {
     for (int l = 1; l < B.L; ++l) n += B.layer[l].grouped ? 1 : 2;
   }
   return n;
+}
+
+// Join the backward streams of an unjoined PIPELINE step into the forward
+// stream (enqueued, not captured).
+erase_status join_pending(Ctx* c) {
+  if (!c->pending) return ERASE_OK;
+  for (size_t b = 0; b < c->eb.size(); ++b) HIPCHK(c, hipStreamWaitEvent(c->sf, c->eb[b], 0));
+  c->pending = false;
+  return ERASE_OK;
 }
 
 erase_status refresh(Ctx* c) {
@@ -801,6 +836,12 @@ erase_status erase_workspace_bytes(const erase_config* cfg, size_t* bytes) {
 
 erase_status erase_init(const erase_config* cfg, const erase_block_buffers* bufs, void* workspace, size_t ws_bytes,
                         void* s_fwd, void* s_bwd, void** ctx_out) {
+  void* const one[1] = {s_bwd};
+  return erase_init_streams(cfg, bufs, workspace, ws_bytes, s_fwd, one, 1, ctx_out);
+}
+
+erase_status erase_init_streams(const erase_config* cfg, const erase_block_buffers* bufs, void* workspace,
+                                size_t ws_bytes, void* s_fwd, void* const* s_bwd, int32_t n_bwd, void** ctx_out) {
   if (!ctx_out) return ERASE_ERR_INVALID_ARG;
   *ctx_out = nullptr;
   std::string err;
@@ -813,7 +854,12 @@ erase_status erase_init(const erase_config* cfg, const erase_block_buffers* bufs
                          reinterpret_cast<uintptr_t>(bufs[b].v) | reinterpret_cast<uintptr_t>(bufs[b].grad);
     if (al % 4) return ERASE_ERR_INVALID_ARG;
   }
-  if (!s_fwd || !s_bwd || s_fwd == s_bwd) return ERASE_ERR_INVALID_ARG;
+  if (!s_fwd || !s_bwd || n_bwd < 1 || n_bwd > kMaxBwdStreams) return ERASE_ERR_INVALID_ARG;
+  for (int i = 0; i < n_bwd; ++i) {
+    if (!s_bwd[i] || s_bwd[i] == s_fwd) return ERASE_ERR_INVALID_ARG;
+    for (int j = 0; j < i; ++j)
+      if (s_bwd[j] == s_bwd[i]) return ERASE_ERR_INVALID_ARG;
+  }
   if (!workspace || reinterpret_cast<uintptr_t>(workspace) % kAlign) return ERASE_ERR_WORKSPACE;
   {
     Plan probe;
@@ -832,7 +878,7 @@ erase_status erase_init(const erase_config* cfg, const erase_block_buffers* bufs
   c->ws = static_cast<char*>(workspace);
   c->ws_bytes = ws_bytes;
   c->sf = static_cast<hipStream_t>(s_fwd);
-  c->sb = static_cast<hipStream_t>(s_bwd);
+  for (int i = 0; i < n_bwd; ++i) c->sbs.push_back(static_cast<hipStream_t>(s_bwd[i]));
   build_plan(c->cfg, reinterpret_cast<uintptr_t>(workspace), &c->P);
   build_segments(&c->P, bufs);
 
@@ -874,13 +920,18 @@ erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t s
   if (reinterpret_cast<uintptr_t>(x) % 16 || reinterpret_cast<uintptr_t>(labels) % 4 ||
       reinterpret_cast<uintptr_t>(losses) % 4)
     return ERASE_ERR_INVALID_ARG;
-  if (schedule < ERASE_SCHED_SERIAL || schedule > ERASE_SCHED_OVERLAP_GRAPH) return ERASE_ERR_INVALID_ARG;
+  if (schedule < ERASE_SCHED_SERIAL || schedule > ERASE_SCHED_PIPELINE) return ERASE_ERR_INVALID_ARG;
   const bool graph = schedule == ERASE_SCHED_SERIAL_GRAPH || schedule == ERASE_SCHED_OVERLAP_GRAPH;
   if (graph && c->timing) return ERASE_ERR_UNSUPPORTED;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != c->device) {
     c->err = "erase_step called with a different current device than erase_init";
     return ERASE_ERR_STATE;
+  }
+  c->par = (int)((c->hstep + 1) & 1);
+  if (schedule != ERASE_SCHED_PIPELINE) {
+    erase_status st = join_pending(c);
+    if (st != ERASE_OK) return st;
   }
   if (!graph) {
     Enqueuer q(c, c->timing);
@@ -898,11 +949,13 @@ erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t s
       c->last = q.launches();
       c->last_valid = true;
     }
+    if (schedule == ERASE_SCHED_PIPELINE) c->pending = true;
+    c->hstep += 1;
     return ERASE_OK;
   }
   GraphEntry* ge = nullptr;
   for (GraphEntry& g : c->graphs)
-    if (g.x == x && g.y == labels && g.losses == losses && g.sched == schedule) ge = &g;
+    if (g.x == x && g.y == labels && g.losses == losses && g.sched == schedule && g.par == c->par) ge = &g;
   if (!ge) {
     if ((int)c->graphs.size() >= kMaxGraphs) {
       // evict the oldest entry; its replays are ordered before anything new on sf
@@ -912,7 +965,7 @@ erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t s
       if (old.graph) (void)hipGraphDestroy(old.graph);
       c->graphs.erase(c->graphs.begin());
     }
-    GraphEntry g{x, labels, losses, schedule, nullptr, nullptr};
+    GraphEntry g{x, labels, losses, schedule, c->par, nullptr, nullptr};
     HIPCHK(c, hipStreamBeginCapture(c->sf, hipStreamCaptureModeThreadLocal));
     Enqueuer q(c, false);
     erase_status st = enqueue_step(c, q, x, labels, schedule, losses);
@@ -932,6 +985,7 @@ erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t s
     ge = &c->graphs.back();
   }
   HIPCHK(c, hipGraphLaunch(ge->exec, c->sf));
+  c->hstep += 1;
   return ERASE_OK;
 }
 
@@ -940,7 +994,8 @@ erase_status erase_sync(void* ctx) {
   if (!c) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
   HIPCHK(c, hipStreamSynchronize(c->sf));
-  HIPCHK(c, hipStreamSynchronize(c->sb));
+  for (hipStream_t sb : c->sbs) HIPCHK(c, hipStreamSynchronize(sb));
+  c->pending = false;
   int status = 0;
   HIPCHK(c, hipMemcpy(&status, c->P.status, sizeof(int), hipMemcpyDeviceToHost));
   if (status != 0) {
@@ -956,6 +1011,8 @@ erase_status erase_get_step(void* ctx, int64_t* t) {
   if (!c || !t) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
   HIPCHK(c, hipStreamSynchronize(c->sf));
+  for (hipStream_t sb : c->sbs) HIPCHK(c, hipStreamSynchronize(sb));
+  c->pending = false;
   HIPCHK(c, hipMemcpy(t, c->P.t, sizeof(int64_t), hipMemcpyDeviceToHost));
   return ERASE_OK;
 }
@@ -965,7 +1022,10 @@ erase_status erase_set_step(void* ctx, int64_t t) {
   if (!c || t < 0) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
   HIPCHK(c, hipStreamSynchronize(c->sf));
+  for (hipStream_t sb : c->sbs) HIPCHK(c, hipStreamSynchronize(sb));
+  c->pending = false;
   HIPCHK(c, hipMemcpy(c->P.t, &t, sizeof(int64_t), hipMemcpyHostToDevice));
+  c->hstep = t;
   return ERASE_OK;
 }
 
@@ -973,6 +1033,8 @@ erase_status erase_refresh_weights(void* ctx) {
   Ctx* c = as_ctx(ctx);
   if (!c) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
+  erase_status st = join_pending(c);
+  if (st != ERASE_OK) return st;
   return refresh(c);
 }
 
@@ -1029,7 +1091,7 @@ erase_status erase_destroy(void* ctx) {
   Ctx* c = as_ctx(ctx);
   if (!c) return ERASE_OK;
   (void)hipStreamSynchronize(c->sf);
-  (void)hipStreamSynchronize(c->sb);
+  for (hipStream_t sb : c->sbs) (void)hipStreamSynchronize(sb);
   destroy_graphs(c);
   for (hipEvent_t e : c->ef) (void)hipEventDestroy(e);
   for (hipEvent_t e : c->eb) (void)hipEventDestroy(e);

@@ -67,11 +67,12 @@ hipError_t launch_bwd_gemm(int bf16, const GemmDesc& gd, const EpiParams& ed, co
 // Step prologue: t += 1, the zero-padded copy xp[m][k] = x[m][k] and the
 // feature-major copy xt[k][m] = x[m][k] (padding of both stays zero).
 // Workspace header (first 256 bytes): step counter t (int64 at 0), status
-// word (int32 at 8), and the Adam step factors of the current step written
-// by the prologue: lr / (1 - beta1^t) (float at 16), sqrt(1 - beta2^t)
-// (float at 20).
+// word (int32 at 8), and the Adam step factors written by the prologue, one
+// pair per step parity p: lr / (1 - beta1^t) (float at 16 + 8p) and
+// sqrt(1 - beta2^t) (float at 20 + 8p).
 struct PrologueArgs {
   int64_t* t;
+  float* hyper;  // this step's Adam factors (one pair per step parity)
   float lr, beta1, beta2;
   const void* x; int64_t ldx;
   void* xp; int64_t ldxp;

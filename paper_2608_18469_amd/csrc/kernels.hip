@@ -459,9 +459,8 @@ __global__ __launch_bounds__(256) void erase_prologue(PrologueArgs a) {
   if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
     const int64_t t = a.t[0] + 1;
     a.t[0] = t;
-    float* hyper = reinterpret_cast<float*>(a.t + 2);
-    hyper[0] = (float)((double)a.lr / (1.0 - pow((double)a.beta1, (double)t)));
-    hyper[1] = (float)sqrt(1.0 - pow((double)a.beta2, (double)t));
+    a.hyper[0] = (float)((double)a.lr / (1.0 - pow((double)a.beta1, (double)t)));
+    a.hyper[1] = (float)sqrt(1.0 - pow((double)a.beta2, (double)t));
   }
   if (a.xp == nullptr) return;
   const T* X = static_cast<const T*>(a.x);

@@ -23,8 +23,9 @@ F32, BF16 = 0, 1
 LINEAR_RELU, CROSS = 0, 1
 LOSS_BCE = 0
 IN_X, IN_PREV = 0, 1
-SERIAL, OVERLAP, SERIAL_GRAPH, OVERLAP_GRAPH = 0, 1, 2, 3
-SCHEDULES = {"serial": SERIAL, "overlap": OVERLAP, "serial_graph": SERIAL_GRAPH, "overlap_graph": OVERLAP_GRAPH}
+SERIAL, OVERLAP, SERIAL_GRAPH, OVERLAP_GRAPH, PIPELINE = 0, 1, 2, 3, 4
+SCHEDULES = {"serial": SERIAL, "overlap": OVERLAP, "serial_graph": SERIAL_GRAPH, "overlap_graph": OVERLAP_GRAPH,
+             "pipeline": PIPELINE}
 KERNEL_KINDS = {0: "prologue", 1: "fwd_gemm", 2: "head_bce", 3: "wgrad_gemm", 4: "dgrad_gemm", 5: "adam",
                 6: "bwd_gemm", 7: "empty"}
 
@@ -60,6 +61,8 @@ SIGNATURES = {
     "erase_workspace_bytes": (c_int32, [POINTER(Config), POINTER(c_size_t)]),
     "erase_init": (c_int32, [POINTER(Config), POINTER(BlockBuffers), c_void_p, c_size_t, c_void_p, c_void_p,
                              POINTER(c_void_p)]),
+    "erase_init_streams": (c_int32, [POINTER(Config), POINTER(BlockBuffers), c_void_p, c_size_t, c_void_p,
+                                     POINTER(c_void_p), c_int32, POINTER(c_void_p)]),
     "erase_step": (c_int32, [c_void_p, c_void_p, c_void_p, c_int32, c_void_p]),
     "erase_sync": (c_int32, [c_void_p]),
     "erase_get_step": (c_int32, [c_void_p, POINTER(c_int64)]),
@@ -176,7 +179,7 @@ class Trainer:
     """Owns the device buffers, two streams and one library context."""
 
     def __init__(self, cfg: dict, params: list, x_ld: int | None = None, keep_grads: bool = True,
-                 m: list | None = None, v: list | None = None, step: int = 0):
+                 m: list | None = None, v: list | None = None, step: int = 0, bwd_streams: int = 1):
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("no HIP device available: the ERASE step runs only on the GPU")
@@ -205,12 +208,14 @@ class Trainer:
         pad = (-self.ws.data_ptr()) % 256
         self.ws_ptr = self.ws.data_ptr() + pad
         self.sf = torch.cuda.Stream(device=self.dev)
-        self.sb = torch.cuda.Stream(device=self.dev)
+        self.sbs = [torch.cuda.Stream(device=self.dev) for _ in range(bwd_streams)]
+        self.sb = self.sbs[0]
         torch.cuda.synchronize(self.dev)
         ctx = c_void_p()
-        _check(lib().erase_init(self.ncfg.ptr(), bufs, c_void_p(self.ws_ptr), self.ws_bytes,
-                                c_void_p(self.sf.cuda_stream), c_void_p(self.sb.cuda_stream), ctypes.byref(ctx)),
-               "erase_init")
+        sb_arr = (c_void_p * bwd_streams)(*[s.cuda_stream for s in self.sbs])
+        _check(lib().erase_init_streams(self.ncfg.ptr(), bufs, c_void_p(self.ws_ptr), self.ws_bytes,
+                                        c_void_p(self.sf.cuda_stream), sb_arr, bwd_streams, ctypes.byref(ctx)),
+               "erase_init_streams")
         self.ctx = ctx
         if step:
             self.set_step(step)

@@ -22,9 +22,9 @@ def rel(a, b):
     return d / nb if nb > 0 else d
 
 
-def run_gpu(cfg, params, batches, schedule="overlap", keep_grads=True, trainer=None):
+def run_gpu(cfg, params, batches, schedule="overlap", keep_grads=True, trainer=None, bwd_streams=1):
     """Step the HIP path over `batches`; return per-step records."""
-    tr = trainer or erase.Trainer(cfg, params, keep_grads=keep_grads)
+    tr = trainer or erase.Trainer(cfg, params, keep_grads=keep_grads, bwd_streams=bwd_streams)
     dev = [tr.device_batch(x, y) for (x, y) in batches]
     recs = []
     for (xd, yd) in dev:
@@ -33,6 +33,23 @@ def run_gpu(cfg, params, batches, schedule="overlap", keep_grads=True, trainer=N
         p, m, v, g = tr.flat_state()
         recs.append({"losses": tr.losses.cpu().numpy().copy(), "params": p, "m": m, "v": v, "grads": g})
     return tr, recs
+
+
+def run_gpu_nosync(cfg, params, batches, schedules, bwd_streams=1):
+    """Enqueue one step per batch (schedules[i % len] for step i) without
+    synchronizing in between, then sync once; returns the per-step losses and
+    the final state as one record list of length 1 plus the losses."""
+    import torch
+    tr = erase.Trainer(cfg, params, keep_grads=True, bwd_streams=bwd_streams)
+    dev = [tr.device_batch(x, y) for (x, y) in batches]
+    outs = [torch.zeros(len(cfg["blocks"]), dtype=torch.float32, device="cuda") for _ in batches]
+    for i, (xd, yd) in enumerate(dev):
+        tr.step(xd, yd, schedules[i % len(schedules)], losses=outs[i], wait_current=(i == 0))
+    tr.sync()
+    p, m, v, g = tr.flat_state()
+    losses = np.stack([o.cpu().numpy() for o in outs])
+    tr.close()
+    return losses, {"losses": losses[-1], "params": p, "m": m, "v": v, "grads": g}
 
 
 def run_oracle(cfg, params, batches, emulate_bf16=False, t0=0, m=None, v=None):

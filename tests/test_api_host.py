@@ -131,6 +131,11 @@ def test_init_rejects_bad_arguments_before_any_hip_call():
     # same stream twice
     assert L.erase_init(nc.ptr(), bufs, ctypes.c_void_p(256), 1 << 20, ctypes.c_void_p(8), ctypes.c_void_p(8),
                         ctypes.byref(ctx)) == erase.ERR_INVALID_ARG
+    # backward-stream arrays: repeated, null, too many, none
+    for arr in ([16, 16], [16, 0], list(range(16, 16 + 9 * 8, 8)), []):
+        sb = (ctypes.c_void_p * max(1, len(arr)))(*arr)
+        assert L.erase_init_streams(nc.ptr(), bufs, ctypes.c_void_p(256), 1 << 20, ctypes.c_void_p(8), sb, len(arr),
+                                    ctypes.byref(ctx)) == erase.ERR_INVALID_ARG
     # misaligned / null / small workspace
     assert L.erase_init(nc.ptr(), bufs, ctypes.c_void_p(100), 1 << 20, ctypes.c_void_p(8), ctypes.c_void_p(16),
                         ctypes.byref(ctx)) == erase.ERR_WORKSPACE

@@ -14,11 +14,11 @@ import numpy as np
 import pytest
 
 from paper_2608_18469_amd import erase, synth
-from tests.gpu_util import assert_bit_identical, check_bf16, compare, run_gpu, run_oracle
+from tests.gpu_util import assert_bit_identical, check_bf16, compare, run_gpu, run_gpu_nosync, run_oracle
 
 pytestmark = pytest.mark.gpu
 
-SCHEDS = ["serial", "overlap", "serial_graph", "overlap_graph"]
+SCHEDS = ["serial", "overlap", "serial_graph", "overlap_graph", "pipeline"]
 
 
 def _say(*a):
@@ -104,12 +104,50 @@ def test_ctr_mlp_bf16_small_vs_oracle(batch):
 
 
 def test_ctr_mlp_bf16_schedules_bit_identical():
+    """Serial, overlapped and graph schedules, with 1 and 3 backward streams,
+    produce the same bits."""
     _say("case: ctr_mlp bf16 schedules bit-identical")
-    cfg = _ctr_small(batch=777, blocks=3)
+    cfg = _ctr_small(batch=777, blocks=4)
     params, batches = synth.make_workload(cfg, 3, 2)
     runs = [run_gpu(cfg, params, batches, s)[1] for s in SCHEDS]
+    runs += [run_gpu(cfg, params, batches, s, bwd_streams=3)[1] for s in ("overlap", "overlap_graph")]
     for other in runs[1:]:
         assert_bit_identical(runs[0], other)
+
+
+@pytest.mark.parametrize("name,streams", [("ctr_small", 2), ("deep_chain", 3), ("mixed", 1)])
+def test_pipelined_steps_match_serial(name, streams):
+    """PIPELINE steps enqueued back to back (no end-of-step join, so one
+    step's last backwards overlap the next step's first forwards), and a mix
+    of schedules, give the same bits as serial steps."""
+    _say(f"case: pipelined steps, {name}, {streams} backward streams")
+    if name == "ctr_small":
+        cfg = _ctr_small(batch=640, blocks=4)
+    elif name == "deep_chain":
+        cfg = synth.config("deep_chain", batch=384)
+    else:
+        cfg = _mixed_fp32(200)
+    params, batches = synth.make_workload(cfg, 11, 5)
+    ref_l, ref = run_gpu_nosync(cfg, params, batches, ["serial"])
+    got_l, got = run_gpu_nosync(cfg, params, batches, ["pipeline"], bwd_streams=streams)
+    assert np.array_equal(ref_l.view(np.uint32), got_l.view(np.uint32))
+    assert_bit_identical([ref], [got])
+    mix_l, mix = run_gpu_nosync(cfg, params, batches, ["pipeline", "serial", "pipeline", "overlap_graph", "pipeline"],
+                                bwd_streams=streams)
+    assert np.array_equal(ref_l.view(np.uint32), mix_l.view(np.uint32))
+    assert_bit_identical([ref], [mix])
+
+
+def test_deep_chain_multi_stream_matches_serial():
+    """A chain with 4 backward streams: bit-identical to the serial schedule."""
+    _say("case: deep_chain, 4 backward streams vs serial")
+    cfg = synth.config("deep_chain", batch=512)
+    params, batches = synth.make_workload(cfg, 7, 2)
+    a = run_gpu(cfg, params, batches, "serial")[1]
+    b = run_gpu(cfg, params, batches, "overlap", bwd_streams=4)[1]
+    c = run_gpu(cfg, params, batches, "overlap_graph", bwd_streams=4)[1]
+    assert_bit_identical(a, b)
+    assert_bit_identical(a, c)
 
 
 def test_ctr_mlp_full_size_vs_oracle():
@@ -226,6 +264,12 @@ def test_kernel_timing_records():
     assert len(recs) == 1 + 2 * 8, [r["kind"] for r in recs]
     assert all(r["end_ms"] >= r["start_ms"] >= 0 for r in recs)
     assert {r["stream"] for r in recs if r["kind"] in ("wgrad_gemm", "bwd_gemm", "adam")} == {1}
+    tr2 = erase.Trainer(cfg, params, bwd_streams=2)
+    tr2.set_timing(True)
+    tr2.step(*tr2.device_batch(*batches[0]), "overlap")
+    tr2.sync()
+    r2 = tr2.read_timing()[1:]
+    assert {r["stream"] for r in r2 if r["kind"] == "adam"} == {1, 2}
     assert {r["stream"] for r in recs if r["kind"] in ("fwd_gemm", "head_bce", "prologue")} == {0}
     with pytest.raises(erase.EraseError):
         tr.step(xd, yd, "overlap_graph")
