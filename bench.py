@@ -21,6 +21,7 @@ The CPU baseline times the float64 oracle on the host on a bounded sample.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -47,6 +48,39 @@ def kernel_class(r, bf16=True):
     return f"{KIND_SYMBOL[r['kind']]}<{t}>"
 
 
+def kernel_source_hash():
+    """Hash of the kernel sources: byte counters taken from other sources are stale."""
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "internal.h"):
+        with open(os.path.join(ROOT, "paper_2608_18469_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ctr_mlp_hbm_traffic.md")
+
+
+def measured_traffic(kernel_class, workload):
+    """HBM bytes per launch of `kernel_class` from the committed byte-counter
+    summary (rocprofv3 FETCH_SIZE and WRITE_SIZE passes, each scaled by the
+    same counter's reading for a copy of known size), or None when there is
+    no summary for this kernel and workload or the kernels changed since."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            lines = f.read().splitlines()
+    except OSError:
+        return None
+    src = kernel_source_hash()
+    for line in lines:
+        parts = line.split()
+        if len(parts) == 6 and parts[0] == "traffic" and parts[1] == workload and parts[2] == kernel_class:
+            if parts[3] != src:
+                return None
+            fetch, write = float(parts[4]), float(parts[5])
+            return {"bytes": fetch + write, "fetch_bytes": fetch, "write_bytes": write, "source": src}
+    return None
+
+
 def overlap_fraction(recs):
     """Share of backward-stream kernel time that runs while a forward-stream
     kernel is running (interval intersection on the device clock)."""
@@ -70,15 +104,21 @@ def overlap_fraction(recs):
     return inter / tot if tot > 0 else 0.0
 
 
-def cpu_baseline(cfg, params, batches, budget_s):
-    """Time the float64 oracle on the host (reported baseline, not a target)."""
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_rate(cfg, params, batches, budget_s):
+    """Full float64 oracle steps until budget_s has passed (at least one)."""
     import oracle
     from paper_2608_18469_amd import synth
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        threads = os.cpu_count() or 1
     m = synth.zero_state(params)
     v = synth.zero_state(params)
     p, t = params, 0
@@ -91,10 +131,25 @@ def cpu_baseline(cfg, params, batches, budget_s):
         steps += 1
         el = time.perf_counter() - t0
         if el >= budget_s:
-            break
+            return steps, el
+
+
+def cpu_baseline(cfg, params, batches, budget_s, budget_1t_s):
+    """Time the float64 oracle on the host (a reported baseline, not a
+    target): with every BLAS thread, then with one thread."""
+    from threadpoolctl import threadpool_info, threadpool_limits
+    info = threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in info] or [1])
+    blas = ", ".join(sorted({f"{i.get('internal_api', '?')} {i.get('version', '')}".strip() for i in info})) or "none"
+    steps, el = _oracle_rate(cfg, params, batches, budget_s)
+    with threadpool_limits(limits=1):
+        steps1, el1 = _oracle_rate(cfg, params, batches, budget_1t_s)
+    what = f"full float64 oracle steps of {cfg['name']} (batch {cfg['batch']}, {len(cfg['blocks'])} blocks)"
     return {"value": steps * cfg["batch"] / el, "unit": "samples/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{steps} full float64 oracle steps of {cfg['name']} (batch {cfg['batch']}, "
-                      f"{len(cfg['blocks'])} blocks) in {el:.1f} s on the host, numpy/OpenBLAS threads={threads}"}
+            "sample": f"{steps} {what} in {el:.1f} s on the host, {threads} BLAS threads",
+            "single_thread": {"value": steps1 * cfg["batch"] / el1, "unit": "samples/s", "cores": 1,
+                              "sample": f"{steps1} {what} in {el1:.1f} s, 1 BLAS thread"},
+            "cpu_model": _cpu_model(), "blas": blas, "os_cpu_count": os.cpu_count()}
 
 
 def main():
@@ -103,8 +158,12 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="ctr_mlp")
+    ap.add_argument("--block", type=int, default=50,
+                    help="schedules are timed interleaved, this many steps at a time")
     ap.add_argument("--timing-steps", type=int, default=20)
-    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--cpu-budget", type=float, default=12.0,
+                    help="seconds of oracle steps with every BLAS thread (then --cpu-budget-1t with one)")
+    ap.add_argument("--cpu-budget-1t", type=float, default=6.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--schedules", default="serial,overlap,serial_graph,overlap_graph,pipeline")
     ap.add_argument("--bwd-streams", type=int, default=1,
@@ -141,34 +200,52 @@ def main():
     M = cfg["batch"]
     scheds = args.schedules.split(",")
 
-    res = {}
+    # Warm every schedule up (graph capture and instantiation happen here),
+    # then time them interleaved in blocks of --block steps so that clock and
+    # thermal drift affect every schedule alike.  One global step counter
+    # picks the batch, so every (batch, step parity) pair a graph schedule
+    # meets is one it has already captured.
+    gstep = 0
+
+    def one_step(s):
+        nonlocal gstep
+        x, y = dev[gstep % len(dev)]
+        gstep += 1
+        tr.step(x, y, s, losses, wait_current=False)
+
     for s in scheds:
         log(f"[bench] {s}: warmup {args.warmup}")
-        for i in range(args.warmup):
-            x, y = dev[i % len(dev)]
-            tr.step(x, y, s, losses, wait_current=False)
+        for _ in range(args.warmup):
+            one_step(s)
         tr.sync()
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-        host = []
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for i in range(args.steps):
-            x, y = dev[i % len(dev)]
-            evs[i][0].record(tr.sf)
-            h0 = time.perf_counter()
-            tr.step(x, y, s, losses, wait_current=False)
-            host.append(time.perf_counter() - h0)
-            evs[i][1].record(tr.sf)
-        torch.cuda.synchronize()
-        el = time.perf_counter() - t0
-        tr.sync()
-        per = np.array([a.elapsed_time(b) for a, b in evs])  # ms per step on the device clock
-        sps = M / (per / 1e3)
+    acc = {s: {"el": 0.0, "per": [], "host": []} for s in scheds}
+    nblk = (args.steps + args.block - 1) // args.block
+    for bi in range(nblk):
+        n = min(args.block, args.steps - bi * args.block)
+        for s in scheds:
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for i in range(n):
+                evs[i][0].record(tr.sf)
+                h0 = time.perf_counter()
+                one_step(s)
+                acc[s]["host"].append(time.perf_counter() - h0)
+                evs[i][1].record(tr.sf)
+            torch.cuda.synchronize()
+            acc[s]["el"] += time.perf_counter() - t0
+            tr.sync()
+            acc[s]["per"] += [a.elapsed_time(b) for a, b in evs]  # ms per step on the device clock
+        log(f"[bench] block {bi + 1}/{nblk} ({n} steps per schedule) done")
+    res = {}
+    for s in scheds:
+        el = acc[s]["el"]
+        sps = M / (np.array(acc[s]["per"]) / 1e3)
         res[s] = {"samples_per_s": M * args.steps / el, "ms_per_step": el / args.steps * 1e3,
                   "p90_samples_per_s": float(np.percentile(sps, 90)), "median_samples_per_s": float(np.median(sps)),
-                  "host_enqueue_us": float(np.median(host) * 1e6), "elapsed_s": el}
+                  "host_enqueue_us": float(np.median(acc[s]["host"]) * 1e6), "elapsed_s": el}
         log(f"[bench] {s}: {res[s]['samples_per_s']:.0f} samples/s, {res[s]['ms_per_step']:.3f} ms/step, "
-            f"enqueue {res[s]['host_enqueue_us']:.1f} us")
+            f"p90 {res[s]['p90_samples_per_s']:.0f}, enqueue {res[s]['host_enqueue_us']:.1f} us")
 
     # Per-launch kernel times from HIP events the library records around each
     # launch on that launch's own stream: a SERIAL pass (each kernel alone on
@@ -178,8 +255,7 @@ def main():
         tr.set_timing(True)
         out = []
         for i in range(n):
-            x, y = dev[i % len(dev)]
-            tr.step(x, y, sched, losses, wait_current=False)
+            one_step(sched)
             tr.sync()
             out.append(tr.read_timing())
         tr.set_timing(False)
@@ -215,8 +291,11 @@ def main():
         achieved = dom["bytes"] / dom["n"] / avg_dur_s / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
+    tr_meas = measured_traffic(dom_name, args.workload)
+    roof["traffic"] = tr_meas["bytes"] if tr_meas else None  # HBM bytes per launch, counters
+    roof["traffic_detail"] = tr_meas if tr_meas else f"null: no byte counters of the current kernels ({kernel_source_hash()})"
     roof["kernel"] = dom_name
+    roof["algorithmic_bytes_per_launch"] = dom["bytes"] / dom["n"]
     roof["avg_launch_us"] = avg_dur_s * 1e6
     roof["launches_per_step"] = dom["n"] / nsteps
     kernels = {k: {"avg_us": v["ms"] / v["n"] * 1e3, "launches_per_step": v["n"] / nsteps,
@@ -268,8 +347,8 @@ def main():
         "kernels": kernels,
     }
     if not args.no_cpu_baseline:
-        log(f"[bench] cpu baseline: oracle for ~{args.cpu_budget:.0f} s")
-        out["cpu_baseline"] = cpu_baseline(cfg, params, batches, args.cpu_budget)
+        log(f"[bench] cpu baseline: oracle for ~{args.cpu_budget:.0f} s + ~{args.cpu_budget_1t:.0f} s on one thread")
+        out["cpu_baseline"] = cpu_baseline(cfg, params, batches, args.cpu_budget, args.cpu_budget_1t)
     tr.close()
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20) // 4

@@ -92,13 +92,19 @@ typedef enum { ERASE_IN_X = 0, ERASE_IN_PREV = 1 } erase_input_src;
  *                  enqueued on the forward stream after a PIPELINE step is
  *                  not ordered after that step's backward; call erase_sync()
  *                  before reading parameters.  Any other schedule, and
- *                  erase_sync(), joins the outstanding backward first. */
+ *                  erase_sync(), joins the outstanding backward first.
+ *   OVERLAP_ADAM_END: early backward as in OVERLAP, but the parameter
+ *                  updates wait for the end of the step: after every
+ *                  backward has finished, the forward stream runs Adam of
+ *                  blocks 1..B (gradients are produced early, the optimizer
+ *                  steps once per step, as in Section 2.2). */
 typedef enum {
   ERASE_SCHED_SERIAL = 0,
   ERASE_SCHED_OVERLAP = 1,
   ERASE_SCHED_SERIAL_GRAPH = 2,
   ERASE_SCHED_OVERLAP_GRAPH = 3,
-  ERASE_SCHED_PIPELINE = 4
+  ERASE_SCHED_PIPELINE = 4,
+  ERASE_SCHED_OVERLAP_ADAM_END = 5
 } erase_schedule;
 
 typedef struct {

@@ -28,7 +28,7 @@ constexpr int kMaxLayers = 16;
 constexpr int64_t kMaxDim = 65536;
 constexpr int64_t kMaxBatch = int64_t(1) << 24;
 constexpr size_t kAlign = 256;
-constexpr int kMaxGraphs = 16;
+constexpr int kMaxGraphs = 32;
 constexpr int kMaxBwdStreams = 8;
 
 int64_t roundup(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
@@ -99,6 +99,7 @@ erase_status validate(const erase_config* c, std::string* err) {
 // ---------------------------------------------------------------------------
 struct GemmPlan {
   int bm = 64, bn = 64, split = 1, kps = 0;
+  int group = 0;  // XCD-aware tile order (xcd_group), set once the plan is final
 };
 
 struct LayerRT {
@@ -278,7 +279,11 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
           R.wgrad = w64;
         }
         R.grouped = (R.dgrad.bm == 64 && R.dgrad.bn == 64) || (R.dgrad.bm == 128 && R.dgrad.bn == 128);
+        R.dgrad.group = xcd_group((int)cdiv(M, R.dgrad.bm), (int)cdiv(R.K, R.dgrad.bn), 1, R.dgrad.bm, R.dgrad.bn);
       }
+      R.fwd.group = xcd_group((int)cdiv(M, R.fwd.bm), (int)cdiv(R.N, R.fwd.bn), 1, R.fwd.bm, R.fwd.bn);
+      R.wgrad.group = xcd_group((int)cdiv(R.N, R.wgrad.bm), (int)cdiv(R.K, R.wgrad.bn), R.wgrad.split, R.wgrad.bm,
+                                R.wgrad.bn);
       R.ldp = ldK;
       R.pstride = int64_t(R.N) * ldK;
       R.part = static_cast<float*>(cv.take(size_t(R.wgrad.split) * R.pstride * 4));
@@ -519,6 +524,7 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
     g.split = 1;
     g.bm = R.fwd.bm;
     g.bn = R.fwd.bn;
+    g.group = R.fwd.group;
     EpiParams e{};
     e.bias = B.buf.param + R.offb;
     e.y = R.y;
@@ -599,6 +605,7 @@ erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStre
     gw.split = R.wgrad.split;
     gw.bm = R.wgrad.bm;
     gw.bn = R.wgrad.bn;
+    gw.group = R.wgrad.group;
     EpiParams ew{};
     ew.part = R.part;
     ew.ldp = R.ldp;
@@ -624,6 +631,7 @@ erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStre
     gd.split = 1;
     gd.bm = R.dgrad.bm;
     gd.bn = R.dgrad.bn;
+    gd.group = R.dgrad.group;
     EpiParams ed{};
     if (R.kind == ERASE_LAYER_CROSS) {
       ed.res = R.g;
@@ -698,7 +706,8 @@ erase_status enqueue_adam(Ctx* c, Enqueuer& q, int b, float* losses, hipStream_t
 erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* labels, int sched, float* losses) {
   const Plan& P = c->P;
   const bool pipeline = sched == ERASE_SCHED_PIPELINE;
-  const bool overlap = sched == ERASE_SCHED_OVERLAP || sched == ERASE_SCHED_OVERLAP_GRAPH || pipeline;
+  const bool adam_end = sched == ERASE_SCHED_OVERLAP_ADAM_END;
+  const bool overlap = sched == ERASE_SCHED_OVERLAP || sched == ERASE_SCHED_OVERLAP_GRAPH || pipeline || adam_end;
   const int nb = (int)P.blk.size();
   const int ns = (int)c->sbs.size();
   hipStream_t sf = c->sf;
@@ -742,12 +751,21 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
       HIPCHK(c, hipStreamWaitEvent(sb, c->ef[b], 0));
       st = enqueue_backward(c, q, b, x, sb, 1 + k);
       if (st != ERASE_OK) return st;
-      st = enqueue_adam(c, q, b, losses, sb, 1 + k);
-      if (st != ERASE_OK) return st;
+      if (!adam_end) {
+        st = enqueue_adam(c, q, b, losses, sb, 1 + k);
+        if (st != ERASE_OK) return st;
+      }
       HIPCHK(c, hipEventRecord(c->eb[b], sb));
     }
     if (!pipeline)
       for (int b = std::max(0, nb - ns); b < nb; ++b) HIPCHK(c, hipStreamWaitEvent(sf, c->eb[b], 0));
+    if (adam_end) {
+      // the optimizer steps once, after every block's backward
+      for (int b = 0; b < nb; ++b) {
+        erase_status st = enqueue_adam(c, q, b, losses, sf, 0);
+        if (st != ERASE_OK) return st;
+      }
+    }
   } else {
     for (int b = 0; b < nb; ++b) {
       erase_status st = enqueue_forward(c, q, b, x, labels, sf, 0);
@@ -920,7 +938,7 @@ erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t s
   if (reinterpret_cast<uintptr_t>(x) % 16 || reinterpret_cast<uintptr_t>(labels) % 4 ||
       reinterpret_cast<uintptr_t>(losses) % 4)
     return ERASE_ERR_INVALID_ARG;
-  if (schedule < ERASE_SCHED_SERIAL || schedule > ERASE_SCHED_PIPELINE) return ERASE_ERR_INVALID_ARG;
+  if (schedule < ERASE_SCHED_SERIAL || schedule > ERASE_SCHED_OVERLAP_ADAM_END) return ERASE_ERR_INVALID_ARG;
   const bool graph = schedule == ERASE_SCHED_SERIAL_GRAPH || schedule == ERASE_SCHED_OVERLAP_GRAPH;
   if (graph && c->timing) return ERASE_ERR_UNSUPPORTED;
   int dev = -1;

@@ -26,7 +26,13 @@ struct GemmDesc {
   int kps;
   int split;
   int bm, bn;  // workgroup tile
+  int group;   // M-tiles per group of the XCD-aware tile order (0: launcher picks)
 };
+
+// M-tiles per group of the XCD-aware tile order (see tile_from in the
+// kernels): the group size that minimises the A and B rows one XCD's
+// contiguous range of tiles touches.
+int xcd_group(int gm, int gn, int split, int bm, int bn);
 
 enum GemmKind { GK_FWD_RELU = 0, GK_FWD_CROSS = 1, GK_WGRAD = 2, GK_DGRAD = 3 };
 

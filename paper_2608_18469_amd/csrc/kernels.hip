@@ -25,6 +25,9 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <climits>
+#include <cstdint>
 #include <type_traits>
 
 #include "internal.h"
@@ -149,6 +152,34 @@ __device__ __forceinline__ T epi_value(const EpiParams& e, int m, int n, float a
 // fp32 tiles keep a 16-byte row pad.
 // The epilogue stages the output tile in LDS and writes it with 16-byte
 // stores, row-major and (forward / input gradient) feature-major.
+// XCD-aware tile order.  A launch's workgroup i runs on XCD (i + c) % 8 for
+// some c, so the workgroups i = r (mod 8) share one XCD and its L2.
+// xcd_linear() renumbers them so that each XCD owns one contiguous range of
+// logical tiles; tile_from() walks logical tiles in groups of `group` M-tiles
+// (M fastest inside a group, then N, then the next group; split-K slices
+// last), so each range is a compact block of output tiles whose A and B rows
+// are fetched into that XCD's L2 once and reused there.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int xcd_linear(int bid, int total) {
+  const int q = total / kXcds, r = total % kXcds;
+  const int x = bid % kXcds, loc = bid / kXcds;
+  return x * q + min(x, r) + loc;
+}
+struct TileIdx {
+  int m, n, z;
+};
+__device__ __forceinline__ TileIdx tile_from(int t, int gm, int gn, int group) {
+  const int per = gm * gn;
+  const int z = t / per;
+  int u = t - z * per;
+  const int gsz = group * gn;
+  const int gi = u / gsz;
+  const int mf = gi * group;
+  const int gh = min(group, gm - mf);
+  u -= gi * gsz;
+  return {mf + u % gh, u / gh, z};
+}
+
 template <typename T, int BM, int BN, int KIND>
 struct GemmSmem {
   static constexpr int BK = GT<T>::BK, KCH = GT<T>::KCH, PITCH = sizeof(T) == 2 ? BK : BK + KCH;
@@ -158,7 +189,7 @@ struct GemmSmem {
   static constexpr int BYTES = MAIN > EPI ? MAIN : EPI;
 };
 
-template <typename T, int BM, int BN, int KIND>
+template <typename T, int BM, int BN, int KIND, int R = 2>
 __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e, int bx, int by, int bz,
                                           char* smem) {
   constexpr int BK = GT<T>::BK, KCH = GT<T>::KCH, KMF = GT<T>::KMF;
@@ -194,7 +225,11 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
 #pragma unroll
   for (int i = 0; i < TM; ++i) rs[i] = 0.f;
 
-  u32x4_t ra0[CA], rb0[CB], ra1[CA], rb1[CB];
+  // R register sets: set r holds k-steps r, r+R, r+2R, ...; the loads of a
+  // k-step are issued R compute phases before it is stored to LDS.  Deeper
+  // look-ahead (R = 3, 4) measured no faster on these shapes: the loop is
+  // bound by the load and LDS paths, not by load latency.
+  u32x4_t ra[R][CA], rb[R][CB];
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
   // k-step j covers [kbeg + j*BK, kbeg + (j+1)*BK); loads past the last
   // k-step are clamped onto it (in bounds, never computed)
@@ -207,23 +242,24 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   const int srow = tid / CPR, sch = tid % CPR;
   const int sofs = srow * PITCH + (SWZ ? (sch ^ (srow & 7)) : sch) * KCH;
 
-  // Statically indexed register sets; macros keep them out of memory.
+  // Register sets are only ever indexed by compile-time constants (the loops
+  // below are fully unrolled), so they stay in VGPRs.
   // Every operand is zero-padded (see GemmDesc): loads are never masked.
-#define ERASE_GLOAD(RA, RB, KSTEP)                                                                    \
+#define ERASE_GLOAD(SET, KSTEP)                                                                       \
   do {                                                                                                \
     const int k0_ = min(kbeg + (KSTEP) * BK, klast);                                                  \
     _Pragma("unroll") for (int i = 0; i < CA; ++i)                                                    \
-        RA[i] = *reinterpret_cast<const u32x4_t*>(pa + (int64_t)(i * RSTEP) * g.lda + k0_);             \
+        ra[SET][i] = *reinterpret_cast<const u32x4_t*>(pa + (int64_t)(i * RSTEP) * g.lda + k0_);        \
     _Pragma("unroll") for (int i = 0; i < CB; ++i)                                                    \
-        RB[i] = *reinterpret_cast<const u32x4_t*>(pb + (int64_t)(i * RSTEP) * g.ldb + k0_);             \
+        rb[SET][i] = *reinterpret_cast<const u32x4_t*>(pb + (int64_t)(i * RSTEP) * g.ldb + k0_);        \
   } while (0)
-#define ERASE_SSTORE(RA, RB, ST)                                                                      \
+#define ERASE_SSTORE(SET, ST)                                                                         \
   do {                                                                                                \
     T* sa_ = lds + (ST) * STAGE;                                                                      \
     _Pragma("unroll") for (int i = 0; i < CA; ++i)                                                    \
-        *reinterpret_cast<u32x4_t*>(sa_ + sofs + i * RSTEP * PITCH) = RA[i];                            \
+        *reinterpret_cast<u32x4_t*>(sa_ + sofs + i * RSTEP * PITCH) = ra[SET][i];                       \
     _Pragma("unroll") for (int i = 0; i < CB; ++i)                                                    \
-        *reinterpret_cast<u32x4_t*>(sa_ + BM * PITCH + sofs + i * RSTEP * PITCH) = RB[i];               \
+        *reinterpret_cast<u32x4_t*>(sa_ + BM * PITCH + sofs + i * RSTEP * PITCH) = rb[SET][i];          \
   } while (0)
 
   // fragment offset within a 16-row slab; slab rows start at multiples of 16,
@@ -263,30 +299,30 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     }                                                                                                 \
   } while (0)
 
-  // stage 0 <- k-step 0; registers: set 1 <- k-step 1, set 0 <- k-step 2
+  // prologue: set r <- k-step r; stage 0 <- k-step 0; set 0 <- k-step R
   if (nk > 0) {
-    ERASE_GLOAD(ra0, rb0, 0);
-    ERASE_GLOAD(ra1, rb1, 1);
-    ERASE_SSTORE(ra0, rb0, 0);
-    ERASE_GLOAD(ra0, rb0, 2);
+#pragma unroll
+    for (int r = 0; r < R; ++r) ERASE_GLOAD(r, r);
+    ERASE_SSTORE(0, 0);
+    ERASE_GLOAD(0, R);
   }
   __syncthreads();
-  int it = 0;
-  for (; it + 1 < nk; it += 2) {
-    // stage 0 holds k-step it, set 1 k-step it+1, set 0 k-step it+2
-    ERASE_COMPUTE(0);
-    ERASE_SSTORE(ra1, rb1, 1);
-    ERASE_GLOAD(ra1, rb1, it + 3);
-    __syncthreads();
-    // stage 1 holds k-step it+1, set 0 k-step it+2, set 1 k-step it+3
-    ERASE_COMPUTE(1);
-    ERASE_SSTORE(ra0, rb0, 0);
-    ERASE_GLOAD(ra0, rb0, it + 4);
-    __syncthreads();
-  }
-  if (it < nk) {  // odd count: the last k-step is in stage 0
-    ERASE_COMPUTE(0);
-    __syncthreads();  // the epilogue below reuses this LDS
+  // phase j: compute k-step j from stage j % 2, store k-step j+1 (set
+  // (j+1) % R) into the other stage, refill that set with k-step j+1+R; one
+  // barrier per phase.  The last phase ends with a barrier, so the epilogue
+  // may reuse the LDS.
+  constexpr int U = (R % 2 == 0) ? R : 2 * R;  // phases per unrolled round
+  for (int base = 0; base < nk; base += U) {
+#pragma unroll
+    for (int p = 0; p < U; ++p) {
+      const int j = base + p;
+      if (j < nk) {
+        ERASE_COMPUTE(p % 2);
+        ERASE_SSTORE((p + 1) % R, (p + 1) % 2);
+        ERASE_GLOAD((p + 1) % R, j + 1 + R);
+        __syncthreads();
+      }
+    }
   }
 #undef ERASE_GLOAD
 #undef ERASE_SSTORE
@@ -387,7 +423,9 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   template <typename T, int BM, int BN>                                                  \
   __global__ __launch_bounds__(256) void NAME(GemmDesc g, EpiParams e) {                 \
     __shared__ __attribute__((aligned(16))) char smem[GemmSmem<T, BM, BN, KIND>::BYTES]; \
-    gemm_body<T, BM, BN, KIND>(g, e, blockIdx.x, blockIdx.y, blockIdx.z, smem);          \
+    const int gm = (g.M + BM - 1) / BM, gn = (g.N + BN - 1) / BN;                        \
+    const TileIdx ti = tile_from(xcd_linear(blockIdx.x, gridDim.x), gm, gn, g.group);   \
+    gemm_body<T, BM, BN, KIND>(g, e, ti.m, ti.n, ti.z, smem);                            \
   }
 ERASE_GEMM_KERNEL(erase_fwd_gemm, GK_FWD_RELU)
 ERASE_GEMM_KERNEL(erase_fwd_cross_gemm, GK_FWD_CROSS)
@@ -402,20 +440,53 @@ template <typename T, int BM, int BN>
 __global__ __launch_bounds__(256) void erase_bwd_gemm(GemmDesc gd, EpiParams ed, GemmDesc gw, EpiParams ew, int nd) {
   constexpr int SD = GemmSmem<T, BM, BN, GK_DGRAD>::BYTES, SW = GemmSmem<T, BM, BN, GK_WGRAD>::BYTES;
   __shared__ __attribute__((aligned(16))) char smem[SD > SW ? SD : SW];
+  // each GEMM is renumbered on its own (workgroups b and b + 8 still share an
+  // XCD after subtracting nd), so both spread evenly over the XCDs
   const int b = blockIdx.x;
   if (b < nd) {
-    const int gx = (gd.M + BM - 1) / BM;
-    gemm_body<T, BM, BN, GK_DGRAD>(gd, ed, b % gx, b / gx, 0, smem);
+    const TileIdx ti = tile_from(xcd_linear(b, nd), (gd.M + BM - 1) / BM, (gd.N + BN - 1) / BN, gd.group);
+    gemm_body<T, BM, BN, GK_DGRAD>(gd, ed, ti.m, ti.n, 0, smem);
   } else {
-    const int i = b - nd;
-    const int gx = (gw.M + BM - 1) / BM, gy = (gw.N + BN - 1) / BN;
-    gemm_body<T, BM, BN, GK_WGRAD>(gw, ew, i % gx, (i / gx) % gy, i / (gx * gy), smem);
+    const int nw = gridDim.x - nd;
+    const TileIdx ti = tile_from(xcd_linear(b - nd, nw), (gw.M + BM - 1) / BM, (gw.N + BN - 1) / BN, gw.group);
+    gemm_body<T, BM, BN, GK_WGRAD>(gw, ew, ti.m, ti.n, ti.z, smem);
   }
 }
 
+int xcd_group(int gm, int gn, int split, int bm, int bn) {
+  // one XCD's range: L tiles from the start of a split-K slice
+  const int64_t per = int64_t(gm) * gn;
+  const int64_t L = std::max<int64_t>(1, std::min<int64_t>(per, per * split / kXcds));
+  int best = 1;
+  int64_t bestc = INT64_MAX;
+  for (int g = 1; g <= gm; ++g) {
+    int64_t mc, nc;
+    if (L <= int64_t(g) * gn) {
+      mc = std::min<int64_t>(g, L);
+      nc = (L + g - 1) / g;
+    } else {
+      mc = std::min<int64_t>(gm, (L + int64_t(g) * gn - 1) / (int64_t(g) * gn) * g);
+      nc = gn;
+    }
+    const int64_t c = mc * bm + nc * bn;
+    if (c < bestc) {
+      bestc = c;
+      best = g;
+    }
+  }
+  return best;
+}
+
+static GemmDesc with_group(const GemmDesc& g0, int BM, int BN) {
+  GemmDesc g = g0;
+  if (g.group <= 0) g.group = xcd_group((g.M + BM - 1) / BM, (g.N + BN - 1) / BN, g.split, BM, BN);
+  return g;
+}
+
 template <typename T, int BM, int BN>
-static hipError_t launch_gemm_t(int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s, const LaunchEv& ev) {
-  dim3 grid((g.M + BM - 1) / BM, (g.N + BN - 1) / BN, g.split), block(256);
+static hipError_t launch_gemm_t(int kind, const GemmDesc& g0, const EpiParams& e, hipStream_t s, const LaunchEv& ev) {
+  const GemmDesc g = with_group(g0, BM, BN);
+  dim3 grid(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN) * g.split), block(256);
   switch (kind) {
     case GK_FWD_RELU: ERASE_LAUNCH((erase_fwd_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;
     case GK_FWD_CROSS: ERASE_LAUNCH((erase_fwd_cross_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;
@@ -427,8 +498,9 @@ static hipError_t launch_gemm_t(int kind, const GemmDesc& g, const EpiParams& e,
 }
 
 template <typename T, int BM, int BN>
-static hipError_t launch_bwd_t(const GemmDesc& gd, const EpiParams& ed, const GemmDesc& gw, const EpiParams& ew,
+static hipError_t launch_bwd_t(const GemmDesc& gd0, const EpiParams& ed, const GemmDesc& gw0, const EpiParams& ew,
                                hipStream_t s, const LaunchEv& ev) {
+  const GemmDesc gd = with_group(gd0, BM, BN), gw = with_group(gw0, BM, BN);
   const int nd = ((gd.M + BM - 1) / BM) * ((gd.N + BN - 1) / BN);
   const int nw = ((gw.M + BM - 1) / BM) * ((gw.N + BN - 1) / BN) * gw.split;
   ERASE_LAUNCH((erase_bwd_gemm<T, BM, BN>), dim3(nd + nw), dim3(256), 0, s, ev, gd, ed, gw, ew, nd);

@@ -18,7 +18,7 @@ from tests.gpu_util import assert_bit_identical, check_bf16, compare, run_gpu, r
 
 pytestmark = pytest.mark.gpu
 
-SCHEDS = ["serial", "overlap", "serial_graph", "overlap_graph", "pipeline"]
+SCHEDS = ["serial", "overlap", "serial_graph", "overlap_graph", "pipeline", "overlap_adam_end"]
 
 
 def _say(*a):
