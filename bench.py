@@ -38,7 +38,7 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 METRIC = "train samples/s, 6-block CTR @1 MI355X; ERASE vs serial speedup; MFMA util %"
 KIND_SYMBOL = {"prologue": "erase_prologue", "fwd_gemm": "erase_fwd_gemm", "head_bce": "erase_head_bce",
                "wgrad_gemm": "erase_wgrad_gemm", "dgrad_gemm": "erase_dgrad_gemm", "adam": "erase_adam",
-               "bwd_gemm": "erase_bwd_gemm"}
+               "bwd_gemm": "erase_bwd_gemm", "fwd_head_gemm": "erase_fwd_head_gemm"}
 
 
 def kernel_class(r, bf16=True):
@@ -166,8 +166,9 @@ def main():
     ap.add_argument("--cpu-budget-1t", type=float, default=6.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--schedules", default="serial,overlap,serial_graph,overlap_graph,pipeline")
-    ap.add_argument("--bwd-streams", type=int, default=1,
-                    help="backward streams of the ERASE schedules (block b uses stream b %% n)")
+    ap.add_argument("--bwd-streams", type=int, default=2,
+                    help="backward streams of the ERASE schedules (block b uses stream b %% n); 2 measured "
+                         "fastest on ctr_mlp (1 leaves the backward chain serial, 3+ exceed the 4 hardware queues)")
     ap.add_argument("--verbose", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the run, copy a buffer of this many MiB once (a plain copy kernel of known size "

@@ -205,7 +205,10 @@ erase_status erase_refresh_weights(void* ctx);
 typedef struct {
   int32_t kind;      /* 0 prologue, 1 forward GEMM, 2 head+loss, 3 weight-grad GEMM,
                         4 input-grad GEMM, 5 Adam, 6 input- and weight-grad GEMMs of one
-                        layer in one launch, 7 empty interval (no kernel) */
+                        layer in one launch, 7 empty interval (no kernel), 8 last
+                        forward GEMM of a block with the head+loss in its epilogue
+                        (used when the last layer is linear+ReLU and at most 128
+                        wide in bf16, 64 in fp32; kind 2 does not appear then) */
   int32_t block;     /* block index, -1 for the step prologue */
   int32_t layer;     /* layer index within the block, -1 if none */
   int32_t stream;    /* 0 forward stream, 1 + k backward stream k */
@@ -213,7 +216,7 @@ typedef struct {
   float end_ms;
   int32_t tile_m;    /* GEMM workgroup tile rows (0 for non-GEMM kernels) */
   int32_t tile_n;    /* GEMM workgroup tile columns */
-  int32_t split;     /* GEMM contraction slices (grid z) */
+  int32_t split;     /* GEMM contraction slices */
   int32_t grid;      /* workgroups launched */
   double flops;      /* algorithmic floating-point operations of the launch */
   double bytes;      /* algorithmic HBM bytes of the launch */

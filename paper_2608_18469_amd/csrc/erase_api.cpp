@@ -124,7 +124,8 @@ struct BlockRT {
   int L = 0;
   LayerRT layer[kMaxLayers];
   int64_t nparam = 0, off_w = 0, off_c = 0;
-  int nhead = 0;
+  int nhead = 0;      // head partial rows (M-tiles of the head)
+  bool head_fused = false;  // head+loss in the last forward GEMM's epilogue
   float* pdw = nullptr;
   float* pdc = nullptr;
   float* ploss = nullptr;
@@ -295,7 +296,21 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
     B.off_c = off;
     off += 1;
     B.nparam = off;
-    B.nhead = (int)cdiv(M, head_rows(NL, esz));
+    // Head+loss fused into the last forward GEMM when one tile spans the
+    // whole width: 32 x 128 (bf16) or 64 x 64 (fp32) workgroups over M.  The
+    // head epilogue is a chain of short dependent steps per workgroup, so
+    // 32-row tiles (twice the workgroups) beat 64-row ones (9.0 vs 12.1 us on
+    // the 4096 x 128 CTR layer).
+    LayerRT& RL = B.layer[B.L - 1];
+    B.head_fused = RL.kind == ERASE_LAYER_LINEAR_RELU && NL <= (P->bf16 ? 128 : 64);
+    if (B.head_fused) {
+      RL.fwd.bm = P->bf16 ? 32 : 64;
+      RL.fwd.bn = P->bf16 ? 128 : 64;
+      RL.fwd.group = xcd_group((int)cdiv(M, RL.fwd.bm), 1, 1, RL.fwd.bm, RL.fwd.bn);
+      B.nhead = (int)cdiv(M, RL.fwd.bm);
+    } else {
+      B.nhead = (int)cdiv(M, head_rows(NL, esz));
+    }
     B.pdw = static_cast<float*>(cv.take(size_t(B.nhead) * NL * 4));
     B.pdc = static_cast<float*>(cv.take(size_t(B.nhead) * 4));
     B.ploss = static_cast<float*>(cv.take(size_t(B.nhead) * 4));
@@ -531,7 +546,8 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
     e.ldy = R.ldy;
     e.yt = R.yt;
     e.ldyt = R.ldyt;
-    const int kind = R.kind == ERASE_LAYER_CROSS ? GK_FWD_CROSS : GK_FWD_RELU;
+    const bool fused = B.head_fused && l == B.L - 1;
+    const int kind = R.kind == ERASE_LAYER_CROSS ? GK_FWD_CROSS : fused ? GK_FWD_HEAD : GK_FWD_RELU;
     if (kind == GK_FWD_CROSS) {
       e.x0 = x0;
       e.ldx0 = ldx0;
@@ -542,9 +558,30 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
     cost.flops = 2.0 * M * R.N * R.K;
     cost.bytes = double(esz) * (double(M) * R.K + double(R.N) * R.K + double(M) * R.N * (R.yt ? 2 : 1)) + 4.0 * R.N +
                  (kind == GK_FWD_CROSS ? 2.0 * esz * M * R.N : 0.0);
+    if (fused) {
+      // z leaves the chip only when the next block reads it
+      if (!R.yt) e.y = nullptr;
+      e.hw = B.buf.param + B.off_w;
+      e.hc = B.buf.param + B.off_c;
+      e.labels = labels;
+      e.lam = B.lam;
+      e.inv_m = 1.0f / float(M);
+      e.dmn = R.dmn;
+      e.lddmn = R.lddmn;
+      e.dnm = R.dnm;
+      e.lddnm = R.lddnm;
+      e.pdw = B.pdw;
+      e.pdc = B.pdc;
+      e.ploss = B.ploss;
+      cost.flops += 4.0 * M * R.N;
+      cost.bytes = double(esz) * (double(M) * R.K + double(R.N) * R.K + double(M) * R.N * ((R.yt ? 2 : 0) + 1 +
+                                                                                           (R.dmn ? 1 : 0))) +
+                   4.0 * R.N + 4.0 * M + 4.0 * R.N + 4.0 * B.nhead * (R.N + 2);
+    }
     const int bf = P.bf16;
-    RUN(1, b, l, sid, s, cost, [&](const LaunchEv& ev) { return launch_gemm(bf, kind, g, e, s, ev); });
+    RUN(fused ? 8 : 1, b, l, sid, s, cost, [&](const LaunchEv& ev) { return launch_gemm(bf, kind, g, e, s, ev); });
   }
+  if (B.head_fused) return ERASE_OK;
   const LayerRT& Rl = B.layer[B.L - 1];
   HeadArgs h{};
   h.z = Rl.y;
@@ -786,7 +823,7 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
 int launches_per_step(const Plan& P) {
   int n = 1;  // prologue
   for (const BlockRT& B : P.blk) {
-    n += B.L + 1 + 1 + 1;  // forward GEMMs, head, first layer's weight gradient, Adam
+    n += B.L + (B.head_fused ? 0 : 1) + 1 + 1;  // forward GEMMs, head, first layer's weight gradient, Adam
     for (int l = 1; l < B.L; ++l) n += B.layer[l].grouped ? 1 : 2;
   }
   return n;

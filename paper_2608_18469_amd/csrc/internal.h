@@ -34,7 +34,10 @@ struct GemmDesc {
 // contiguous range of tiles touches.
 int xcd_group(int gm, int gn, int split, int bm, int bn);
 
-enum GemmKind { GK_FWD_RELU = 0, GK_FWD_CROSS = 1, GK_WGRAD = 2, GK_DGRAD = 3 };
+// GK_FWD_HEAD: the last linear+ReLU layer of a block with the local head
+// (Section 2.1) fused into its epilogue; the tile spans the whole width
+// (N <= BN), so each workgroup holds complete rows of the block output.
+enum GemmKind { GK_FWD_RELU = 0, GK_FWD_CROSS = 1, GK_WGRAD = 2, GK_DGRAD = 3, GK_FWD_HEAD = 4 };
 
 // Optional timing events of one launch: when set, the kernel is dispatched
 // with hipExtLaunchKernelGGL, which stamps e0/e1 at the kernel's own start
@@ -61,6 +64,15 @@ struct EpiParams {
   void* dmn;  int64_t lddmn;
   void* dnm;  int64_t lddnm;
   int below_cross;
+  // fused head: s = z hw + hc, loss and ds = lam (sigmoid(s) - y) inv_m,
+  // dz = ds hw [z > 0] into dmn (nullable) / dnm, per-M-tile partials
+  const float* hw;
+  const float* hc;
+  const float* labels;
+  float lam, inv_m;
+  float* pdw;    // [M-tiles][N]
+  float* pdc;    // [M-tiles]
+  float* ploss;  // [M-tiles]
 };
 
 hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s,
@@ -119,8 +131,10 @@ hipError_t launch_head(int bf16, const HeadArgs& a, hipStream_t s, const LaunchE
 // Fused split-reduction + Adam + GEMM-copy refresh for one block.  The
 // segment table lives in device memory (written once at init).  A segment
 // is a [rows][cols] parameter matrix (a vector is one row) processed in
-// tiles of ADAM_TR rows x ADAM_TC columns, one workgroup per tile.
-constexpr int ADAM_TR = 8, ADAM_TC = 256;
+// tiles of ADAM_TR rows x ADAM_TC columns, one workgroup per tile (a
+// thread owns 4 columns of one row of a matrix tile, one element of a
+// vector).
+constexpr int ADAM_TR = 4, ADAM_TC = 256;
 struct AdamSeg {
   float* p; float* m; float* v; float* g;   // flat [rows*cols] fp32 (g nullable)
   const float* part;                        // partial sums [nsplit][rows][ldpart]

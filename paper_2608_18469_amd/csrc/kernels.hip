@@ -51,12 +51,9 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));  // 16-byte chunk 
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x0040u);  // NaN stays NaN
-  u += 0x7fffu + ((u >> 16) & 1u);  // round to nearest, ties to even
-  return (uint16_t)(u >> 16);
-}
+// gfx950 converts in hardware (v_cvt_pk_bf16_f32): round to nearest, ties to
+// even, NaN stays NaN, no branch.
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 
 template <typename T> __device__ __forceinline__ float ldf(const T* p);
 template <> __device__ __forceinline__ float ldf<float>(const float* p) { return *p; }
@@ -117,7 +114,7 @@ __device__ __forceinline__ float sum8_bf16(const u32x4_t& a) {
 // Value of the fused epilogue at (m, n), m < M and n < N, in the output type.
 template <typename T, int KIND>
 __device__ __forceinline__ T epi_value(const EpiParams& e, int m, int n, float acc, float bn) {
-  if constexpr (KIND == GK_FWD_RELU) {
+  if constexpr (KIND == GK_FWD_RELU || KIND == GK_FWD_HEAD) {
     const float v = acc + bn;
     return cvt<T>(v < 0.f ? 0.f : v);  // keeps NaN, like max(h, 0) on the host
   } else if constexpr (KIND == GK_FWD_CROSS) {
@@ -185,8 +182,11 @@ struct GemmSmem {
   static constexpr int BK = GT<T>::BK, KCH = GT<T>::KCH, PITCH = sizeof(T) == 2 ? BK : BK + KCH;
   using OT = typename std::conditional<KIND == GK_WGRAD, float, T>::type;
   static constexpr int MAIN = 2 * (BM + BN) * PITCH * (int)sizeof(T);
-  static constexpr int EPI = BM * (BN + 16 / (int)sizeof(OT)) * (int)sizeof(OT);
-  static constexpr int BYTES = MAIN > EPI ? MAIN : EPI;
+  static constexpr int TILE = BM * (BN + 16 / (int)sizeof(OT)) * (int)sizeof(OT);
+  // fused head: hw[BN], labels[BM], ds[BM], loss[BM], dw[2][BN], c (fp32),
+  // past both the main-loop stages and the output tile
+  static constexpr int HOFF = MAIN > TILE ? MAIN : TILE;
+  static constexpr int BYTES = HOFF + (KIND == GK_FWD_HEAD ? (3 * BN + 3 * BM + 4) * 4 : 0);
 };
 
 template <typename T, int BM, int BN, int KIND, int R = 2>
@@ -219,6 +219,14 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  if constexpr (KIND == GK_FWD_HEAD) {
+    // head inputs into LDS now; their latency hides behind the main loop
+    float* hs = reinterpret_cast<float*>(smem + GemmSmem<T, BM, BN, KIND>::HOFF);
+    for (int n = tid; n < BN; n += 256) hs[n] = n < g.N ? e.hw[n] : 0.f;
+    for (int r = tid; r < BM; r += 256) hs[BN + r] = m0 + r < g.M ? e.labels[m0 + r] : 0.f;
+    if (tid == 0) hs[3 * BN + 3 * BM] = e.hc[0];
+  }
 
   const bool do_rows = (KIND == GK_WGRAD) && e.bpart != nullptr && by == 0 && wn == 0;
   float rs[TM];
@@ -339,32 +347,11 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     }
   }
 
-  // epilogue: values -> LDS tile [BM][OPITCH] -> 16-byte stores
+  // epilogue: values -> LDS tile [BM][OPITCH] -> 16-byte row-major stores.
+  // The feature-major copy goes out straight from the accumulators: a lane
+  // holds four consecutive rows of one column (one 8- or 16-byte store).
   OT* sc = reinterpret_cast<OT*>(smem);
   const int M = g.M, N = g.N;
-#pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int nl = wn * WN + j * 16 + (lane & 15);
-    const int n = n0 + nl;
-    float bn = 0.f;
-    if constexpr (KIND == GK_FWD_RELU || KIND == GK_FWD_CROSS) bn = (n < N) ? e.bias[n] : 0.f;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int ml = wm * WM + i * 16 + (lane >> 4) * 4 + q;
-        const int m = m0 + ml;
-        OT v;
-        if constexpr (KIND == GK_WGRAD) {
-          v = acc[i][j][q];
-        } else {
-          v = (m < M && n < N) ? epi_value<T, KIND>(e, m, n, acc[i][j][q], bn) : OT(0);
-        }
-        sc[ml * OPITCH + nl] = v;
-      }
-    }
-  }
-  __syncthreads();
   OT* omn;
   int64_t ldmn;
   OT* onm = nullptr;
@@ -383,6 +370,59 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     onm = static_cast<OT*>(e.yt);
     ldnm = e.ldyt;
   }
+  // pass 1 (every load of the epilogue): values into the LDS tile and back
+  // into the accumulators; pass 2 (stores only): the feature-major copy.
+  // Keeping loads and stores apart avoids waits on the stores (on gfx9 the
+  // load counter also counts stores).
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int nl = wn * WN + j * 16 + (lane & 15);
+    const int n = n0 + nl;
+    float bn = 0.f;
+    if constexpr (KIND == GK_FWD_RELU || KIND == GK_FWD_CROSS || KIND == GK_FWD_HEAD) bn = (n < N) ? e.bias[n] : 0.f;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int ml = wm * WM + i * 16 + (lane >> 4) * 4 + q;
+        const int m = m0 + ml;
+        OT v;
+        if constexpr (KIND == GK_WGRAD) {
+          v = acc[i][j][q];
+        } else {
+          v = (m < M && n < N) ? epi_value<T, KIND>(e, m, n, acc[i][j][q], bn) : OT(0);
+          acc[i][j][q] = asf(v);
+        }
+        sc[ml * OPITCH + nl] = v;
+      }
+    }
+  }
+  if constexpr (KIND != GK_WGRAD) {
+    if (onm) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int n = n0 + wn * WN + j * 16 + (lane & 15);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4;
+          if (n < N && m < M) {
+            OT v4[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) v4[q] = cvt<OT>(acc[i][j][q]);
+            OT* dst = onm + (int64_t)n * ldnm + m;
+            if (m + 4 <= M) {
+              st4(dst, v4);
+            } else {
+#pragma unroll
+              for (int q = 0; q < 4; ++q)
+                if (m + q < M) dst[q] = v4[q];
+            }
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
   if (omn) {
     constexpr int CPRO = BN / OCH;
     for (int c = tid; c < BM * CPRO; c += 256) {
@@ -398,22 +438,120 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
       }
     }
   }
-  if (onm) {
-    constexpr int IPC = BM / OCH;  // items of OCH rows per column
-    for (int c = tid; c < BN * IPC; c += 256) {
-      const int nl = c / IPC, ml = (c % IPC) * OCH;
-      const int n = n0 + nl, m = m0 + ml;
-      if (n >= N || m >= M) continue;
-      OT o[OCH];
+
+  if constexpr (KIND == GK_FWD_HEAD) {
+    // Fused local head (Section 2.1, Eq. 2).  The tile holds complete rows
+    // of the block output z (N <= BN, one tile column, n0 = 0):
+    //   s_m = sum_n z_mn w_n + c,  loss_m = max(s,0) - s y_m + log1p(e^-|s|),
+    //   ds_m = lam (sigmoid(s_m) - y_m) / M,  dz_mn = ds_m w_n [z_mn > 0]
+    // in both layouts, and this M-tile's partials dw_n = sum_m z_mn ds_m,
+    // dc = sum_m ds_m and sum_m loss_m, every sum in a fixed order.
+    float* s_w = reinterpret_cast<float*>(smem + GemmSmem<T, BM, BN, KIND>::HOFF);
+    float* s_y = s_w + BN;
+    float* s_ds = s_y + BM;
+    float* s_l = s_ds + BM;
+    float* s_dw = s_l + BM;  // [2][BN]: per row-half of the waves
+    const float hc = s_dw[2 * BN];
+    constexpr int KC = OCH;
+    {  // logits: TPR lanes per row over contiguous column slices, fixed butterfly
+      constexpr int TPR = 256 / BM;
+      static_assert(TPR * BM == 256 && (TPR & (TPR - 1)) == 0 && TPR <= 64, "head rows do not match 256 threads");
+      constexpr int CPT = BN / TPR;
+      const int r = tid / TPR, jj = tid % TPR;
+      float part = 0.f;
+#pragma unroll 8
+      for (int q = 0; q < CPT; ++q) part = fmaf(asf(sc[r * OPITCH + jj * CPT + q]), s_w[jj * CPT + q], part);
+      for (int off = 1; off < TPR; off <<= 1) part += __shfl_xor(part, off, 64);
+      if (jj == 0) {
+        float ds = 0.f, l = 0.f;
+        if (m0 + r < M) {
+          const float sv = part + hc;
+          const float yv = s_y[r];
+          const float en = __expf(-fabsf(sv));
+          const float sig = sv >= 0.f ? 1.f / (1.f + en) : en / (1.f + en);
+          ds = e.lam * (sig - yv) * e.inv_m;
+          l = fmaxf(sv, 0.f) - sv * yv + log1pf(en);
+        }
+        s_ds[r] = ds;
+        s_l[r] = l;
+      }
+    }
+    __syncthreads();
+    // from the accumulators: dz feature-major (A operand of the last layer's
+    // weight gradient) and this wave's column sums of z ds
 #pragma unroll
-      for (int q = 0; q < OCH; ++q) o[q] = sc[(ml + q) * OPITCH + nl];
-      OT* dst = onm + (int64_t)n * ldnm + m;
-      if (m + OCH <= M) {
-        uint4 v;
-        __builtin_memcpy(&v, o, 16);
-        *reinterpret_cast<uint4*>(dst) = v;
-      } else {
-        for (int q = 0; q < OCH && m + q < M; ++q) dst[q] = o[q];
+    for (int j = 0; j < TN; ++j) {
+      const int nl = wn * WN + j * 16 + (lane & 15);
+      const int n = n0 + nl;
+      const float w = s_w[nl];
+      float dwp = 0.f;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int ml0 = wm * WM + i * 16 + (lane >> 4) * 4;
+        OT d4[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float zq = acc[i][j][q];  // z as stored (zero outside M x N)
+          const float ds = s_ds[ml0 + q];
+          d4[q] = cvt<T>(zq > 0.f ? ds * w : 0.f);
+          dwp = fmaf(zq, ds, dwp);
+        }
+        const int m = m0 + ml0;
+        if (n < N && m < M) {
+          OT* dst = static_cast<OT*>(e.dnm) + (int64_t)n * e.lddnm + m;
+          if (m + 4 <= M) {
+            st4(dst, d4);
+          } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              if (m + q < M) dst[q] = d4[q];
+          }
+        }
+      }
+      // lanes l, l^16, l^32, l^48 hold the same column (rows 4 apart)
+      dwp += __shfl_xor(dwp, 16, 64);
+      dwp += __shfl_xor(dwp, 32, 64);
+      if (lane < 16) s_dw[wm * BN + nl] = dwp;
+    }
+    // dz row-major (input gradient of the last layer's GEMM; nullable)
+    if (e.dmn) {
+      constexpr int CPRO = BN / KC;
+      for (int c = tid; c < BM * CPRO; c += 256) {
+        const int r = c / CPRO, nl = (c % CPRO) * KC;
+        const int m = m0 + r, n = n0 + nl;
+        if (m >= M || n >= N) continue;
+        const float ds = s_ds[r];
+        OT o[KC];
+#pragma unroll
+        for (int q = 0; q < KC; ++q) {
+          const float zq = asf(sc[r * OPITCH + nl + q]);
+          o[q] = cvt<T>(zq > 0.f ? ds * s_w[nl + q] : 0.f);
+        }
+        OT* dst = static_cast<OT*>(e.dmn) + (int64_t)m * e.lddmn + n;
+        if (n + KC <= N) {
+          uint4 v;
+          __builtin_memcpy(&v, o, 16);
+          *reinterpret_cast<uint4*>(dst) = v;
+        } else {
+#pragma unroll
+          for (int q = 0; q < KC; ++q)
+            if (n + q < N) dst[q] = o[q];
+        }
+      }
+    }
+    __syncthreads();
+    for (int n = tid; n < N; n += 256) e.pdw[(int64_t)bx * N + n] = s_dw[n] + s_dw[BN + n];
+    if (tid < 64) {
+      float d = 0.f, l = 0.f;
+      for (int r = tid; r < BM; r += 64) {
+        d += s_ds[r];
+        l += s_l[r];
+      }
+      d = wave_sum(d);
+      l = wave_sum(l);
+      if (tid == 0) {
+        e.pdc[bx] = d;
+        e.ploss[bx] = l;
       }
     }
   }
@@ -431,6 +569,7 @@ ERASE_GEMM_KERNEL(erase_fwd_gemm, GK_FWD_RELU)
 ERASE_GEMM_KERNEL(erase_fwd_cross_gemm, GK_FWD_CROSS)
 ERASE_GEMM_KERNEL(erase_wgrad_gemm, GK_WGRAD)
 ERASE_GEMM_KERNEL(erase_dgrad_gemm, GK_DGRAD)
+ERASE_GEMM_KERNEL(erase_fwd_head_gemm, GK_FWD_HEAD)
 #undef ERASE_GEMM_KERNEL
 
 // One launch for both backward GEMMs of a layer (they read the same
@@ -492,6 +631,15 @@ static hipError_t launch_gemm_t(int kind, const GemmDesc& g0, const EpiParams& e
     case GK_FWD_CROSS: ERASE_LAUNCH((erase_fwd_cross_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;
     case GK_WGRAD: ERASE_LAUNCH((erase_wgrad_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;
     case GK_DGRAD: ERASE_LAUNCH((erase_dgrad_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;
+    case GK_FWD_HEAD:
+      // the tile must span the whole width; 32- and 64-row tiles only
+      if constexpr (BM <= 64) {
+        if (g.N > BN) return hipErrorInvalidValue;
+        ERASE_LAUNCH((erase_fwd_head_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e);
+      } else {
+        return hipErrorInvalidValue;
+      }
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -526,6 +674,7 @@ hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e
     if (g.bm == 128 && g.bn == 64) return launch_gemm_t<uint16_t, 128, 64>(kind, g, e, s, ev);
     if (g.bm == 64 && g.bn == 128) return launch_gemm_t<uint16_t, 64, 128>(kind, g, e, s, ev);
     if (g.bm == 64 && g.bn == 64) return launch_gemm_t<uint16_t, 64, 64>(kind, g, e, s, ev);
+    if (g.bm == 32 && g.bn == 128 && kind == GK_FWD_HEAD) return launch_gemm_t<uint16_t, 32, 128>(kind, g, e, s, ev);
   } else {
     if (g.bm == 64 && g.bn == 64) return launch_gemm_t<float, 64, 64>(kind, g, e, s, ev);
   }
@@ -755,98 +904,166 @@ __device__ __forceinline__ int find_seg(const AdamArgs& a, int64_t chunk) {
 // Thread = one column of an ADAM_TR-row tile: rows are read and written
 // coalesced across the workgroup, and the transposed GEMM copy gets the
 // tile's ADAM_TR consecutive values of one column as 16-byte stores.
+// 16-byte access at 4-byte alignment (rows of the flat parameter arrays
+// start anywhere; gfx950 serves unaligned vector accesses)
+typedef float f32x4u_t __attribute__((ext_vector_type(4), aligned(4)));
+
+__device__ __forceinline__ void adam_elem(float& p, float& m, float& v, float g, float b1, float b2, float step,
+                                          float bc2s, float eps) {
+  m = fmaf(b1, m, (1.f - b1) * g);
+  v = fmaf(b2, v, (1.f - b2) * g * g);
+  p = p - step * m / (sqrtf(v) / bc2s + eps);
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
-  constexpr int TR = ADAM_TR;
   const int64_t chunk = blockIdx.x;
   const AdamSeg sg = a.seg[find_seg(a, chunk)];
   const float step = a.hyper[0];  // lr / (1 - beta1^t)
   const float bc2s = a.hyper[1];  // sqrt(1 - beta2^t)
-  const float b1 = a.beta1, b2 = a.beta2;
+  const float b1 = a.beta1, b2 = a.beta2, eps = a.eps;
   const int tile = (int)(chunk - sg.chunk0);
-  const int r0 = (tile / sg.tcols) * TR;
-  const int c = (tile % sg.tcols) * ADAM_TC + (int)threadIdx.x;
-  const bool colok = c < sg.cols;
-  const int cc = colok ? c : 0;  // clamped: loads stay in bounds
   auto P = gmem(sg.p);
   auto Mo = gmem(sg.m);
   auto V = gmem(sg.v);
   auto PART = gmem(sg.part);
 
-  bool ok[TR];
-  int64_t fi[TR], po[TR];
-  float g[TR], pv[TR], mv[TR], vv[TR];
-#pragma unroll
-  for (int q = 0; q < TR; ++q) {
-    const int r = r0 + q;
-    ok[q] = colok && r < sg.rows;
-    const int rr = r < sg.rows ? r : 0;
-    fi[q] = (int64_t)rr * sg.cols + cc;
-    po[q] = (int64_t)rr * sg.ldpart + cc;
-    g[q] = 0.f;
-    pv[q] = P[fi[q]];
-    mv[q] = Mo[fi[q]];
-    vv[q] = V[fi[q]];
-  }
-  // ordered reduction of the split partials: slice 0, 1, ..., nsplit-1
   if (sg.rows == 1) {
     // a vector (bias or head parameter): one element per thread, possibly
-    // many partials (one per head workgroup): 32 loads in flight per batch
+    // many partials (one per head workgroup), 32 loads in flight per batch,
+    // added in slice order
+    const int c = tile * ADAM_TC + (int)threadIdx.x;
+    const bool ok = c < sg.cols;
+    const int cc = ok ? c : 0;  // clamped: loads stay in bounds
+    float p = P[cc], m = Mo[cc], v = V[cc], g = 0.f;
     constexpr int ZV = 32;
     for (int z0 = 0; z0 < sg.nsplit; z0 += ZV) {
       float tv[ZV];
 #pragma unroll
-      for (int j = 0; j < ZV; ++j) tv[j] = (z0 + j < sg.nsplit) ? PART[po[0] + (int64_t)(z0 + j) * sg.pstride] : 0.f;
+      for (int j = 0; j < ZV; ++j) tv[j] = (z0 + j < sg.nsplit) ? PART[cc + (int64_t)(z0 + j) * sg.pstride] : 0.f;
 #pragma unroll
       for (int j = 0; j < ZV; ++j)
-        if (z0 + j < sg.nsplit) g[0] += tv[j];
+        if (z0 + j < sg.nsplit) g += tv[j];
+    }
+    adam_elem(p, m, v, g, b1, b2, step, bc2s, eps);
+    if (ok) {
+      if (sg.g) gmem(sg.g)[c] = g;
+      Mo[c] = m;
+      V[c] = v;
+      P[c] = p;
+      if (sg.sh) gmem(static_cast<T*>(sg.sh))[c] = cvt<T>(p);
     }
   } else {
-    // slice-outer, four slices in flight: TR*4 independent loads, added in
-    // slice order
+    // a matrix: a workgroup covers ADAM_TR (4) rows x ADAM_TC (256) columns,
+    // a thread 4 consecutive columns of one row (16-byte loads and stores)
+    static_assert(ADAM_TR == 4 && ADAM_TC == 256, "matrix tile is 4 rows x 64 threads x 4 columns");
+    const int r0 = (tile / sg.tcols) * ADAM_TR;
+    const int r = r0 + (int)(threadIdx.x >> 6);
+    const int c0 = (tile % sg.tcols) * ADAM_TC + (int)(threadIdx.x & 63) * 4;
+    const bool any = r < sg.rows && c0 < sg.cols;
+    const bool full = c0 + 4 <= sg.cols;
+    const int rr = any ? r : 0, cc = any ? c0 : 0;  // clamped: loads stay in bounds
+    const int64_t fi = (int64_t)rr * sg.cols + cc;
+    // split partials: rows padded to a multiple of 64 columns, so the 4
+    // columns from c0 are in bounds and 16-byte aligned
+    const int64_t po = (int64_t)rr * sg.ldpart + cc;
+    // Ordered reduction of the split partials, slices added in order 0, 1,
+    // ...  Four slices per batch; the first batch is issued together with the
+    // parameter loads.  Slices past the last one are clamped loads added as
+    // zeros (a select, not a branch, so no wait splits a batch).
     constexpr int ZS = 4;
-    for (int z0 = 0; z0 < sg.nsplit; z0 += ZS) {
-      float tv[ZS][TR];
-#pragma unroll
-      for (int j = 0; j < ZS; ++j) {
-        const int64_t zo = (int64_t)min(z0 + j, sg.nsplit - 1) * sg.pstride;
-#pragma unroll
-        for (int q = 0; q < TR; ++q) tv[j][q] = PART[zo + po[q]];
-      }
+    f32x4_t tv[ZS];
+    auto load_batch = [&](int z0) {
 #pragma unroll
       for (int j = 0; j < ZS; ++j)
-        if (z0 + j < sg.nsplit) {
+        tv[j] = *reinterpret_cast<const __attribute__((address_space(1))) f32x4_t*>(
+            PART + (int64_t)min(z0 + j, sg.nsplit - 1) * sg.pstride + po);
+    };
+    float g[4] = {0.f, 0.f, 0.f, 0.f};
+    auto add_batch = [&](int z0) {
 #pragma unroll
-          for (int q = 0; q < TR; ++q) g[q] += tv[j][q];
-        }
-    }
-  }
-  T o[TR];
+      for (int j = 0; j < ZS; ++j) {
+        const bool in = z0 + j < sg.nsplit;
 #pragma unroll
-  for (int q = 0; q < TR; ++q) {
-    const float m = fmaf(b1, mv[q], (1.f - b1) * g[q]);
-    const float v = fmaf(b2, vv[q], (1.f - b2) * g[q] * g[q]);
-    const float p = pv[q] - step * m / (sqrtf(v) / bc2s + a.eps);
-    o[q] = cvt<T>(p);
-    if (!ok[q]) continue;
-    if (sg.g) gmem(sg.g)[fi[q]] = g[q];
-    Mo[fi[q]] = m;
-    V[fi[q]] = v;
-    P[fi[q]] = p;
-    if (sg.sh) gmem(static_cast<T*>(sg.sh))[(int64_t)(r0 + q) * sg.ldsh + c] = o[q];
-  }
-  if (sg.sht && colok) {
-    auto D = gmem(static_cast<T*>(sg.sht)) + (int64_t)c * sg.ldsht + r0;
-    if (r0 + TR <= sg.rows) {  // TR consecutive values, 16-byte aligned (ldsht and r0 are multiples of 8)
-      constexpr int NV = TR * (int)sizeof(T) / 16;
-#pragma unroll
-      for (int w = 0; w < NV; ++w) {
-        u32x4_t v;
-        __builtin_memcpy(&v, &o[w * (16 / (int)sizeof(T))], 16);
-        *reinterpret_cast<__attribute__((address_space(1))) u32x4_t*>(D + w * (16 / (int)sizeof(T))) = v;
+        for (int k = 0; k < 4; ++k) g[k] += in ? tv[j][k] : 0.f;
       }
-    } else {
-      for (int q = 0; q < TR && r0 + q < sg.rows; ++q) D[q] = o[q];
+    };
+    load_batch(0);
+    // Unconditional 16-byte loads (no branch, so they are all in flight
+    // together).  At a row's ragged end they read up to 3 elements past the
+    // row; past the matrix's last row that is its bias and the head, which
+    // follow every weight matrix in the block's flat arrays (at least 3
+    // elements), so the loads stay in bounds.  Only stores are masked.
+    const f32x4u_t pv = *reinterpret_cast<const __attribute__((address_space(1))) f32x4u_t*>(P + fi);
+    const f32x4u_t mv = *reinterpret_cast<const __attribute__((address_space(1))) f32x4u_t*>(Mo + fi);
+    const f32x4u_t vv = *reinterpret_cast<const __attribute__((address_space(1))) f32x4u_t*>(V + fi);
+    add_batch(0);
+    for (int z0 = ZS; z0 < sg.nsplit; z0 += ZS) {
+      load_batch(z0);
+      add_batch(z0);
+    }
+    float p[4], m[4], v[4];
+    T o[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      p[k] = pv[k];
+      m[k] = mv[k];
+      v[k] = vv[k];
+      adam_elem(p[k], m[k], v[k], g[k], b1, b2, step, bc2s, eps);
+      o[k] = cvt<T>(p[k]);
+    }
+    if (any) {
+      if (full) {
+        auto st = [&](float* base, const float* x) {
+          f32x4u_t w = {x[0], x[1], x[2], x[3]};
+          *reinterpret_cast<__attribute__((address_space(1))) f32x4u_t*>(gmem(base) + fi) = w;
+        };
+        if (sg.g) st(sg.g, g);
+        st(sg.m, m);
+        st(sg.v, v);
+        st(sg.p, p);
+      } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if (c0 + k < sg.cols) {
+            if (sg.g) gmem(sg.g)[fi + k] = g[k];
+            Mo[fi + k] = m[k];
+            V[fi + k] = v[k];
+            P[fi + k] = p[k];
+          }
+      }
+      // GEMM copy [rows][ldsh]: 4 columns of row r
+      if (sg.sh) {
+        T* D = static_cast<T*>(sg.sh) + (int64_t)r * sg.ldsh + c0;
+        if (full) {
+          st4(D, o);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            if (c0 + k < sg.cols) D[k] = o[k];
+        }
+      }
+    }
+    // transposed GEMM copy [cols][ldsht]: the 4 rows of each column, through
+    // LDS (one 8- or 16-byte store per column)
+    if (sg.sht) {
+      __shared__ T s_o[ADAM_TR][ADAM_TC];
+      const int cl = (int)(threadIdx.x & 63) * 4, rl = (int)(threadIdx.x >> 6);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) s_o[rl][cl + k] = o[k];
+      __syncthreads();
+      const int c = (tile % sg.tcols) * ADAM_TC + (int)threadIdx.x;
+      if (c < sg.cols && r0 < sg.rows) {
+        T t4[4] = {s_o[0][threadIdx.x], s_o[1][threadIdx.x], s_o[2][threadIdx.x], s_o[3][threadIdx.x]};
+        T* D = static_cast<T*>(sg.sht) + (int64_t)c * sg.ldsht + r0;
+        if (r0 + 4 <= sg.rows) {
+          st4(D, t4);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (r0 + i < sg.rows) D[i] = t4[i];
+        }
+      }
     }
   }
   if (chunk == 0 && threadIdx.x < 64 && a.ploss) {

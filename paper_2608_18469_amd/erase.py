@@ -27,7 +27,7 @@ SERIAL, OVERLAP, SERIAL_GRAPH, OVERLAP_GRAPH, PIPELINE, OVERLAP_ADAM_END = 0, 1,
 SCHEDULES = {"serial": SERIAL, "overlap": OVERLAP, "serial_graph": SERIAL_GRAPH, "overlap_graph": OVERLAP_GRAPH,
              "pipeline": PIPELINE, "overlap_adam_end": OVERLAP_ADAM_END}
 KERNEL_KINDS = {0: "prologue", 1: "fwd_gemm", 2: "head_bce", 3: "wgrad_gemm", 4: "dgrad_gemm", 5: "adam",
-                6: "bwd_gemm", 7: "empty"}
+                6: "bwd_gemm", 7: "empty", 8: "fwd_head_gemm"}
 
 
 class LayerSpec(ctypes.Structure):

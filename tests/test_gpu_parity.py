@@ -103,6 +103,41 @@ def test_ctr_mlp_bf16_small_vs_oracle(batch):
     _say("  ", check_bf16(cfg, g, params, batches))
 
 
+def _mixed_bf16(batch):
+    # last layers of 64, 128 (head fused into the forward GEMM; the first is
+    # read by a chained block), 40 on a single-layer block (no input gradient
+    # of the last layer) and 200 (standalone head kernel)
+    blocks = [
+        {"input": "x", "layers": [("linear_relu", 200, 96), ("linear_relu", 96, 64)], "lam": 1.0},
+        {"input": "prev", "layers": [("linear_relu", 64, 100), ("linear_relu", 100, 128)], "lam": 0.5},
+        {"input": "x", "layers": [("linear_relu", 200, 40)], "lam": 2.0},
+        {"input": "x", "layers": [("linear_relu", 200, 72), ("linear_relu", 72, 200)], "lam": 1.0},
+    ]
+    return synth.custom("bf16", batch, 200, blocks, label_p=0.3)
+
+
+@pytest.mark.parametrize("batch", [333, 64])
+def test_fused_and_standalone_head_bf16_vs_oracle(batch):
+    """bf16 blocks whose head is fused into the last forward GEMM (chained and
+    not, with and without an input gradient of the last layer) next to one
+    with the standalone head kernel; every schedule gives the same bits."""
+    _say(f"case: mixed bf16 heads batch={batch}")
+    cfg = _mixed_bf16(batch)
+    params, batches = synth.make_workload(cfg, 6, 2)
+    runs = [run_gpu(cfg, params, batches, s)[1] for s in SCHEDS]
+    for other in runs[1:]:
+        assert_bit_identical(runs[0], other)
+    _say("  ", check_bf16(cfg, runs[0], params, batches))
+    tr = erase.Trainer(cfg, params)
+    tr.set_timing(True)
+    tr.step(*tr.device_batch(*batches[0]), "serial")
+    tr.sync()
+    kinds = [(r["block"], r["kind"]) for r in tr.read_timing()[1:]]
+    assert [b for b, k in kinds if k == "fwd_head_gemm"] == [0, 1, 2]
+    assert [b for b, k in kinds if k == "head_bce"] == [3]
+    tr.close()
+
+
 def test_ctr_mlp_bf16_schedules_bit_identical():
     """Serial, overlapped and graph schedules, with 1 and 3 backward streams,
     produce the same bits."""
@@ -259,9 +294,11 @@ def test_kernel_timing_records():
     recs = tr.read_timing()
     assert recs[0]["kind"] == "empty" and recs[0]["end_ms"] >= recs[0]["start_ms"]
     recs = recs[1:]
-    # prologue + per block: 3 forward GEMMs, head, 2 grouped backward GEMMs,
+    # prologue + per block: 3 forward GEMMs (the last with the head and loss
+    # in its epilogue: the last layer is 128 wide), 2 grouped backward GEMMs,
     # the first layer's weight gradient, Adam
-    assert len(recs) == 1 + 2 * 8, [r["kind"] for r in recs]
+    assert len(recs) == 1 + 2 * 7, [r["kind"] for r in recs]
+    assert [r["kind"] for r in recs[1:4]] == ["fwd_gemm", "fwd_gemm", "fwd_head_gemm"]
     assert all(r["end_ms"] >= r["start_ms"] >= 0 for r in recs)
     assert {r["stream"] for r in recs if r["kind"] in ("wgrad_gemm", "bwd_gemm", "adam")} == {1}
     tr2 = erase.Trainer(cfg, params, bwd_streams=2)
@@ -270,6 +307,6 @@ def test_kernel_timing_records():
     tr2.sync()
     r2 = tr2.read_timing()[1:]
     assert {r["stream"] for r in r2 if r["kind"] == "adam"} == {1, 2}
-    assert {r["stream"] for r in recs if r["kind"] in ("fwd_gemm", "head_bce", "prologue")} == {0}
+    assert {r["stream"] for r in recs if r["kind"] in ("fwd_gemm", "fwd_head_gemm", "prologue")} == {0}
     with pytest.raises(erase.EraseError):
         tr.step(xd, yd, "overlap_graph")
