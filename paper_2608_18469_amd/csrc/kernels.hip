@@ -228,6 +228,15 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     if (tid == 0) hs[3 * BN + 3 * BM] = e.hc[0];
   }
 
+  // forward biases: loaded now, their latency hides behind the main loop
+  float bnv[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int n = n0 + wn * WN + j * 16 + (lane & 15);
+    bnv[j] = 0.f;
+    if constexpr (KIND == GK_FWD_RELU || KIND == GK_FWD_CROSS || KIND == GK_FWD_HEAD) bnv[j] = (n < g.N) ? e.bias[n] : 0.f;
+  }
+
   const bool do_rows = (KIND == GK_WGRAD) && e.bpart != nullptr && by == 0 && wn == 0;
   float rs[TM];
 #pragma unroll
@@ -320,16 +329,29 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   // barrier per phase.  The last phase ends with a barrier, so the epilogue
   // may reuse the LDS.
   constexpr int U = (R % 2 == 0) ? R : 2 * R;  // phases per unrolled round
-  for (int base = 0; base < nk; base += U) {
+  // Main loop: rounds of U phases whose loads are all real, with no branch
+  // inside, so the waits before each LDS store count exactly the loads that
+  // may stay in flight (behind a branch the compiler waits for all of them).
+  // Tail: the last phases, straight-line, loading and staging only real
+  // k-steps, so no load is left in flight for the epilogue to wait on.
+  int base = 0;
+  for (; base + U + R < nk; base += U) {
 #pragma unroll
     for (int p = 0; p < U; ++p) {
-      const int j = base + p;
-      if (j < nk) {
-        ERASE_COMPUTE(p % 2);
-        ERASE_SSTORE((p + 1) % R, (p + 1) % 2);
-        ERASE_GLOAD((p + 1) % R, j + 1 + R);
-        __syncthreads();
-      }
+      ERASE_COMPUTE(p % 2);
+      ERASE_SSTORE((p + 1) % R, (p + 1) % 2);
+      ERASE_GLOAD((p + 1) % R, base + p + 1 + R);
+      __syncthreads();
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < U + R + 1; ++p) {
+    const int j = base + p;
+    if (j < nk) {
+      ERASE_COMPUTE(p % 2);
+      if (j + 1 < nk) ERASE_SSTORE((p + 1) % R, (p + 1) % 2);
+      if (j + 1 + R < nk) ERASE_GLOAD((p + 1) % R, j + 1 + R);
+      __syncthreads();
     }
   }
 #undef ERASE_GLOAD
@@ -378,8 +400,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   for (int j = 0; j < TN; ++j) {
     const int nl = wn * WN + j * 16 + (lane & 15);
     const int n = n0 + nl;
-    float bn = 0.f;
-    if constexpr (KIND == GK_FWD_RELU || KIND == GK_FWD_CROSS || KIND == GK_FWD_HEAD) bn = (n < N) ? e.bias[n] : 0.f;
+    const float bn = bnv[j];
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
