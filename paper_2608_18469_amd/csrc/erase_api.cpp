@@ -107,10 +107,9 @@ struct LayerRT {
   int64_t offW = 0, offb = 0;
   void* wsh = nullptr; int64_t ldwsh = 0;
   void* wsht = nullptr; int64_t ldwsht = 0;
-  void* y = nullptr; int64_t ldy = 0;
-  void* yt = nullptr; int64_t ldyt = 0;
-  void* dmn = nullptr; int64_t lddmn = 0;
-  void* dnm = nullptr; int64_t lddnm = 0;
+  void* y = nullptr; int64_t ldy = 0;      // activation [Mr][ldy]
+  bool needy = true;                        // y is read later (not a fused head's unchained output)
+  void* dmn = nullptr; int64_t lddmn = 0;  // activation gradient [Mr][lddmn]
   void* g = nullptr; int64_t ldg = 0;
   float* part = nullptr; int64_t ldp = 0, pstride = 0;
   float* bpart = nullptr;
@@ -137,14 +136,13 @@ struct BlockRT {
 
 struct Plan {
   int bf16 = 1, esz = 2, M = 0;
-  int64_t ldm = 0;  // feature-major leading dimension: roundup(M, 64)
   int64_t Mr = 0;   // allocated rows of row-major arrays: roundup(M, 128)
   int64_t* t = nullptr;
   int* status = nullptr;
   // zero-padded and feature-major copies of x, one pair per step parity so a
   // step's prologue never overwrites what the previous step's backward reads
   void* xp[2] = {nullptr, nullptr}; int64_t ldxp = 0;
-  void* xt[2] = {nullptr, nullptr}; int64_t ldxt = 0;
+
   std::vector<BlockRT> blk;
   size_t bytes = 0;
 };
@@ -201,7 +199,6 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
   P->M = c.batch;
   const int esz = P->esz;
   const int64_t M = c.batch;
-  P->ldm = roundup(M, 64);
   P->Mr = roundup(M, 128);
   const int64_t Mr = P->Mr;
   Carver cv{base};
@@ -210,12 +207,10 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
   bool any_x = false;
   for (int b = 0; b < c.n_blocks; ++b) any_x |= c.blocks[b].input_src == ERASE_IN_X;
   if (any_x) {
-    P->ldxp = roundup(c.in_dim, 64);
-    P->ldxt = P->ldm;
-    for (int q = 0; q < 2; ++q) {
-      P->xp[q] = cv.take(size_t(Mr) * P->ldxp * esz);
-      P->xt[q] = cv.take(size_t(roundup(c.in_dim, 128)) * P->ldxt * esz);
-    }
+    // zero-padded copy of x, one per step parity; 128-column rows (the
+    // weight gradient reads k-major tiles up to 128 columns wide)
+    P->ldxp = roundup(c.in_dim, 128);
+    for (int q = 0; q < 2; ++q) P->xp[q] = cv.take(size_t(Mr) * P->ldxp * esz);
   }
   P->blk.assign(c.n_blocks, BlockRT{});
   for (int b = 0; b < c.n_blocks; ++b) {
@@ -235,8 +230,11 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
       off += int64_t(R.K) * R.N;
       R.offb = off;
       off += R.N;
-      // Every GEMM operand is zero-padded: rows to a multiple of 128 (the
-      // largest tile), leading dimensions to a multiple of 64 (the k-step).
+      // Every GEMM operand is zero-padded: weight copies to rows of a
+      // multiple of 128 (the largest tile) and a leading dimension of a
+      // multiple of 64 (the k-step); activations and their gradients to
+      // roundup(M, 128) rows of a multiple of 128 columns (the k-major
+      // weight-gradient tiles).
       const int64_t ldK = roundup(R.K, 64), ldN = roundup(R.N, 64);
       const int64_t Kr = roundup(R.K, 128), Nr = roundup(R.N, 128);
       R.ldwsh = ldK;
@@ -245,21 +243,14 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
         R.ldwsht = ldN;
         R.wsht = cv.take(size_t(Kr) * ldN * esz);
       }
-      R.ldy = ldN;
-      R.y = cv.take(size_t(Mr) * ldN * esz);
-      if (l + 1 < B.L || next_chained) {
-        R.ldyt = P->ldm;
-        R.yt = cv.take(size_t(Nr) * P->ldm * esz);
-      }
-      R.lddnm = P->ldm;
-      R.dnm = cv.take(size_t(Nr) * P->ldm * esz);
-      if (l >= 1) {
-        R.lddmn = ldN;
-        R.dmn = cv.take(size_t(Mr) * ldN * esz);
-      }
+      R.ldy = Nr;
+      R.y = cv.take(size_t(Mr) * Nr * esz);
+      R.needy = l + 1 < B.L || next_chained;
+      R.lddmn = Nr;
+      R.dmn = cv.take(size_t(Mr) * Nr * esz);
       if (R.kind == ERASE_LAYER_CROSS && l >= 1) {
-        R.ldg = ldN;
-        R.g = cv.take(size_t(Mr) * ldN * esz);
+        R.ldg = Nr;
+        R.g = cv.take(size_t(Mr) * Nr * esz);
       }
       // launch shapes (contraction lengths padded to the k-step)
       const int BK = P->bf16 ? 64 : 32;
@@ -487,29 +478,22 @@ class Enqueuer {
     if (st_ != ERASE_OK) return st_;               \
   } while (0)
 
-// Input of layer l of block b, row-major and feature-major.
-void layer_input(const Ctx* c, int b, int l, const void* x, const void** mn, int64_t* ldmn, const void** nm,
-                 int64_t* ldnm) {
+// Input of layer l of block b (row-major).
+void layer_input(const Ctx* c, int b, int l, const void* x, const void** mn, int64_t* ldmn) {
   const Plan& P = c->P;
   const BlockRT& B = P.blk[b];
   if (l > 0) {
     *mn = B.layer[l - 1].y;
     *ldmn = B.layer[l - 1].ldy;
-    *nm = B.layer[l - 1].yt;
-    *ldnm = B.layer[l - 1].ldyt;
   } else if (B.input_src == ERASE_IN_X) {
     (void)x;
     *mn = P.xp[c->par];
     *ldmn = P.ldxp;
-    *nm = P.xt[c->par];
-    *ldnm = P.ldxt;
   } else {
     const BlockRT& A = P.blk[b - 1];
     const LayerRT& R = A.layer[A.L - 1];
     *mn = R.y;
     *ldmn = R.ldy;
-    *nm = R.yt;
-    *ldnm = R.ldyt;
   }
 }
 
@@ -519,14 +503,12 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
   const int M = P.M, esz = P.esz;
   const void* x0;
   int64_t ldx0;
-  const void* unused;
-  int64_t unused_ld;
-  layer_input(c, b, 0, x, &x0, &ldx0, &unused, &unused_ld);
+  layer_input(c, b, 0, x, &x0, &ldx0);
   for (int l = 0; l < B.L; ++l) {
     const LayerRT& R = B.layer[l];
     const void* a;
     int64_t lda;
-    layer_input(c, b, l, x, &a, &lda, &unused, &unused_ld);
+    layer_input(c, b, l, x, &a, &lda);
     GemmDesc g{};
     g.A = a;
     g.lda = lda;
@@ -544,8 +526,6 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
     e.bias = B.buf.param + R.offb;
     e.y = R.y;
     e.ldy = R.ldy;
-    e.yt = R.yt;
-    e.ldyt = R.ldyt;
     const bool fused = B.head_fused && l == B.L - 1;
     const int kind = R.kind == ERASE_LAYER_CROSS ? GK_FWD_CROSS : fused ? GK_FWD_HEAD : GK_FWD_RELU;
     if (kind == GK_FWD_CROSS) {
@@ -556,11 +536,11 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
     }
     Cost cost = gemm_cost(g);
     cost.flops = 2.0 * M * R.N * R.K;
-    cost.bytes = double(esz) * (double(M) * R.K + double(R.N) * R.K + double(M) * R.N * (R.yt ? 2 : 1)) + 4.0 * R.N +
+    cost.bytes = double(esz) * (double(M) * R.K + double(R.N) * R.K + double(M) * R.N) + 4.0 * R.N +
                  (kind == GK_FWD_CROSS ? 2.0 * esz * M * R.N : 0.0);
     if (fused) {
       // z leaves the chip only when the next block reads it
-      if (!R.yt) e.y = nullptr;
+      if (!R.needy) e.y = nullptr;
       e.hw = B.buf.param + B.off_w;
       e.hc = B.buf.param + B.off_c;
       e.labels = labels;
@@ -568,14 +548,11 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
       e.inv_m = 1.0f / float(M);
       e.dmn = R.dmn;
       e.lddmn = R.lddmn;
-      e.dnm = R.dnm;
-      e.lddnm = R.lddnm;
       e.pdw = B.pdw;
       e.pdc = B.pdc;
       e.ploss = B.ploss;
       cost.flops += 4.0 * M * R.N;
-      cost.bytes = double(esz) * (double(M) * R.K + double(R.N) * R.K + double(M) * R.N * ((R.yt ? 2 : 0) + 1 +
-                                                                                           (R.dmn ? 1 : 0))) +
+      cost.bytes = double(esz) * (double(M) * R.K + double(R.N) * R.K + double(M) * R.N * ((R.needy ? 1 : 0) + 1)) +
                    4.0 * R.N + 4.0 * M + 4.0 * R.N + 4.0 * B.nhead * (R.N + 2);
     }
     const int bf = P.bf16;
@@ -595,8 +572,7 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
   h.N = Rl.N;
   h.dmn = Rl.dmn;
   h.lddmn = Rl.lddmn;
-  h.dnm = Rl.dnm;
-  h.lddnm = Rl.lddnm;
+
   h.pdw = B.pdw;
   h.pdc = B.pdc;
   h.ploss = B.ploss;
@@ -620,21 +596,18 @@ erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStre
   const int M = P.M, esz = P.esz, bf = P.bf16;
   const void* x0;
   int64_t ldx0;
-  const void* unused;
-  int64_t unused_ld;
-  layer_input(c, b, 0, x, &x0, &ldx0, &unused, &unused_ld);
+  layer_input(c, b, 0, x, &x0, &ldx0);
   for (int l = B.L - 1; l >= 0; --l) {
     const LayerRT& R = B.layer[l];
     const void* inmn;
     int64_t ldinmn;
-    const void* innm;
-    int64_t ldinnm;
-    layer_input(c, b, l, x, &inmn, &ldinmn, &innm, &ldinnm);
+    layer_input(c, b, l, x, &inmn, &ldinmn);
+    // dW[n][k] = sum over the batch of dH[m][n] a[m][k]: both row-major
     GemmDesc gw{};
-    gw.A = R.dnm;
-    gw.lda = R.lddnm;
-    gw.B = innm;
-    gw.ldb = ldinnm;
+    gw.A = R.dmn;
+    gw.lda = R.lddmn;
+    gw.B = inmn;
+    gw.ldb = ldinmn;
     gw.M = R.N;
     gw.N = R.K;
     gw.K = (int)roundup(M, P.bf16 ? 64 : 32);
@@ -676,8 +649,6 @@ erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStre
     }
     ed.dmn = Rb.dmn;
     ed.lddmn = Rb.lddmn;
-    ed.dnm = Rb.dnm;
-    ed.lddnm = Rb.lddnm;
     if (Rb.kind == ERASE_LAYER_CROSS) {
       ed.below_cross = 1;
       ed.x0 = x0;
@@ -691,7 +662,7 @@ erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStre
     }
     Cost cd = gemm_cost(gd);
     cd.flops = 2.0 * M * R.N * R.K;
-    const double outs = 1.0 + (Rb.dmn ? 1.0 : 0.0) + (ed.gout ? 1.0 : 0.0);
+    const double outs = 1.0 + (ed.gout ? 1.0 : 0.0);
     cd.bytes = double(esz) * (double(M) * R.N + double(R.N) * R.K + double(M) * R.K * (outs + 1.0) +
                               (ed.res ? double(M) * R.K : 0.0));
     if (R.grouped) {
@@ -759,12 +730,11 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
     pa.hyper = reinterpret_cast<float*>(P.t + 2) + 2 * c->par;
     pa.xp = P.xp[c->par];
     pa.ldxp = P.ldxp;
-    pa.xt = P.xt[c->par];
-    pa.ldxt = P.ldxt;
+
     pa.M = P.M;
     pa.K = c->cfg.in_dim;
     Cost cost;
-    cost.bytes = P.xt[0] ? 3.0 * P.esz * double(P.M) * c->cfg.in_dim : 0.0;
+    cost.bytes = P.xp[0] ? 2.0 * P.esz * double(P.M) * c->cfg.in_dim : 0.0;
     const int bf = P.bf16;
     RUN(0, -1, -1, 0, sf, cost, [&](const LaunchEv& ev) { return launch_prologue(bf, pa, sf, ev); });
   }

@@ -7,16 +7,21 @@
 
 namespace erase {
 
-// One GEMM launch: C[m][n] = sum_k A[m][k] * B[n][k] (both operands stored
-// with the contraction index contiguous), fp32 accumulation.  The
-// contraction range is split into `split` slices of `kps` elements; slice z
-// is handled by blockIdx.z.
+// One GEMM launch, fp32 accumulation:
+//   forward / input gradient: C[m][n] = sum_k A[m][k] * B[n][k] (both
+//     operands stored with the contraction index contiguous);
+//   weight gradient (GK_WGRAD): C[m][n] = sum_k A[k][m] * B[k][n] (both
+//     operands row-major over the contraction: activation gradient and layer
+//     input as produced).
+// The contraction range is split into `split` slices of `kps` elements.
 //
 // Operand contract (no loads are masked): K is the padded contraction length,
-// a multiple of the k-step (64 bf16 / 32 fp32 elements); A holds at least
-// roundup(M, 128) rows and B roundup(N, 128) rows of at least K elements, and
-// every element outside the logical [M or N][K_logical] block is zero.  M and
-// N are the logical output extents the epilogue stores.
+// a multiple of the k-step (64 bf16 / 32 fp32 elements).  Forward / input
+// gradient: A holds at least roundup(M, 128) rows and B roundup(N, 128) rows
+// of at least K elements.  Weight gradient: A and B hold at least K rows of
+// at least roundup(M, 128) and roundup(N, 128) elements.  Every element
+// outside the logical block is zero.  M and N are the logical output extents
+// the epilogue stores.
 struct GemmDesc {
   const void* A;
   int64_t lda;
@@ -94,7 +99,6 @@ struct PrologueArgs {
   float lr, beta1, beta2;
   const void* x; int64_t ldx;
   void* xp; int64_t ldxp;
-  void* xt; int64_t ldxt;
   int M, K;
 };
 hipError_t launch_prologue(int bf16, const PrologueArgs& a, hipStream_t s, const LaunchEv& ev = {});

@@ -1,24 +1,27 @@
 // HIP kernels of the detached-block training step, written for gfx950
 // (CDNA4: 64-wide wavefronts, MFMA matrix cores, 160 KB LDS per CU).
 //
-//  * erase_{fwd,fwd_cross,wgrad,dgrad}_gemm: one LDS-tiled MFMA GEMM core
-//    C[m][n] = sum_k A[m][k] B[n][k] (contraction index contiguous in both
-//    operands, fp32 accumulation) with role-specific fused epilogues:
+//  * erase_{fwd,fwd_cross,fwd_head,wgrad,dgrad}_gemm: one LDS-tiled MFMA
+//    GEMM core with fp32 accumulation and role-specific fused epilogues:
 //      forward      y = relu(acc + b)                (Eq. 1, linear block body)
 //      forward DCN  y = x0 * (acc + b) + x_l         (cross layer)
+//      forward+head the last layer with the local head and loss (Eq. 2)
 //      weight grad  dW partial slice, plus the bias gradient as row sums of
-//                   the A operand (A = activation gradient, feature-major)
+//                   the A operand (the activation gradient)
 //      input grad   g = acc (+ g_out for a cross layer), then either the ReLU
 //                   mask of the layer below or the cross-layer factor x0.
-//    Every activation and activation gradient is produced in both a
-//    row-major [M][N] and a feature-major [N][M] copy so that all three
-//    GEMMs of a layer read K-contiguous operands with 16-byte loads.
+//    Every activation and activation gradient exists once, row-major
+//    [batch][features].  The forward and input-gradient GEMMs contract over
+//    contiguous features; the weight gradient contracts over the batch, i.e.
+//    over rows: its tiles are stored k-major in LDS and the MFMA operands
+//    come from gfx950's transposing LDS reads (ds_read_b64_tr_b16).
 //  * erase_head_bce: local head s = z w + c, sigmoid-BCE loss and its
 //    gradient at z (the block's local objective, Section 2.1), with
 //    deterministic per-workgroup partial sums.
 //  * erase_adam: ordered reduction of the split partials, Adam update of the
 //    fp32 master weights, and the bf16 GEMM copies of the new weights.
-//  * erase_prologue: step counter increment and the feature-major copy of x.
+//  * erase_prologue: step counter increment, Adam factors, and the
+//    zero-padded copy of x the GEMMs read.
 //
 // No float atomics anywhere: every reduction has a fixed order, so every
 // schedule of the same step produces bit-identical results.
@@ -111,6 +114,18 @@ __device__ __forceinline__ float sum8_bf16(const u32x4_t& a) {
   return s;
 }
 
+// An MFMA operand fragment (8 consecutive contraction indices of one row) from
+// a k-major bf16 LDS tile: two transposing 8-byte reads, rows p and p + 4*pitch.
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+template <typename T>
+__device__ __forceinline__ u32x4_t tr_frag(const T* p, int pitch) {
+  typedef __attribute__((address_space(3))) s16x4_t lds_s16x4;
+  const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));
+  const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 4 * pitch));
+  const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
+  return u32x4_t{a.x, a.y, b.x, b.y};
+}
+
 // Value of the fused epilogue at (m, n), m < M and n < N, in the output type.
 template <typename T, int KIND>
 __device__ __forceinline__ T epi_value(const EpiParams& e, int m, int n, float acc, float bn) {
@@ -180,8 +195,12 @@ __device__ __forceinline__ TileIdx tile_from(int t, int gm, int gn, int group) {
 template <typename T, int BM, int BN, int KIND>
 struct GemmSmem {
   static constexpr int BK = GT<T>::BK, KCH = GT<T>::KCH, PITCH = sizeof(T) == 2 ? BK : BK + KCH;
+  // weight gradient: k-major tiles [BK][BM] and [BK][BN] (fp32 rows padded by 16)
+  static constexpr bool KMAJ = KIND == GK_WGRAD;
+  static constexpr int PAD = sizeof(T) == 2 ? 0 : 16;
+  static constexpr int STAGE = KMAJ ? BK * (BM + BN + 2 * PAD) : (BM + BN) * PITCH;
   using OT = typename std::conditional<KIND == GK_WGRAD, float, T>::type;
-  static constexpr int MAIN = 2 * (BM + BN) * PITCH * (int)sizeof(T);
+  static constexpr int MAIN = 2 * STAGE * (int)sizeof(T);
   static constexpr int TILE = BM * (BN + 16 / (int)sizeof(OT)) * (int)sizeof(OT);
   // fused head: hw[BN], labels[BM], ds[BM], loss[BM], dw[2][BN], c (fp32),
   // past both the main-loop stages and the output tile
@@ -199,7 +218,22 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   constexpr int CPR = BK / KCH;
   constexpr int CA = BM * CPR / 256, CB = BN * CPR / 256;
   static_assert(CA * 256 == BM * CPR && CB * 256 == BN * CPR, "tile does not match 256 threads");
-  constexpr int STAGE = (BM + BN) * PITCH;
+  // Operand layouts.  Forward and input gradient ("NT"): A [M][K] and B [N][K]
+  // with the contraction contiguous; LDS tiles keep rows of BK elements.
+  // Weight gradient (k-major): A [K][M] and B [K][N], i.e. activation
+  // gradients and layer inputs in their row-major layout with the batch as
+  // the contraction; LDS tiles are k-major, rows of BM (BN) elements, and
+  // bf16 fragments come from pairs of transposing LDS reads.
+  constexpr bool KMAJ = GemmSmem<T, BM, BN, KIND>::KMAJ;
+  constexpr int PAD = GemmSmem<T, BM, BN, KIND>::PAD;
+  constexpr int PA = BM + PAD, PB = BN + PAD;  // k-major row pitches
+  constexpr int CPA = BM / KCH, CPB = BN / KCH;  // 16-byte chunks per k-major row
+  constexpr int RPA = 256 / CPA, RPB = 256 / CPB;  // k-major rows per pass of 256 threads
+  static_assert(!KMAJ || (BK % RPA == 0 && BK % RPB == 0), "k-major tile does not match 256 threads");
+  static_assert(!KMAJ || !SWZ || ((CPA == 8 || CPA == 16) && (CPB == 8 || CPB == 16)),
+                "k-major chunk permutation: 8 or 16 chunks per row");
+  constexpr int AREG = KMAJ ? BK * PA : BM * PITCH;  // elements of the A part of a stage
+  constexpr int STAGE = GemmSmem<T, BM, BN, KIND>::STAGE;
   using OT = typename std::conditional<KIND == GK_WGRAD, float, T>::type;
   constexpr int OCH = 16 / (int)sizeof(OT);
   constexpr int OPITCH = BN + OCH;
@@ -251,40 +285,122 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   // k-step j covers [kbeg + j*BK, kbeg + (j+1)*BK); loads past the last
   // k-step are clamped onto it (in bounds, never computed)
   const int klast = kbeg + (nk > 0 ? nk - 1 : 0) * BK;
-  // per-thread chunk coordinates (row offset, k offset) of the tile loads
-  const T* pa = A + (int64_t)(m0 + tid / CPR) * g.lda + (tid % CPR) * KCH;
-  const T* pb = B + (int64_t)(n0 + tid / CPR) * g.ldb + (tid % CPR) * KCH;
-  constexpr int RSTEP = 256 / CPR;  // tile rows between a thread's chunks
+  // per-thread tile chunks: address of the first, element strides between a
+  // thread's chunks (ia, ib) and per contraction index (ka, kb), LDS offsets
+  constexpr int RSTEP = 256 / CPR;  // NT: tile rows between a thread's chunks
   static_assert(!SWZ || (CPR == 8 && RSTEP % 8 == 0), "chunk permutation assumes 8 chunks per row");
-  const int srow = tid / CPR, sch = tid % CPR;
-  const int sofs = srow * PITCH + (SWZ ? (sch ^ (srow & 7)) : sch) * KCH;
+  // k-major rows r are stored with 16-byte chunk j at j ^ kperm(r): with it
+  // the transposing fragment reads (32 lanes per pass over 64 banks) and the
+  // tile stores are conflict-free (measured with the LDS bank counters)
+  auto kperm = [](int r, int cpr) { return 2 * ((r >> 1) & 1) + 4 * ((r >> 3) & 1) + (cpr == 16 ? 8 * (r & 1) : 0); };
+  const T* pa;
+  const T* pb;
+  int64_t ia, ib, ka, kb;
+  int sofa, sofb, sia, sib;
+  if constexpr (KMAJ) {
+    const int ra_ = tid / CPA, ca_ = tid % CPA, rb_ = tid / CPB, cb_ = tid % CPB;
+    pa = A + (int64_t)ra_ * g.lda + m0 + ca_ * KCH;
+    pb = B + (int64_t)rb_ * g.ldb + n0 + cb_ * KCH;
+    ia = (int64_t)RPA * g.lda;
+    ib = (int64_t)RPB * g.ldb;
+    ka = g.lda;
+    kb = g.ldb;
+    sofa = ra_ * PA + (SWZ ? (ca_ ^ kperm(ra_, CPA)) : ca_) * KCH;
+    sofb = AREG + rb_ * PB + (SWZ ? (cb_ ^ kperm(rb_, CPB)) : cb_) * KCH;
+    sia = RPA * PA;
+    sib = RPB * PB;
+  } else {
+    const int srow = tid / CPR, sch = tid % CPR;
+    pa = A + (int64_t)(m0 + srow) * g.lda + sch * KCH;
+    pb = B + (int64_t)(n0 + srow) * g.ldb + sch * KCH;
+    ia = (int64_t)RSTEP * g.lda;
+    ib = (int64_t)RSTEP * g.ldb;
+    ka = 1;
+    kb = 1;
+    sofa = srow * PITCH + (SWZ ? (sch ^ (srow & 7)) : sch) * KCH;
+    sofb = BM * PITCH + sofa;
+    sia = RSTEP * PITCH;
+    sib = RSTEP * PITCH;
+  }
 
   // Register sets are only ever indexed by compile-time constants (the loops
   // below are fully unrolled), so they stay in VGPRs.
   // Every operand is zero-padded (see GemmDesc): loads are never masked.
 #define ERASE_GLOAD(SET, KSTEP)                                                                       \
   do {                                                                                                \
-    const int k0_ = min(kbeg + (KSTEP) * BK, klast);                                                  \
+    const int64_t k0_ = min(kbeg + (KSTEP) * BK, klast);                                              \
     _Pragma("unroll") for (int i = 0; i < CA; ++i)                                                    \
-        ra[SET][i] = *reinterpret_cast<const u32x4_t*>(pa + (int64_t)(i * RSTEP) * g.lda + k0_);        \
+        ra[SET][i] = *reinterpret_cast<const u32x4_t*>(pa + i * ia + k0_ * ka);                         \
     _Pragma("unroll") for (int i = 0; i < CB; ++i)                                                    \
-        rb[SET][i] = *reinterpret_cast<const u32x4_t*>(pb + (int64_t)(i * RSTEP) * g.ldb + k0_);        \
+        rb[SET][i] = *reinterpret_cast<const u32x4_t*>(pb + i * ib + k0_ * kb);                         \
   } while (0)
 #define ERASE_SSTORE(SET, ST)                                                                         \
   do {                                                                                                \
     T* sa_ = lds + (ST) * STAGE;                                                                      \
     _Pragma("unroll") for (int i = 0; i < CA; ++i)                                                    \
-        *reinterpret_cast<u32x4_t*>(sa_ + sofs + i * RSTEP * PITCH) = ra[SET][i];                       \
+        *reinterpret_cast<u32x4_t*>(sa_ + sofa + i * sia) = ra[SET][i];                                 \
     _Pragma("unroll") for (int i = 0; i < CB; ++i)                                                    \
-        *reinterpret_cast<u32x4_t*>(sa_ + BM * PITCH + sofs + i * RSTEP * PITCH) = rb[SET][i];          \
+        *reinterpret_cast<u32x4_t*>(sa_ + sofb + i * sib) = rb[SET][i];                                 \
   } while (0)
 
   // fragment offset within a 16-row slab; slab rows start at multiples of 16,
   // so a lane's row & 7 is lane & 7
   const int frow = (lane & 15) * PITCH + (SWZ ? 0 : (lane >> 4) * (KMF / 4));
   const int fch = (lane >> 4) ^ (lane & 7);  // bf16: permuted chunk of k-offset 0
+  // k-major bf16 fragments: lane (g, q, c) = (lane >> 4, (lane & 15) >> 2,
+  // lane & 3) reads 4 elements of row ks + 8g + q (then + 4) at column
+  // 4c of its 16-column block; within each 16 lanes the transposing read
+  // hands lane l element l & 3 of the chunks read by lanes 4q' + (l >> 2),
+  // i.e. rows ks + 8g + q' of column l & 15: the MFMA operand layout.
+  // The rows' permutation bits do not depend on ks or the half.
+  const int tg = lane >> 4, tq = (lane & 15) >> 2, tc = lane & 3;
+  const int trow = 8 * tg + tq;
+  const int hpa = kperm(trow, CPA), hpb = kperm(trow, CPB);
+  int foa[TM], fob[TN];  // element offsets of the lane's fragment chunks in a stage
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int col = wm * WM + i * 16;
+    foa[i] = KMAJ ? (SWZ ? trow * PA + (((col >> 3) + (tc >> 1)) ^ hpa) * 8 + (tc & 1) * 4
+                         : tg * PA + col + (lane & 15))
+                  : 0;
+  }
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int col = wn * WN + j * 16;
+    fob[j] = KMAJ ? AREG + (SWZ ? trow * PB + (((col >> 3) + (tc >> 1)) ^ hpb) * 8 + (tc & 1) * 4
+                                : tg * PB + col + (lane & 15))
+                  : 0;
+  }
 #define ERASE_COMPUTE(ST)                                                                             \
   do {                                                                                                \
+    if constexpr (KMAJ) {                                                                             \
+      const T* st_ = lds + (ST) * STAGE;                                                              \
+      _Pragma("unroll") for (int ks = 0; ks < BK; ks += KMF) {                                        \
+        if constexpr (sizeof(T) == 2) {                                                               \
+          u32x4_t fa[TM], fb[TN];                                                                       \
+          _Pragma("unroll") for (int i = 0; i < TM; ++i) fa[i] = tr_frag(st_ + foa[i] + ks * PA, PA);  \
+          _Pragma("unroll") for (int j = 0; j < TN; ++j) fb[j] = tr_frag(st_ + fob[j] + ks * PB, PB);  \
+          _Pragma("unroll") for (int i = 0; i < TM; ++i)                                              \
+          _Pragma("unroll") for (int j = 0; j < TN; ++j)                                              \
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(                                    \
+                  __builtin_bit_cast(bf16x8_t, fa[i]), __builtin_bit_cast(bf16x8_t, fb[j]), acc[i][j], 0, 0, 0); \
+          if (do_rows) {                                                                              \
+            _Pragma("unroll") for (int i = 0; i < TM; ++i) rs[i] += sum8_bf16(fa[i]);                 \
+          }                                                                                           \
+        } else {                                                                                      \
+          float fa[TM], fb[TN];                                                                       \
+          _Pragma("unroll") for (int i = 0; i < TM; ++i) fa[i] = asf(st_[foa[i] + ks * PA]);          \
+          _Pragma("unroll") for (int j = 0; j < TN; ++j) fb[j] = asf(st_[fob[j] + ks * PB]);          \
+          _Pragma("unroll") for (int i = 0; i < TM; ++i)                                              \
+          _Pragma("unroll") for (int j = 0; j < TN; ++j)                                              \
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[i], fb[j], acc[i][j], 0, 0, 0);     \
+          if (do_rows) {                                                                              \
+            _Pragma("unroll") for (int i = 0; i < TM; ++i) rs[i] += fa[i];                            \
+          }                                                                                           \
+        }                                                                                             \
+      }                                                                                               \
+      break;                                                                                          \
+    }                                                                                                 \
     const T* sa_ = lds + (ST) * STAGE + wm * WM * PITCH + frow;                                       \
     const T* sb_ = lds + (ST) * STAGE + BM * PITCH + wn * WN * PITCH + frow;                          \
     _Pragma("unroll") for (int ks = 0; ks < BK; ks += KMF) {                                          \
@@ -518,7 +634,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
           dwp = fmaf(zq, ds, dwp);
         }
         const int m = m0 + ml0;
-        if (n < N && m < M) {
+        if (e.dnm && n < N && m < M) {
           OT* dst = static_cast<OT*>(e.dnm) + (int64_t)n * e.lddnm + m;
           if (m + 4 <= M) {
             st4(dst, d4);
@@ -650,7 +766,13 @@ static hipError_t launch_gemm_t(int kind, const GemmDesc& g0, const EpiParams& e
   switch (kind) {
     case GK_FWD_RELU: ERASE_LAUNCH((erase_fwd_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;
     case GK_FWD_CROSS: ERASE_LAUNCH((erase_fwd_cross_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;
-    case GK_WGRAD: ERASE_LAUNCH((erase_wgrad_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;
+    case GK_WGRAD:
+      if constexpr (BM >= 64) {  // k-major tiles of 64 or 128 columns
+        ERASE_LAUNCH((erase_wgrad_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e);
+      } else {
+        return hipErrorInvalidValue;
+      }
+      break;
     case GK_DGRAD: ERASE_LAUNCH((erase_dgrad_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;
     case GK_FWD_HEAD:
       // the tile must span the whole width; 32- and 64-row tiles only
@@ -708,60 +830,38 @@ hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void erase_prologue(PrologueArgs a) {
-  constexpr int KCH = 16 / sizeof(T);
-  constexpr int TP = 64 + KCH;  // LDS pitch (elements)
-  __shared__ __attribute__((aligned(16))) T tile[64 * TP];
-  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
     const int64_t t = a.t[0] + 1;
     a.t[0] = t;
     a.hyper[0] = (float)((double)a.lr / (1.0 - pow((double)a.beta1, (double)t)));
     a.hyper[1] = (float)sqrt(1.0 - pow((double)a.beta2, (double)t));
   }
   if (a.xp == nullptr) return;
+  // xp[m][k] = x[m][k] for k < K, zero for the rest of the 16-byte chunk;
+  // columns past the chunk and rows past M stay zero from initialisation
+  constexpr int KCH = 16 / sizeof(T);
   const T* X = static_cast<const T*>(a.x);
-  const int k0 = blockIdx.x * 64, m0 = blockIdx.y * 64;
-  constexpr int CPR = 64 / KCH;  // chunks per tile row
-  for (int c = threadIdx.x; c < 64 * CPR; c += 256) {
-    const int r = c / CPR, kc = (c % CPR) * KCH;
-    const int m = m0 + r, k = k0 + kc;
-    uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if (m < a.M && k < a.K) {
-      // x rows hold at least roundup(K, KCH) elements (16-byte row pitch)
-      v = *reinterpret_cast<const uint4*>(X + (int64_t)m * a.ldx + k);
-      if (k + KCH > a.K) {
-        T e[KCH];
-        __builtin_memcpy(e, &v, 16);
+  const int cpr = (a.K + KCH - 1) / KCH;  // chunks per row
+  const int64_t nch = (int64_t)a.M * cpr;
+  for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < nch; c += (int64_t)gridDim.x * 256) {
+    const int m = (int)(c / cpr), k = (int)(c - (int64_t)m * cpr) * KCH;
+    // x rows hold at least roundup(K, KCH) elements (16-byte row pitch)
+    uint4 v = *reinterpret_cast<const uint4*>(X + (int64_t)m * a.ldx + k);
+    if (k + KCH > a.K) {
+      T e[KCH];
+      __builtin_memcpy(e, &v, 16);
 #pragma unroll
-        for (int q = 0; q < KCH; ++q)
-          if (k + q >= a.K) e[q] = T(0);
-        __builtin_memcpy(&v, e, 16);
-      }
-      *reinterpret_cast<uint4*>(static_cast<T*>(a.xp) + (int64_t)m * a.ldxp + k) = v;
+      for (int q = 0; q < KCH; ++q)
+        if (k + q >= a.K) e[q] = T(0);
+      __builtin_memcpy(&v, e, 16);
     }
-    *reinterpret_cast<uint4*>(&tile[r * TP + kc]) = v;
-  }
-  __syncthreads();
-  // xt rows k, KCH consecutive m per item
-  for (int c = threadIdx.x; c < 64 * CPR; c += 256) {
-    const int kr = c / CPR, mc = (c % CPR) * KCH;
-    const int k = k0 + kr, m = m0 + mc;
-    if (k >= a.K || m >= a.M) continue;
-    T o[KCH];
-#pragma unroll
-    for (int q = 0; q < KCH; ++q) o[q] = tile[(mc + q) * TP + kr];
-    T* dst = static_cast<T*>(a.xt) + (int64_t)k * a.ldxt + m;
-    if (m + KCH <= a.M) {
-      uint4 v;
-      __builtin_memcpy(&v, o, 16);
-      *reinterpret_cast<uint4*>(dst) = v;
-    } else {
-      for (int q = 0; q < KCH && m + q < a.M; ++q) dst[q] = o[q];
-    }
+    *reinterpret_cast<uint4*>(static_cast<T*>(a.xp) + (int64_t)m * a.ldxp + k) = v;
   }
 }
 
 hipError_t launch_prologue(int bf16, const PrologueArgs& a, hipStream_t s, const LaunchEv& ev) {
-  dim3 grid(a.xp ? (a.K + 63) / 64 : 1, a.xp ? (a.M + 63) / 64 : 1), block(256);
+  const int64_t nch = a.xp ? (int64_t)a.M * ((a.K + 16 / (bf16 ? 2 : 4) - 1) / (16 / (bf16 ? 2 : 4))) : 1;
+  dim3 grid((unsigned)std::min<int64_t>((nch + 255) / 256, 4096)), block(256);
   if (bf16)
     ERASE_LAUNCH(erase_prologue<uint16_t>, grid, block, 0, s, ev, a);
   else
@@ -860,8 +960,8 @@ __global__ __launch_bounds__(256) void erase_head_bce(HeadArgs a) {
       }
     }
   }
-  // dz feature-major: items of KCH consecutive rows of one column
-  {
+  // dz feature-major: items of KCH consecutive rows of one column (nullable)
+  if (a.dnm) {
     T* D = static_cast<T*>(a.dnm);
     const int ipc = R / KCH;  // items per column
     for (int it = tid; it < N * ipc; it += 256) {
