@@ -80,9 +80,11 @@ def block_forward(blk: dict, p: dict, a0: np.ndarray, emulate_bf16: bool = False
     """
     rnd = _bf16 if emulate_bf16 else _ident
     acts = [a0]
+    pre = []
     a = a0
     for (kind, _fin, _fout), (W, b) in zip(blk["layers"], p["layers"]):
         h = a @ rnd(W).T + b
+        pre.append(h)
         if kind == "linear_relu":
             a = np.maximum(h, 0)
         elif kind == "cross":
@@ -93,11 +95,11 @@ def block_forward(blk: dict, p: dict, a0: np.ndarray, emulate_bf16: bool = False
         acts.append(a)
     w, c = p["head"]
     s = acts[-1] @ w + c[0]
-    return {"acts": acts, "s": s}
+    return {"acts": acts, "pre": pre, "s": s}
 
 
 def block_backward(blk: dict, p: dict, cache: dict, y: np.ndarray,
-                   emulate_bf16: bool = False):
+                   emulate_bf16: bool = False, g_out=None, want_input_grad: bool = False):
     """Local loss and exact gradient of lam_b * l_b w.r.t. theta_b only.
 
     l_b = mean_i BCE(s_i, y_i).  With g_s = lam (sigma(s) - y) / M:
@@ -109,6 +111,13 @@ def block_backward(blk: dict, p: dict, cache: dict, y: np.ndarray,
                    gradient at a_{l-1} = u W_l + g         (only if l > 1)
     No gradient is formed for the block input a_0: it is detached (Eq. 1).
     Returns (loss, grads) with grads shaped like p.
+
+    For the undetached baseline (conventional backpropagation through the
+    cuts, the comparison of Section 3): ``g_out`` is added to g at z (the
+    gradient later blocks send back), and ``want_input_grad`` also forms the
+    gradient at a_0, u W_1 (+ g for a first cross layer) plus g_l * h_l for
+    every cross layer l (a_0 enters each cross layer as a factor).  Then the
+    return value is (loss, grads, gradient at a_0).
     """
     rnd = _bf16 if emulate_bf16 else _ident
     acts, s = cache["acts"], cache["s"]
@@ -120,9 +129,12 @@ def block_backward(blk: dict, p: dict, cache: dict, y: np.ndarray,
     dw = acts[-1].T @ gs
     dc = np.array([gs.sum()], dtype=s.dtype)
     g = np.outer(gs, w)
+    if g_out is not None:
+        g = g + g_out
     a0 = acts[0]
     kinds = [k for (k, _i, _o) in blk["layers"]]
     grads = [None] * len(kinds)
+    g_in = np.zeros_like(a0) if want_input_grad else None
     for l in range(len(kinds), 0, -1):
         W, _b = p["layers"][l - 1]
         if kinds[l - 1] == "linear_relu":
@@ -130,12 +142,19 @@ def block_backward(blk: dict, p: dict, cache: dict, y: np.ndarray,
         else:
             g = rnd(g)
             u = rnd(g * a0)
+            if want_input_grad:
+                g_in = g_in + g * cache["pre"][l - 1]
         grads[l - 1] = (u.T @ acts[l - 1], u.sum(axis=0))
-        if l > 1:
+        if l > 1 or want_input_grad:
             g_below = u @ rnd(W)
             if kinds[l - 1] == "cross":
                 g_below = g_below + g
-            g = g_below
+            if l > 1:
+                g = g_below
+            else:
+                g_in = g_in + g_below
+    if want_input_grad:
+        return loss, {"layers": grads, "head": (dw, dc)}, g_in
     return loss, {"layers": grads, "head": (dw, dc)}
 
 
@@ -171,22 +190,40 @@ def forward_all(cfg: dict, params: list, x: np.ndarray, emulate_bf16: bool = Fal
 
 
 def step(cfg: dict, params: list, m: list, v: list, t: int, x: np.ndarray, y: np.ndarray,
-         emulate_bf16: bool = False, dtype=np.float64) -> dict:
+         emulate_bf16: bool = False, dtype=np.float64, detach: bool = True) -> dict:
     """One training step of the detached network.
 
     ``params``, ``m``, ``v``: one dict per block ({"layers": [(W, b)...],
     "head": (w, c)}).  ``t`` is the step count before this step; the Adam
     update uses t+1.  Returns losses (unweighted l_b), grads (of
     L = sum lam_b l_b), and the updated params/m/v and step count.
+
+    ``detach=False`` is the conventional (undetached) baseline: the same
+    forward and objective, but the gradient of L flows back across every cut
+    of a chain (a block reading the previous block's output sends the
+    gradient at its input back to that block).  For blocks reading the
+    shared input x nothing crosses a cut, so both give the same result.
     """
     y = np.asarray(y, dtype=dtype)
     caches = forward_all(cfg, params, x, emulate_bf16, dtype)
     ad = cfg["adam"]
     t1 = t + 1
+    nb = len(cfg["blocks"])
+    back = [None] * nb   # (loss, grads) per block
+    g_next = [None] * nb  # gradient sent back to block b's output
+    for b in range(nb - 1, -1, -1):
+        blk = cfg["blocks"][b]
+        p = _cast(params[b], dtype)
+        send = (not detach) and blk["input"] == "prev" and b > 0
+        if send:
+            loss, gr, g_in = block_backward(blk, p, caches[b], y, emulate_bf16, g_next[b], True)
+            g_next[b - 1] = g_in
+        else:
+            loss, gr = block_backward(blk, p, caches[b], y, emulate_bf16, g_next[b])
+        back[b] = (loss, gr)
     losses, grads, new_p, new_m, new_v = [], [], [], [], []
-    for blk, p, mb, vb, cache in zip(cfg["blocks"], params, m, v, caches):
+    for blk, p, mb, vb, (loss, gr) in zip(cfg["blocks"], params, m, v, back):
         p, mb, vb = _cast(p, dtype), _cast(mb, dtype), _cast(vb, dtype)
-        loss, gr = block_backward(blk, p, cache, y, emulate_bf16)
         losses.append(float(loss))
         grads.append(gr)
         pl, ml, vl = [], [], []
