@@ -97,14 +97,25 @@ typedef enum { ERASE_IN_X = 0, ERASE_IN_PREV = 1 } erase_input_src;
  *                  updates wait for the end of the step: after every
  *                  backward has finished, the forward stream runs Adam of
  *                  blocks 1..B (gradients are produced early, the optimizer
- *                  steps once per step, as in Section 2.2). */
+ *                  steps once per step, as in Section 2.2).
+ *   UNDETACHED:    the conventional baseline the paper compares against
+ *                  (Section 3): the same network and objective without the
+ *                  stop-gradient at the cuts.  A block reading the previous
+ *                  block's output sends the gradient at its input back into
+ *                  that block, so the gradients differ from the detached
+ *                  schedules for chains (identical for blocks on the shared
+ *                  input).  Every forward, then one backward from the last
+ *                  block to the first, then Adam, all on the forward stream.
+ *                  ERASE_ERR_UNSUPPORTED unless each chained block starts,
+ *                  and the block it reads ends, with a linear+ReLU layer. */
 typedef enum {
   ERASE_SCHED_SERIAL = 0,
   ERASE_SCHED_OVERLAP = 1,
   ERASE_SCHED_SERIAL_GRAPH = 2,
   ERASE_SCHED_OVERLAP_GRAPH = 3,
   ERASE_SCHED_PIPELINE = 4,
-  ERASE_SCHED_OVERLAP_ADAM_END = 5
+  ERASE_SCHED_OVERLAP_ADAM_END = 5,
+  ERASE_SCHED_UNDETACHED = 6
 } erase_schedule;
 
 typedef struct {

@@ -123,6 +123,7 @@ struct BlockRT {
   int L = 0;
   LayerRT layer[kMaxLayers];
   int64_t nparam = 0, off_w = 0, off_c = 0;
+  bool send = false;  // undetached schedule: the input gradient goes back to the previous block
   int nhead = 0;      // head partial rows (M-tiles of the head)
   bool head_fused = false;  // head+loss in the last forward GEMM's epilogue
   float* pdw = nullptr;
@@ -136,6 +137,7 @@ struct BlockRT {
 
 struct Plan {
   int bf16 = 1, esz = 2, M = 0;
+  bool undet_ok = true;  // every chained block can send its input gradient back
   int64_t Mr = 0;   // allocated rows of row-major arrays: roundup(M, 128)
   int64_t* t = nullptr;
   int* status = nullptr;
@@ -239,7 +241,11 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
       const int64_t Kr = roundup(R.K, 128), Nr = roundup(R.N, 128);
       R.ldwsh = ldK;
       R.wsh = cv.take(size_t(Nr) * ldK * esz);
-      if (l >= 1) {
+      // the input gradient of a layer: every layer but a block's first, and
+      // (undetached schedule) the first layer of a block reading the
+      // previous block's output
+      const bool dgrad = l >= 1 || S.input_src == ERASE_IN_PREV;
+      if (dgrad) {
         R.ldwsht = ldN;
         R.wsht = cv.take(size_t(Kr) * ldN * esz);
       }
@@ -256,6 +262,10 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
       const int BK = P->bf16 ? 64 : 32;
       R.fwd = choose_gemm(P->bf16, M, R.N, roundup(R.K, BK), false);
       R.wgrad = choose_gemm(P->bf16, R.N, R.K, roundup(M, BK), true);
+      if (l == 0 && dgrad) {
+        R.dgrad = choose_gemm(P->bf16, M, R.K, roundup(R.N, BK), false);
+        R.dgrad.group = xcd_group((int)cdiv(M, R.dgrad.bm), (int)cdiv(R.K, R.dgrad.bn), 1, R.dgrad.bm, R.dgrad.bn);
+      }
       if (l >= 1) {
         R.dgrad = choose_gemm(P->bf16, M, R.K, roundup(R.N, BK), false);
         // one launch for both backward GEMMs when they can share a tile
@@ -280,6 +290,14 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
       R.pstride = int64_t(R.N) * ldK;
       R.part = static_cast<float*>(cv.take(size_t(R.wgrad.split) * R.pstride * 4));
       R.bpart = static_cast<float*>(cv.take(size_t(R.wgrad.split) * R.N * 4));
+    }
+    if (S.input_src == ERASE_IN_PREV) {
+      // the gradient at this block's input reaches the previous block's
+      // output through a linear+ReLU first layer into a linear+ReLU last layer
+      const erase_block_spec& Sp = c.blocks[b - 1];
+      B.send = S.layers[0].kind == ERASE_LAYER_LINEAR_RELU &&
+               Sp.layers[Sp.n_layers - 1].kind == ERASE_LAYER_LINEAR_RELU;
+      P->undet_ok = P->undet_ok && B.send;
     }
     const int NL = B.layer[B.L - 1].N;
     B.off_w = off;
@@ -590,7 +608,7 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
 // input gradient of the layer below; the block input is detached (Eq. 1), so
 // layer 0 has no input gradient.  When both GEMMs of a layer share a tile
 // they go out as one launch.
-erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStream_t s, int sid) {
+erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStream_t s, int sid, bool send = false) {
   const Plan& P = c->P;
   const BlockRT& B = P.blk[b];
   const int M = P.M, esz = P.esz, bf = P.bf16;
@@ -626,6 +644,37 @@ erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStre
     cw.bytes = double(esz) * M * (double(R.N) + R.K) + 4.0 * R.wgrad.split * (double(R.N) * R.K + R.N);
     if (l == 0) {
       RUN(3, b, l, sid, s, cw, [&](const LaunchEv& ev) { return launch_gemm(bf, GK_WGRAD, gw, ew, s, ev); });
+      if (send && B.send) {
+        // undetached: the gradient at the block input, dX = dH_0 W_0, is
+        // added to the previous block's output gradient (its head's term,
+        // already in place) under that block's ReLU mask
+        const LayerRT& Rp = P.blk[b - 1].layer[P.blk[b - 1].L - 1];
+        GemmDesc gx{};
+        gx.A = R.dmn;
+        gx.lda = R.lddmn;
+        gx.B = R.wsht;
+        gx.ldb = R.ldwsht;
+        gx.M = M;
+        gx.N = R.K;
+        gx.K = (int)roundup(R.N, P.bf16 ? 64 : 32);
+        gx.kps = R.dgrad.kps;
+        gx.split = 1;
+        gx.bm = R.dgrad.bm;
+        gx.bn = R.dgrad.bn;
+        gx.group = R.dgrad.group;
+        EpiParams ex{};
+        ex.res = Rp.dmn;
+        ex.ldres = Rp.lddmn;
+        ex.mask = Rp.y;
+        ex.ldmask = Rp.ldy;
+        ex.below_cross = 0;
+        ex.dmn = Rp.dmn;
+        ex.lddmn = Rp.lddmn;
+        Cost cx = gemm_cost(gx);
+        cx.flops = 2.0 * M * R.N * R.K;
+        cx.bytes = double(esz) * (double(M) * R.N + double(R.N) * R.K + 3.0 * double(M) * R.K);
+        RUN(4, b, l, sid, s, cx, [&](const LaunchEv& ev) { return launch_gemm(bf, GK_DGRAD, gx, ex, s, ev); });
+      }
       break;
     }
     const LayerRT& Rb = B.layer[l - 1];
@@ -774,12 +823,15 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
       }
     }
   } else {
+    // SERIAL, and the conventional (undetached) baseline: every forward,
+    // then one backward from the last block to the first, then Adam
+    const bool send = sched == ERASE_SCHED_UNDETACHED;
     for (int b = 0; b < nb; ++b) {
       erase_status st = enqueue_forward(c, q, b, x, labels, sf, 0);
       if (st != ERASE_OK) return st;
     }
     for (int b = nb - 1; b >= 0; --b) {
-      erase_status st = enqueue_backward(c, q, b, x, sf, 0);
+      erase_status st = enqueue_backward(c, q, b, x, sf, 0, send);
       if (st != ERASE_OK) return st;
     }
     for (int b = 0; b < nb; ++b) {
@@ -794,6 +846,7 @@ int launches_per_step(const Plan& P) {
   int n = 1;  // prologue
   for (const BlockRT& B : P.blk) {
     n += B.L + (B.head_fused ? 0 : 1) + 1 + 1;  // forward GEMMs, head, first layer's weight gradient, Adam
+    n += B.send ? 1 : 0;                         // undetached: input gradient sent to the previous block
     for (int l = 1; l < B.L; ++l) n += B.layer[l].grouped ? 1 : 2;
   }
   return n;
@@ -945,7 +998,11 @@ erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t s
   if (reinterpret_cast<uintptr_t>(x) % 16 || reinterpret_cast<uintptr_t>(labels) % 4 ||
       reinterpret_cast<uintptr_t>(losses) % 4)
     return ERASE_ERR_INVALID_ARG;
-  if (schedule < ERASE_SCHED_SERIAL || schedule > ERASE_SCHED_OVERLAP_ADAM_END) return ERASE_ERR_INVALID_ARG;
+  if (schedule < ERASE_SCHED_SERIAL || schedule > ERASE_SCHED_UNDETACHED) return ERASE_ERR_INVALID_ARG;
+  if (schedule == ERASE_SCHED_UNDETACHED && !c->P.undet_ok) {
+    c->err = "undetached schedule: a chained block must start, and the block it reads must end, with linear+ReLU";
+    return ERASE_ERR_UNSUPPORTED;
+  }
   const bool graph = schedule == ERASE_SCHED_SERIAL_GRAPH || schedule == ERASE_SCHED_OVERLAP_GRAPH;
   if (graph && c->timing) return ERASE_ERR_UNSUPPORTED;
   int dev = -1;

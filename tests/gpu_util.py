@@ -52,13 +52,13 @@ def run_gpu_nosync(cfg, params, batches, schedules, bwd_streams=1):
     return losses, {"losses": losses[-1], "params": p, "m": m, "v": v, "grads": g}
 
 
-def run_oracle(cfg, params, batches, emulate_bf16=False, t0=0, m=None, v=None):
+def run_oracle(cfg, params, batches, emulate_bf16=False, t0=0, m=None, v=None, detach=True):
     m = m or synth.zero_state(params)
     v = v or synth.zero_state(params)
     p, t = params, t0
     recs = []
     for (x, y) in batches:
-        r = oracle.step(cfg, p, m, v, t, x, y, emulate_bf16=emulate_bf16)
+        r = oracle.step(cfg, p, m, v, t, x, y, emulate_bf16=emulate_bf16, detach=detach)
         p, m, v, t = r["params"], r["m"], r["v"], r["t"]
         recs.append({"losses": np.array(r["losses"]),
                      "params": [erase.pack_block(q) for q in p],
@@ -99,7 +99,7 @@ def compare(cfg, gpu, ref, tol, what=FIELDS):
     return worst
 
 
-def check_bf16(cfg, gpu, params, batches, tol=2e-2, slack=1.5):
+def check_bf16(cfg, gpu, params, batches, tol=2e-2, slack=1.5, detach=True):
     """bf16 parity against two oracles on the same inputs: the float64 oracle
     and the one that rounds to bf16 exactly the tensors the GPU stores in bf16.
 
@@ -110,8 +110,8 @@ def check_bf16(cfg, gpu, params, batches, tol=2e-2, slack=1.5):
     bf16 arithmetic can attain depends on the workload and is measured by e,
     not assumed.  Where e is small (the CTR MLP) the bound is tol itself.
     """
-    r64 = run_oracle(cfg, params, batches)
-    rbf = run_oracle(cfg, params, batches, emulate_bf16=True)
+    r64 = run_oracle(cfg, params, batches, detach=detach)
+    rbf = run_oracle(cfg, params, batches, emulate_bf16=True, detach=detach)
     inherent = worst_errors(cfg, rbf, r64)
     bounds = {k: max(tol, slack * inherent[k]) for k in FIELDS}
     w_emul = worst_errors(cfg, gpu, rbf)

@@ -138,6 +138,56 @@ def test_fused_and_standalone_head_bf16_vs_oracle(batch):
     tr.close()
 
 
+@pytest.mark.parametrize("name", ["tiny_chain", "mixed", "odd"])
+def test_undetached_fp32_vs_oracle(name):
+    """The conventional (undetached) baseline: gradients cross the cuts of a
+    chain; fp32 against the float64 oracle's undetached step."""
+    _say(f"case: undetached fp32 {name}")
+    if name == "tiny_chain":
+        cfg = synth.config("tiny_chain")
+    elif name == "mixed":
+        cfg = _mixed_fp32(150)
+    else:
+        blocks = [{"input": "x", "layers": [("linear_relu", 3, 1)], "lam": 1.0},
+                  {"input": "prev", "layers": [("linear_relu", 1, 5), ("linear_relu", 5, 2)], "lam": 1.0}]
+        cfg = synth.custom("f32", 7, 3, blocks, label_p=0.5)
+    params, batches = synth.make_workload(cfg, 8, 3)
+    _, g = run_gpu(cfg, params, batches, "undetached")
+    r = run_oracle(cfg, params, batches, detach=False)
+    compare(cfg, g, r, 1e-4)
+    if name != "odd":  # (the odd case's 1-wide cut is a dead ReLU on this batch: nothing flows back)
+        # and it is not the detached step
+        rd = run_oracle(cfg, params, batches)
+        assert max(float(np.abs(a - b).max()) for a, b in zip(g[0]["grads"][0], rd[0]["grads"][0])) > 1e-6
+
+
+def test_undetached_bf16_chain_vs_oracle():
+    _say("case: undetached bf16 deep chain")
+    cfg = synth.config("deep_chain", batch=384)
+    cfg["blocks"] = cfg["blocks"][:5]
+    params, batches = synth.make_workload(cfg, 9, 2)
+    _, g = run_gpu(cfg, params, batches, "undetached")
+    _say("  ", check_bf16(cfg, g, params, batches, detach=False))
+
+
+def test_undetached_equals_serial_on_shared_input_and_rejects_cross_chains():
+    _say("case: undetached on shared input; unsupported chain")
+    cfg = _ctr_small(batch=300, blocks=2)
+    params, batches = synth.make_workload(cfg, 4, 2)
+    assert_bit_identical(run_gpu(cfg, params, batches, "serial")[1], run_gpu(cfg, params, batches, "undetached")[1])
+    blocks = [{"input": "x", "layers": [("linear_relu", 8, 6)], "lam": 1.0},
+              {"input": "prev", "layers": [("cross", 6, 6), ("linear_relu", 6, 4)], "lam": 1.0}]
+    bad = synth.custom("f32", 16, 8, blocks)
+    p2, b2 = synth.make_workload(bad, 0, 1)
+    tr = erase.Trainer(bad, p2)
+    x, y = tr.device_batch(*b2[0])
+    with pytest.raises(erase.EraseError):
+        tr.step(x, y, "undetached")
+    tr.step(x, y, "serial")  # the context stays usable
+    tr.sync()
+    tr.close()
+
+
 def test_ctr_mlp_bf16_schedules_bit_identical():
     """Serial, overlapped and graph schedules, with 1 and 3 backward streams,
     produce the same bits."""
