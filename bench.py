@@ -49,10 +49,11 @@ def kernel_class(r, bf16=True):
 
 
 def kernel_source_hash():
-    """Hash of the kernel sources: byte counters taken from other sources are stale."""
+    """Hash of the kernel sources and build flags: byte counters taken from
+    other sources are stale."""
     h = hashlib.sha256()
-    for f in ("kernels.hip", "internal.h"):
-        with open(os.path.join(ROOT, "paper_2608_18469_amd", "csrc", f), "rb") as fh:
+    for f in ("csrc/kernels.hip", "csrc/internal.h", "build.py"):
+        with open(os.path.join(ROOT, "paper_2608_18469_amd", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 

@@ -4,6 +4,10 @@
 
 Compiles the HIP kernels and the C-ABI dispatcher into one shared library
 next to this file.  Packed-FP32 instructions are disabled for all device code.
+MFMA accumulators are allocated in the architectural VGPRs: with the default
+heuristic (accumulation registers) the register allocator permutes the
+accumulators between the unrolled halves of the GEMM main loops and repairs
+the permutation with register copies that wait on MFMA results.
 """
 from __future__ import annotations
 
@@ -30,6 +34,7 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           "-mllvm", "-amdgpu-mfma-vgpr-form",
            "-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc"),
            *SOURCES, "-o", tmp]
     if verbose:
