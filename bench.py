@@ -17,6 +17,12 @@ with identical kernels.  Per-kernel durations for
 the roofline and the measured backward/forward overlap come from HIP events
 recorded by the library around each launch, on the stream of that launch.
 The CPU baseline times the float64 oracle on the host on a bounded sample.
+
+A second measurement reproduces the paper's comparison of ERASE with
+conventional backpropagation (one backward of the summed block losses at the
+end of the step, gradients crossing every cut) on the 12-block chain, where
+detachment removes the cross-cut input gradients; on the shared-input CTR
+workload the two coincide.
 """
 from __future__ import annotations
 
@@ -153,6 +159,122 @@ def cpu_baseline(cfg, params, batches, budget_s, budget_1t_s):
             "cpu_model": _cpu_model(), "blas": blas, "os_cpu_count": os.cpu_count()}
 
 
+def time_schedules(tr, dev, scheds, steps, warmup, block, losses, M, log):
+    """Warm every schedule up (graph capture and instantiation happen here),
+    then time them interleaved in blocks of `block` steps so that clock and
+    thermal drift affect every schedule alike.  One global step counter picks
+    the batch, so every (batch, step parity) pair a graph schedule meets is
+    one it has already captured.  Returns per-schedule throughput, the p90 and
+    median of per-step samples/s (HIP events on the forward stream) and the
+    host enqueue time, plus the step function for later passes."""
+    import torch
+    gstep = 0
+
+    def one_step(s):
+        nonlocal gstep
+        x, y = dev[gstep % len(dev)]
+        gstep += 1
+        tr.step(x, y, s, losses, wait_current=False)
+
+    for s in scheds:
+        log(f"[bench] {s}: warmup {warmup}")
+        for _ in range(warmup):
+            one_step(s)
+        tr.sync()
+    acc = {s: {"el": 0.0, "per": [], "host": []} for s in scheds}
+    nblk = (steps + block - 1) // block
+    for bi in range(nblk):
+        n = min(block, steps - bi * block)
+        for s in scheds:
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for i in range(n):
+                evs[i][0].record(tr.sf)
+                h0 = time.perf_counter()
+                one_step(s)
+                acc[s]["host"].append(time.perf_counter() - h0)
+                evs[i][1].record(tr.sf)
+            torch.cuda.synchronize()
+            acc[s]["el"] += time.perf_counter() - t0
+            tr.sync()
+            acc[s]["per"] += [a.elapsed_time(b) for a, b in evs]  # ms per step on the device clock
+        log(f"[bench] block {bi + 1}/{nblk} ({n} steps per schedule) done")
+    res = {}
+    for s in scheds:
+        el = acc[s]["el"]
+        sps = M / (np.array(acc[s]["per"]) / 1e3)
+        res[s] = {"samples_per_s": M * steps / el, "ms_per_step": el / steps * 1e3,
+                  "p90_samples_per_s": float(np.percentile(sps, 90)), "median_samples_per_s": float(np.median(sps)),
+                  "host_enqueue_us": float(np.median(acc[s]["host"]) * 1e6), "elapsed_s": el}
+        log(f"[bench] {s}: {res[s]['samples_per_s']:.0f} samples/s, {res[s]['ms_per_step']:.3f} ms/step, "
+            f"p90 {res[s]['p90_samples_per_s']:.0f}, enqueue {res[s]['host_enqueue_us']:.1f} us")
+    return res, one_step
+
+
+def timed_records(tr, one_step, sched, n):
+    """Per-launch records (HIP events stamped at each kernel's own start and
+    end) of n steps of one schedule."""
+    tr.set_timing(True)
+    out = []
+    for _ in range(n):
+        one_step(sched)
+        tr.sync()
+        out.append(tr.read_timing())
+    tr.set_timing(False)
+    return out
+
+
+BWD_KINDS = ("wgrad_gemm", "dgrad_gemm", "bwd_gemm", "adam")
+
+
+def conventional_comparison(args, log):
+    """ERASE against conventional backpropagation on the 12-block chain: the
+    paper's comparison (one backward of the aggregate objective at the end of
+    the step, gradients crossing every cut) beside the detached step run
+    serially and the ERASE schedules.  On shared-input workloads nothing
+    crosses a cut, so the conventional step is the serial one; the chain is
+    where detachment changes the backward work."""
+    import torch
+
+    from paper_2608_18469_amd import erase, synth
+    cfg = synth.config("deep_chain")
+    M = cfg["batch"]
+    params, batches = synth.make_workload(cfg, 0, 8)
+    tr = erase.Trainer(cfg, params, keep_grads=True, bwd_streams=args.bwd_streams)
+    dev = [tr.device_batch(x, y) for (x, y) in batches]
+    losses = torch.zeros(len(cfg["blocks"]), device="cuda")
+    scheds = ["undetached", "undetached_graph", "serial", "serial_graph", "overlap", "overlap_graph", "pipeline"]
+    log(f"[bench] conventional vs ERASE on deep_chain (batch {M}, {len(cfg['blocks'])} chained blocks)")
+    res, one_step = time_schedules(tr, dev, scheds, args.steps, args.warmup, args.block, losses, M, log)
+    bwd = {}
+    for s in ("undetached", "serial"):
+        recs = [r[1:] for r in timed_records(tr, one_step, s, args.timing_steps)]
+        bwd[s] = float(np.mean([sum(r["end_ms"] - r["start_ms"] for r in rs if r["kind"] in BWD_KINDS)
+                                for rs in recs])) * 1e3
+    tr.close()
+    best = max(("overlap", "overlap_graph", "pipeline"), key=lambda k: res[k]["samples_per_s"])
+    conv = max(("undetached", "undetached_graph"), key=lambda k: res[k]["samples_per_s"])
+    det = max(("serial", "serial_graph"), key=lambda k: res[k]["samples_per_s"])
+    return {
+        "workload": f"deep_chain: {len(cfg['blocks'])} blocks chained through the stop-gradient, each "
+                    f"256->256->256 + Linear(256->1) BCE head, batch {M}, bf16, Adam",
+        "conventional": "the same network without the cuts, one backward of the sum of the block losses after the "
+                        "last forward (gradients cross every cut); schedules 'undetached' (launched) and "
+                        "'undetached_graph' (replayed HIP graph)",
+        "schedules": res,
+        "erase_schedule": best,
+        "conventional_schedule": conv,
+        "detached_serial_schedule": det,
+        "erase_vs_conventional": res[best]["samples_per_s"] / res[conv]["samples_per_s"],
+        "erase_vs_conventional_p90": res[best]["p90_samples_per_s"] / res[conv]["p90_samples_per_s"],
+        "detached_serial_vs_conventional": res[det]["samples_per_s"] / res[conv]["samples_per_s"],
+        "erase_vs_detached_serial": res[best]["samples_per_s"] / res[det]["samples_per_s"],
+        "backward_kernel_us_per_step": {"conventional": bwd["undetached"], "detached": bwd["serial"],
+                                        "reduction": 1.0 - bwd["serial"] / bwd["undetached"]},
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -166,6 +288,8 @@ def main():
                     help="seconds of oracle steps with every BLAS thread (then --cpu-budget-1t with one)")
     ap.add_argument("--cpu-budget-1t", type=float, default=6.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-conventional", action="store_true",
+                    help="skip the ERASE vs conventional backpropagation comparison on the 12-block chain")
     ap.add_argument("--schedules", default="serial,overlap,serial_graph,overlap_graph,pipeline")
     ap.add_argument("--bwd-streams", type=int, default=2,
                     help="backward streams of the ERASE schedules (block b uses stream b %% n); 2 measured "
@@ -202,70 +326,15 @@ def main():
     M = cfg["batch"]
     scheds = args.schedules.split(",")
 
-    # Warm every schedule up (graph capture and instantiation happen here),
-    # then time them interleaved in blocks of --block steps so that clock and
-    # thermal drift affect every schedule alike.  One global step counter
-    # picks the batch, so every (batch, step parity) pair a graph schedule
-    # meets is one it has already captured.
-    gstep = 0
-
-    def one_step(s):
-        nonlocal gstep
-        x, y = dev[gstep % len(dev)]
-        gstep += 1
-        tr.step(x, y, s, losses, wait_current=False)
-
-    for s in scheds:
-        log(f"[bench] {s}: warmup {args.warmup}")
-        for _ in range(args.warmup):
-            one_step(s)
-        tr.sync()
-    acc = {s: {"el": 0.0, "per": [], "host": []} for s in scheds}
-    nblk = (args.steps + args.block - 1) // args.block
-    for bi in range(nblk):
-        n = min(args.block, args.steps - bi * args.block)
-        for s in scheds:
-            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
-            torch.cuda.synchronize()
-            t0 = time.perf_counter()
-            for i in range(n):
-                evs[i][0].record(tr.sf)
-                h0 = time.perf_counter()
-                one_step(s)
-                acc[s]["host"].append(time.perf_counter() - h0)
-                evs[i][1].record(tr.sf)
-            torch.cuda.synchronize()
-            acc[s]["el"] += time.perf_counter() - t0
-            tr.sync()
-            acc[s]["per"] += [a.elapsed_time(b) for a, b in evs]  # ms per step on the device clock
-        log(f"[bench] block {bi + 1}/{nblk} ({n} steps per schedule) done")
-    res = {}
-    for s in scheds:
-        el = acc[s]["el"]
-        sps = M / (np.array(acc[s]["per"]) / 1e3)
-        res[s] = {"samples_per_s": M * args.steps / el, "ms_per_step": el / args.steps * 1e3,
-                  "p90_samples_per_s": float(np.percentile(sps, 90)), "median_samples_per_s": float(np.median(sps)),
-                  "host_enqueue_us": float(np.median(acc[s]["host"]) * 1e6), "elapsed_s": el}
-        log(f"[bench] {s}: {res[s]['samples_per_s']:.0f} samples/s, {res[s]['ms_per_step']:.3f} ms/step, "
-            f"p90 {res[s]['p90_samples_per_s']:.0f}, enqueue {res[s]['host_enqueue_us']:.1f} us")
+    res, one_step = time_schedules(tr, dev, scheds, args.steps, args.warmup, args.block, losses, M, log)
 
     # Per-launch kernel times from HIP events the library records around each
     # launch on that launch's own stream: a SERIAL pass (each kernel alone on
     # the device: the kernel table and the roofline) and an OVERLAP pass (the
     # measured backward/forward overlap).
-    def timed(sched, n):
-        tr.set_timing(True)
-        out = []
-        for i in range(n):
-            one_step(sched)
-            tr.sync()
-            out.append(tr.read_timing())
-        tr.set_timing(False)
-        return out
-
     log(f"[bench] kernel timing: {args.timing_steps} serial + {args.timing_steps} overlap steps")
-    recs_all = timed("serial", args.timing_steps)
-    recs_ovl = timed("overlap", args.timing_steps)
+    recs_all = timed_records(tr, one_step, "serial", args.timing_steps)
+    recs_ovl = timed_records(tr, one_step, "overlap", args.timing_steps)
     # an empty event pair per step (reported only: kernel events are stamped by the kernel dispatch)
     ev_cost_ms = float(np.median([r[0]["end_ms"] - r[0]["start_ms"] for r in recs_all]))
     recs_all = [r[1:] for r in recs_all]
@@ -352,6 +421,8 @@ def main():
         log(f"[bench] cpu baseline: oracle for ~{args.cpu_budget:.0f} s + ~{args.cpu_budget_1t:.0f} s on one thread")
         out["cpu_baseline"] = cpu_baseline(cfg, params, batches, args.cpu_budget, args.cpu_budget_1t)
     tr.close()
+    if not args.no_conventional:
+        out["erase_vs_conventional"] = conventional_comparison(args, log)
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")

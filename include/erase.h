@@ -107,7 +107,10 @@ typedef enum { ERASE_IN_X = 0, ERASE_IN_PREV = 1 } erase_input_src;
  *                  input).  Every forward, then one backward from the last
  *                  block to the first, then Adam, all on the forward stream.
  *                  ERASE_ERR_UNSUPPORTED unless each chained block starts,
- *                  and the block it reads ends, with a linear+ReLU layer. */
+ *                  and the block it reads ends, with a linear+ReLU layer.
+ *   UNDETACHED_GRAPH: UNDETACHED captured as a HIP graph and replayed (the
+ *                  conventional step without per-launch host cost, the
+ *                  control of OVERLAP_GRAPH); same results as UNDETACHED. */
 typedef enum {
   ERASE_SCHED_SERIAL = 0,
   ERASE_SCHED_OVERLAP = 1,
@@ -115,7 +118,8 @@ typedef enum {
   ERASE_SCHED_OVERLAP_GRAPH = 3,
   ERASE_SCHED_PIPELINE = 4,
   ERASE_SCHED_OVERLAP_ADAM_END = 5,
-  ERASE_SCHED_UNDETACHED = 6
+  ERASE_SCHED_UNDETACHED = 6,
+  ERASE_SCHED_UNDETACHED_GRAPH = 7
 } erase_schedule;
 
 typedef struct {

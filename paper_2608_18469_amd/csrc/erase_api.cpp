@@ -830,7 +830,7 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
   } else {
     // SERIAL, and the conventional (undetached) baseline: every forward,
     // then one backward from the last block to the first, then Adam
-    const bool send = sched == ERASE_SCHED_UNDETACHED;
+    const bool send = sched == ERASE_SCHED_UNDETACHED || sched == ERASE_SCHED_UNDETACHED_GRAPH;
     for (int b = 0; b < nb; ++b) {
       erase_status st = enqueue_forward(c, q, b, x, labels, sf, 0);
       if (st != ERASE_OK) return st;
@@ -1003,12 +1003,13 @@ erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t s
   if (reinterpret_cast<uintptr_t>(x) % 16 || reinterpret_cast<uintptr_t>(labels) % 4 ||
       reinterpret_cast<uintptr_t>(losses) % 4)
     return ERASE_ERR_INVALID_ARG;
-  if (schedule < ERASE_SCHED_SERIAL || schedule > ERASE_SCHED_UNDETACHED) return ERASE_ERR_INVALID_ARG;
-  if (schedule == ERASE_SCHED_UNDETACHED && !c->P.undet_ok) {
+  if (schedule < ERASE_SCHED_SERIAL || schedule > ERASE_SCHED_UNDETACHED_GRAPH) return ERASE_ERR_INVALID_ARG;
+  if ((schedule == ERASE_SCHED_UNDETACHED || schedule == ERASE_SCHED_UNDETACHED_GRAPH) && !c->P.undet_ok) {
     c->err = "undetached schedule: a chained block must start, and the block it reads must end, with linear+ReLU";
     return ERASE_ERR_UNSUPPORTED;
   }
-  const bool graph = schedule == ERASE_SCHED_SERIAL_GRAPH || schedule == ERASE_SCHED_OVERLAP_GRAPH;
+  const bool graph = schedule == ERASE_SCHED_SERIAL_GRAPH || schedule == ERASE_SCHED_OVERLAP_GRAPH ||
+                     schedule == ERASE_SCHED_UNDETACHED_GRAPH;
   if (graph && c->timing) return ERASE_ERR_UNSUPPORTED;
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != c->device) {

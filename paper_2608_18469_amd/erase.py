@@ -23,9 +23,10 @@ F32, BF16 = 0, 1
 LINEAR_RELU, CROSS = 0, 1
 LOSS_BCE = 0
 IN_X, IN_PREV = 0, 1
-SERIAL, OVERLAP, SERIAL_GRAPH, OVERLAP_GRAPH, PIPELINE, OVERLAP_ADAM_END, UNDETACHED = 0, 1, 2, 3, 4, 5, 6
+SERIAL, OVERLAP, SERIAL_GRAPH, OVERLAP_GRAPH, PIPELINE, OVERLAP_ADAM_END, UNDETACHED, UNDETACHED_GRAPH = range(8)
 SCHEDULES = {"serial": SERIAL, "overlap": OVERLAP, "serial_graph": SERIAL_GRAPH, "overlap_graph": OVERLAP_GRAPH,
-             "pipeline": PIPELINE, "overlap_adam_end": OVERLAP_ADAM_END, "undetached": UNDETACHED}
+             "pipeline": PIPELINE, "overlap_adam_end": OVERLAP_ADAM_END, "undetached": UNDETACHED,
+             "undetached_graph": UNDETACHED_GRAPH}
 KERNEL_KINDS = {0: "prologue", 1: "fwd_gemm", 2: "head_bce", 3: "wgrad_gemm", 4: "dgrad_gemm", 5: "adam",
                 6: "bwd_gemm", 7: "empty", 8: "fwd_head_gemm"}
 

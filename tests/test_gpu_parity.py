@@ -170,6 +170,37 @@ def test_undetached_bf16_chain_vs_oracle():
     _say("  ", check_bf16(cfg, g, params, batches, detach=False))
 
 
+def _replayed(cfg, params, batches, schedule, steps):
+    """`steps` steps cycling over the same device batches (a graph schedule
+    replays its graph from the third step on), the state read back after each."""
+    tr = erase.Trainer(cfg, params, keep_grads=True)
+    dev = [tr.device_batch(x, y) for (x, y) in batches]
+    recs = []
+    for i in range(steps):
+        xd, yd = dev[i % len(dev)]
+        tr.step(xd, yd, schedule)
+        tr.sync()
+        p, m, v, g = tr.flat_state()
+        recs.append({"losses": tr.losses.cpu().numpy().copy(), "params": p, "m": m, "v": v, "grads": g})
+    tr.close()
+    return recs
+
+
+@pytest.mark.parametrize("name", ["tiny_chain", "deep_chain5"])
+def test_undetached_graph_replays_match_eager(name):
+    """The conventional step captured as a HIP graph: every replay, with host
+    reads in between, bit-identical to the eager conventional step."""
+    _say(f"case: undetached_graph {name}")
+    if name == "tiny_chain":
+        cfg = synth.config("tiny_chain")
+    else:
+        cfg = synth.config("deep_chain", batch=256)
+        cfg["blocks"] = cfg["blocks"][:5]
+    params, batches = synth.make_workload(cfg, 11, 2)
+    assert_bit_identical(_replayed(cfg, params, batches, "undetached", 5),
+                         _replayed(cfg, params, batches, "undetached_graph", 5))
+
+
 def test_undetached_equals_serial_on_shared_input_and_rejects_cross_chains():
     _say("case: undetached on shared input; unsupported chain")
     cfg = _ctr_small(batch=300, blocks=2)
