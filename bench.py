@@ -11,8 +11,10 @@ already resident in HBM (8 batches, cycled).
 
 The headline value is samples/s of the fastest ERASE schedule (OVERLAP,
 OVERLAP_GRAPH captured as a HIP graph, or PIPELINE, the ERASE order without
-the end-of-step join; the config names it).  The same kernels are also timed
-in the serial order (SERIAL, SERIAL_GRAPH); the speedups compare schedules
+the end-of-step join, each ERASE order also with the backward streams' work
+enqueued by the library's worker thread, "+worker"; the config names it).
+The same kernels are also timed in the serial order (SERIAL, SERIAL_GRAPH);
+the speedups compare schedules
 with identical kernels.  Per-kernel durations for
 the roofline and the measured backward/forward overlap come from HIP events
 recorded by the library around each launch, on the stream of that launch.
@@ -169,12 +171,20 @@ def time_schedules(tr, dev, scheds, steps, warmup, block, losses, M, log):
     host enqueue time, plus the step function for later passes."""
     import torch
     gstep = 0
+    mode = ["caller"]
 
     def one_step(s):
+        # "<schedule>+worker": the library's worker thread enqueues the
+        # backward streams' work (non-blocking dispatch)
         nonlocal gstep
+        base, _, disp = s.partition("+")
+        disp = disp or "caller"
+        if disp != mode[0]:
+            tr.set_dispatch(disp)
+            mode[0] = disp
         x, y = dev[gstep % len(dev)]
         gstep += 1
-        tr.step(x, y, s, losses, wait_current=False)
+        tr.step(x, y, base, losses, wait_current=False)
 
     for s in scheds:
         log(f"[bench] {s}: warmup {warmup}")
@@ -195,9 +205,9 @@ def time_schedules(tr, dev, scheds, steps, warmup, block, losses, M, log):
                 one_step(s)
                 acc[s]["host"].append(time.perf_counter() - h0)
                 evs[i][1].record(tr.sf)
+            tr.sync()  # waits for the worker's enqueues too, then for every stream
             torch.cuda.synchronize()
             acc[s]["el"] += time.perf_counter() - t0
-            tr.sync()
             acc[s]["per"] += [a.elapsed_time(b) for a, b in evs]  # ms per step on the device clock
         log(f"[bench] block {bi + 1}/{nblk} ({n} steps per schedule) done")
     res = {}
@@ -244,16 +254,19 @@ def conventional_comparison(args, log):
     tr = erase.Trainer(cfg, params, keep_grads=True, bwd_streams=args.bwd_streams)
     dev = [tr.device_batch(x, y) for (x, y) in batches]
     losses = torch.zeros(len(cfg["blocks"]), device="cuda")
-    scheds = ["undetached", "undetached_graph", "serial", "serial_graph", "overlap", "overlap_graph", "pipeline"]
+    scheds = ["undetached", "undetached_graph", "serial", "serial_graph", "overlap", "overlap_graph", "pipeline",
+              "overlap+worker", "pipeline+worker"]
     log(f"[bench] conventional vs ERASE on deep_chain (batch {M}, {len(cfg['blocks'])} chained blocks)")
     res, one_step = time_schedules(tr, dev, scheds, args.steps, args.warmup, args.block, losses, M, log)
     bwd = {}
+    tr.set_dispatch("caller")
     for s in ("undetached", "serial"):
         recs = [r[1:] for r in timed_records(tr, one_step, s, args.timing_steps)]
         bwd[s] = float(np.mean([sum(r["end_ms"] - r["start_ms"] for r in rs if r["kind"] in BWD_KINDS)
                                 for rs in recs])) * 1e3
     tr.close()
-    best = max(("overlap", "overlap_graph", "pipeline"), key=lambda k: res[k]["samples_per_s"])
+    best = max(("overlap", "overlap_graph", "pipeline", "overlap+worker", "pipeline+worker"),
+               key=lambda k: res[k]["samples_per_s"])
     conv = max(("undetached", "undetached_graph"), key=lambda k: res[k]["samples_per_s"])
     det = max(("serial", "serial_graph"), key=lambda k: res[k]["samples_per_s"])
     return {
@@ -290,7 +303,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-conventional", action="store_true",
                     help="skip the ERASE vs conventional backpropagation comparison on the 12-block chain")
-    ap.add_argument("--schedules", default="serial,overlap,serial_graph,overlap_graph,pipeline")
+    ap.add_argument("--schedules", default="serial,overlap,serial_graph,overlap_graph,pipeline,overlap+worker,"
+                                           "pipeline+worker")
     ap.add_argument("--bwd-streams", type=int, default=2,
                     help="backward streams of the ERASE schedules (block b uses stream b %% n); 2 measured "
                          "fastest on ctr_mlp (1 leaves the backward chain serial, 3+ exceed the 4 hardware queues)")
@@ -332,6 +346,7 @@ def main():
     # launch on that launch's own stream: a SERIAL pass (each kernel alone on
     # the device: the kernel table and the roofline) and an OVERLAP pass (the
     # measured backward/forward overlap).
+    tr.set_dispatch("caller")
     log(f"[bench] kernel timing: {args.timing_steps} serial + {args.timing_steps} overlap steps")
     recs_all = timed_records(tr, one_step, "serial", args.timing_steps)
     recs_ovl = timed_records(tr, one_step, "overlap", args.timing_steps)
@@ -376,7 +391,8 @@ def main():
                for k, v in sorted(classes.items(), key=lambda kv: -kv[1]["ms"])}
 
     # headline: the fastest ERASE schedule (named in the config)
-    erase_scheds = [k for k in ("overlap", "overlap_graph", "pipeline") if k in res]
+    erase_scheds = [k for k in ("overlap", "overlap_graph", "pipeline", "overlap+worker", "pipeline+worker")
+                    if k in res]
     head = max(erase_scheds, key=lambda k: res[k]["samples_per_s"]) if erase_scheds else scheds[-1]
     out = {
         "metric": METRIC,
@@ -404,6 +420,8 @@ def main():
                                               if "overlap_graph" in res and "serial_graph" in res else None),
             "pipeline_vs_serial": (res["pipeline"]["samples_per_s"] / res["serial"]["samples_per_s"]
                                    if "pipeline" in res and "serial" in res else None),
+            "pipeline_worker_vs_serial": (res["pipeline+worker"]["samples_per_s"] / res["serial"]["samples_per_s"]
+                                          if "pipeline+worker" in res and "serial" in res else None),
             "headline_vs_best_serial": (res[head]["samples_per_s"] /
                                         max(res[k]["samples_per_s"] for k in ("serial", "serial_graph") if k in res)
                                         if any(k in res for k in ("serial", "serial_graph")) else None)},

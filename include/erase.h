@@ -240,8 +240,29 @@ typedef struct {
 erase_status erase_set_timing(void* ctx, int32_t enable);
 erase_status erase_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, int32_t* n);
 
-/* Destroy the context: waits for its streams, frees events and graphs.
- * Never frees caller memory.  NULL is accepted. */
+/* Host dispatch of the ERASE schedules (Section 2.2: blocking dispatch on
+ * the main thread vs non-blocking dispatch on a thread pool).
+ *   ERASE_DISPATCH_CALLER (default): erase_step() enqueues every launch and
+ *       event on the calling thread.
+ *   ERASE_DISPATCH_WORKER: for OVERLAP, OVERLAP_ADAM_END and PIPELINE, a
+ *       host thread owned by the context enqueues each block's backward,
+ *       Adam and backward-stream events while the calling thread goes on
+ *       with the next block's forward.  erase_step() may return before the
+ *       worker has enqueued the step's backward work; the next
+ *       erase_step() orders itself against it, and erase_sync() (like every
+ *       other call) first waits for it.  HIP errors on the worker surface at
+ *       the next call.  Graph schedules, the serial schedules and timed
+ *       steps (erase_set_timing) always dispatch on the caller.
+ * Results are bit-identical in both modes; the order in which the two
+ * streams' launches reach the device is not fixed in worker mode.  The
+ * thread is started on the first switch to ERASE_DISPATCH_WORKER (the
+ * calling thread's current device must be the context's) and joined by
+ * erase_destroy().  ERASE_ERR_INVALID_ARG for an unknown mode. */
+typedef enum { ERASE_DISPATCH_CALLER = 0, ERASE_DISPATCH_WORKER = 1 } erase_dispatch;
+erase_status erase_set_dispatch(void* ctx, int32_t mode);
+
+/* Destroy the context: waits for its dispatch thread and streams, frees
+ * events and graphs.  Never frees caller memory.  NULL is accepted. */
 erase_status erase_destroy(void* ctx);
 
 /* Static description of a status code. */

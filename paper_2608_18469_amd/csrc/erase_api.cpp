@@ -6,14 +6,22 @@
 // stream as soon as its forward and local loss are done, with events
 // enforcing the remaining dependencies, so it overlaps block b+1's forward.
 // HIP graphs fix the launch order and remove per-launch host cost (the
-// paper's CUDA-Graph variant).
+// paper's CUDA-Graph variant).  A worker host thread can enqueue the backward
+// streams' work while the calling thread enqueues the next forward (the
+// paper's non-blocking dispatch).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cmath>
+#include <condition_variable>
 #include <cstdio>
 #include <cstring>
+#include <deque>
+#include <functional>
+#include <memory>
+#include <mutex>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "erase.h"
@@ -394,6 +402,94 @@ struct GraphEntry {
   hipGraphExec_t exec;
 };
 
+// Error state of HIP calls made on a worker thread: hip_ok reports there
+// instead of into the context, which only the calling thread writes.
+struct ErrSink {
+  erase_status st = ERASE_OK;
+  std::string msg;
+};
+thread_local ErrSink* tl_sink = nullptr;
+
+// One host thread running enqueue jobs in submission order.  Jobs are
+// numbered from 1; wait(id) returns once jobs 1..id have finished.  After a
+// failed job the remaining ones are skipped (counted as finished), and the
+// first error is kept until take_error().
+class Worker {
+ public:
+  explicit Worker(int device) : device_(device) { th_ = std::thread([this] { loop(); }); }
+  ~Worker() {
+    {
+      std::lock_guard<std::mutex> lk(mu_);
+      stop_ = true;
+    }
+    cv_.notify_all();
+    th_.join();
+  }
+  uint64_t push(std::function<erase_status()> f) {
+    std::lock_guard<std::mutex> lk(mu_);
+    jobs_.push_back(std::move(f));
+    const uint64_t id = ++pushed_;
+    cv_.notify_all();
+    return id;
+  }
+  void wait(uint64_t id) {
+    std::unique_lock<std::mutex> lk(mu_);
+    done_cv_.wait(lk, [&] { return done_ >= id; });
+  }
+  void drain() {
+    std::unique_lock<std::mutex> lk(mu_);
+    done_cv_.wait(lk, [&] { return done_ >= pushed_; });
+  }
+  bool take_error(ErrSink* out) {
+    std::lock_guard<std::mutex> lk(mu_);
+    if (err_.st == ERASE_OK) return false;
+    *out = err_;
+    err_ = ErrSink{};
+    return true;
+  }
+
+ private:
+  void loop() {
+    (void)hipSetDevice(device_);
+    for (;;) {
+      std::function<erase_status()> f;
+      bool skip;
+      {
+        std::unique_lock<std::mutex> lk(mu_);
+        cv_.wait(lk, [&] { return stop_ || !jobs_.empty(); });
+        if (jobs_.empty()) return;  // stop requested and nothing left
+        f = std::move(jobs_.front());
+        jobs_.pop_front();
+        skip = err_.st != ERASE_OK;
+      }
+      ErrSink local;
+      erase_status st = ERASE_OK;
+      if (!skip) {
+        tl_sink = &local;
+        st = f();
+        tl_sink = nullptr;
+      }
+      {
+        std::lock_guard<std::mutex> lk(mu_);
+        if (st != ERASE_OK && err_.st == ERASE_OK) {
+          err_.st = st;
+          err_.msg = local.msg.empty() ? "backward enqueue failed on the worker thread" : local.msg;
+        }
+        ++done_;
+      }
+      done_cv_.notify_all();
+    }
+  }
+  int device_;
+  std::mutex mu_;
+  std::condition_variable cv_, done_cv_;
+  std::deque<std::function<erase_status()>> jobs_;
+  uint64_t pushed_ = 0, done_ = 0;
+  bool stop_ = false;
+  ErrSink err_;
+  std::thread th_;
+};
+
 struct Ctx {
   erase_config cfg{};
   std::vector<erase_block_spec> blocks;
@@ -417,17 +513,57 @@ struct Ctx {
   int64_t hstep = 0;     // host copy of the step counter (steps enqueued)
   int par = 0;           // parity of the step being enqueued
   bool pending = false;  // a PIPELINE step left backward work unjoined
+  // worker dispatch: the backward streams' launches are enqueued by
+  // `worker` (created on first use); job_of[b] is the job that enqueued
+  // block b's backward most recently
+  bool use_worker = false;
+  std::unique_ptr<Worker> worker;
+  std::vector<uint64_t> job_of;
 };
 
 bool hip_ok(Ctx* c, hipError_t e, const char* what) {
   if (e == hipSuccess) return true;
-  if (c) {
-    char buf[256];
-    std::snprintf(buf, sizeof buf, "%s: %s", what, hipGetErrorString(e));
+  char buf[256];
+  std::snprintf(buf, sizeof buf, "%s: %s", what, hipGetErrorString(e));
+  if (tl_sink) {  // worker thread: reported when the calling thread joins it
+    if (tl_sink->st == ERASE_OK) {
+      tl_sink->st = ERASE_ERR_HIP;
+      tl_sink->msg = buf;
+    }
+  } else if (c) {
     c->err = buf;
     c->sticky = ERASE_ERR_HIP;
   }
   return false;
+}
+
+// Wait for every job handed to the worker (if any) and move its first error
+// into the context.  Every entry point that enqueues or reads stream work
+// calls this first.
+erase_status quiesce(Ctx* c) {
+  if (!c->worker) return ERASE_OK;
+  c->worker->drain();
+  ErrSink e;
+  if (c->worker->take_error(&e)) {
+    c->err = e.msg;
+    c->sticky = e.st;
+    return e.st;
+  }
+  return ERASE_OK;
+}
+
+// Wait for worker job `id` (and those before it); its error, if any, goes
+// into the context.
+erase_status wait_job(Ctx* c, uint64_t id) {
+  if (!c->worker || id == 0) return ERASE_OK;
+  c->worker->wait(id);
+  ErrSink e;
+  if (c->worker->take_error(&e)) {
+    c->err = e.msg;
+    c->sticky = e.st;
+    return e.st;
+  }
+  return ERASE_OK;
 }
 
 #define HIPCHK(c, call)                                  \
@@ -502,7 +638,7 @@ class Enqueuer {
   } while (0)
 
 // Input of layer l of block b (row-major).
-void layer_input(const Ctx* c, int b, int l, const void* x, const void** mn, int64_t* ldmn) {
+void layer_input(const Ctx* c, int b, int l, const void* x, int par, const void** mn, int64_t* ldmn) {
   const Plan& P = c->P;
   const BlockRT& B = P.blk[b];
   if (l > 0) {
@@ -510,7 +646,7 @@ void layer_input(const Ctx* c, int b, int l, const void* x, const void** mn, int
     *ldmn = B.layer[l - 1].ldy;
   } else if (B.input_src == ERASE_IN_X) {
     (void)x;
-    *mn = P.xp[c->par];
+    *mn = P.xp[par];
     *ldmn = P.ldxp;
   } else {
     const BlockRT& A = P.blk[b - 1];
@@ -526,12 +662,12 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
   const int M = P.M, esz = P.esz;
   const void* x0;
   int64_t ldx0;
-  layer_input(c, b, 0, x, &x0, &ldx0);
+  layer_input(c, b, 0, x, c->par, &x0, &ldx0);
   for (int l = 0; l < B.L; ++l) {
     const LayerRT& R = B.layer[l];
     const void* a;
     int64_t lda;
-    layer_input(c, b, l, x, &a, &lda);
+    layer_input(c, b, l, x, c->par, &a, &lda);
     GemmDesc g{};
     g.A = a;
     g.lda = lda;
@@ -613,18 +749,19 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
 // input gradient of the layer below; the block input is detached (Eq. 1), so
 // layer 0 has no input gradient.  When both GEMMs of a layer share a tile
 // they go out as one launch.
-erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStream_t s, int sid, bool send = false) {
+erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStream_t s, int sid, int par,
+                              bool send = false) {
   const Plan& P = c->P;
   const BlockRT& B = P.blk[b];
   const int M = P.M, esz = P.esz, bf = P.bf16;
   const void* x0;
   int64_t ldx0;
-  layer_input(c, b, 0, x, &x0, &ldx0);
+  layer_input(c, b, 0, x, par, &x0, &ldx0);
   for (int l = B.L - 1; l >= 0; --l) {
     const LayerRT& R = B.layer[l];
     const void* inmn;
     int64_t ldinmn;
-    layer_input(c, b, l, x, &inmn, &ldinmn);
+    layer_input(c, b, l, x, par, &inmn, &ldinmn);
     // dW[n][k] = sum over the batch of dH[m][n] a[m][k]: both row-major
     GemmDesc gw{};
     gw.A = R.dmn;
@@ -734,7 +871,7 @@ erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStre
   return ERASE_OK;
 }
 
-erase_status enqueue_adam(Ctx* c, Enqueuer& q, int b, float* losses, hipStream_t s, int sid) {
+erase_status enqueue_adam(Ctx* c, Enqueuer& q, int b, float* losses, hipStream_t s, int sid, int par) {
   const Plan& P = c->P;
   const BlockRT& B = P.blk[b];
   AdamArgs a{};
@@ -742,7 +879,7 @@ erase_status enqueue_adam(Ctx* c, Enqueuer& q, int b, float* losses, hipStream_t
   a.nseg = (int)B.segs.size();
   for (int i = 0; i < a.nseg; ++i) a.chunk0[i] = B.segs[i].chunk0;
   a.nchunks = B.nchunks;
-  a.hyper = reinterpret_cast<const float*>(P.t + 2) + 2 * c->par;
+  a.hyper = reinterpret_cast<const float*>(P.t + 2) + 2 * par;
   a.beta1 = c->cfg.beta1;
   a.beta2 = c->cfg.beta2;
   a.eps = c->cfg.eps;
@@ -764,14 +901,19 @@ erase_status enqueue_adam(Ctx* c, Enqueuer& q, int b, float* losses, hipStream_t
 }
 
 // One step's launches.  `sched` selects serial or overlapped order; graph
-// schedules call this under stream capture.
-erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* labels, int sched, float* losses) {
+// schedules call this under stream capture.  With `threaded` (uncaptured,
+// untimed, worker dispatch on) the ERASE schedules hand each block's backward
+// and Adam to the worker thread, which enqueues them on the backward stream
+// while this thread goes on with the next block's forward.
+erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* labels, int sched, float* losses,
+                          bool threaded = false) {
   const Plan& P = c->P;
   const bool pipeline = sched == ERASE_SCHED_PIPELINE;
   const bool adam_end = sched == ERASE_SCHED_OVERLAP_ADAM_END;
   const bool overlap = sched == ERASE_SCHED_OVERLAP || sched == ERASE_SCHED_OVERLAP_GRAPH || pipeline || adam_end;
   const int nb = (int)P.blk.size();
   const int ns = (int)c->sbs.size();
+  const int par = c->par;
   hipStream_t sf = c->sf;
   {
     PrologueArgs pa{};
@@ -781,8 +923,8 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
     pa.beta2 = c->cfg.beta2;
     pa.x = x;
     pa.ldx = c->cfg.x_ld;
-    pa.hyper = reinterpret_cast<float*>(P.t + 2) + 2 * c->par;
-    pa.xp = P.xp[c->par];
+    pa.hyper = reinterpret_cast<float*>(P.t + 2) + 2 * par;
+    pa.xp = P.xp[par];
     pa.ldxp = P.ldxp;
 
     pa.M = P.M;
@@ -796,34 +938,66 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
     // ERASE: block b's backward and Adam go to backward stream b % ns as soon
     // as its forward and local loss are enqueued; the step ends with the
     // forward stream joined on every backward stream used.
+    threaded = threaded && c->worker != nullptr;
     for (int b = 0; b < nb; ++b) {
       const int k = b % ns;
       hipStream_t sb = c->sbs[k];
+      const bool chained_next = b + 1 < nb && P.blk[b + 1].input_src == ERASE_IN_PREV;
       if (pipeline && c->pending) {
         // no end-of-step join: block b's forward waits only for the previous
         // step's backward of block b (its weights, its activation buffers)
-        // and, in a chain, of block b+1 (which reads block b's output)
+        // and, in a chain, of block b+1 (which reads block b's output).  With
+        // the worker, those backward launches (and their event records) must
+        // have been enqueued before this thread waits on the events.
+        if (threaded) {
+          erase_status st = wait_job(c, c->job_of[b]);
+          if (st == ERASE_OK && chained_next) st = wait_job(c, c->job_of[b + 1]);
+          if (st != ERASE_OK) return st;
+        }
         HIPCHK(c, hipStreamWaitEvent(sf, c->eb[b], 0));
-        if (b + 1 < nb && P.blk[b + 1].input_src == ERASE_IN_PREV) HIPCHK(c, hipStreamWaitEvent(sf, c->eb[b + 1], 0));
+        if (chained_next) HIPCHK(c, hipStreamWaitEvent(sf, c->eb[b + 1], 0));
       }
       erase_status st = enqueue_forward(c, q, b, x, labels, sf, 0);
       if (st != ERASE_OK) return st;
       HIPCHK(c, hipEventRecord(c->ef[b], sf));
+      if (threaded) {
+        // ef[b] is recorded again only in a later step, after this job has
+        // finished (the waits above, or the join below), so the job's wait
+        // always binds to this step's record
+        hipEvent_t efb = c->ef[b], ebb = c->eb[b];
+        c->job_of[b] = c->worker->push([c, b, x, losses, sb, k, par, adam_end, efb, ebb]() -> erase_status {
+          HIPCHK(c, hipStreamWaitEvent(sb, efb, 0));
+          Enqueuer wq(c, false);
+          erase_status s2 = enqueue_backward(c, wq, b, x, sb, 1 + k, par);
+          if (s2 != ERASE_OK) return s2;
+          if (!adam_end) {
+            s2 = enqueue_adam(c, wq, b, losses, sb, 1 + k, par);
+            if (s2 != ERASE_OK) return s2;
+          }
+          HIPCHK(c, hipEventRecord(ebb, sb));
+          return ERASE_OK;
+        });
+        continue;
+      }
       HIPCHK(c, hipStreamWaitEvent(sb, c->ef[b], 0));
-      st = enqueue_backward(c, q, b, x, sb, 1 + k);
+      st = enqueue_backward(c, q, b, x, sb, 1 + k, par);
       if (st != ERASE_OK) return st;
       if (!adam_end) {
-        st = enqueue_adam(c, q, b, losses, sb, 1 + k);
+        st = enqueue_adam(c, q, b, losses, sb, 1 + k, par);
         if (st != ERASE_OK) return st;
       }
       HIPCHK(c, hipEventRecord(c->eb[b], sb));
+    }
+    if (threaded && !pipeline) {
+      erase_status st = quiesce(c);
+      if (st != ERASE_OK) return st;
     }
     if (!pipeline)
       for (int b = std::max(0, nb - ns); b < nb; ++b) HIPCHK(c, hipStreamWaitEvent(sf, c->eb[b], 0));
     if (adam_end) {
       // the optimizer steps once, after every block's backward
       for (int b = 0; b < nb; ++b) {
-        erase_status st = enqueue_adam(c, q, b, losses, sf, 0);
+        erase_status st = enqueue_adam(c, q, b, losses, sf, 0, par);
         if (st != ERASE_OK) return st;
       }
     }
@@ -836,11 +1010,11 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
       if (st != ERASE_OK) return st;
     }
     for (int b = nb - 1; b >= 0; --b) {
-      erase_status st = enqueue_backward(c, q, b, x, sf, 0, send);
+      erase_status st = enqueue_backward(c, q, b, x, sf, 0, par, send);
       if (st != ERASE_OK) return st;
     }
     for (int b = 0; b < nb; ++b) {
-      erase_status st = enqueue_adam(c, q, b, losses, sf, 0);
+      erase_status st = enqueue_adam(c, q, b, losses, sf, 0, par);
       if (st != ERASE_OK) return st;
     }
   }
@@ -861,6 +1035,8 @@ int launches_per_step(const Plan& P) {
 // stream (enqueued, not captured).
 erase_status join_pending(Ctx* c) {
   if (!c->pending) return ERASE_OK;
+  erase_status st = quiesce(c);
+  if (st != ERASE_OK) return st;
   for (size_t b = 0; b < c->eb.size(); ++b) HIPCHK(c, hipStreamWaitEvent(c->sf, c->eb[b], 0));
   c->pending = false;
   return ERASE_OK;
@@ -1016,6 +1192,15 @@ erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t s
     c->err = "erase_step called with a different current device than erase_init";
     return ERASE_ERR_STATE;
   }
+  const bool erase_order = schedule == ERASE_SCHED_OVERLAP || schedule == ERASE_SCHED_PIPELINE ||
+                           schedule == ERASE_SCHED_OVERLAP_ADAM_END;
+  const bool threaded = c->use_worker && erase_order && !c->timing;
+  // a worker-dispatched PIPELINE step orders itself against the previous
+  // step's jobs block by block; everything else starts with the worker idle
+  if (!(threaded && schedule == ERASE_SCHED_PIPELINE)) {
+    erase_status st = quiesce(c);
+    if (st != ERASE_OK) return st;
+  }
   c->par = (int)((c->hstep + 1) & 1);
   if (schedule != ERASE_SCHED_PIPELINE) {
     erase_status st = join_pending(c);
@@ -1028,7 +1213,7 @@ erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t s
       HIPCHK(c, hipEventRecord(c->tnull0, c->sf));
       HIPCHK(c, hipEventRecord(c->tnull1, c->sf));
     }
-    erase_status st = enqueue_step(c, q, x, labels, schedule, losses);
+    erase_status st = enqueue_step(c, q, x, labels, schedule, losses, threaded);
     if (st != ERASE_OK) {
       c->sticky = st == ERASE_ERR_HIP ? st : c->sticky;
       return st;
@@ -1081,6 +1266,7 @@ erase_status erase_sync(void* ctx) {
   Ctx* c = as_ctx(ctx);
   if (!c) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
+  if (erase_status q_ = quiesce(c); q_ != ERASE_OK) return q_;
   HIPCHK(c, hipStreamSynchronize(c->sf));
   for (hipStream_t sb : c->sbs) HIPCHK(c, hipStreamSynchronize(sb));
   c->pending = false;
@@ -1098,6 +1284,7 @@ erase_status erase_get_step(void* ctx, int64_t* t) {
   Ctx* c = as_ctx(ctx);
   if (!c || !t) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
+  if (erase_status q_ = quiesce(c); q_ != ERASE_OK) return q_;
   HIPCHK(c, hipStreamSynchronize(c->sf));
   for (hipStream_t sb : c->sbs) HIPCHK(c, hipStreamSynchronize(sb));
   c->pending = false;
@@ -1109,6 +1296,7 @@ erase_status erase_set_step(void* ctx, int64_t t) {
   Ctx* c = as_ctx(ctx);
   if (!c || t < 0) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
+  if (erase_status q_ = quiesce(c); q_ != ERASE_OK) return q_;
   HIPCHK(c, hipStreamSynchronize(c->sf));
   for (hipStream_t sb : c->sbs) HIPCHK(c, hipStreamSynchronize(sb));
   c->pending = false;
@@ -1121,6 +1309,7 @@ erase_status erase_refresh_weights(void* ctx) {
   Ctx* c = as_ctx(ctx);
   if (!c) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
+  if (erase_status q_ = quiesce(c); q_ != ERASE_OK) return q_;
   erase_status st = join_pending(c);
   if (st != ERASE_OK) return st;
   return refresh(c);
@@ -1130,6 +1319,7 @@ erase_status erase_set_timing(void* ctx, int32_t enable) {
   Ctx* c = as_ctx(ctx);
   if (!c) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
+  if (erase_status q_ = quiesce(c); q_ != ERASE_OK) return q_;
   if (enable && c->tev.empty()) {
     const int n = 2 * launches_per_step(c->P);
     for (int i = 0; i < n; ++i) {
@@ -1175,9 +1365,32 @@ erase_status erase_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, i
   return ERASE_OK;
 }
 
+erase_status erase_set_dispatch(void* ctx, int32_t mode) {
+  Ctx* c = as_ctx(ctx);
+  if (!c) return ERASE_ERR_INVALID_ARG;
+  if (mode != ERASE_DISPATCH_CALLER && mode != ERASE_DISPATCH_WORKER) return ERASE_ERR_INVALID_ARG;
+  if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
+  if (erase_status q_ = quiesce(c); q_ != ERASE_OK) return q_;
+  if (mode == ERASE_DISPATCH_WORKER && !c->worker) {
+    try {
+      c->worker.reset(new Worker(c->device));
+    } catch (...) {
+      c->err = "could not start the dispatch thread";
+      return ERASE_ERR_STATE;
+    }
+    c->job_of.assign(c->P.blk.size(), 0);
+  }
+  c->use_worker = mode == ERASE_DISPATCH_WORKER;
+  return ERASE_OK;
+}
+
 erase_status erase_destroy(void* ctx) {
   Ctx* c = as_ctx(ctx);
   if (!c) return ERASE_OK;
+  if (c->worker) {
+    c->worker->drain();
+    c->worker.reset();
+  }
   (void)hipStreamSynchronize(c->sf);
   for (hipStream_t sb : c->sbs) (void)hipStreamSynchronize(sb);
   destroy_graphs(c);

@@ -27,6 +27,8 @@ SERIAL, OVERLAP, SERIAL_GRAPH, OVERLAP_GRAPH, PIPELINE, OVERLAP_ADAM_END, UNDETA
 SCHEDULES = {"serial": SERIAL, "overlap": OVERLAP, "serial_graph": SERIAL_GRAPH, "overlap_graph": OVERLAP_GRAPH,
              "pipeline": PIPELINE, "overlap_adam_end": OVERLAP_ADAM_END, "undetached": UNDETACHED,
              "undetached_graph": UNDETACHED_GRAPH}
+DISPATCH_CALLER, DISPATCH_WORKER = 0, 1
+DISPATCH = {"caller": DISPATCH_CALLER, "worker": DISPATCH_WORKER}
 KERNEL_KINDS = {0: "prologue", 1: "fwd_gemm", 2: "head_bce", 3: "wgrad_gemm", 4: "dgrad_gemm", 5: "adam",
                 6: "bwd_gemm", 7: "empty", 8: "fwd_head_gemm"}
 
@@ -70,6 +72,7 @@ SIGNATURES = {
     "erase_set_step": (c_int32, [c_void_p, c_int64]),
     "erase_refresh_weights": (c_int32, [c_void_p]),
     "erase_set_timing": (c_int32, [c_void_p, c_int32]),
+    "erase_set_dispatch": (c_int32, [c_void_p, c_int32]),
     "erase_read_timing": (c_int32, [c_void_p, POINTER(KernelTime), c_int32, POINTER(c_int32)]),
     "erase_destroy": (c_int32, [c_void_p]),
     "erase_status_str": (ctypes.c_char_p, [c_int32]),
@@ -261,6 +264,12 @@ class Trainer:
 
     def set_timing(self, on: bool):
         _check(lib().erase_set_timing(self.ctx, 1 if on else 0), "erase_set_timing", self.ctx)
+
+    def set_dispatch(self, mode: str):
+        """'caller' (every launch from the calling thread) or 'worker' (a
+        library-owned host thread enqueues the backward streams' work of the
+        ERASE schedules)."""
+        _check(lib().erase_set_dispatch(self.ctx, DISPATCH[mode]), "erase_set_dispatch", self.ctx)
 
     def read_timing(self):
         n = c_int32(0)

@@ -35,12 +35,13 @@ def run_gpu(cfg, params, batches, schedule="overlap", keep_grads=True, trainer=N
     return tr, recs
 
 
-def run_gpu_nosync(cfg, params, batches, schedules, bwd_streams=1):
+def run_gpu_nosync(cfg, params, batches, schedules, bwd_streams=1, dispatch="caller"):
     """Enqueue one step per batch (schedules[i % len] for step i) without
     synchronizing in between, then sync once; returns the per-step losses and
     the final state as one record list of length 1 plus the losses."""
     import torch
     tr = erase.Trainer(cfg, params, keep_grads=True, bwd_streams=bwd_streams)
+    tr.set_dispatch(dispatch)
     dev = [tr.device_batch(x, y) for (x, y) in batches]
     outs = [torch.zeros(len(cfg["blocks"]), dtype=torch.float32, device="cuda") for _ in batches]
     for i, (xd, yd) in enumerate(dev):

@@ -147,6 +147,7 @@ def test_init_rejects_bad_arguments_before_any_hip_call():
     # step/sync on a NULL context
     assert L.erase_step(None, None, None, 0, None) == erase.ERR_INVALID_ARG
     assert L.erase_sync(None) == erase.ERR_INVALID_ARG
+    assert L.erase_set_dispatch(None, erase.DISPATCH_WORKER) == erase.ERR_INVALID_ARG
     assert L.erase_destroy(None) == erase.OK
 
 

@@ -254,6 +254,59 @@ def test_pipelined_steps_match_serial(name, streams):
     assert_bit_identical([ref], [mix])
 
 
+@pytest.mark.parametrize("name,streams", [("ctr_small", 2), ("deep_chain", 2), ("deep_chain", 1), ("mixed", 3)])
+def test_worker_dispatch_matches_serial(name, streams):
+    """The backward streams' work enqueued by the library's worker thread
+    (non-blocking dispatch): PIPELINE and OVERLAP steps back to back, and a
+    mix with graph, serial and undetached-free schedules, give the same bits
+    as serial steps dispatched from the caller."""
+    _say(f"case: worker dispatch, {name}, {streams} backward streams")
+    if name == "ctr_small":
+        cfg = _ctr_small(batch=640, blocks=4)
+    elif name == "deep_chain":
+        cfg = synth.config("deep_chain", batch=384)
+    else:
+        cfg = _mixed_fp32(200)
+    params, batches = synth.make_workload(cfg, 13, 6)
+    ref_l, ref = run_gpu_nosync(cfg, params, batches, ["serial"])
+    for scheds in (["pipeline"], ["overlap"], ["overlap_adam_end", "pipeline"],
+                   ["pipeline", "pipeline", "serial", "overlap_graph", "pipeline", "overlap"]):
+        got_l, got = run_gpu_nosync(cfg, params, batches, scheds, bwd_streams=streams, dispatch="worker")
+        assert np.array_equal(ref_l.view(np.uint32), got_l.view(np.uint32)), scheds
+        assert_bit_identical([ref], [got])
+
+
+def test_worker_dispatch_switch_and_state_calls():
+    """Switching dispatch modes between steps, and the state calls
+    (step counter, timing) in the middle of worker-dispatched steps."""
+    _say("case: worker dispatch switching")
+    cfg = _ctr_small(batch=320, blocks=3)
+    params, batches = synth.make_workload(cfg, 17, 6)
+    ref_l, ref = run_gpu_nosync(cfg, params, batches, ["serial"])
+    tr = erase.Trainer(cfg, params, keep_grads=True, bwd_streams=2)
+    dev = [tr.device_batch(x, y) for (x, y) in batches]
+    import torch
+    outs = [torch.zeros(len(cfg["blocks"]), dtype=torch.float32, device="cuda") for _ in batches]
+    modes = ["worker", "worker", "caller", "worker", "caller", "worker"]
+    for i, (xd, yd) in enumerate(dev):
+        tr.set_dispatch(modes[i])
+        tr.step(xd, yd, "pipeline", losses=outs[i], wait_current=(i == 0))
+        if i == 2:
+            assert tr.get_step() == 3
+        if i == 3:
+            tr.set_timing(True)
+            tr.set_timing(False)
+    tr.sync()
+    p, m, v, g = tr.flat_state()
+    tr.close()
+    got_l = np.stack([o.cpu().numpy() for o in outs])
+    assert np.array_equal(ref_l.view(np.uint32), got_l.view(np.uint32))
+    assert_bit_identical([ref], [{"losses": got_l[-1], "params": p, "m": m, "v": v, "grads": g}])
+    tr2 = erase.Trainer(cfg, params)
+    assert erase.lib().erase_set_dispatch(tr2.ctx, 5) == erase.ERR_INVALID_ARG
+    tr2.close()
+
+
 def test_deep_chain_multi_stream_matches_serial():
     """A chain with 4 backward streams: bit-identical to the serial schedule."""
     _say("case: deep_chain, 4 backward streams vs serial")
