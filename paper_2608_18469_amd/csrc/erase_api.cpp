@@ -656,7 +656,12 @@ void layer_input(const Ctx* c, int b, int l, const void* x, int par, const void*
   }
 }
 
-erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const float* labels, hipStream_t s, int sid) {
+erase_status enqueue_head(Ctx* c, Enqueuer& q, int b, const float* labels, hipStream_t s, int sid);
+
+// Block b's forward GEMMs and, unless it is fused into the last GEMM or
+// `with_head` is false, its local head and loss.
+erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const float* labels, hipStream_t s, int sid,
+                             bool with_head = true) {
   const Plan& P = c->P;
   const BlockRT& B = P.blk[b];
   const int M = P.M, esz = P.esz;
@@ -717,7 +722,15 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
     const int bf = P.bf16;
     RUN(fused ? 8 : 1, b, l, sid, s, cost, [&](const LaunchEv& ev) { return launch_gemm(bf, kind, g, e, s, ev); });
   }
-  if (B.head_fused) return ERASE_OK;
+  if (B.head_fused || !with_head) return ERASE_OK;
+  return enqueue_head(c, q, b, labels, s, sid);
+}
+
+// Standalone local head, loss and loss gradient of block b (Section 2.1).
+erase_status enqueue_head(Ctx* c, Enqueuer& q, int b, const float* labels, hipStream_t s, int sid) {
+  const Plan& P = c->P;
+  const BlockRT& B = P.blk[b];
+  const int M = P.M, esz = P.esz;
   const LayerRT& Rl = B.layer[B.L - 1];
   HeadArgs h{};
   h.z = Rl.y;
@@ -957,7 +970,10 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
         HIPCHK(c, hipStreamWaitEvent(sf, c->eb[b], 0));
         if (chained_next) HIPCHK(c, hipStreamWaitEvent(sf, c->eb[b + 1], 0));
       }
-      erase_status st = enqueue_forward(c, q, b, x, labels, sf, 0);
+      // a standalone head goes to the backward stream, in front of the
+      // block's backward: the next block's forward waits only for the body
+      const bool head_b = !P.blk[b].head_fused;
+      erase_status st = enqueue_forward(c, q, b, x, labels, sf, 0, !head_b);
       if (st != ERASE_OK) return st;
       HIPCHK(c, hipEventRecord(c->ef[b], sf));
       if (threaded) {
@@ -965,10 +981,13 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
         // finished (the waits above, or the join below), so the job's wait
         // always binds to this step's record
         hipEvent_t efb = c->ef[b], ebb = c->eb[b];
-        c->job_of[b] = c->worker->push([c, b, x, losses, sb, k, par, adam_end, efb, ebb]() -> erase_status {
+        c->job_of[b] = c->worker->push([c, b, x, labels, losses, sb, k, par, adam_end, head_b, efb,
+                                        ebb]() -> erase_status {
           HIPCHK(c, hipStreamWaitEvent(sb, efb, 0));
           Enqueuer wq(c, false);
-          erase_status s2 = enqueue_backward(c, wq, b, x, sb, 1 + k, par);
+          erase_status s2 = head_b ? enqueue_head(c, wq, b, labels, sb, 1 + k) : ERASE_OK;
+          if (s2 != ERASE_OK) return s2;
+          s2 = enqueue_backward(c, wq, b, x, sb, 1 + k, par);
           if (s2 != ERASE_OK) return s2;
           if (!adam_end) {
             s2 = enqueue_adam(c, wq, b, losses, sb, 1 + k, par);
@@ -980,6 +999,10 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
         continue;
       }
       HIPCHK(c, hipStreamWaitEvent(sb, c->ef[b], 0));
+      if (head_b) {
+        st = enqueue_head(c, q, b, labels, sb, 1 + k);
+        if (st != ERASE_OK) return st;
+      }
       st = enqueue_backward(c, q, b, x, sb, 1 + k, par);
       if (st != ERASE_OK) return st;
       if (!adam_end) {

@@ -444,3 +444,18 @@ def test_kernel_timing_records():
     assert {r["stream"] for r in recs if r["kind"] in ("fwd_gemm", "fwd_head_gemm", "prologue")} == {0}
     with pytest.raises(erase.EraseError):
         tr.step(xd, yd, "overlap_graph")
+    # a standalone head (256-wide chain blocks) runs on the backward stream in
+    # the ERASE order, on the forward stream in the serial one
+    cc = synth.config("deep_chain", batch=256)
+    cc["blocks"] = cc["blocks"][:3]
+    pc, bc = synth.make_workload(cc, 9, 1)
+    tc = erase.Trainer(cc, pc)
+    xc, yc = tc.device_batch(*bc[0])
+    tc.set_timing(True)
+    for sched, want in (("overlap", {1}), ("serial", {0})):
+        tc.step(xc, yc, sched)
+        tc.sync()
+        rc = tc.read_timing()[1:]
+        assert {r["stream"] for r in rc if r["kind"] == "head_bce"} == want, sched
+        assert len([r for r in rc if r["kind"] == "head_bce"]) == 3
+    tc.close()
