@@ -60,7 +60,7 @@ def kernel_source_hash():
     """Hash of the kernel sources and build flags: byte counters taken from
     other sources are stale."""
     h = hashlib.sha256()
-    for f in ("csrc/kernels.hip", "csrc/internal.h", "build.py"):
+    for f in ("csrc/kernels.hip", "csrc/embed.hip", "csrc/internal.h", "build.py"):
         with open(os.path.join(ROOT, "paper_2608_18469_amd", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -261,6 +261,45 @@ erase_status erase_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, i
 typedef enum { ERASE_DISPATCH_CALLER = 0, ERASE_DISPATCH_WORKER = 1 } erase_dispatch;
 erase_status erase_set_dispatch(void* ctx, int32_t mode);
 
+/* Embedding-bag input stage of the CTR workload.  The paper feeds its CTR
+ * model (Section 3.2) an input embedding x (Section 2.1) without describing
+ * it; this is the synthetic CTR input recipe of the benchmark workload, on
+ * the device:
+ *   x[m][j]                   = log1p(dense[m][j])                 j < n_dense
+ *   x[m][n_dense + t*dim + d] = sum over i in bag (t, m) of tables[t][indices[i]][d]
+ *   x[m][k]                   = 0        n_dense + n_tables*dim <= k < x_ld
+ * Bag (t, m) is indices[offsets[t*(batch+1) + m] .. offsets[t*(batch+1) + m + 1]).
+ * Each bag is summed in fp32 in index order, then rounded (to nearest even)
+ * to x's dtype; log1p is evaluated in fp32.
+ * Device pointers: dense fp32 [batch][n_dense] (NULL when n_dense = 0),
+ * offsets int64 [n_tables][batch+1], indices int32 [nnz] (NULL when
+ * nnz = 0), tables fp32 [n_tables][rows][dim] (16-byte aligned), x
+ * [batch][x_ld] of dtype (16-byte aligned, x_ld*esz a multiple of 16
+ * bytes), status int32 [1] or NULL.  The caller owns all of them.
+ * Invalid offsets (not 0 <= begin <= end <= nnz) or indices (outside
+ * [0, rows)) read nothing and contribute zero; they set *status = 1, which
+ * the library never clears.  Enqueued on `stream` (a HIP stream handle,
+ * NULL for the default stream); returns without waiting.
+ * ERASE_ERR_INVALID_ARG (null or misaligned pointer) / ERASE_ERR_SHAPE
+ * (batch 1..2^24, n_dense 0..4096, n_tables 1..4096 with n_tables*batch <
+ * 2^31, dim a multiple of 4 in 4..256, rows 1..2^31-1, nnz 0..2^31-1,
+ * x_ld >= n_dense + n_tables*dim) before anything is enqueued;
+ * ERASE_ERR_HIP if the launch fails. */
+typedef struct {
+  int32_t batch;
+  int32_t n_dense;
+  int32_t n_tables;
+  int32_t dim;
+  int64_t rows;
+  int64_t nnz;
+  int32_t dtype;  /* erase_dtype of x */
+  int64_t x_ld;
+} erase_bag_config;
+
+erase_status erase_embed_bags(const erase_bag_config* cfg, const float* dense, const int64_t* offsets,
+                              const int32_t* indices, const float* tables, void* x, int32_t* status,
+                              void* stream);
+
 /* Destroy the context: waits for its dispatch thread and streams, frees
  * events and graphs.  Never frees caller memory.  NULL is accepted. */
 erase_status erase_destroy(void* ctx);

@@ -1,3 +1,4 @@
-"""CPU oracle (test infrastructure only; see erase_oracle.py)."""
+"""CPU oracle (test infrastructure only; see erase_oracle.py and embed_oracle.py)."""
 from .erase_oracle import *  # noqa: F401,F403
 from .erase_oracle import total_loss  # noqa: F401
+from .embed_oracle import embed_bags  # noqa: F401

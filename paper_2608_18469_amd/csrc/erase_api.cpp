@@ -1407,6 +1407,42 @@ erase_status erase_set_dispatch(void* ctx, int32_t mode) {
   return ERASE_OK;
 }
 
+erase_status erase_embed_bags(const erase_bag_config* cfg, const float* dense, const int64_t* offsets,
+                              const int32_t* indices, const float* tables, void* x, int32_t* status,
+                              void* stream) {
+  if (!cfg) return ERASE_ERR_INVALID_ARG;
+  const erase_bag_config& b = *cfg;
+  if (b.dtype != ERASE_F32 && b.dtype != ERASE_BF16) return ERASE_ERR_INVALID_ARG;
+  const int esz = b.dtype == ERASE_BF16 ? 2 : 4;
+  if (b.batch < 1 || b.batch > kMaxBatch || b.n_dense < 0 || b.n_dense > 4096 || b.n_tables < 1 ||
+      b.n_tables > 4096 || int64_t(b.n_tables) * b.batch >= (int64_t(1) << 31) || b.dim < 4 || b.dim > 256 ||
+      b.dim % 4 || b.rows < 1 || b.rows >= (int64_t(1) << 31) || b.nnz < 0 || b.nnz >= (int64_t(1) << 31) ||
+      b.x_ld < int64_t(b.n_dense) + int64_t(b.n_tables) * b.dim || (b.x_ld * esz) % 16)
+    return ERASE_ERR_SHAPE;
+  auto mis = [](const void* p, uintptr_t a) { return reinterpret_cast<uintptr_t>(p) % a != 0; };
+  if ((b.n_dense > 0 && (!dense || mis(dense, 4))) || !offsets || mis(offsets, 8) ||
+      (b.nnz > 0 && (!indices || mis(indices, 4))) || !tables || mis(tables, 16) || !x || mis(x, 16) ||
+      (status && mis(status, 4)))
+    return ERASE_ERR_INVALID_ARG;
+  EmbedArgs a{};
+  a.dense = dense;
+  a.offsets = offsets;
+  a.indices = indices;
+  a.tables = tables;
+  a.x = x;
+  a.ldx = b.x_ld;
+  a.status = status;
+  a.nnz = b.nnz;
+  a.rows = b.rows;
+  a.M = b.batch;
+  a.n_dense = b.n_dense;
+  a.T = b.n_tables;
+  a.dim = b.dim;
+  if (launch_embed_bags(b.dtype == ERASE_BF16, a, static_cast<hipStream_t>(stream)) != hipSuccess)
+    return ERASE_ERR_HIP;
+  return ERASE_OK;
+}
+
 erase_status erase_destroy(void* ctx) {
   Ctx* c = as_ctx(ctx);
   if (!c) return ERASE_OK;

@@ -166,4 +166,20 @@ hipError_t launch_adam(int bf16, const AdamArgs& a, hipStream_t s, const LaunchE
 // Weight copies only (init / refresh): same segments, no update.
 hipError_t launch_refresh(int bf16, const AdamArgs& a, hipStream_t s);
 
+// Embedding-bag input stage: x[m] = [log1p(dense[m]) | bag sums | 0...].
+// Bag m of table t is indices[offsets[t][m] .. offsets[t][m+1]); rows of
+// table t are tables[t][row][0 .. dim).  Invalid offsets or indices are
+// skipped (read nothing) and set status[0] = 1 (status nullable).
+struct EmbedArgs {
+  const float* dense;     // [M][n_dense]
+  const int64_t* offsets; // [T][M+1]
+  const int32_t* indices; // [nnz]
+  const float* tables;    // [T][rows][dim], 16-byte aligned
+  void* x; int64_t ldx;   // [M][ldx] of the activation dtype
+  int* status;
+  int64_t nnz, rows;
+  int M, n_dense, T, dim;  // dim % 4 == 0, 4 <= dim <= 256
+};
+hipError_t launch_embed_bags(int bf16, const EmbedArgs& a, hipStream_t s);
+
 }  // namespace erase

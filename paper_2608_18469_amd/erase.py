@@ -59,6 +59,12 @@ class KernelTime(ctypes.Structure):
 
 
 # every entry point of include/erase.h with its ctypes signature
+class BagConfig(ctypes.Structure):
+    """erase_bag_config: shape of the embedding-bag input stage."""
+    _fields_ = [("batch", c_int32), ("n_dense", c_int32), ("n_tables", c_int32), ("dim", c_int32),
+                ("rows", c_int64), ("nnz", c_int64), ("dtype", c_int32), ("x_ld", c_int64)]
+
+
 SIGNATURES = {
     "erase_param_count": (c_int32, [POINTER(Config), c_int32, POINTER(c_int64)]),
     "erase_workspace_bytes": (c_int32, [POINTER(Config), POINTER(c_size_t)]),
@@ -73,6 +79,8 @@ SIGNATURES = {
     "erase_refresh_weights": (c_int32, [c_void_p]),
     "erase_set_timing": (c_int32, [c_void_p, c_int32]),
     "erase_set_dispatch": (c_int32, [c_void_p, c_int32]),
+    "erase_embed_bags": (c_int32, [POINTER(BagConfig), c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                   c_void_p]),
     "erase_read_timing": (c_int32, [c_void_p, POINTER(KernelTime), c_int32, POINTER(c_int32)]),
     "erase_destroy": (c_int32, [c_void_p]),
     "erase_status_str": (ctypes.c_char_p, [c_int32]),
@@ -179,11 +187,40 @@ def unpack_block(blk: dict, flat: np.ndarray) -> dict:
     return {"layers": layers, "head": (w, c)}
 
 
+def embed_bags(dense, offsets, indices, tables, x, status=None, stream=None):
+    """The embedding-bag input stage (erase_embed_bags) on device tensors:
+    dense fp32 [M][n_dense] (or None), offsets int64 [T][M+1], indices int32
+    [nnz], tables fp32 [T][rows][dim], x [M][x_ld] float32 or bfloat16 (the
+    output), status int32 [1] or None.  Enqueued on `stream` (a torch stream;
+    default: the current one); returns without waiting."""
+    import torch
+    M, x_ld = x.shape
+    T, rows, dim = tables.shape
+    n_dense = 0 if dense is None else dense.shape[1]
+    for name, t, dt in (("offsets", offsets, torch.int64), ("indices", indices, torch.int32),
+                        ("tables", tables, torch.float32)):
+        if t.dtype != dt or not t.is_contiguous():
+            raise EraseError(ERR_INVALID_ARG, "embed_bags", f"{name} must be a contiguous {dt} tensor")
+    if dense is not None and (dense.dtype != torch.float32 or not dense.is_contiguous()):
+        raise EraseError(ERR_INVALID_ARG, "embed_bags", "dense must be a contiguous float32 tensor")
+    if x.dtype not in (torch.float32, torch.bfloat16) or x.stride(1) != 1:
+        raise EraseError(ERR_INVALID_ARG, "embed_bags", "x must be float32 or bfloat16 with unit column stride")
+    if tuple(offsets.shape) != (T, M + 1):
+        raise EraseError(ERR_SHAPE, "embed_bags", "offsets must be [n_tables][batch + 1]")
+    cfg = BagConfig(M, n_dense, T, dim, rows, indices.numel(), BF16 if x.dtype == torch.bfloat16 else F32,
+                    x.stride(0))
+    s = (stream or torch.cuda.current_stream()).cuda_stream
+    ptr = (lambda t: None if t is None or t.numel() == 0 else t.data_ptr())
+    _check(lib().erase_embed_bags(ctypes.byref(cfg), ptr(dense), offsets.data_ptr(), ptr(indices),
+                                  tables.data_ptr(), x.data_ptr(), ptr(status), s), "erase_embed_bags")
+
+
 class Trainer:
     """Owns the device buffers, two streams and one library context."""
 
     def __init__(self, cfg: dict, params: list, x_ld: int | None = None, keep_grads: bool = True,
-                 m: list | None = None, v: list | None = None, step: int = 0, bwd_streams: int = 1):
+                 m: list | None = None, v: list | None = None, step: int = 0, bwd_streams: int = 1,
+                 streams=None):
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("no HIP device available: the ERASE step runs only on the GPU")
@@ -211,8 +248,14 @@ class Trainer:
         self.ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=self.dev)
         pad = (-self.ws.data_ptr()) % 256
         self.ws_ptr = self.ws.data_ptr() + pad
-        self.sf = torch.cuda.Stream(device=self.dev)
-        self.sbs = [torch.cuda.Stream(device=self.dev) for _ in range(bwd_streams)]
+        if streams is not None:
+            # caller-owned streams (torch streams, or torch.cuda.ExternalStream
+            # around HIP handles): (forward, [backward, ...])
+            self.sf, self.sbs = streams[0], list(streams[1])
+            bwd_streams = len(self.sbs)
+        else:
+            self.sf = torch.cuda.Stream(device=self.dev)
+            self.sbs = [torch.cuda.Stream(device=self.dev) for _ in range(bwd_streams)]
         self.sb = self.sbs[0]
         torch.cuda.synchronize(self.dev)
         ctx = c_void_p()

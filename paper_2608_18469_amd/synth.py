@@ -165,18 +165,37 @@ class CtrTables:
         self.cdf = _bounded_zipf_cdf(rows, CTR_ZIPF_S)
 
 
-def make_ctr_x(tables: CtrTables, M: int, rng: np.random.Generator) -> np.ndarray:
-    """CTR input rows: log1p(LogNormal(0,1)) dense features followed by 26
-    sum-pooled bags of 1..20 bounded-Zipf(1.1) row ids each."""
-    dense = np.log1p(rng.lognormal(0.0, 1.0, size=(M, CTR_DENSE)))
-    x = np.empty((M, CTR_DENSE + CTR_TABLES * CTR_DIM), dtype=np.float32)
-    x[:, :CTR_DENSE] = dense
+def make_ctr_raw(tables: CtrTables, M: int, rng: np.random.Generator) -> dict:
+    """Raw CTR features of M rows: LogNormal(0,1) dense values and, per
+    table, bags of 1..20 bounded-Zipf(1.1) row ids.  ``offsets[t][m]`` ..
+    ``offsets[t][m+1]`` delimit bag (t, m) in the flat ``indices`` list."""
+    dense = rng.lognormal(0.0, 1.0, size=(M, CTR_DENSE))
+    offsets = np.zeros((CTR_TABLES, M + 1), dtype=np.int64)
+    ids_all = []
+    base = 0
     for t in range(CTR_TABLES):
         lens = rng.integers(CTR_BAG_MIN, CTR_BAG_MAX + 1, size=M)
         total = int(lens.sum())
         u = rng.random(total)
         ids = np.minimum(np.searchsorted(tables.cdf, u, side="left"), tables.rows - 1)
-        seg = np.repeat(np.arange(M), lens)
+        offsets[t, 0] = base
+        offsets[t, 1:] = base + np.cumsum(lens)
+        ids_all.append(ids.astype(np.int32))
+        base += total
+    return {"dense": dense, "offsets": offsets, "indices": np.concatenate(ids_all)}
+
+
+def make_ctr_x(tables: CtrTables, M: int, rng: np.random.Generator) -> np.ndarray:
+    """CTR input rows: log1p(LogNormal(0,1)) dense features followed by 26
+    sum-pooled bags of 1..20 bounded-Zipf(1.1) row ids each (bags summed in
+    float32 in index order)."""
+    raw = make_ctr_raw(tables, M, rng)
+    x = np.empty((M, CTR_DENSE + CTR_TABLES * CTR_DIM), dtype=np.float32)
+    x[:, :CTR_DENSE] = np.log1p(raw["dense"])
+    for t in range(CTR_TABLES):
+        o = raw["offsets"][t]
+        ids = raw["indices"][o[0]:o[-1]]
+        seg = np.repeat(np.arange(M), np.diff(o))
         pooled = np.zeros((M, CTR_DIM), dtype=np.float32)
         np.add.at(pooled, seg, tables.tables[t][ids])
         x[:, CTR_DENSE + t * CTR_DIM: CTR_DENSE + (t + 1) * CTR_DIM] = pooled

@@ -156,3 +156,30 @@ def test_gemm_flop_count_of_ctr_mlp():
     # gradient of every layer but the first of each block
     f = synth.gemm_flops_per_step(synth.config("ctr_mlp"))
     assert abs(f / 4096 / 1e6 - 26.51) < 0.01
+
+
+def test_embed_bags_validation():
+    """Shape, pointer and alignment checks of erase_embed_bags happen on the
+    host before anything is enqueued (fake pointers are never dereferenced)."""
+    L = erase.lib()
+    good = dict(batch=8, n_dense=13, n_tables=2, dim=64, rows=100, nnz=10, dtype=erase.F32, x_ld=144)
+
+    def call(cfg=None, **ptrs):
+        c = dict(good)
+        c.update(cfg or {})
+        bc = erase.BagConfig(c["batch"], c["n_dense"], c["n_tables"], c["dim"], c["rows"], c["nnz"], c["dtype"],
+                             c["x_ld"])
+        p = dict(dense=256, offsets=512, indices=768, tables=1024, x=2048, status=None)
+        p.update(ptrs)
+        return L.erase_embed_bags(ctypes.byref(bc), p["dense"], p["offsets"], p["indices"], p["tables"], p["x"],
+                                  p["status"], None)
+
+    assert L.erase_embed_bags(None, None, None, None, None, None, None, None) == erase.ERR_INVALID_ARG
+    for bad in ({"batch": 0}, {"n_dense": -1}, {"n_dense": 5000}, {"n_tables": 0}, {"dim": 0}, {"dim": 6},
+                {"dim": 260}, {"rows": 0}, {"rows": 1 << 31}, {"nnz": -1}, {"x_ld": 140}, {"x_ld": 145},
+                {"batch": 1 << 20, "n_tables": 4096}):
+        assert call(bad) == erase.ERR_SHAPE, bad
+    assert call({"dtype": 5}) == erase.ERR_INVALID_ARG
+    for bad in (dict(dense=None), dict(offsets=None), dict(offsets=516), dict(indices=None), dict(indices=770),
+                dict(tables=None), dict(tables=1032), dict(x=None), dict(x=2056), dict(status=258)):
+        assert call(**bad) == erase.ERR_INVALID_ARG, bad

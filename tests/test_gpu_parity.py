@@ -13,6 +13,7 @@ import sys
 import numpy as np
 import pytest
 
+import oracle
 from paper_2608_18469_amd import erase, synth
 from tests.gpu_util import assert_bit_identical, check_bf16, compare, run_gpu, run_gpu_nosync, run_oracle
 
@@ -305,6 +306,126 @@ def test_worker_dispatch_switch_and_state_calls():
     tr2 = erase.Trainer(cfg, params)
     assert erase.lib().erase_set_dispatch(tr2.ctx, 5) == erase.ERR_INVALID_ARG
     tr2.close()
+
+
+def test_caller_owned_streams():
+    """Streams supplied by the caller (here torch streams) instead of the
+    binding's own: same bits as the default construction."""
+    import torch
+    _say("case: caller-owned streams")
+    cfg = _ctr_small(batch=256, blocks=3)
+    params, batches = synth.make_workload(cfg, 21, 3)
+    ref = run_gpu(cfg, params, batches, "overlap", bwd_streams=2)[1]
+    streams = (torch.cuda.Stream(), [torch.cuda.Stream(), torch.cuda.Stream()])
+    tr = erase.Trainer(cfg, params, keep_grads=True, streams=streams)
+    assert tr.sf is streams[0] and tr.sbs == streams[1]
+    got = run_gpu(cfg, params, batches, "overlap", trainer=tr)[1]
+    tr.close()
+    assert_bit_identical(ref, got)
+
+
+def _bags(seed, M, T, rows, dim, n_dense, max_len, allow_empty=True):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    tables = rng.normal(0, 1, size=(T, rows, dim)).astype(np.float32)
+    dense = rng.lognormal(0, 1, size=(M, n_dense)).astype(np.float32)
+    offsets = np.zeros((T, M + 1), dtype=np.int64)
+    ids, base = [], 0
+    for t in range(T):
+        lens = rng.integers(0 if allow_empty else 1, max_len + 1, size=M)
+        offsets[t, 0] = base
+        offsets[t, 1:] = base + np.cumsum(lens)
+        ids.append(rng.integers(0, rows, size=int(lens.sum())).astype(np.int32))
+        base += int(lens.sum())
+    return dense, offsets, np.concatenate(ids), tables
+
+
+def _run_bags(dense, offsets, indices, tables, dtype, x_ld):
+    import torch
+    M = offsets.shape[1] - 1
+    dev = "cuda"
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    x = torch.full((M, x_ld), float("nan"), dtype=tdt, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    d = torch.from_numpy(dense).to(dev) if dense.shape[1] else None
+    erase.embed_bags(d, torch.from_numpy(offsets).to(dev), torch.from_numpy(indices).to(dev),
+                     torch.from_numpy(tables).to(dev), x, status)
+    torch.cuda.synchronize()
+    return x.float().cpu().numpy(), int(status.item())
+
+
+@pytest.mark.parametrize("dtype,dim,n_dense,M,T", [("f32", 64, 13, 37, 5), ("bf16", 64, 13, 37, 5),
+                                                   ("f32", 4, 0, 5, 3), ("bf16", 12, 3, 64, 2),
+                                                   ("f32", 256, 1, 9, 2), ("bf16", 64, 13, 1, 26)])
+def test_embed_bags_vs_oracle(dtype, dim, n_dense, M, T):
+    """The embedding-bag input stage against the float64 oracle: ragged batch,
+    empty bags, widths that leave lanes idle, no dense features."""
+    _say(f"case: embed_bags {dtype} dim={dim} n_dense={n_dense} M={M} T={T}")
+    dense, offsets, indices, tables = _bags(M * 31 + dim, M, T, 300, dim, n_dense, 7)
+    width = n_dense + T * dim
+    x_ld = (width + 5 + 7) // 8 * 8
+    x, status = _run_bags(dense, offsets, indices, tables, dtype, x_ld)
+    ref = oracle.embed_bags(dense.astype(np.float64), offsets, indices, tables.astype(np.float64))
+    assert status == 0
+    assert np.array_equal(x[:, width:], np.zeros((M, x_ld - width)))
+    if dtype == "f32":
+        # fp32 sum of <= 7 N(0,1) rows and fp32 log1p: a few ulp of the sum of magnitudes
+        mag = oracle.embed_bags(dense.astype(np.float64), offsets, indices, np.abs(tables.astype(np.float64)))
+        assert np.all(np.abs(x[:, :width] - ref) <= 4e-7 * (np.abs(mag) + 1e-30) * 8 + 1e-7 * np.abs(ref))
+    else:
+        # one bf16 rounding of an fp32 value: half an ulp (2^-9 relative) plus the fp32 error
+        assert np.all(np.abs(x[:, :width] - ref) <= 2.0 ** -8 * np.abs(ref) + 1e-6)
+
+
+def test_embed_bags_full_ctr_shape():
+    """The CTR workload's input stage at full size (4096 rows, 26 tables of
+    100000 x 64, bags of 1..20 Zipf(1.1) ids): float32 output, pooled
+    columns bit-identical to the input generator's float32 pooling in index
+    order, and the float64 oracle within float32 rounding."""
+    import torch
+    _say("case: embed_bags full CTR shape")
+    rng = np.random.Generator(np.random.PCG64(0))
+    tabs = synth.CtrTables(rng)
+    state = rng.bit_generator.state
+    raw = synth.make_ctr_raw(tabs, 4096, rng)
+    rng.bit_generator.state = state
+    xg = synth.make_ctr_x(tabs, 4096, rng)
+    tables = np.stack(tabs.tables)
+    dense = raw["dense"].astype(np.float32)
+    x, status = _run_bags(dense, raw["offsets"], raw["indices"], tables, "f32", 1680)
+    assert status == 0
+    assert np.array_equal(x[:, 13:1677].view(np.uint32), xg[:, 13:].view(np.uint32))
+    assert np.array_equal(x[:, 1677:], np.zeros((4096, 3)))
+    ref = oracle.embed_bags(dense.astype(np.float64), raw["offsets"], raw["indices"], tables.astype(np.float64))
+    np.testing.assert_allclose(x[:, :1677], ref, rtol=1e-6, atol=2e-8)
+
+
+def test_embed_bags_invalid_entries_flagged():
+    """Out-of-range ids and reversed or out-of-range bag bounds read nothing:
+    they contribute zero and set the status word; every other bag is exact."""
+    _say("case: embed_bags invalid entries")
+    dense, offsets, indices, tables = _bags(41, 16, 3, 50, 64, 2, 5, allow_empty=False)
+    good_x, st = _run_bags(dense, offsets, indices, tables, "f32", 200)
+    assert st == 0
+    bad_idx = indices.copy()
+    o = offsets
+    bad_idx[o[1, 3]] = 50          # table 1, bag 3: first id past the last row
+    bad_idx[o[2, 7]] = -1          # table 2, bag 7: negative id
+    bad_off = offsets.copy()
+    bad_off[0, 5] = bad_off[0, 6] + 1  # table 0: bag 4 runs past its end, bag 5 is reversed
+    x, st = _run_bags(dense, bad_off, bad_idx, tables, "f32", 200)
+    assert st == 1
+    ref = oracle.embed_bags(dense.astype(np.float64), offsets, indices, tables.astype(np.float64))
+    tab64 = tables.astype(np.float64)
+    exp = ref.copy()
+    exp[3, 2 + 64: 2 + 128] -= tab64[1][indices[o[1, 3]]]
+    exp[7, 2 + 128: 2 + 192] -= tab64[2][indices[o[2, 7]]]
+    # bag (0, 4) now reads indices[o[0,4] : o[0,6]+1] (valid range, longer); bag (0, 5) is reversed: zero
+    exp[4, 2:66] = tab64[0][indices[o[0, 4]: o[0, 6] + 1]].sum(axis=0)
+    exp[5, 2:66] = 0.0
+    np.testing.assert_allclose(x[:, :194], exp, rtol=1e-5, atol=1e-5)
+    for m in range(16):
+        if m not in (3, 4, 5, 7):
+            assert np.array_equal(x[m, :194], good_x[m, :194])
 
 
 def test_deep_chain_multi_stream_matches_serial():
