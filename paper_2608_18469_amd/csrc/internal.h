@@ -56,7 +56,6 @@ struct EpiParams {
   // forward: y = relu(acc + bias) or x0 * (acc + bias) + xl
   const float* bias;
   void* y;   int64_t ldy;    // [M][ldy] row-major output
-  void* yt;  int64_t ldyt;   // [N][ldyt] feature-major copy, nullable
   const void* x0; int64_t ldx0;  // block input (cross forward, and cross-below dgrad)
   const void* xl; int64_t ldxl;  // layer input (cross forward residual)
   // weight gradient: part[z][m][n], row sums of A into bpart[z][m]
@@ -67,10 +66,9 @@ struct EpiParams {
   const void* mask; int64_t ldmask;
   void* gout; int64_t ldgout;
   void* dmn;  int64_t lddmn;
-  void* dnm;  int64_t lddnm;
   int below_cross;
   // fused head: s = z hw + hc, loss and ds = lam (sigmoid(s) - y) inv_m,
-  // dz = ds hw [z > 0] into dmn (nullable) / dnm, per-M-tile partials
+  // dz = ds hw [z > 0] into dmn, per-M-tile partials
   const float* hw;
   const float* hc;
   const float* labels;
@@ -87,8 +85,8 @@ hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e
 hipError_t launch_bwd_gemm(int bf16, const GemmDesc& gd, const EpiParams& ed, const GemmDesc& gw, const EpiParams& ew,
                            hipStream_t s, const LaunchEv& ev = {});
 
-// Step prologue: t += 1, the zero-padded copy xp[m][k] = x[m][k] and the
-// feature-major copy xt[k][m] = x[m][k] (padding of both stays zero).
+// Step prologue: t += 1 and the zero-padded copy xp[m][k] = x[m][k] (its
+// padding stays zero).
 // Workspace header (first 256 bytes): step counter t (int64 at 0), status
 // word (int32 at 8), and the Adam step factors written by the prologue, one
 // pair per step parity p: lr / (1 - beta1^t) (float at 16 + 8p) and
@@ -111,8 +109,7 @@ struct HeadArgs {
   const float* y;                // labels [M]
   float lam, inv_m;
   int M, N;
-  void* dmn; int64_t lddmn;      // dz row-major (nullable)
-  void* dnm; int64_t lddnm;      // dz feature-major
+  void* dmn; int64_t lddmn;      // dz row-major
   float* pdw;                    // [nblk][N]
   float* pdc;                    // [nblk]
   float* ploss;                  // [nblk]

@@ -486,30 +486,22 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   }
 
   // epilogue: values -> LDS tile [BM][OPITCH] -> 16-byte row-major stores.
-  // The feature-major copy goes out straight from the accumulators: a lane
-  // holds four consecutive rows of one column (one 8- or 16-byte store).
   OT* sc = reinterpret_cast<OT*>(smem);
   const int M = g.M, N = g.N;
   OT* omn;
   int64_t ldmn;
-  OT* onm = nullptr;
-  int64_t ldnm = 0;
   if constexpr (KIND == GK_WGRAD) {
     omn = e.part + (int64_t)z * e.pstride;
     ldmn = e.ldp;
   } else if constexpr (KIND == GK_DGRAD) {
     omn = static_cast<OT*>(e.dmn);
     ldmn = e.lddmn;
-    onm = static_cast<OT*>(e.dnm);
-    ldnm = e.lddnm;
   } else {
     omn = static_cast<OT*>(e.y);
     ldmn = e.ldy;
-    onm = static_cast<OT*>(e.yt);
-    ldnm = e.ldyt;
   }
   // pass 1 (every load of the epilogue): values into the LDS tile and back
-  // into the accumulators; pass 2 (stores only): the feature-major copy.
+  // into the accumulators; pass 2 (stores only): the row-major tile.
   // Keeping loads and stores apart avoids waits on the stores (on gfx9 the
   // load counter also counts stores).
 #pragma unroll
@@ -531,31 +523,6 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
           acc[i][j][q] = asf(v);
         }
         sc[ml * OPITCH + nl] = v;
-      }
-    }
-  }
-  if constexpr (KIND != GK_WGRAD) {
-    if (onm) {
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int n = n0 + wn * WN + j * 16 + (lane & 15);
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-          const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4;
-          if (n < N && m < M) {
-            OT v4[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) v4[q] = cvt<OT>(acc[i][j][q]);
-            OT* dst = onm + (int64_t)n * ldnm + m;
-            if (m + 4 <= M) {
-              st4(dst, v4);
-            } else {
-#pragma unroll
-              for (int q = 0; q < 4; ++q)
-                if (m + q < M) dst[q] = v4[q];
-            }
-          }
-        }
       }
     }
   }
@@ -614,36 +581,16 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
       }
     }
     __syncthreads();
-    // from the accumulators: dz feature-major (A operand of the last layer's
-    // weight gradient) and this wave's column sums of z ds
+    // this wave's column sums of z ds, from the accumulators
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
       const int nl = wn * WN + j * 16 + (lane & 15);
-      const int n = n0 + nl;
-      const float w = s_w[nl];
       float dwp = 0.f;
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int ml0 = wm * WM + i * 16 + (lane >> 4) * 4;
-        OT d4[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float zq = acc[i][j][q];  // z as stored (zero outside M x N)
-          const float ds = s_ds[ml0 + q];
-          d4[q] = cvt<T>(zq > 0.f ? ds * w : 0.f);
-          dwp = fmaf(zq, ds, dwp);
-        }
-        const int m = m0 + ml0;
-        if (e.dnm && n < N && m < M) {
-          OT* dst = static_cast<OT*>(e.dnm) + (int64_t)n * e.lddnm + m;
-          if (m + 4 <= M) {
-            st4(dst, d4);
-          } else {
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              if (m + q < M) dst[q] = d4[q];
-          }
-        }
+        for (int q = 0; q < 4; ++q) dwp = fmaf(acc[i][j][q], s_ds[ml0 + q], dwp);  // z as stored (0 outside M x N)
       }
       // lanes l, l^16, l^32, l^48 hold the same column (rows 4 apart)
       dwp += __shfl_xor(dwp, 16, 64);
@@ -957,29 +904,6 @@ __global__ __launch_bounds__(256) void erase_head_bce(HeadArgs a) {
         *reinterpret_cast<uint4*>(p) = v;
       } else {
         for (int e = 0; e < KCH && k + e < N; ++e) p[e] = o[e];
-      }
-    }
-  }
-  // dz feature-major: items of KCH consecutive rows of one column (nullable)
-  if (a.dnm) {
-    T* D = static_cast<T*>(a.dnm);
-    const int ipc = R / KCH;  // items per column
-    for (int it = tid; it < N * ipc; it += 256) {
-      const int n = it / ipc, rb = (it - n * ipc) * KCH;
-      const float wn = s_w[n];
-      T o[KCH];
-#pragma unroll
-      for (int e = 0; e < KCH; ++e) {
-        const float zv = asf(tile[(rb + e) * pitch + n]);
-        o[e] = cvt<T>(zv > 0.f ? s_ds[rb + e] * wn : 0.f);
-      }
-      T* p = D + (int64_t)n * a.lddnm + r0 + rb;
-      if (rb + KCH <= rows) {
-        uint4 v;
-        __builtin_memcpy(&v, o, 16);
-        *reinterpret_cast<uint4*>(p) = v;
-      } else {
-        for (int e = 0; e < KCH && rb + e < rows; ++e) p[e] = o[e];
       }
     }
   }
