@@ -46,7 +46,7 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 METRIC = "train samples/s, 6-block CTR @1 MI355X; ERASE vs serial speedup; MFMA util %"
 KIND_SYMBOL = {"prologue": "erase_prologue", "fwd_gemm": "erase_fwd_gemm", "head_bce": "erase_head_bce",
                "wgrad_gemm": "erase_wgrad_gemm", "dgrad_gemm": "erase_dgrad_gemm", "adam": "erase_adam",
-               "bwd_gemm": "erase_bwd_gemm", "fwd_head_gemm": "erase_fwd_head_gemm"}
+               "bwd_gemm": "erase_bwd_gemm", "fwd_head_gemm": "erase_fwd_head_gemm", "fwd_gemm_kg2": "erase_fwd_gemm_kg2"}
 
 
 def kernel_class(r, bf16=True):
@@ -437,11 +437,11 @@ def main():
     nsteps = len(recs_all)
     ovl = float(np.mean([overlap_fraction(r) for r in recs_ovl]))
     dom_name, dom = max(classes.items(), key=lambda kv: kv[1]["ms"])
-    gemm_ms = sum(c["ms"] for c in classes.values() if c["kind"].endswith("gemm"))
-    gemm_flops = sum(c["flops"] for c in classes.values() if c["kind"].endswith("gemm"))
+    gemm_ms = sum(c["ms"] for c in classes.values() if c["kind"].find("gemm") >= 0)
+    gemm_flops = sum(c["flops"] for c in classes.values() if c["kind"].find("gemm") >= 0)
     peak_mfma = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
     avg_dur_s = dom["ms"] / dom["n"] / 1e3
-    if dom["kind"].endswith("gemm"):
+    if dom["kind"].find("gemm") >= 0:
         achieved = dom["flops"] / dom["n"] / avg_dur_s / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": peak_mfma, "unit": "TFLOP/s"}
     else:
@@ -457,7 +457,7 @@ def main():
     roof["launches_per_step"] = dom["n"] / nsteps
     kernels = {k: {"avg_us": v["ms"] / v["n"] * 1e3, "launches_per_step": v["n"] / nsteps,
                    "us_per_step": v["ms"] / nsteps * 1e3,
-                   "tflops": (v["flops"] / (v["ms"] / 1e3) / 1e12) if v["kind"].endswith("gemm") else None,
+                   "tflops": (v["flops"] / (v["ms"] / 1e3) / 1e12) if v["kind"].find("gemm") >= 0 else None,
                    "gbs": v["bytes"] / (v["ms"] / 1e3) / 1e9}
                for k, v in sorted(classes.items(), key=lambda kv: -kv[1]["ms"])}
 

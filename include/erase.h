@@ -223,7 +223,9 @@ typedef struct {
                         layer in one launch, 7 empty interval (no kernel), 8 last
                         forward GEMM of a block with the head+loss in its epilogue
                         (used when the last layer is linear+ReLU and at most 128
-                        wide in bf16, 64 in fp32; kind 2 does not appear then) */
+                        wide in bf16, 64 in fp32; kind 2 does not appear then),
+                        9 forward GEMM with two k-groups per workgroup (bf16
+                        forward launches of at most one workgroup per CU) */
   int32_t block;     /* block index, -1 for the step prologue */
   int32_t layer;     /* layer index within the block, -1 if none */
   int32_t stream;    /* 0 forward stream, 1 + k backward stream k */

@@ -107,7 +107,8 @@ erase_status validate(const erase_config* c, std::string* err) {
 // ---------------------------------------------------------------------------
 struct GemmPlan {
   int bm = 64, bn = 64, split = 1, kps = 0;
-  int group = 0;  // XCD-aware tile order (xcd_group), set once the plan is final
+  int group = 0;    // XCD-aware tile order (xcd_group), set once the plan is final
+  int kgroups = 1;  // k-groups of four waves per workgroup
 };
 
 struct LayerRT {
@@ -195,8 +196,14 @@ GemmPlan choose_gemm(int bf16, int64_t Mg, int64_t Ng, int64_t Kc, bool allow_sp
   const int tiles[3][2] = {{128, 128}, {128, 64}, {64, 128}};
   for (int i = 0; i < 3; ++i)
     if (wgs(tiles[i][0], tiles[i][1]) >= target) return finish(tiles[i][0], tiles[i][1], 1);
-  if (!allow_split && Kc >= 1024 && wgs(64, 128) >= 256) return finish(64, 128, 1);
+  if (!allow_split && Kc >= 1024 && wgs(64, 128) >= 256) {
+    // one workgroup per CU: two k-groups give each SIMD two waves
+    p.kgroups = 2;
+    return finish(64, 128, 1);
+  }
   if (wgs(64, 64) >= target) return finish(64, 64, 1);
+  // at most one 64x64 workgroup per CU: two k-groups give each SIMD two waves
+  if (!allow_split && wgs(64, 64) <= 256) p.kgroups = 2;
   if (allow_split) {
     int s = 1;
     while (s < 16 && wgs(128, 128) * s < target && Kc / (s * 2) >= 2048) s *= 2;
@@ -328,6 +335,7 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
     if (B.head_fused) {
       RL.fwd.bm = P->bf16 ? 32 : 64;
       RL.fwd.bn = P->bf16 ? 128 : 64;
+      RL.fwd.kgroups = 1;
       RL.fwd.group = xcd_group((int)cdiv(M, RL.fwd.bm), 1, 1, RL.fwd.bm, RL.fwd.bn);
       B.nhead = (int)cdiv(M, RL.fwd.bm);
     } else {
@@ -686,6 +694,7 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
     g.bm = R.fwd.bm;
     g.bn = R.fwd.bn;
     g.group = R.fwd.group;
+    g.kgroups = R.fwd.kgroups;
     EpiParams e{};
     e.bias = B.buf.param + R.offb;
     e.y = R.y;
@@ -720,7 +729,8 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
                    4.0 * R.N + 4.0 * M + 4.0 * R.N + 4.0 * B.nhead * (R.N + 2);
     }
     const int bf = P.bf16;
-    RUN(fused ? 8 : 1, b, l, sid, s, cost, [&](const LaunchEv& ev) { return launch_gemm(bf, kind, g, e, s, ev); });
+    RUN(fused ? 8 : g.kgroups == 2 ? 9 : 1, b, l, sid, s, cost,
+        [&](const LaunchEv& ev) { return launch_gemm(bf, kind, g, e, s, ev); });
   }
   if (B.head_fused || !with_head) return ERASE_OK;
   return enqueue_head(c, q, b, labels, s, sid);

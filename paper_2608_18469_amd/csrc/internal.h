@@ -32,6 +32,7 @@ struct GemmDesc {
   int split;
   int bm, bn;  // workgroup tile
   int group;   // M-tiles per group of the XCD-aware tile order (0: launcher picks)
+  int kgroups; // 2: two k-groups of four waves (bf16 64x128 / 64x64 forward tiles); else one
 };
 
 // M-tiles per group of the XCD-aware tile order (see tile_from in the

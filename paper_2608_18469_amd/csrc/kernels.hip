@@ -208,16 +208,23 @@ struct GemmSmem {
   static constexpr int BYTES = HOFF + (KIND == GK_FWD_HEAD ? (3 * BN + 3 * BM + 4) * 4 : 0);
 };
 
-template <typename T, int BM, int BN, int KIND, int R = 2>
+// KG k-groups of four waves (256 * KG threads): every k-group owns the whole
+// output tile and computes it over its own 1/KG of each k-step (KG = 2 gives
+// a one-workgroup-per-CU tile two waves per SIMD); the partial tiles are
+// added through LDS after the main loop.
+template <typename T, int BM, int BN, int KIND, int R = 2, int KG = 1>
 __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e, int bx, int by, int bz,
                                           char* smem) {
   constexpr int BK = GT<T>::BK, KCH = GT<T>::KCH, KMF = GT<T>::KMF;
+  constexpr int NT = 256 * KG;  // threads
   constexpr bool SWZ = sizeof(T) == 2;  // chunk-permuted rows (bf16) or padded rows (fp32)
   constexpr int PITCH = SWZ ? BK : BK + KCH;
   constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 16, TN = WN / 16;
   constexpr int CPR = BK / KCH;
-  constexpr int CA = BM * CPR / 256, CB = BN * CPR / 256;
-  static_assert(CA * 256 == BM * CPR && CB * 256 == BN * CPR, "tile does not match 256 threads");
+  constexpr int CA = BM * CPR / NT, CB = BN * CPR / NT;
+  static_assert(CA * NT == BM * CPR && CB * NT == BN * CPR, "tile does not match the thread count");
+  static_assert(KG == 1 || (KG == 2 && KIND != GK_WGRAD && KIND != GK_FWD_HEAD && (BK / KG) % KMF == 0),
+                "two k-groups: forward and input-gradient tiles only");
   // Operand layouts.  Forward and input gradient ("NT"): A [M][K] and B [N][K]
   // with the contraction contiguous; LDS tiles keep rows of BK elements.
   // Weight gradient (k-major): A [K][M] and B [K][N], i.e. activation
@@ -240,7 +247,8 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   T* lds = reinterpret_cast<T*>(smem);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int kg = KG == 1 ? 0 : __builtin_amdgcn_readfirstlane(wave >> 2);  // k-group
+  const int wm = (wave >> 1) & 1, wn = wave & 1;
   const int m0 = bx * BM, n0 = by * BN;
   const int z = bz;
   const int kbeg = z * g.kps;
@@ -287,7 +295,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   const int klast = kbeg + (nk > 0 ? nk - 1 : 0) * BK;
   // per-thread tile chunks: address of the first, element strides between a
   // thread's chunks (ia, ib) and per contraction index (ka, kb), LDS offsets
-  constexpr int RSTEP = 256 / CPR;  // NT: tile rows between a thread's chunks
+  constexpr int RSTEP = NT / CPR;  // NT: tile rows between a thread's chunks
   static_assert(!SWZ || (CPR == 8 && RSTEP % 8 == 0), "chunk permutation assumes 8 chunks per row");
   // k-major rows r are stored with 16-byte chunk j at j ^ kperm(r): with it
   // the transposing fragment reads (32 lanes per pass over 64 banks) and the
@@ -403,7 +411,8 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     }                                                                                                 \
     const T* sa_ = lds + (ST) * STAGE + wm * WM * PITCH + frow;                                       \
     const T* sb_ = lds + (ST) * STAGE + BM * PITCH + wn * WN * PITCH + frow;                          \
-    _Pragma("unroll") for (int ks = 0; ks < BK; ks += KMF) {                                          \
+    _Pragma("unroll") for (int kk_ = 0; kk_ < BK / KG; kk_ += KMF) {                                  \
+      const int ks = kg * (BK / KG) + kk_; /* this k-group's part of the k-step */                     \
       if constexpr (sizeof(T) == 2) {                                                                 \
         const int ko_ = (fch ^ (ks / KCH)) * KCH;                                                     \
         u32x4_t fa[TM], fb[TN];                                                                         \
@@ -485,6 +494,32 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     }
   }
 
+  if constexpr (KG == 2) {
+    // k-group 1's partial tile into the (now free) stage memory, one 64-float
+    // row per accumulator register and wave; k-group 0 adds it
+    float* red = reinterpret_cast<float*>(smem);
+    static_assert(4 * TM * TN * 4 * 64 * 4 <= GemmSmem<T, BM, BN, KIND>::MAIN, "reduction buffer");
+    const int sw = wave & 3;
+    if (kg == 1) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) red[(((sw * TM + i) * TN + j) * 4 + q) * 64 + lane] = acc[i][j][q];
+    }
+    __syncthreads();
+    if (kg == 0) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) acc[i][j][q] += red[(((sw * TM + i) * TN + j) * 4 + q) * 64 + lane];
+    }
+    __syncthreads();
+  }
+
   // epilogue: values -> LDS tile [BM][OPITCH] -> 16-byte row-major stores.
   OT* sc = reinterpret_cast<OT*>(smem);
   const int M = g.M, N = g.N;
@@ -503,9 +538,11 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   // pass 1 (every load of the epilogue): values into the LDS tile and back
   // into the accumulators; pass 2 (stores only): the row-major tile.
   // Keeping loads and stores apart avoids waits on the stores (on gfx9 the
-  // load counter also counts stores).
+  // load counter also counts stores).  With two k-groups, k-group 0 holds
+  // the sums.
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
+    if (kg != 0) break;
     const int nl = wn * WN + j * 16 + (lane & 15);
     const int n = n0 + nl;
     const float bn = bnv[j];
@@ -529,7 +566,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   __syncthreads();
   if (omn) {
     constexpr int CPRO = BN / OCH;
-    for (int c = tid; c < BM * CPRO; c += 256) {
+    for (int c = tid; c < BM * CPRO; c += NT) {
       const int ml = c / CPRO, nl = (c % CPRO) * OCH;
       const int m = m0 + ml, n = n0 + nl;
       if (m >= M || n >= N) continue;
@@ -656,6 +693,20 @@ ERASE_GEMM_KERNEL(erase_dgrad_gemm, GK_DGRAD)
 ERASE_GEMM_KERNEL(erase_fwd_head_gemm, GK_FWD_HEAD)
 #undef ERASE_GEMM_KERNEL
 
+// Two k-groups of four waves (512 threads): forward tiles of launches with at
+// most one workgroup per CU, which then run two waves per SIMD.
+#define ERASE_GEMM_KERNEL_KG2(NAME, KIND)                                                \
+  template <typename T, int BM, int BN>                                                  \
+  __global__ __launch_bounds__(512) void NAME(GemmDesc g, EpiParams e) {                 \
+    __shared__ __attribute__((aligned(16))) char smem[GemmSmem<T, BM, BN, KIND>::BYTES]; \
+    const int gm = (g.M + BM - 1) / BM, gn = (g.N + BN - 1) / BN;                        \
+    const TileIdx ti = tile_from(xcd_linear(blockIdx.x, gridDim.x), gm, gn, g.group);   \
+    gemm_body<T, BM, BN, KIND, 2, 2>(g, e, ti.m, ti.n, ti.z, smem);                      \
+  }
+ERASE_GEMM_KERNEL_KG2(erase_fwd_gemm_kg2, GK_FWD_RELU)
+ERASE_GEMM_KERNEL_KG2(erase_fwd_cross_gemm_kg2, GK_FWD_CROSS)
+#undef ERASE_GEMM_KERNEL_KG2
+
 // One launch for both backward GEMMs of a layer (they read the same
 // activation gradient and are independent): workgroups [0, nd) compute the
 // input-gradient tiles, the rest the weight-gradient tiles and slices.
@@ -710,6 +761,20 @@ template <typename T, int BM, int BN>
 static hipError_t launch_gemm_t(int kind, const GemmDesc& g0, const EpiParams& e, hipStream_t s, const LaunchEv& ev) {
   const GemmDesc g = with_group(g0, BM, BN);
   dim3 grid(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN) * g.split), block(256);
+  if (g.kgroups == 2) {
+    // two k-groups: bf16 64x128 and 64x64 forward tiles only
+    if constexpr (sizeof(T) == 2 && BM == 64 && (BN == 128 || BN == 64)) {
+      if (kind == GK_FWD_RELU) {
+        ERASE_LAUNCH((erase_fwd_gemm_kg2<T, BM, BN>), grid, dim3(512), 0, s, ev, g, e);
+        return hipGetLastError();
+      }
+      if (kind == GK_FWD_CROSS) {
+        ERASE_LAUNCH((erase_fwd_cross_gemm_kg2<T, BM, BN>), grid, dim3(512), 0, s, ev, g, e);
+        return hipGetLastError();
+      }
+    }
+    return hipErrorInvalidValue;
+  }
   switch (kind) {
     case GK_FWD_RELU: ERASE_LAUNCH((erase_fwd_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;
     case GK_FWD_CROSS: ERASE_LAUNCH((erase_fwd_cross_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;

@@ -553,7 +553,8 @@ def test_kernel_timing_records():
     # in its epilogue: the last layer is 128 wide), 2 grouped backward GEMMs,
     # the first layer's weight gradient, Adam
     assert len(recs) == 1 + 2 * 7, [r["kind"] for r in recs]
-    assert [r["kind"] for r in recs[1:4]] == ["fwd_gemm", "fwd_gemm", "fwd_head_gemm"]
+    # (a forward GEMM of at most one workgroup per CU runs with two k-groups)
+    assert [r["kind"].replace("_kg2", "") for r in recs[1:4]] == ["fwd_gemm", "fwd_gemm", "fwd_head_gemm"]
     assert all(r["end_ms"] >= r["start_ms"] >= 0 for r in recs)
     assert {r["stream"] for r in recs if r["kind"] in ("wgrad_gemm", "bwd_gemm", "adam")} == {1}
     tr2 = erase.Trainer(cfg, params, bwd_streams=2)
@@ -562,7 +563,7 @@ def test_kernel_timing_records():
     tr2.sync()
     r2 = tr2.read_timing()[1:]
     assert {r["stream"] for r in r2 if r["kind"] == "adam"} == {1, 2}
-    assert {r["stream"] for r in recs if r["kind"] in ("fwd_gemm", "fwd_head_gemm", "prologue")} == {0}
+    assert {r["stream"] for r in recs if r["kind"] in ("fwd_gemm", "fwd_gemm_kg2", "fwd_head_gemm", "prologue")} == {0}
     with pytest.raises(erase.EraseError):
         tr.step(xd, yd, "overlap_graph")
     # a standalone head (256-wide chain blocks) runs on the backward stream in
