@@ -301,6 +301,18 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
           R.wgrad = w64;
         }
         R.grouped = (R.dgrad.bm == 64 && R.dgrad.bn == 64) || (R.dgrad.bm == 128 && R.dgrad.bn == 128);
+        if (R.grouped && R.wgrad.split > 1) {
+          // the input-gradient tiles of the same launch fill the chip: the
+          // weight gradient keeps slices of >= 1024 batch rows, so Adam reads
+          // fewer fp32 partial slices (CTR layers 2 and 3: 4 slices instead
+          // of 16; the launch alone is longer, 10.6 vs 8.3 us, but leaves
+          // CUs to the overlapped kernels: 11.96M vs 11.0M samples/s)
+          const int64_t Kc = roundup(M, BK);
+          int sp = R.wgrad.split;
+          while (sp > 1 && Kc / sp < 1024) sp /= 2;
+          R.wgrad.kps = (int)roundup(cdiv(Kc, sp), BK);
+          R.wgrad.split = (int)cdiv(Kc, R.wgrad.kps);
+        }
         R.dgrad.group = xcd_group((int)cdiv(M, R.dgrad.bm), (int)cdiv(R.K, R.dgrad.bn), 1, R.dgrad.bm, R.dgrad.bn);
       }
       R.fwd.group = xcd_group((int)cdiv(M, R.fwd.bm), (int)cdiv(R.N, R.fwd.bn), 1, R.fwd.bm, R.fwd.bn);

@@ -708,22 +708,23 @@ ERASE_GEMM_KERNEL_KG2(erase_fwd_cross_gemm_kg2, GK_FWD_CROSS)
 #undef ERASE_GEMM_KERNEL_KG2
 
 // One launch for both backward GEMMs of a layer (they read the same
-// activation gradient and are independent): workgroups [0, nd) compute the
-// input-gradient tiles, the rest the weight-gradient tiles and slices.
+// activation gradient and are independent): workgroups [0, nw) compute the
+// weight-gradient tiles and slices (the longer contractions, so they start
+// first), the rest the input-gradient tiles.
 template <typename T, int BM, int BN>
-__global__ __launch_bounds__(256) void erase_bwd_gemm(GemmDesc gd, EpiParams ed, GemmDesc gw, EpiParams ew, int nd) {
+__global__ __launch_bounds__(256) void erase_bwd_gemm(GemmDesc gd, EpiParams ed, GemmDesc gw, EpiParams ew, int nw) {
   constexpr int SD = GemmSmem<T, BM, BN, GK_DGRAD>::BYTES, SW = GemmSmem<T, BM, BN, GK_WGRAD>::BYTES;
   __shared__ __attribute__((aligned(16))) char smem[SD > SW ? SD : SW];
   // each GEMM is renumbered on its own (workgroups b and b + 8 still share an
-  // XCD after subtracting nd), so both spread evenly over the XCDs
+  // XCD after subtracting nw), so both spread evenly over the XCDs
   const int b = blockIdx.x;
-  if (b < nd) {
-    const TileIdx ti = tile_from(xcd_linear(b, nd), (gd.M + BM - 1) / BM, (gd.N + BN - 1) / BN, gd.group);
-    gemm_body<T, BM, BN, GK_DGRAD>(gd, ed, ti.m, ti.n, 0, smem);
-  } else {
-    const int nw = gridDim.x - nd;
-    const TileIdx ti = tile_from(xcd_linear(b - nd, nw), (gw.M + BM - 1) / BM, (gw.N + BN - 1) / BN, gw.group);
+  if (b < nw) {
+    const TileIdx ti = tile_from(xcd_linear(b, nw), (gw.M + BM - 1) / BM, (gw.N + BN - 1) / BN, gw.group);
     gemm_body<T, BM, BN, GK_WGRAD>(gw, ew, ti.m, ti.n, ti.z, smem);
+  } else {
+    const int nd = gridDim.x - nw;
+    const TileIdx ti = tile_from(xcd_linear(b - nw, nd), (gd.M + BM - 1) / BM, (gd.N + BN - 1) / BN, gd.group);
+    gemm_body<T, BM, BN, GK_DGRAD>(gd, ed, ti.m, ti.n, 0, smem);
   }
 }
 
@@ -806,7 +807,7 @@ static hipError_t launch_bwd_t(const GemmDesc& gd0, const EpiParams& ed, const G
   const GemmDesc gd = with_group(gd0, BM, BN), gw = with_group(gw0, BM, BN);
   const int nd = ((gd.M + BM - 1) / BM) * ((gd.N + BN - 1) / BN);
   const int nw = ((gw.M + BM - 1) / BM) * ((gw.N + BN - 1) / BN) * gw.split;
-  ERASE_LAUNCH((erase_bwd_gemm<T, BM, BN>), dim3(nd + nw), dim3(256), 0, s, ev, gd, ed, gw, ew, nd);
+  ERASE_LAUNCH((erase_bwd_gemm<T, BM, BN>), dim3(nd + nw), dim3(256), 0, s, ev, gd, ed, gw, ew, nw);
   return hipGetLastError();
 }
 
