@@ -15,6 +15,9 @@
 //    contiguous features; the weight gradient contracts over the batch, i.e.
 //    over rows: its tiles are stored k-major in LDS and the MFMA operands
 //    come from gfx950's transposing LDS reads (ds_read_b64_tr_b16).
+//    erase_bwd_gemm runs a layer's weight- and input-gradient GEMMs in one
+//    launch; the *_kg2 forward kernels split every k-step over two groups of
+//    four waves (launches of at most one workgroup per CU).
 //  * erase_head_bce: local head s = z w + c, sigmoid-BCE loss and its
 //    gradient at z (the block's local objective, Section 2.1), with
 //    deterministic per-workgroup partial sums.
