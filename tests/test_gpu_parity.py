@@ -15,7 +15,8 @@ import pytest
 
 import oracle
 from paper_2608_18469_amd import erase, synth
-from tests.gpu_util import assert_bit_identical, check_bf16, compare, run_gpu, run_gpu_nosync, run_oracle
+from tests.gpu_util import (assert_bit_identical, check_bf16, check_f32, compare, run_gpu, run_gpu_nosync,
+                            run_oracle)
 
 pytestmark = pytest.mark.gpu
 
@@ -426,6 +427,68 @@ def test_embed_bags_invalid_entries_flagged():
     for m in range(16):
         if m not in (3, 4, 5, 7):
             assert np.array_equal(x[m, :194], good_x[m, :194])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_zero_lambda_block_is_frozen(dtype):
+    """lambda_b = 0 (Eq. 2): the block's gradient is exactly zero, so Adam
+    leaves its parameters bit-identical (m = v = 0, update 0/(0 + eps)); the
+    other blocks still match the oracle."""
+    _say(f"case: zero lambda, {dtype}")
+    blocks = [{"input": "x", "layers": [("linear_relu", 40, 24), ("linear_relu", 24, 16)], "lam": 0.0},
+              {"input": "x", "layers": [("linear_relu", 40, 32)], "lam": 1.0},
+              {"input": "prev", "layers": [("linear_relu", 32, 8)], "lam": 0.0}]
+    cfg = synth.custom(dtype, 97, 40, blocks, label_p=0.4)
+    params, batches = synth.make_workload(cfg, 23, 3)
+    _, g = run_gpu(cfg, params, batches, "overlap")
+    init = [erase.pack_block(p) for p in params]
+    for b in (0, 2):
+        assert np.array_equal(g[-1]["params"][b].view(np.uint32), init[b].view(np.uint32)), b
+        assert not np.any(g[-1]["m"][b]) and not np.any(g[-1]["v"][b]) and not np.any(g[-1]["grads"][b])
+    if dtype == "f32":
+        compare(cfg, g, run_oracle(cfg, params, batches), 1e-4)
+    else:
+        _say("  ", check_bf16(cfg, g, params, batches))
+
+
+def test_maximum_block_and_layer_counts_fp32():
+    """64 chained blocks (the most a context takes) and a 16-layer block."""
+    _say("case: 64 chained blocks; a 16-layer block")
+    blocks = [{"input": "x" if b == 0 else "prev", "layers": [("linear_relu", 6 if b == 0 else 5, 5)],
+               "lam": 1.0} for b in range(64)]
+    cfg = synth.custom("f32", 33, 6, blocks, label_p=0.5)
+    params, batches = synth.make_workload(cfg, 29, 2)
+    _, g = run_gpu(cfg, params, batches, "pipeline")
+    _say("  ", check_f32(cfg, g, params, batches))
+    widths = [9] + [7 if i % 2 else 11 for i in range(16)]
+    blocks = [{"input": "x", "layers": [("linear_relu", widths[i], widths[i + 1]) for i in range(16)], "lam": 1.0}]
+    cfg = synth.custom("f32", 45, 9, blocks, label_p=0.5)
+    params, batches = synth.make_workload(cfg, 31, 2)
+    _, g = run_gpu(cfg, params, batches, "overlap")
+    compare(cfg, g, run_oracle(cfg, params, batches), 1e-4)
+
+
+def test_widest_hidden_layer_fp32():
+    """A 65536-wide hidden layer (the widest a layer may be): its GEMMs have
+    65536 output columns and a 65536-long contraction."""
+    _say("case: 16 -> 65536 -> 48 fp32")
+    blocks = [{"input": "x", "layers": [("linear_relu", 16, 65536), ("linear_relu", 65536, 48)], "lam": 1.0}]
+    cfg = synth.custom("f32", 40, 16, blocks, label_p=0.5)
+    params, batches = synth.make_workload(cfg, 37, 2)
+    _, g = run_gpu(cfg, params, batches, "serial")
+    compare(cfg, g, run_oracle(cfg, params, batches), 1e-4)
+
+
+def test_long_ragged_batch_bf16():
+    """70001 rows: ragged M tiles, and weight gradients whose split
+    contraction ends in a ragged k-step."""
+    _say("case: batch 70001 bf16")
+    blocks = [{"input": "x", "layers": [("linear_relu", 24, 40), ("linear_relu", 40, 16)], "lam": 1.0},
+              {"input": "prev", "layers": [("linear_relu", 16, 24)], "lam": 0.5}]
+    cfg = synth.custom("bf16", 70001, 24, blocks, label_p=0.1)
+    params, batches = synth.make_workload(cfg, 41, 2)
+    _, g = run_gpu(cfg, params, batches, "pipeline")
+    _say("  ", check_bf16(cfg, g, params, batches))
 
 
 def test_deep_chain_multi_stream_matches_serial():
