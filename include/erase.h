@@ -225,7 +225,10 @@ typedef struct {
                         (used when the last layer is linear+ReLU and at most 128
                         wide in bf16, 64 in fp32; kind 2 does not appear then),
                         9 forward GEMM with two k-groups per workgroup (bf16
-                        forward launches of at most one workgroup per CU) */
+                        forward launches of at most one workgroup per CU),
+                        10 weight-grad GEMM of a block's first layer with two
+                        k-groups and that layer's Adam update in its epilogue
+                        (kind 5 then updates the block's other parameters) */
   int32_t block;     /* block index, -1 for the step prologue */
   int32_t layer;     /* layer index within the block, -1 if none */
   int32_t stream;    /* 0 forward stream, 1 + k backward stream k */

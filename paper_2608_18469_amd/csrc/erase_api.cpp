@@ -124,6 +124,9 @@ struct LayerRT {
   float* bpart = nullptr;
   GemmPlan fwd, wgrad, dgrad;
   bool grouped = false;  // input- and weight-gradient GEMMs share one launch
+  // Adam of the weight matrix fused into its (standalone, unsplit, two
+  // k-group) weight-gradient launch
+  bool fused_adam = false;
 };
 
 struct BlockRT {
@@ -138,7 +141,10 @@ struct BlockRT {
   float* pdw = nullptr;
   float* pdc = nullptr;
   float* ploss = nullptr;
-  AdamSeg* segs_dev = nullptr;
+  AdamSeg* segs_dev = nullptr;   // segments the Adam kernel updates
+  AdamSeg* rsegs_dev = nullptr;  // every segment (GEMM-copy refresh)
+  std::vector<AdamSeg> rsegs;
+  int64_t rnchunks = 0;
   std::vector<AdamSeg> segs;
   int64_t nchunks = 0;
   erase_block_buffers buf{};
@@ -320,6 +326,20 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
                                 R.wgrad.bn);
       R.ldp = ldK;
       R.pstride = int64_t(R.N) * ldK;
+      // A block's first layer has a weight-gradient launch of its own: its
+      // workgroups hold whole 64x64 tiles of the gradient (two k-groups of
+      // four waves over the whole batch, no split), so the layer's Adam runs
+      // in that launch's epilogue and no partial slice goes to memory.  Not
+      // when the transposed GEMM copy is needed (the undetached schedule's
+      // input gradient), which only the Adam kernel writes.
+      if (l == 0 && !dgrad) {
+        R.fused_adam = true;
+        R.wgrad.bm = R.wgrad.bn = 64;
+        R.wgrad.split = 1;
+        R.wgrad.kps = (int)roundup(M, BK);
+        R.wgrad.kgroups = 2;
+        R.wgrad.group = xcd_group((int)cdiv(R.N, 64), (int)cdiv(R.K, 64), 1, 64, 64);
+      }
       R.part = static_cast<float*>(cv.take(size_t(R.wgrad.split) * R.pstride * 4));
       R.bpart = static_cast<float*>(cv.take(size_t(R.wgrad.split) * R.N * 4));
     }
@@ -358,6 +378,7 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
     B.ploss = static_cast<float*>(cv.take(size_t(B.nhead) * 4));
     const int nseg = 2 * B.L + 2;
     B.segs_dev = static_cast<AdamSeg*>(cv.take(sizeof(AdamSeg) * nseg));
+    B.rsegs_dev = static_cast<AdamSeg*>(cv.take(sizeof(AdamSeg) * nseg));
   }
   P->bytes = cv.off;
   return cv.off;
@@ -369,7 +390,9 @@ void build_segments(Plan* P, const erase_block_buffers* bufs) {
     BlockRT& B = P->blk[b];
     B.buf = bufs[b];
     B.segs.clear();
-    int64_t chunk = 0;
+    B.rsegs.clear();
+    int64_t chunk = 0, rchunk = 0;
+    bool fused = false;  // the segment being added is updated by its weight-gradient launch
     auto add = [&](int64_t off, int rows, int cols, const float* part, int64_t pstride, int ldpart, int nsplit,
                     void* sh, int64_t ldsh, void* sht, int64_t ldsht) {
       AdamSeg s{};
@@ -387,20 +410,27 @@ void build_segments(Plan* P, const erase_block_buffers* bufs) {
       s.ldsh = ldsh;
       s.sht = sht;
       s.ldsht = ldsht;
-      s.chunk0 = chunk;
       s.tcols = (int)cdiv(cols, ADAM_TC);
+      s.chunk0 = rchunk;
+      rchunk += cdiv(rows, ADAM_TR) * s.tcols;
+      B.rsegs.push_back(s);
+      if (fused) return;
+      s.chunk0 = chunk;
       chunk += cdiv(rows, ADAM_TR) * s.tcols;
       B.segs.push_back(s);
     };
     for (int l = 0; l < B.L; ++l) {
       LayerRT& R = B.layer[l];
+      fused = R.fused_adam;
       add(R.offW, R.N, R.K, R.part, R.pstride, (int)R.ldp, R.wgrad.split, R.wsh, R.ldwsh, R.wsht, R.ldwsht);
+      fused = false;
       add(R.offb, 1, R.N, R.bpart, R.N, R.N, R.wgrad.split, nullptr, 0, nullptr, 0);
     }
     const int NL = B.layer[B.L - 1].N;
     add(B.off_w, 1, NL, B.pdw, NL, NL, B.nhead, nullptr, 0, nullptr, 0);
     add(B.off_c, 1, 1, B.pdc, 1, 1, B.nhead, nullptr, 0, nullptr, 0);
     B.nchunks = chunk;
+    B.rnchunks = rchunk;
   }
 }
 
@@ -819,8 +849,26 @@ erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStre
     Cost cw = gemm_cost(gw);
     cw.flops = 2.0 * M * R.N * R.K;
     cw.bytes = double(esz) * M * (double(R.N) + R.K) + 4.0 * R.wgrad.split * (double(R.N) * R.K + R.N);
+    gw.kgroups = R.wgrad.kgroups;
+    if (R.fused_adam) {
+      ew.ap = B.buf.param + R.offW;
+      ew.am = B.buf.m + R.offW;
+      ew.av = B.buf.v + R.offW;
+      ew.ag = B.buf.grad ? B.buf.grad + R.offW : nullptr;
+      ew.ash = R.wsh;
+      ew.ldash = R.ldwsh;
+      ew.hyper = reinterpret_cast<const float*>(P.t + 2) + 2 * par;
+      ew.b1 = c->cfg.beta1;
+      ew.b2 = c->cfg.beta2;
+      ew.eps = c->cfg.eps;
+      // no partial slice is stored; Adam's per-parameter traffic moves here
+      const double n = double(R.N) * R.K;
+      cw.flops += 12.0 * n;
+      cw.bytes += n * (24.0 + (ew.ag ? 4.0 : 0.0) + esz) - 4.0 * n;
+    }
     if (l == 0) {
-      RUN(3, b, l, sid, s, cw, [&](const LaunchEv& ev) { return launch_gemm(bf, GK_WGRAD, gw, ew, s, ev); });
+      RUN(gw.kgroups == 2 ? 10 : 3, b, l, sid, s, cw,
+          [&](const LaunchEv& ev) { return launch_gemm(bf, GK_WGRAD, gw, ew, s, ev); });
       if (send && B.send) {
         // undetached: the gradient at the block input, dX = dH_0 W_0, is
         // added to the previous block's output gradient (its head's term,
@@ -1090,10 +1138,10 @@ erase_status join_pending(Ctx* c) {
 erase_status refresh(Ctx* c) {
   for (const BlockRT& B : c->P.blk) {
     AdamArgs a{};
-    a.seg = B.segs_dev;
-    a.nseg = (int)B.segs.size();
-    for (int i = 0; i < a.nseg; ++i) a.chunk0[i] = B.segs[i].chunk0;
-    a.nchunks = B.nchunks;
+    a.seg = B.rsegs_dev;
+    a.nseg = (int)B.rsegs.size();
+    for (int i = 0; i < a.nseg; ++i) a.chunk0[i] = B.rsegs[i].chunk0;
+    a.nchunks = B.rnchunks;
     HIPCHK(c, launch_refresh(c->P.bf16, a, c->sf));
   }
   return ERASE_OK;
@@ -1206,7 +1254,9 @@ erase_status erase_init_streams(const erase_config* cfg, const erase_block_buffe
   if (hipMemsetAsync(c->ws, 0, c->P.bytes, c->sf) != hipSuccess) return bail(ERASE_ERR_HIP);
   for (BlockRT& B : c->P.blk) {
     if (hipMemcpyAsync(B.segs_dev, B.segs.data(), sizeof(AdamSeg) * B.segs.size(), hipMemcpyHostToDevice, c->sf) !=
-        hipSuccess)
+            hipSuccess ||
+        hipMemcpyAsync(B.rsegs_dev, B.rsegs.data(), sizeof(AdamSeg) * B.rsegs.size(), hipMemcpyHostToDevice,
+                       c->sf) != hipSuccess)
       return bail(ERASE_ERR_HIP);
   }
   if (refresh(c) != ERASE_OK) return bail(ERASE_ERR_HIP);

@@ -77,6 +77,15 @@ struct EpiParams {
   float* pdw;    // [M-tiles][N]
   float* pdc;    // [M-tiles]
   float* ploss;  // [M-tiles]
+  // weight gradient with the Adam update fused (ap non-null; unsplit
+  // contraction): the workgroup updates its tile of the parameter matrix
+  // [M][N] (flat, row-major), its Adam state, the gradient (ag nullable) and
+  // the GEMM copy [M][ldash] from the finished gradient tile; no partial
+  // slice is stored
+  float* ap; float* am; float* av; float* ag;
+  void* ash; int64_t ldash;
+  const float* hyper;  // lr / (1 - beta1^t), sqrt(1 - beta2^t) of this step
+  float b1, b2, eps;
 };
 
 hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s,

@@ -195,6 +195,15 @@ __device__ __forceinline__ TileIdx tile_from(int t, int gm, int gn, int group) {
   return {mf + u % gh, u / gh, z};
 }
 
+// One Adam update (PyTorch semantics: bias-corrected moments, eps outside
+// the square root): step = lr / (1 - beta1^t), bc2s = sqrt(1 - beta2^t).
+__device__ __forceinline__ void adam_elem(float& p, float& m, float& v, float g, float b1, float b2, float step,
+                                          float bc2s, float eps) {
+  m = fmaf(b1, m, (1.f - b1) * g);
+  v = fmaf(b2, v, (1.f - b2) * g * g);
+  p = p - step * m / (sqrtf(v) / bc2s + eps);
+}
+
 template <typename T, int BM, int BN, int KIND>
 struct GemmSmem {
   static constexpr int BK = GT<T>::BK, KCH = GT<T>::KCH, PITCH = sizeof(T) == 2 ? BK : BK + KCH;
@@ -226,8 +235,8 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   constexpr int CPR = BK / KCH;
   constexpr int CA = BM * CPR / NT, CB = BN * CPR / NT;
   static_assert(CA * NT == BM * CPR && CB * NT == BN * CPR, "tile does not match the thread count");
-  static_assert(KG == 1 || (KG == 2 && KIND != GK_WGRAD && KIND != GK_FWD_HEAD && (BK / KG) % KMF == 0),
-                "two k-groups: forward and input-gradient tiles only");
+  static_assert(KG == 1 || (KG == 2 && KIND != GK_FWD_HEAD && (BK / KG) % KMF == 0),
+                "two k-groups: not with the fused head");
   // Operand layouts.  Forward and input gradient ("NT"): A [M][K] and B [N][K]
   // with the contraction contiguous; LDS tiles keep rows of BK elements.
   // Weight gradient (k-major): A [K][M] and B [K][N], i.e. activation
@@ -238,7 +247,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   constexpr int PAD = GemmSmem<T, BM, BN, KIND>::PAD;
   constexpr int PA = BM + PAD, PB = BN + PAD;  // k-major row pitches
   constexpr int CPA = BM / KCH, CPB = BN / KCH;  // 16-byte chunks per k-major row
-  constexpr int RPA = 256 / CPA, RPB = 256 / CPB;  // k-major rows per pass of 256 threads
+  constexpr int RPA = NT / CPA, RPB = NT / CPB;  // k-major rows per pass of the workgroup's threads
   static_assert(!KMAJ || (BK % RPA == 0 && BK % RPB == 0), "k-major tile does not match 256 threads");
   static_assert(!KMAJ || !SWZ || ((CPA == 8 || CPA == 16) && (CPB == 8 || CPB == 16)),
                 "k-major chunk permutation: 8 or 16 chunks per row");
@@ -386,7 +395,8 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   do {                                                                                                \
     if constexpr (KMAJ) {                                                                             \
       const T* st_ = lds + (ST) * STAGE;                                                              \
-      _Pragma("unroll") for (int ks = 0; ks < BK; ks += KMF) {                                        \
+      _Pragma("unroll") for (int kk_ = 0; kk_ < BK / KG; kk_ += KMF) {                                \
+        const int ks = kg * (BK / KG) + kk_; /* this k-group's part of the k-step */                   \
         if constexpr (sizeof(T) == 2) {                                                               \
           u32x4_t fa[TM], fb[TN];                                                                       \
           _Pragma("unroll") for (int i = 0; i < TM; ++i) fa[i] = tr_frag(st_ + foa[i] + ks * PA, PA);  \
@@ -486,23 +496,14 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
 #undef ERASE_SSTORE
 #undef ERASE_COMPUTE
 
-  if (do_rows) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      float sr = rs[i];
-      sr += __shfl_xor(sr, 16, 64);
-      sr += __shfl_xor(sr, 32, 64);
-      const int m = m0 + wm * WM + i * 16 + lane;
-      if (lane < 16 && m < g.M) e.bpart[(int64_t)z * g.M + m] = sr;
-    }
-  }
-
   if constexpr (KG == 2) {
-    // k-group 1's partial tile into the (now free) stage memory, one 64-float
-    // row per accumulator register and wave; k-group 0 adds it
+    // k-group 1's partial tile (and bias row sums) into the (now free) stage
+    // memory, one 64-float row per accumulator register and wave; k-group 0
+    // adds them
     float* red = reinterpret_cast<float*>(smem);
-    static_assert(4 * TM * TN * 4 * 64 * 4 <= GemmSmem<T, BM, BN, KIND>::MAIN, "reduction buffer");
+    static_assert(4 * (TM * TN * 4 + TM) * 64 * 4 <= GemmSmem<T, BM, BN, KIND>::MAIN, "reduction buffer");
     const int sw = wave & 3;
+    float* rrs = red + 4 * TM * TN * 4 * 64;
     if (kg == 1) {
 #pragma unroll
       for (int i = 0; i < TM; ++i)
@@ -510,6 +511,10 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
         for (int j = 0; j < TN; ++j)
 #pragma unroll
           for (int q = 0; q < 4; ++q) red[(((sw * TM + i) * TN + j) * 4 + q) * 64 + lane] = acc[i][j][q];
+      if (do_rows) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) rrs[(sw * TM + i) * 64 + lane] = rs[i];
+      }
     }
     __syncthreads();
     if (kg == 0) {
@@ -519,8 +524,23 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
         for (int j = 0; j < TN; ++j)
 #pragma unroll
           for (int q = 0; q < 4; ++q) acc[i][j][q] += red[(((sw * TM + i) * TN + j) * 4 + q) * 64 + lane];
+      if (do_rows) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) rs[i] += rrs[(sw * TM + i) * 64 + lane];
+      }
     }
     __syncthreads();
+  }
+
+  if (do_rows && kg == 0) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      float sr = rs[i];
+      sr += __shfl_xor(sr, 16, 64);
+      sr += __shfl_xor(sr, 32, 64);
+      const int m = m0 + wm * WM + i * 16 + lane;
+      if (lane < 16 && m < g.M) e.bpart[(int64_t)z * g.M + m] = sr;
+    }
   }
 
   // epilogue: values -> LDS tile [BM][OPITCH] -> 16-byte row-major stores.
@@ -567,7 +587,9 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     }
   }
   __syncthreads();
-  if (omn) {
+  bool store_tile = omn != nullptr;
+  if constexpr (KIND == GK_WGRAD) store_tile = store_tile && e.ap == nullptr;  // fused Adam reads the LDS tile
+  if (store_tile) {
     constexpr int CPRO = BN / OCH;
     for (int c = tid; c < BM * CPRO; c += NT) {
       const int ml = c / CPRO, nl = (c % CPRO) * OCH;
@@ -579,6 +601,73 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
         *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(src);
       } else {
         for (int q = 0; q < OCH && n + q < N; ++q) dst[q] = src[q];
+      }
+    }
+  }
+
+  if constexpr (KIND == GK_WGRAD) {
+    if (e.ap) {
+      // Fused Adam: the LDS tile holds this tile's finished gradient (the
+      // contraction is not split).  Items of 4 consecutive columns of one
+      // row; every item's loads are issued before any store (16-byte
+      // accesses at 4-byte alignment: parameter rows start anywhere), a
+      // row's ragged end goes element by element.
+      typedef float f32x4a_t __attribute__((ext_vector_type(4), aligned(4)));
+      typedef __attribute__((address_space(1))) f32x4a_t gvec;
+      const float step = e.hyper[0], bc2s = e.hyper[1];
+      constexpr int Q = BN / 4;
+      constexpr int IT = (BM * Q + NT - 1) / NT;
+      f32x4_t gv[IT];
+      f32x4a_t pv[IT], mv[IT], vv[IT];
+      bool full[IT];
+      int64_t fi[IT];
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        const int c = tid + it * NT;
+        const int ml = c / Q, nl = (c % Q) * 4;
+        const int m = m0 + ml, n = n0 + nl;
+        full[it] = c < BM * Q && m < M && n + 4 <= N;
+        fi[it] = (int64_t)m * N + n;
+        if (full[it]) {
+          gv[it] = *reinterpret_cast<const f32x4_t*>(&sc[ml * OPITCH + nl]);
+          pv[it] = *reinterpret_cast<const gvec*>(gmem(e.ap) + fi[it]);
+          mv[it] = *reinterpret_cast<const gvec*>(gmem(e.am) + fi[it]);
+          vv[it] = *reinterpret_cast<const gvec*>(gmem(e.av) + fi[it]);
+        }
+      }
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        const int c = tid + it * NT;
+        const int ml = c / Q, nl = (c % Q) * 4;
+        const int m = m0 + ml, n = n0 + nl;
+        if (full[it]) {
+          float pp[4], mm[4], vq[4];
+          T o[4];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            pp[k] = pv[it][k];
+            mm[k] = mv[it][k];
+            vq[k] = vv[it][k];
+            adam_elem(pp[k], mm[k], vq[k], gv[it][k], e.b1, e.b2, step, bc2s, e.eps);
+            o[k] = cvt<T>(pp[k]);
+          }
+          if (e.ag) *reinterpret_cast<gvec*>(gmem(e.ag) + fi[it]) = f32x4a_t{gv[it][0], gv[it][1], gv[it][2], gv[it][3]};
+          *reinterpret_cast<gvec*>(gmem(e.am) + fi[it]) = f32x4a_t{mm[0], mm[1], mm[2], mm[3]};
+          *reinterpret_cast<gvec*>(gmem(e.av) + fi[it]) = f32x4a_t{vq[0], vq[1], vq[2], vq[3]};
+          *reinterpret_cast<gvec*>(gmem(e.ap) + fi[it]) = f32x4a_t{pp[0], pp[1], pp[2], pp[3]};
+          st4(static_cast<T*>(e.ash) + (int64_t)m * e.ldash + n, o);  // copy rows: 64-element multiples
+        } else if (c < BM * Q && m < M && n < N) {
+          for (int k = 0; k < N - n && k < 4; ++k) {
+            const float gk = sc[ml * OPITCH + nl + k];
+            float pp = e.ap[fi[it] + k], mm = e.am[fi[it] + k], vq = e.av[fi[it] + k];
+            adam_elem(pp, mm, vq, gk, e.b1, e.b2, step, bc2s, e.eps);
+            if (e.ag) e.ag[fi[it] + k] = gk;
+            e.am[fi[it] + k] = mm;
+            e.av[fi[it] + k] = vq;
+            e.ap[fi[it] + k] = pp;
+            static_cast<T*>(e.ash)[(int64_t)m * e.ldash + n + k] = cvt<T>(pp);
+          }
+        }
       }
     }
   }
@@ -708,6 +797,7 @@ ERASE_GEMM_KERNEL(erase_fwd_head_gemm, GK_FWD_HEAD)
   }
 ERASE_GEMM_KERNEL_KG2(erase_fwd_gemm_kg2, GK_FWD_RELU)
 ERASE_GEMM_KERNEL_KG2(erase_fwd_cross_gemm_kg2, GK_FWD_CROSS)
+ERASE_GEMM_KERNEL_KG2(erase_wgrad_gemm_kg2, GK_WGRAD)
 #undef ERASE_GEMM_KERNEL_KG2
 
 // One launch for both backward GEMMs of a layer (they read the same
@@ -766,7 +856,14 @@ static hipError_t launch_gemm_t(int kind, const GemmDesc& g0, const EpiParams& e
   const GemmDesc g = with_group(g0, BM, BN);
   dim3 grid(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN) * g.split), block(256);
   if (g.kgroups == 2) {
-    // two k-groups: bf16 64x128 and 64x64 forward tiles only
+    // two k-groups: the unsplit 64x64 weight gradient (fp32 or bf16)
+    if constexpr (BM == 64 && BN == 64) {
+      if (kind == GK_WGRAD && g.split == 1) {
+        ERASE_LAUNCH((erase_wgrad_gemm_kg2<T, BM, BN>), grid, dim3(512), 0, s, ev, g, e);
+        return hipGetLastError();
+      }
+    }
+    // and bf16 64x128 and 64x64 forward tiles
     if constexpr (sizeof(T) == 2 && BM == 64 && (BN == 128 || BN == 64)) {
       if (kind == GK_FWD_RELU) {
         ERASE_LAUNCH((erase_fwd_gemm_kg2<T, BM, BN>), grid, dim3(512), 0, s, ev, g, e);
@@ -1022,12 +1119,6 @@ __device__ __forceinline__ int find_seg(const AdamArgs& a, int64_t chunk) {
 // start anywhere; gfx950 serves unaligned vector accesses)
 typedef float f32x4u_t __attribute__((ext_vector_type(4), aligned(4)));
 
-__device__ __forceinline__ void adam_elem(float& p, float& m, float& v, float g, float b1, float b2, float step,
-                                          float bc2s, float eps) {
-  m = fmaf(b1, m, (1.f - b1) * g);
-  v = fmaf(b2, v, (1.f - b2) * g * g);
-  p = p - step * m / (sqrtf(v) / bc2s + eps);
-}
 
 template <typename T>
 __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {

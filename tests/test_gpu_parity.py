@@ -619,7 +619,7 @@ def test_kernel_timing_records():
     # (a forward GEMM of at most one workgroup per CU runs with two k-groups)
     assert [r["kind"].replace("_kg2", "") for r in recs[1:4]] == ["fwd_gemm", "fwd_gemm", "fwd_head_gemm"]
     assert all(r["end_ms"] >= r["start_ms"] >= 0 for r in recs)
-    assert {r["stream"] for r in recs if r["kind"] in ("wgrad_gemm", "bwd_gemm", "adam")} == {1}
+    assert {r["stream"] for r in recs if r["kind"] in ("wgrad_gemm", "wgrad_gemm_kg2", "bwd_gemm", "adam")} == {1}
     tr2 = erase.Trainer(cfg, params, bwd_streams=2)
     tr2.set_timing(True)
     tr2.step(*tr2.device_batch(*batches[0]), "overlap")
