@@ -19,7 +19,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "liberase.so")
-SOURCES = [os.path.join(HERE, "csrc", f) for f in ("kernels.hip", "embed.hip", "erase_api.cpp")]
+SOURCES = [os.path.join(HERE, "csrc", f) for f in ("kernels.hip", "embed.hip", "transformer.hip", "erase_api.cpp", "tf_api.cpp")]
 ARCH = "gfx950"
 
 

@@ -43,7 +43,19 @@ int xcd_group(int gm, int gn, int split, int bm, int bn);
 // GK_FWD_HEAD: the last linear+ReLU layer of a block with the local head
 // (Section 2.1) fused into its epilogue; the tile spans the whole width
 // (N <= BN), so each workgroup holds complete rows of the block output.
-enum GemmKind { GK_FWD_RELU = 0, GK_FWD_CROSS = 1, GK_WGRAD = 2, GK_DGRAD = 3, GK_FWD_HEAD = 4 };
+//
+// Transformer kinds (bf16 only):
+//   GK_FWD_LIN     y = acc (+ res)                       (projections, residual adds)
+//   GK_FWD_GELU    y = gelu(acc), and acc itself into gout (the MLP up-projection)
+//   GK_DGRAD_GELU  g = acc * gelu'(u), u read from mask  (input gradient below the GELU)
+//   GK_FWD_LOGITS  y = acc, plus per row the maximum and the sum of exp(y - max)
+//                  over this tile's columns into lstat, and y at the row's target
+//                  column into tlogit                     (vocabulary head)
+// GK_DGRAD with neither mask nor below_cross stores g = acc (+ res) as is.
+enum GemmKind {
+  GK_FWD_RELU = 0, GK_FWD_CROSS = 1, GK_WGRAD = 2, GK_DGRAD = 3, GK_FWD_HEAD = 4,
+  GK_FWD_LIN = 5, GK_FWD_GELU = 6, GK_DGRAD_GELU = 7, GK_FWD_LOGITS = 8
+};
 
 // Optional timing events of one launch: when set, the kernel is dispatched
 // with hipExtLaunchKernelGGL, which stamps e0/e1 at the kernel's own start
@@ -86,6 +98,12 @@ struct EpiParams {
   void* ash; int64_t ldash;
   const float* hyper;  // lr / (1 - beta1^t), sqrt(1 - beta2^t) of this step
   float b1, b2, eps;
+  // logits (GK_FWD_LOGITS): lstat[m][2 t], lstat[m][2 t + 1] = max and sum
+  // of exp(y - max) of row m over the columns of N-tile t (values as stored);
+  // tlogit[m] = y[m][target[m]] (written by the tile holding that column)
+  float* lstat; int64_t ldlstat;
+  const int32_t* target;
+  float* tlogit;
 };
 
 hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s,
@@ -188,5 +206,86 @@ struct EmbedArgs {
   int M, n_dense, T, dim;  // dim % 4 == 0, 4 <= dim <= 256
 };
 hipError_t launch_embed_bags(int bf16, const EmbedArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// small-transformer kernels (transformer.hip), bf16 activations
+// ---------------------------------------------------------------------------
+// a0[n] = emb[tokens[b][t]] (n = b T + t), input[n] = that token,
+// target[n] = tokens[b][t + 1]; an id outside [0, V) reads nothing (zero row,
+// id -1) and sets status[0] = 2.
+struct TfEmbedArgs {
+  const int32_t* tokens;  // [B][T + 1]
+  int B, T, V, d;
+  const uint16_t* emb; int64_t ldemb;  // bf16 copy [V][ldemb]
+  uint16_t* a0; int64_t lda0;
+  int32_t* target;
+  int32_t* input;
+  int* status;
+};
+hipError_t launch_tf_embed(const TfEmbedArgs& a, hipStream_t s, const LaunchEv& ev = {});
+
+// Forward: y = x r, r = 1 / sqrt(mean(x^2) + eps) per row (r written).
+// Backward: dx = r (dy - y mean(dy y)) + res (res nullable), y = x r, into
+// out_f32 (fp32) when set, else y (bf16).  N rows of width d (d % 8 == 0,
+// d <= 4096).
+struct TfRmsArgs {
+  const uint16_t* x; int64_t ldx;
+  uint16_t* y; int64_t ldy;
+  float* r;
+  const uint16_t* dy; int64_t lddy;
+  const uint16_t* res; int64_t ldres;
+  float* out_f32; int64_t ldout;
+  int64_t N;
+  int d;
+  float eps;
+};
+hipError_t launch_tf_rms(int backward, const TfRmsArgs& a, hipStream_t s, const LaunchEv& ev = {});
+
+// Causal attention over qkv [B T][3 d] (q | k | v, head h at columns
+// 64 h .. 64 h + 63 of each), head size 64.  part 0: o and lse
+// [B][H][T] (natural log); 1: dsum = rowsum(dout * o); 2: dK and dV; 3: dQ,
+// into dqkv (same layout as qkv).
+struct TfAttnArgs {
+  const uint16_t* qkv; int64_t ldqkv;
+  uint16_t* o; int64_t ldo;
+  float* lse;
+  const uint16_t* dout; int64_t lddo;
+  float* dsum;
+  uint16_t* dqkv; int64_t lddqkv;
+  int B, T, H, d;
+  float scale;  // 1 / sqrt(64)
+};
+hipError_t launch_tf_attn(int part, const TfAttnArgs& a, hipStream_t s, const LaunchEv& ev = {});
+
+// Softmax cross-entropy of N rows of V logits (bf16, in place): lse from the
+// per-tile statistics of the logits GEMM, loss_n = lse - tlogit[n], and
+// logits[n][v] <- scale (exp(logit - lse) - [v == target[n]]); ploss[w] = sum
+// of the losses of rows 4 w .. 4 w + 3.
+struct TfXentArgs {
+  uint16_t* logits; int64_t ldlog;
+  const float* lstat; int64_t ldlstat;
+  int ntiles;
+  const float* tlogit;
+  const int32_t* target;
+  int64_t N;
+  int V;
+  float scale;
+  float* ploss;
+};
+hipError_t launch_tf_xent(const TfXentArgs& a, hipStream_t s, const LaunchEv& ev = {});
+
+// Embedding gradient: grad[v] = sum over positions n with input[n] == v, in
+// increasing n, of dx[n] (fp32); zero rows for absent tokens.  count and
+// fill [V] must be zero on entry (count is zero again on exit); start [V],
+// bucket [N] scratch.  Four launches.
+struct TfEmbGradArgs {
+  const int32_t* input;
+  int64_t N;
+  int V, d;
+  int32_t* count; int32_t* start; int32_t* fill; int32_t* bucket;
+  const float* dx; int64_t lddx;
+  float* grad; int64_t ldgrad;
+};
+hipError_t launch_tf_emb_grad(const TfEmbGradArgs& a, hipStream_t s);
 
 }  // namespace erase

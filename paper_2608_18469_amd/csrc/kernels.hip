@@ -129,6 +129,19 @@ __device__ __forceinline__ u32x4_t tr_frag(const T* p, int pitch) {
   return u32x4_t{a.x, a.y, b.x, b.y};
 }
 
+// GELU in its tanh form, 0.5 u (1 + tanh(c (u + a u^3))) with c = sqrt(2/pi),
+// a = 0.044715, and its derivative
+// 0.5 (1 + t) + 0.5 u (1 - t^2) c (1 + 3 a u^2), t = tanh(c (u + a u^3)).
+constexpr float kGeluC = 0.7978845608028654f, kGeluA = 0.044715f;
+__device__ __forceinline__ float gelu_f(float u) {
+  const float t = tanhf(kGeluC * fmaf(kGeluA * u * u, u, u));
+  return 0.5f * u * (1.f + t);
+}
+__device__ __forceinline__ float gelu_grad_f(float u) {
+  const float t = tanhf(kGeluC * fmaf(kGeluA * u * u, u, u));
+  return 0.5f * (1.f + t) + 0.5f * u * (1.f - t * t) * kGeluC * fmaf(3.f * kGeluA, u * u, 1.f);
+}
+
 // Value of the fused epilogue at (m, n), m < M and n < N, in the output type.
 template <typename T, int KIND>
 __device__ __forceinline__ T epi_value(const EpiParams& e, int m, int n, float acc, float bn) {
@@ -139,10 +152,21 @@ __device__ __forceinline__ T epi_value(const EpiParams& e, int m, int n, float a
     const float x0 = ldf(static_cast<const T*>(e.x0) + (int64_t)m * e.ldx0 + n);
     const float xl = ldf(static_cast<const T*>(e.xl) + (int64_t)m * e.ldxl + n);
     return cvt<T>(fmaf(x0, acc + bn, xl));
+  } else if constexpr (KIND == GK_FWD_LIN) {
+    float v = acc;
+    if (e.res) v += ldf(static_cast<const T*>(e.res) + (int64_t)m * e.ldres + n);
+    return cvt<T>(v);
+  } else if constexpr (KIND == GK_FWD_GELU) {
+    return cvt<T>(gelu_f(acc));
+  } else if constexpr (KIND == GK_DGRAD_GELU) {
+    return cvt<T>(acc * gelu_grad_f(ldf(static_cast<const T*>(e.mask) + (int64_t)m * e.ldmask + n)));
+  } else if constexpr (KIND == GK_FWD_LOGITS) {
+    return cvt<T>(acc);
   } else {  // GK_DGRAD
     float v = acc;
     if (e.res) v += ldf(static_cast<const T*>(e.res) + (int64_t)m * e.ldres + n);
     if (!e.below_cross) {
+      if (!e.mask) return cvt<T>(v);
       const float mk = ldf(static_cast<const T*>(e.mask) + (int64_t)m * e.ldmask + n);
       return cvt<T>(mk > 0.f ? v : 0.f);
     }
@@ -217,7 +241,9 @@ struct GemmSmem {
   // fused head: hw[BN], labels[BM], ds[BM], loss[BM], dw[2][BN], c (fp32),
   // past both the main-loop stages and the output tile
   static constexpr int HOFF = MAIN > TILE ? MAIN : TILE;
-  static constexpr int BYTES = HOFF + (KIND == GK_FWD_HEAD ? (3 * BN + 3 * BM + 4) * 4 : 0);
+  // logits: per wave column half, per row, (max, sum) pairs
+  static constexpr int BYTES = HOFF + (KIND == GK_FWD_HEAD ? (3 * BN + 3 * BM + 4) * 4
+                                       : KIND == GK_FWD_LOGITS ? 2 * BM * 2 * 4 : 0);
 };
 
 // KG k-groups of four waves (256 * KG threads): every k-group owns the whole
@@ -551,12 +577,22 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   if constexpr (KIND == GK_WGRAD) {
     omn = e.part + (int64_t)z * e.pstride;
     ldmn = e.ldp;
-  } else if constexpr (KIND == GK_DGRAD) {
+  } else if constexpr (KIND == GK_DGRAD || KIND == GK_DGRAD_GELU) {
     omn = static_cast<OT*>(e.dmn);
     ldmn = e.lddmn;
   } else {
     omn = static_cast<OT*>(e.y);
     ldmn = e.ldy;
+  }
+  int tgt[KIND == GK_FWD_LOGITS ? TM : 1][4];  // target column of each of the lane's rows
+  if constexpr (KIND == GK_FWD_LOGITS) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + q;
+        tgt[i][q] = m < M ? e.target[m] : -1;
+      }
   }
   // pass 1 (every load of the epilogue): values into the LDS tile and back
   // into the accumulators; pass 2 (stores only): the row-major tile.
@@ -580,7 +616,10 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
           v = acc[i][j][q];
         } else {
           v = (m < M && n < N) ? epi_value<T, KIND>(e, m, n, acc[i][j][q], bn) : OT(0);
-          acc[i][j][q] = asf(v);
+          if constexpr (KIND != GK_FWD_GELU) acc[i][j][q] = asf(v);  // GELU keeps the pre-activation
+          if constexpr (KIND == GK_FWD_LOGITS) {
+            if (m < M && n < N && n == tgt[i][q]) e.tlogit[m] = asf(v);
+          }
         }
         sc[ml * OPITCH + nl] = v;
       }
@@ -602,6 +641,79 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
       } else {
         for (int q = 0; q < OCH && n + q < N; ++q) dst[q] = src[q];
       }
+    }
+  }
+
+  if constexpr (KIND == GK_FWD_GELU) {
+    // the pre-activation u = acc into gout, through the same LDS tile
+    if (e.gout) {
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int nl = wn * WN + j * 16 + (lane & 15);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int ml = wm * WM + i * 16 + (lane >> 4) * 4 + q;
+            sc[ml * OPITCH + nl] = (m0 + ml < M && n0 + nl < N) ? cvt<T>(acc[i][j][q]) : OT(0);
+          }
+      }
+      __syncthreads();
+      constexpr int CPRO = BN / OCH;
+      for (int c = tid; c < BM * CPRO; c += NT) {
+        const int ml = c / CPRO, nl = (c % CPRO) * OCH;
+        const int m = m0 + ml, n = n0 + nl;
+        if (m >= M || n >= N) continue;
+        const OT* src = &sc[ml * OPITCH + nl];
+        OT* dst = static_cast<OT*>(e.gout) + (int64_t)m * e.ldgout + n;
+        if (n + OCH <= N) {
+          *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(src);
+        } else {
+          for (int q = 0; q < OCH && n + q < N; ++q) dst[q] = src[q];
+        }
+      }
+    }
+  }
+
+  if constexpr (KIND == GK_FWD_LOGITS) {
+    // Row statistics of this tile's columns from the stored (rounded)
+    // values: every lane reduces its row over its TN columns, then the 16
+    // lanes sharing the row, then the two waves of a row half through LDS,
+    // all in a fixed order.
+    float* st = reinterpret_cast<float*>(smem + GemmSmem<T, BM, BN, KIND>::HOFF);  // [2][BM][2]
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int ml = wm * WM + i * 16 + (lane >> 4) * 4 + q;
+        float mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          if (n0 + wn * WN + j * 16 + (lane & 15) < N) mx = fmaxf(mx, acc[i][j][q]);
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+        float se = 0.f;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          if (n0 + wn * WN + j * 16 + (lane & 15) < N) se += __expf(acc[i][j][q] - mx);
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) se += __shfl_xor(se, o, 64);
+        if ((lane & 15) == 0) {
+          st[(wn * BM + ml) * 2] = mx;
+          st[(wn * BM + ml) * 2 + 1] = se;
+        }
+      }
+    __syncthreads();
+    for (int r = tid; r < BM; r += NT) {
+      const int m = m0 + r;
+      if (m >= M) continue;
+      const float ma = st[r * 2], sa = st[r * 2 + 1];
+      const float mb = st[(BM + r) * 2], sb = st[(BM + r) * 2 + 1];
+      const float mx = fmaxf(ma, mb);  // finite: every tile holds at least one column
+      const float se = (sa > 0.f ? sa * __expf(ma - mx) : 0.f) + (sb > 0.f ? sb * __expf(mb - mx) : 0.f);
+      e.lstat[(int64_t)m * e.ldlstat + 2 * by] = mx;
+      e.lstat[(int64_t)m * e.ldlstat + 2 * by + 1] = se;
     }
   }
 
@@ -783,6 +895,10 @@ ERASE_GEMM_KERNEL(erase_fwd_cross_gemm, GK_FWD_CROSS)
 ERASE_GEMM_KERNEL(erase_wgrad_gemm, GK_WGRAD)
 ERASE_GEMM_KERNEL(erase_dgrad_gemm, GK_DGRAD)
 ERASE_GEMM_KERNEL(erase_fwd_head_gemm, GK_FWD_HEAD)
+ERASE_GEMM_KERNEL(erase_fwd_lin_gemm, GK_FWD_LIN)
+ERASE_GEMM_KERNEL(erase_fwd_gelu_gemm, GK_FWD_GELU)
+ERASE_GEMM_KERNEL(erase_dgrad_gelu_gemm, GK_DGRAD_GELU)
+ERASE_GEMM_KERNEL(erase_fwd_logits_gemm, GK_FWD_LOGITS)
 #undef ERASE_GEMM_KERNEL
 
 // Two k-groups of four waves (512 threads): forward tiles of launches with at
@@ -887,6 +1003,20 @@ static hipError_t launch_gemm_t(int kind, const GemmDesc& g0, const EpiParams& e
       }
       break;
     case GK_DGRAD: ERASE_LAUNCH((erase_dgrad_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e); break;
+    case GK_FWD_LIN:
+    case GK_FWD_GELU:
+    case GK_DGRAD_GELU:
+    case GK_FWD_LOGITS:
+      // transformer kinds: bf16, 64- and 128-row tiles
+      if constexpr (sizeof(T) == 2 && BM >= 64) {
+        if (kind == GK_FWD_LIN) ERASE_LAUNCH((erase_fwd_lin_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e);
+        if (kind == GK_FWD_GELU) ERASE_LAUNCH((erase_fwd_gelu_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e);
+        if (kind == GK_DGRAD_GELU) ERASE_LAUNCH((erase_dgrad_gelu_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e);
+        if (kind == GK_FWD_LOGITS) ERASE_LAUNCH((erase_fwd_logits_gemm<T, BM, BN>), grid, block, 0, s, ev, g, e);
+      } else {
+        return hipErrorInvalidValue;
+      }
+      break;
     case GK_FWD_HEAD:
       // the tile must span the whole width; 32- and 64-row tiles only
       if constexpr (BM <= 64) {
