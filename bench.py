@@ -358,6 +358,131 @@ def input_stage(args, log, tr, cfg, head, labels, losses):
                     "traffic is lower than the algorithmic bytes"}
 
 
+def _merge(iv):
+    out = []
+    for a, b in sorted(iv):
+        if out and a <= out[-1][1]:
+            out[-1][1] = max(out[-1][1], b)
+        else:
+            out.append([a, b])
+    return out
+
+
+def _concurrent(recs, sel):
+    """Share of the time of the backward-stream records `sel` picks that a
+    forward-stream kernel runs at the same time."""
+    fwd = _merge([(r["start_ms"], r["end_ms"]) for r in recs if r["stream"] == 0 and r["kind"] != "empty"])
+    tot = inter = 0.0
+    for r in recs:
+        if r["stream"] != 1 or not sel(r):
+            continue
+        a, b = r["start_ms"], r["end_ms"]
+        tot += b - a
+        for c, d in fwd:
+            lo, hi = max(a, c), min(b, d)
+            if hi > lo:
+                inter += hi - lo
+    return inter / tot if tot > 0 else None
+
+
+def transformer_section(args, log):
+    """The detached small transformer (vocabulary 32768, width 512, 8 heads,
+    8 layers, sequences of 1024, batch 16): tokens/s of SERIAL and OVERLAP,
+    per-kernel times, GEMM MFMA utilisation, and how much backward work runs
+    beside forward work, for all of it and for the attention backward."""
+    import torch
+
+    from paper_2608_18469_amd import erase_tf, synth_tf
+    cfg = synth_tf.tf_config("tf_c5")
+    log(f"[bench] transformer tf_c5: V {cfg['vocab']}, d {cfg['d']}, {cfg['heads']} heads, {cfg['layers']} layers, "
+        f"T {cfg['seq']}, B {cfg['batch']}")
+    params, toks = synth_tf.make_workload(cfg, 0, 2)
+    tr = erase_tf.TfTrainer(cfg, params, keep_grads=False)
+    dev = [tr.device_tokens(t) for t in toks]
+    ntok = cfg["batch"] * cfg["seq"]
+    scheds = ["serial", "overlap"]
+    times = {s: [] for s in scheds}
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    i = 0
+    for s in scheds:
+        for _ in range(args.tf_warmup):
+            tr.step(dev[i % 2], s, wait_current=False)
+            i += 1
+    tr.sync()
+    for blk in range(2):
+        for s in scheds:
+            tr.sync()
+            t0 = time.perf_counter()
+            for _ in range(args.tf_steps // 2):
+                tr.step(dev[i % 2], s, wait_current=False)
+                i += 1
+            tr.sync()
+            times[s].append((time.perf_counter() - t0) / (args.tf_steps // 2))
+        log(f"[bench] transformer block {blk + 1}/2 done")
+    res = {s: {"tokens_per_s": ntok / float(np.mean(v)), "ms_per_step": float(np.mean(v)) * 1e3} for s, v in times.items()}
+    for s in scheds:
+        log(f"[bench] transformer {s}: {res[s]['tokens_per_s']:.0f} tokens/s, {res[s]['ms_per_step']:.2f} ms/step")
+    # per-launch timing
+    tr.set_timing(True)
+    recs = {}
+    for s in scheds:
+        recs[s] = []
+        for _ in range(3):
+            tr.step(dev[i % 2], s, wait_current=False)
+            i += 1
+            tr.sync()
+            recs[s].append(tr.read_timing()[1:])
+    tr.set_timing(False)
+    tr.close()
+    classes = {}
+    for rs in recs["serial"]:
+        for r in rs:
+            name = r["kind"] + (":" + erase_tf.GEMM_NAMES[r["layer"]] if r["kind"].endswith("gemm") else
+                                f":{r['layer']}" if r["kind"] == "attn_bwd" else "")
+            c = classes.setdefault(name, {"ms": 0.0, "n": 0, "flops": 0.0, "bytes": 0.0})
+            c["ms"] += r["end_ms"] - r["start_ms"]
+            c["n"] += 1
+            c["flops"] += r["flops"]
+            c["bytes"] += r["bytes"]
+    n = len(recs["serial"])
+    kernels = {k: {"avg_us": v["ms"] / v["n"] * 1e3, "us_per_step": v["ms"] / n * 1e3,
+                   "launches_per_step": v["n"] / n,
+                   "tflops": v["flops"] / (v["ms"] / 1e3) / 1e12 if v["flops"] else None,
+                   "gbs": v["bytes"] / (v["ms"] / 1e3) / 1e9 if v["bytes"] else None}
+               for k, v in sorted(classes.items(), key=lambda kv: -kv[1]["ms"])}
+    gm = [v for k, v in classes.items() if "gemm" in k]
+    gemm_util = sum(v["flops"] for v in gm) / (sum(v["ms"] for v in gm) / 1e3) / 1e12 / PEAK_BF16_TFLOPS
+    fl = synth_tf.flops_per_step(cfg)
+    best = max(("overlap",), key=lambda s: res[s]["tokens_per_s"])
+    ovl_all = float(np.mean([_concurrent(r, lambda x: True) for r in recs["overlap"]]))
+    ovl_att = [_concurrent(r, lambda x: x["kind"] == "attn_bwd" and x["layer"] >= 2) for r in recs["overlap"]]
+    ovl_voc = [_concurrent(r, lambda x: x["kind"].endswith("gemm") and x["layer"] == 4) for r in recs["overlap"]]
+    dom = max(kernels.items(), key=lambda kv: kv[1]["us_per_step"])
+    return {
+        "workload": "tf_c5: detached small transformer, vocabulary 32768, d_model 512, 8 heads of 64, 8 layers "
+                    "(causal attention + 4x GELU MLP, pre-RMSNorm), each layer with its own RMSNorm + "
+                    "Linear(512->32768) next-token softmax-CE head; batch 16 x 1024 tokens, uniform random "
+                    "token ids, bf16 operands, fp32 accumulation, Adam",
+        "metric": "train tokens/s @1 MI355X",
+        "value": res[best]["tokens_per_s"],
+        "unit": "tokens/s",
+        "schedule": best,
+        "schedules": res,
+        "overlap_vs_serial": res["overlap"]["tokens_per_s"] / res["serial"]["tokens_per_s"],
+        "steps": args.tf_steps, "warmup": args.tf_warmup,
+        "flops_per_step": fl["total"],
+        "mfma_util": {"gemm_kernels": gemm_util,
+                      "whole_step": fl["total"] / (res[best]["ms_per_step"] / 1e3) / 1e12 / PEAK_BF16_TFLOPS},
+        "bwd_fwd_overlap_fraction": ovl_all,
+        "attention_bwd_overlap_fraction": float(np.mean([x for x in ovl_att if x is not None])) if any(
+            x is not None for x in ovl_att) else None,
+        "vocab_gemm_overlap_fraction": float(np.mean([x for x in ovl_voc if x is not None])) if any(
+            x is not None for x in ovl_voc) else None,
+        "dominant_kernel": dom[0],
+        "kernels": kernels,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -380,6 +505,11 @@ def main():
     ap.add_argument("--bwd-streams", type=int, default=2,
                     help="backward streams of the ERASE schedules (block b uses stream b %% n); 2 measured "
                          "fastest on ctr_mlp (1 leaves the backward chain serial, 3+ exceed the 4 hardware queues)")
+    ap.add_argument("--no-transformer", action="store_true", help="skip the small-transformer measurement")
+    ap.add_argument("--transformer-only", action="store_true",
+                    help="only the small-transformer measurement (its JSON object on stdout)")
+    ap.add_argument("--tf-steps", type=int, default=30)
+    ap.add_argument("--tf-warmup", type=int, default=5)
     ap.add_argument("--verbose", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the run, copy a buffer of this many MiB once (a plain copy kernel of known size "
@@ -400,6 +530,10 @@ def main():
         sys.exit(1)
     torch.cuda.set_device(0)
     log = (lambda *a: print(*a, file=sys.stderr, flush=True))
+
+    if args.transformer_only:
+        print(json.dumps(transformer_section(args, log)))
+        return
 
     cfg = synth.config(args.workload)
     bf16 = cfg["dtype"] == "bf16"
@@ -513,6 +647,8 @@ def main():
     if cfg.get("input_kind") == "ctr" and not args.no_input_stage:
         out["input_stage"] = input_stage(args, log, tr, cfg, head, dev[0][1], losses)
     tr.close()
+    if not args.no_transformer:
+        out["transformer"] = transformer_section(args, log)
     if not args.no_conventional:
         out["erase_vs_conventional"] = conventional_comparison(args, log)
     if args.calib_copy_mib:
