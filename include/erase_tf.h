@@ -99,7 +99,8 @@ erase_status erase_tf_refresh_weights(void* ctx);
  * the empty interval, kind 7).  Kinds of this step: 0 prologue, 1 forward
  * GEMM (layer: 0 qkv, 1 output projection, 2 MLP up, 3 MLP down, 4
  * vocabulary logits), 3 weight-grad GEMM and 4 input-grad GEMM (layer as for
- * 1), 5 Adam, 11 embedding gather, 12 RMSNorm forward, 13 RMSNorm backward,
+ * 1), 6 both gradient GEMMs of one weight in one launch (layer as for 1),
+ * 5 Adam, 11 embedding gather, 12 RMSNorm forward, 13 RMSNorm backward,
  * 14 attention forward, 15 attention backward (layer 1 row sums, 2 dK/dV,
  * 3 dQ), 16 softmax cross-entropy, 17 embedding gradient (four launches,
  * bracketed by stream events rather than kernel-stamped ones). */

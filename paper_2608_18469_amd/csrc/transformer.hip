@@ -543,18 +543,28 @@ __global__ __launch_bounds__(256) void tf_xent(TfXentArgs a) {
     const int tg = a.target[n];
     loss = tg >= 0 ? lse - a.tlogit[n] : 0.f;
     uint16_t* row = a.logits + n * a.ldlog;
-    for (int c = lane; c < a.V / 8; c += 64) {
-      u32x4_t v = *reinterpret_cast<const u32x4_t*>(row + c * 8);
-      u32x4_t o;
+    const int nch = a.V / 8;
+    // four 16-byte chunks per lane in flight: all loads, then all stores
+    for (int c0 = lane; c0 < nch; c0 += 256) {
+      u32x4_t v[4];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int col = c * 8 + 2 * k;
-        float p0 = __expf(lo16(v[k]) - lse), p1 = __expf(hi16(v[k]) - lse);
-        if (col == tg) p0 -= 1.f;
-        if (col + 1 == tg) p1 -= 1.f;
-        o[k] = pack2(p0 * a.scale, p1 * a.scale);
+      for (int u = 0; u < 4; ++u)
+        if (c0 + 64 * u < nch) v[u] = *reinterpret_cast<const u32x4_t*>(row + (c0 + 64 * u) * 8);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int c = c0 + 64 * u;
+        if (c >= nch) continue;
+        u32x4_t o;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int col = c * 8 + 2 * k;
+          float p0 = __expf(lo16(v[u][k]) - lse), p1 = __expf(hi16(v[u][k]) - lse);
+          if (col == tg) p0 -= 1.f;
+          if (col + 1 == tg) p1 -= 1.f;
+          o[k] = pack2(p0 * a.scale, p1 * a.scale);
+        }
+        *reinterpret_cast<u32x4_t*>(row + c * 8) = o;
       }
-      *reinterpret_cast<u32x4_t*>(row + c * 8) = o;
     }
   }
   if (lane == 0) sloss[wave] = loss;

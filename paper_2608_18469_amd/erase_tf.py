@@ -15,7 +15,7 @@ import numpy as np
 from . import erase, synth_tf
 from .erase import BlockBuffers, EraseError, KernelTime, OK
 
-TF_KERNEL_KINDS = {0: "prologue", 1: "fwd_gemm", 3: "wgrad_gemm", 4: "dgrad_gemm", 5: "adam", 7: "empty",
+TF_KERNEL_KINDS = {0: "prologue", 1: "fwd_gemm", 3: "wgrad_gemm", 4: "dgrad_gemm", 5: "adam", 6: "bwd_gemm", 7: "empty",
                    11: "embed", 12: "rms_fwd", 13: "rms_bwd", 14: "attn_fwd", 15: "attn_bwd", 16: "xent",
                    17: "emb_grad"}
 GEMM_NAMES = {0: "qkv", 1: "proj", 2: "mlp_up", 3: "mlp_down", 4: "vocab"}
