@@ -162,6 +162,34 @@ def cpu_baseline(cfg, params, batches, budget_s, budget_1t_s):
             "cpu_model": _cpu_model(), "blas": blas, "os_cpu_count": os.cpu_count()}
 
 
+def tf_cpu_baseline(cfg, params, toks, budget_s):
+    """The float64 transformer oracle on the host, on a bounded sample: whole
+    steps of one layer (block 1, with the embedding) on one sequence of the
+    full length; tokens/s of the 8-layer model = sample tokens / (time per
+    one-layer step x layers)."""
+    from threadpoolctl import threadpool_info
+    from oracle import transformer_oracle
+    from paper_2608_18469_amd import synth_tf
+    info = threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in info] or [1])
+    one = dict(cfg, batch=1, layers=1)
+    p = [params[0]]
+    m = synth_tf.zero_state(p)
+    steps, t0 = 0, time.perf_counter()
+    while True:
+        r = transformer_oracle.tf_step(one, p, m, m, steps, toks[0][:1])
+        steps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    per = el / steps
+    return {"value": cfg["seq"] / (per * cfg["layers"]), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{steps} float64 oracle steps of one layer (with the embedding and its 32768-way head) on one "
+                      f"sequence of {cfg['seq']} tokens in {el:.1f} s, {threads} BLAS threads; scaled to "
+                      f"{cfg['layers']} layers",
+            "cpu_model": _cpu_model()}
+
+
 def time_schedules(tr, dev, scheds, steps, warmup, block, losses, M, log):
     """Warm every schedule up (graph capture and instantiation happen here),
     then time them interleaved in blocks of `block` steps so that clock and
@@ -458,6 +486,10 @@ def transformer_section(args, log):
     ovl_att = [_concurrent(r, lambda x: x["kind"] == "attn_bwd" and x["layer"] >= 2) for r in recs["overlap"]]
     ovl_voc = [_concurrent(r, lambda x: x["kind"].endswith("gemm") and x["layer"] == 4) for r in recs["overlap"]]
     dom = max(kernels.items(), key=lambda kv: kv[1]["us_per_step"])
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"[bench] transformer cpu baseline: oracle for ~{args.tf_cpu_budget:.0f} s")
+        cpu = tf_cpu_baseline(cfg, params, toks, args.tf_cpu_budget)
     return {
         "workload": "tf_c5: detached small transformer, vocabulary 32768, d_model 512, 8 heads of 64, 8 layers "
                     "(causal attention + 4x GELU MLP, pre-RMSNorm), each layer with its own RMSNorm + "
@@ -480,6 +512,7 @@ def transformer_section(args, log):
             x is not None for x in ovl_voc) else None,
         "dominant_kernel": dom[0],
         "kernels": kernels,
+        "cpu_baseline": cpu,
     }
 
 
@@ -510,6 +543,8 @@ def main():
                     help="only the small-transformer measurement (its JSON object on stdout)")
     ap.add_argument("--tf-steps", type=int, default=30)
     ap.add_argument("--tf-warmup", type=int, default=5)
+    ap.add_argument("--tf-cpu-budget", type=float, default=10.0,
+                    help="seconds of transformer oracle steps for its CPU baseline")
     ap.add_argument("--verbose", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the run, copy a buffer of this many MiB once (a plain copy kernel of known size "
