@@ -228,9 +228,9 @@ __device__ __forceinline__ void adam_elem(float& p, float& m, float& v, float g,
   p = p - step * m / (sqrtf(v) / bc2s + eps);
 }
 
-template <typename T, int BM, int BN, int KIND>
+template <typename T, int BM, int BN, int KIND, int BKX = 0>
 struct GemmSmem {
-  static constexpr int BK = GT<T>::BK, KCH = GT<T>::KCH, PITCH = sizeof(T) == 2 ? BK : BK + KCH;
+  static constexpr int BK = BKX ? BKX : GT<T>::BK, KCH = GT<T>::KCH, PITCH = sizeof(T) == 2 ? BK : BK + KCH;
   // weight gradient: k-major tiles [BK][BM] and [BK][BN] (fp32 rows padded by 16)
   static constexpr bool KMAJ = KIND == GK_WGRAD;
   static constexpr int PAD = sizeof(T) == 2 ? 0 : 16;
@@ -250,10 +250,10 @@ struct GemmSmem {
 // output tile and computes it over its own 1/KG of each k-step (KG = 2 gives
 // a one-workgroup-per-CU tile two waves per SIMD); the partial tiles are
 // added through LDS after the main loop.
-template <typename T, int BM, int BN, int KIND, int R = 2, int KG = 1>
+template <typename T, int BM, int BN, int KIND, int R = 2, int KG = 1, int BKX = 0>
 __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e, int bx, int by, int bz,
                                           char* smem) {
-  constexpr int BK = GT<T>::BK, KCH = GT<T>::KCH, KMF = GT<T>::KMF;
+  constexpr int BK = BKX ? BKX : GT<T>::BK, KCH = GT<T>::KCH, KMF = GT<T>::KMF;
   constexpr int NT = 256 * KG;  // threads
   constexpr bool SWZ = sizeof(T) == 2;  // chunk-permuted rows (bf16) or padded rows (fp32)
   constexpr int PITCH = SWZ ? BK : BK + KCH;
@@ -269,8 +269,8 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   // gradients and layer inputs in their row-major layout with the batch as
   // the contraction; LDS tiles are k-major, rows of BM (BN) elements, and
   // bf16 fragments come from pairs of transposing LDS reads.
-  constexpr bool KMAJ = GemmSmem<T, BM, BN, KIND>::KMAJ;
-  constexpr int PAD = GemmSmem<T, BM, BN, KIND>::PAD;
+  constexpr bool KMAJ = GemmSmem<T, BM, BN, KIND, BKX>::KMAJ;
+  constexpr int PAD = GemmSmem<T, BM, BN, KIND, BKX>::PAD;
   constexpr int PA = BM + PAD, PB = BN + PAD;  // k-major row pitches
   constexpr int CPA = BM / KCH, CPB = BN / KCH;  // 16-byte chunks per k-major row
   constexpr int RPA = NT / CPA, RPB = NT / CPB;  // k-major rows per pass of the workgroup's threads
@@ -278,7 +278,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   static_assert(!KMAJ || !SWZ || ((CPA == 8 || CPA == 16) && (CPB == 8 || CPB == 16)),
                 "k-major chunk permutation: 8 or 16 chunks per row");
   constexpr int AREG = KMAJ ? BK * PA : BM * PITCH;  // elements of the A part of a stage
-  constexpr int STAGE = GemmSmem<T, BM, BN, KIND>::STAGE;
+  constexpr int STAGE = GemmSmem<T, BM, BN, KIND, BKX>::STAGE;
   using OT = typename std::conditional<KIND == GK_WGRAD, float, T>::type;
   constexpr int OCH = 16 / (int)sizeof(OT);
   constexpr int OPITCH = BN + OCH;
@@ -302,7 +302,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
 
   if constexpr (KIND == GK_FWD_HEAD) {
     // head inputs into LDS now; their latency hides behind the main loop
-    float* hs = reinterpret_cast<float*>(smem + GemmSmem<T, BM, BN, KIND>::HOFF);
+    float* hs = reinterpret_cast<float*>(smem + GemmSmem<T, BM, BN, KIND, BKX>::HOFF);
     for (int n = tid; n < BN; n += 256) hs[n] = n < g.N ? e.hw[n] : 0.f;
     for (int r = tid; r < BM; r += 256) hs[BN + r] = m0 + r < g.M ? e.labels[m0 + r] : 0.f;
     if (tid == 0) hs[3 * BN + 3 * BM] = e.hc[0];
@@ -347,7 +347,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   // per-thread tile chunks: address of the first, element strides between a
   // thread's chunks (ia, ib) and per contraction index (ka, kb), LDS offsets
   constexpr int RSTEP = NT / CPR;  // NT: tile rows between a thread's chunks
-  static_assert(!SWZ || (CPR == 8 && RSTEP % 8 == 0), "chunk permutation assumes 8 chunks per row");
+  static_assert(KMAJ || !SWZ || (CPR == 8 && RSTEP % 8 == 0), "chunk permutation assumes 8 chunks per row");
   // k-major rows r are stored with 16-byte chunk j at j ^ kperm(r): with it
   // the transposing fragment reads (32 lanes per pass over 64 banks) and the
   // tile stores are conflict-free (measured with the LDS bank counters)
@@ -540,7 +540,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     // memory, one 64-float row per accumulator register and wave; k-group 0
     // adds them
     float* red = reinterpret_cast<float*>(smem);
-    static_assert(4 * (TM * TN * 4 + TM) * 64 * 4 <= GemmSmem<T, BM, BN, KIND>::MAIN, "reduction buffer");
+    static_assert(4 * (TM * TN * 4 + TM) * 64 * 4 <= GemmSmem<T, BM, BN, KIND, BKX>::MAIN, "reduction buffer");
     const int sw = wave & 3;
     float* rrs = red + 4 * TM * TN * 4 * 64;
     if (kg == 1) {
@@ -685,7 +685,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     // values: every lane reduces its row over its TN columns, then the 16
     // lanes sharing the row, then the two waves of a row half through LDS,
     // all in a fixed order.
-    float* st = reinterpret_cast<float*>(smem + GemmSmem<T, BM, BN, KIND>::HOFF);  // [2][BM][2]
+    float* st = reinterpret_cast<float*>(smem + GemmSmem<T, BM, BN, KIND, BKX>::HOFF);  // [2][BM][2]
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -798,7 +798,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     //   ds_m = lam (sigmoid(s_m) - y_m) / M,  dz_mn = ds_m w_n [z_mn > 0]
     // in both layouts, and this M-tile's partials dw_n = sum_m z_mn ds_m,
     // dc = sum_m ds_m and sum_m loss_m, every sum in a fixed order.
-    float* s_w = reinterpret_cast<float*>(smem + GemmSmem<T, BM, BN, KIND>::HOFF);
+    float* s_w = reinterpret_cast<float*>(smem + GemmSmem<T, BM, BN, KIND, BKX>::HOFF);
     float* s_y = s_w + BN;
     float* s_ds = s_y + BM;
     float* s_l = s_ds + BM;
@@ -910,17 +910,20 @@ ERASE_GEMM_KERNEL(erase_fwd_logits_gemm, GK_FWD_LOGITS)
 
 // Two k-groups of four waves (512 threads): forward tiles of launches with at
 // most one workgroup per CU, which then run two waves per SIMD.
-#define ERASE_GEMM_KERNEL_KG2(NAME, KIND)                                                \
-  template <typename T, int BM, int BN>                                                  \
-  __global__ __launch_bounds__(512) void NAME(GemmDesc g, EpiParams e) {                 \
-    __shared__ __attribute__((aligned(16))) char smem[GemmSmem<T, BM, BN, KIND>::BYTES]; \
-    const int gm = (g.M + BM - 1) / BM, gn = (g.N + BN - 1) / BN;                        \
-    const TileIdx ti = tile_from(xcd_linear(blockIdx.x, gridDim.x), gm, gn, g.group);   \
-    gemm_body<T, BM, BN, KIND, 2, 2>(g, e, ti.m, ti.n, ti.z, smem);                      \
+#define ERASE_GEMM_KERNEL_KG2(NAME, KIND, BKX)                                                \
+  template <typename T, int BM, int BN>                                                       \
+  __global__ __launch_bounds__(512) void NAME(GemmDesc g, EpiParams e) {                      \
+    constexpr int BKK = sizeof(T) == 2 ? BKX : 0;                                            \
+    __shared__ __attribute__((aligned(16))) char smem[GemmSmem<T, BM, BN, KIND, BKK>::BYTES]; \
+    const int gm = (g.M + BM - 1) / BM, gn = (g.N + BN - 1) / BN;                             \
+    const TileIdx ti = tile_from(xcd_linear(blockIdx.x, gridDim.x), gm, gn, g.group);        \
+    gemm_body<T, BM, BN, KIND, 2, 2, BKK>(g, e, ti.m, ti.n, ti.z, smem);                      \
   }
-ERASE_GEMM_KERNEL_KG2(erase_fwd_gemm_kg2, GK_FWD_RELU)
-ERASE_GEMM_KERNEL_KG2(erase_fwd_cross_gemm_kg2, GK_FWD_CROSS)
-ERASE_GEMM_KERNEL_KG2(erase_wgrad_gemm_kg2, GK_WGRAD)
+ERASE_GEMM_KERNEL_KG2(erase_fwd_gemm_kg2, GK_FWD_RELU, 0)
+ERASE_GEMM_KERNEL_KG2(erase_fwd_cross_gemm_kg2, GK_FWD_CROSS, 0)
+// the weight gradient: k-steps of 128 batch rows (bf16), two MFMA k-steps
+// per k-group between barriers
+ERASE_GEMM_KERNEL_KG2(erase_wgrad_gemm_kg2, GK_WGRAD, 128)
 #undef ERASE_GEMM_KERNEL_KG2
 
 // One launch for both backward GEMMs of a layer (they read the same
