@@ -7,7 +7,9 @@
 //  * tf_rms_fwd:    y = x r with r = 1 / sqrt(mean(x^2) + eps) per row.
 //  * tf_rms_bwd:    dx = r (dy - y mean(dy y)) (+ a residual gradient).
 //  * tf_attn_fwd:   causal softmax attention of every head (head size 64),
-//                   online over key blocks of 64; o and the row log-sum-exp.
+//                   online over key blocks of 64 (the next block's loads in
+//                   flight during the current one); o and the row
+//                   log-sum-exp.
 //  * tf_attn_bwd_*: D = rowsum(do * o), then dK/dV per key block and dQ per
 //                   query block (no atomics: every output has one writer).
 //  * tf_xent:       log-sum-exp per row from the logits GEMM's per-tile
@@ -93,18 +95,31 @@ __device__ __forceinline__ u32x4_t col_frag(const uint16_t* t, int r0, int c16, 
   return u32x4_t{a.x, a.y, b.x, b.y};
 }
 
-// Stage rows [row0, row0 + 64) of a [.. x ld] bf16 matrix, columns
-// [col0, col0 + 64), into an LDS tile with 256 threads; rows at or past
-// `rows` are zero.
-__device__ __forceinline__ void stage64(uint16_t* t, const uint16_t* g, int64_t ld, int row0, int rows, int64_t col0,
-                                        int tid) {
+// Staging of rows [row0, row0 + 64), columns [col0, col0 + 64) of a bf16
+// matrix into an LDS tile by 256 threads (rows at or past `rows` are zero),
+// in two halves: the thread's two chunks into registers, then into the
+// tile, so the loads of the next block are in flight while the current one
+// is computed.
+struct Stage2 {
+  u32x4_t v[2];
+};
+__device__ __forceinline__ Stage2 load64(const uint16_t* g, int64_t ld, int row0, int rows, int64_t col0, int tid) {
+  Stage2 r;
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int c = tid + 256 * i;
-    const int r = c >> 3, ch = c & 7;
-    u32x4_t v = {0u, 0u, 0u, 0u};
-    if (row0 + r < rows) v = *reinterpret_cast<const u32x4_t*>(g + (int64_t)(row0 + r) * ld + col0 + ch * 8);
-    *reinterpret_cast<u32x4_t*>(t + r * 64 + ((ch ^ (r & 7)) << 3)) = v;
+    const int rr = c >> 3, ch = c & 7;
+    r.v[i] = u32x4_t{0u, 0u, 0u, 0u};
+    if (row0 + rr < rows) r.v[i] = *reinterpret_cast<const u32x4_t*>(g + (int64_t)(row0 + rr) * ld + col0 + ch * 8);
+  }
+  return r;
+}
+__device__ __forceinline__ void store64(uint16_t* t, const Stage2& r, int tid) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int c = tid + 256 * i;
+    const int rr = c >> 3, ch = c & 7;
+    *reinterpret_cast<u32x4_t*>(t + rr * 64 + ((ch ^ (rr & 7)) << 3)) = r.v[i];
   }
 }
 
@@ -261,12 +276,18 @@ __global__ __launch_bounds__(256) void tf_attn_fwd(TfAttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) ot[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  const uint16_t* kvbase = a.qkv + base * a.ldqkv;
+  Stage2 nk = load64(kvbase, a.ldqkv, 0, a.T, colk, tid), nv = load64(kvbase, a.ldqkv, 0, a.T, colv, tid);
   for (int kb = 0; kb <= qb; ++kb) {
     const int k0 = kb * 64;
     __syncthreads();  // previous block's reads done
-    stage64(sk, a.qkv + base * a.ldqkv, a.ldqkv, k0, a.T, colk, tid);
-    stage64(sv, a.qkv + base * a.ldqkv, a.ldqkv, k0, a.T, colv, tid);
+    store64(sk, nk, tid);
+    store64(sv, nv, tid);
     __syncthreads();
+    if (kb < qb) {  // next block's loads in flight during this block's compute
+      nk = load64(kvbase, a.ldqkv, k0 + 64, a.T, colk, tid);
+      nv = load64(kvbase, a.ldqkv, k0 + 64, a.T, colv, tid);
+    }
     // scores of keys k0 + 32 st + 8 g + 4 t + q
     f32x4_t st4[2][2];
 #pragma unroll
@@ -388,17 +409,33 @@ __global__ __launch_bounds__(256) void tf_attn_bwd_dkdv(TfAttnArgs a) {
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) dvt[dt] = dkt[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  const uint16_t* qbase = a.qkv + base * a.ldqkv;
+  const uint16_t* dobase = a.dout + base * a.lddo;
+  Stage2 nq = load64(qbase, a.ldqkv, kb * 64, a.T, colq, tid), nd = load64(dobase, a.lddo, kb * 64, a.T, colq, tid);
+  float nl = 0.f, ns = 0.f;
+  if (tid < 64 && kb * 64 + tid < a.T) {
+    nl = lse[kb * 64 + tid] * kLog2e;
+    ns = dsum[kb * 64 + tid];
+  }
   for (int qb = kb; qb < nb; ++qb) {
     const int q0 = qb * 64;
     __syncthreads();
-    stage64(sq, a.qkv + base * a.ldqkv, a.ldqkv, q0, a.T, colq, tid);
-    stage64(sdo, a.dout + base * a.lddo, a.lddo, q0, a.T, colq, tid);
+    store64(sq, nq, tid);
+    store64(sdo, nd, tid);
     if (tid < 64) {
-      const bool ok = q0 + tid < a.T;
-      sl[tid] = ok ? lse[q0 + tid] * kLog2e : 0.f;
-      sd[tid] = ok ? dsum[q0 + tid] : 0.f;
+      sl[tid] = nl;
+      sd[tid] = ns;
     }
     __syncthreads();
+    if (qb + 1 < nb) {  // next block's loads in flight during this block's compute
+      nq = load64(qbase, a.ldqkv, q0 + 64, a.T, colq, tid);
+      nd = load64(dobase, a.lddo, q0 + 64, a.T, colq, tid);
+      nl = ns = 0.f;
+      if (tid < 64 && q0 + 64 + tid < a.T) {
+        nl = lse[q0 + 64 + tid] * kLog2e;
+        ns = dsum[q0 + 64 + tid];
+      }
+    }
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
       f32x4_t s4[2], p4[2];
@@ -477,12 +514,18 @@ __global__ __launch_bounds__(256) void tf_attn_bwd_dq(TfAttnArgs a) {
   f32x4_t acc[4];
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) acc[dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const uint16_t* kvbase = a.qkv + base * a.ldqkv;
+  Stage2 nk = load64(kvbase, a.ldqkv, 0, a.T, colk, tid), nv = load64(kvbase, a.ldqkv, 0, a.T, colv, tid);
   for (int kb = 0; kb <= qb; ++kb) {
     const int k0 = kb * 64;
     __syncthreads();
-    stage64(sk, a.qkv + base * a.ldqkv, a.ldqkv, k0, a.T, colk, tid);
-    stage64(sv, a.qkv + base * a.ldqkv, a.ldqkv, k0, a.T, colv, tid);
+    store64(sk, nk, tid);
+    store64(sv, nv, tid);
     __syncthreads();
+    if (kb < qb) {
+      nk = load64(kvbase, a.ldqkv, k0 + 64, a.T, colk, tid);
+      nv = load64(kvbase, a.ldqkv, k0 + 64, a.T, colv, tid);
+    }
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
       f32x4_t s4[2], p4[2];
