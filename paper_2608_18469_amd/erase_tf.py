@@ -91,7 +91,8 @@ def workspace_bytes(cfg: dict) -> int:
 class TfTrainer:
     """Owns the device buffers, two streams and one transformer context."""
 
-    def __init__(self, cfg: dict, params: list, keep_grads: bool = True):
+    def __init__(self, cfg: dict, params: list, keep_grads: bool = True, m: list | None = None,
+                 v: list | None = None, step: int = 0):
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("no HIP device available: the ERASE step runs only on the GPU")
@@ -108,8 +109,10 @@ class TfTrainer:
             flat = synth_tf.pack_block(cfg, b, params[b])
             assert flat.size == n, (flat.size, n)
             P = torch.from_numpy(flat).to(self.dev)
-            Mm = torch.zeros(n, device=self.dev)
-            Vv = torch.zeros(n, device=self.dev)
+            Mm = (torch.from_numpy(synth_tf.pack_block(cfg, b, m[b])).to(self.dev) if m
+                  else torch.zeros(n, device=self.dev))
+            Vv = (torch.from_numpy(synth_tf.pack_block(cfg, b, v[b])).to(self.dev) if v
+                  else torch.zeros(n, device=self.dev))
             G = torch.zeros(n, device=self.dev) if keep_grads else None
             self.param.append(P); self.m.append(Mm); self.v.append(Vv); self.grad.append(G)
             bufs[b] = BlockBuffers(P.data_ptr(), Mm.data_ptr(), Vv.data_ptr(), G.data_ptr() if G is not None else None)
@@ -125,6 +128,8 @@ class TfTrainer:
                                    c_void_p(self.sf.cuda_stream), c_void_p(self.sb.cuda_stream), ctypes.byref(ctx)),
                "erase_tf_init")
         self.ctx = ctx
+        if step:
+            self.set_step(step)
         self.losses = torch.zeros(L, dtype=torch.float32, device=self.dev)
 
     def device_tokens(self, tokens: np.ndarray):

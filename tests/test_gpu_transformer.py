@@ -209,3 +209,58 @@ def test_tf_c5_full_size_sampled():
     mx = s.max(-1, keepdims=True)
     ref = (mx + np.log(np.exp(s - mx).sum(-1, keepdims=True)))[..., 0]
     assert np.max(np.abs(lse0 - ref)) < 5e-2, np.max(np.abs(lse0 - ref))
+
+
+def test_tf_checkpoint_resume_is_bit_identical():
+    """Two steps in one run equal one step, a save of params / m / v / t, a
+    fresh context resumed from them, and a second step; also after the
+    caller rewrites the parameters and refreshes the weight copies."""
+    from paper_2608_18469_amd import erase_tf
+    cfg = synth_tf.tf_config("tf_small")
+    params, batches = synth_tf.make_workload(cfg, seed=7, n_batches=2)
+    _, full = _gpu_run(cfg, params, batches, "overlap")
+    tr1, one = _gpu_run(cfg, params, batches[:1], "overlap")
+    assert tr1.get_step() == 1
+    unpack = lambda flat: [synth_tf.unpack_block(cfg, b, flat[b]) for b in range(cfg["layers"])]
+    p1, m1, v1 = unpack(one[0]["params"]), unpack(one[0]["m"]), unpack(one[0]["v"])
+    tr1.close()
+    tr2 = erase_tf.TfTrainer(cfg, p1, m=m1, v=v1, step=1)
+    _, resumed = _gpu_run(cfg, p1, batches[1:], "overlap", tr=tr2)
+    _bits_equal(full[1:], resumed)
+    # overwrite the parameters in place, refresh the copies, step again
+    for b in range(cfg["layers"]):
+        tr2.param[b].copy_(tr2.torch.from_numpy(synth_tf.pack_block(cfg, b, p1[b])).to(tr2.dev))
+        tr2.m[b].copy_(tr2.torch.from_numpy(synth_tf.pack_block(cfg, b, m1[b])).to(tr2.dev))
+        tr2.v[b].copy_(tr2.torch.from_numpy(synth_tf.pack_block(cfg, b, v1[b])).to(tr2.dev))
+    tr2.torch.cuda.synchronize()
+    tr2.set_step(1)
+    tr2.refresh_weights()
+    _, again = _gpu_run(cfg, p1, batches[1:], "overlap", tr=tr2)
+    _bits_equal(full[1:], again)
+    tr2.close()
+
+
+def test_tf_timing_records():
+    cfg = synth_tf.tf_config("tf_small", layers=2)
+    params, batches = synth_tf.make_workload(cfg, seed=8, n_batches=1)
+    tr = _trainer(cfg, params)
+    t = tr.device_tokens(batches[0])
+    tr.set_timing(True)
+    for sched in ("serial", "overlap"):
+        tr.step(t, sched)
+        tr.sync()
+        recs = tr.read_timing()
+        assert recs[0]["kind"] == "empty"
+        kinds = {r["kind"] for r in recs[1:]}
+        assert {"prologue", "embed", "rms_fwd", "fwd_gemm", "attn_fwd", "xent", "rms_bwd", "attn_bwd",
+                "adam", "emb_grad"} <= kinds, kinds
+        assert any(k in kinds for k in ("bwd_gemm", "wgrad_gemm"))
+        for r in recs[1:]:
+            assert r["end_ms"] >= r["start_ms"] >= 0.0
+        streams = {r["stream"] for r in recs[1:]}
+        assert streams == ({0} if sched == "serial" else {0, 1}), streams
+        # per block: the forward body on stream 0, the head on the backward stream when overlapped
+        heads = [r for r in recs[1:] if r["kind"] == "xent"]
+        assert len(heads) == cfg["layers"] and all(r["stream"] == (0 if sched == "serial" else 1) for r in heads)
+    tr.set_timing(False)
+    tr.close()
