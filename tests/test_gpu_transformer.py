@@ -264,3 +264,38 @@ def test_tf_timing_records():
         assert len(heads) == cfg["layers"] and all(r["stream"] == (0 if sched == "serial" else 1) for r in heads)
     tr.set_timing(False)
     tr.close()
+
+
+def test_tf_widest_model():
+    """The widest model the ABI accepts: d 4096 = 64 heads of 64 (RMSNorm and
+    embedding-gradient rows at their maximum width)."""
+    cfg = synth_tf.tf_config("tf_tiny", vocab=64, d=4096, heads=64, layers=1, seq=3, batch=2)
+    params, batches = synth_tf.make_workload(cfg, seed=9, n_batches=1)
+    print("[tf] d=4096 H=64", flush=True)
+    _, gpu = _gpu_run(cfg, params, batches, "overlap")
+    _check_bf16(cfg, gpu, params, batches)
+
+
+def test_tf_long_sequence():
+    cfg = synth_tf.tf_config("tf_tiny", vocab=128, d=64, heads=1, layers=2, seq=2048, batch=1)
+    params, batches = synth_tf.make_workload(cfg, seed=10, n_batches=1)
+    print("[tf] T=2048", flush=True)
+    _, gpu = _gpu_run(cfg, params, batches, "overlap")
+    _check_bf16(cfg, gpu, params, batches)
+
+
+def test_tf_repeated_tokens_embedding_gradient():
+    """One token at almost every position: its bucket (about 500 positions)
+    takes the embedding gradient's ordering path for buckets over 64; the
+    rest of the rows are empty or small."""
+    cfg = synth_tf.tf_config("tf_tiny", vocab=128, d=128, heads=2, layers=1, seq=256, batch=2)
+    params, batches = synth_tf.make_workload(cfg, seed=11, n_batches=1)
+    tok = batches[0].copy()
+    rng = np.random.Generator(np.random.PCG64(12))
+    mask = rng.random(tok.shape) < 0.97
+    tok[mask] = 7
+    print("[tf] repeated token", flush=True)
+    _, gpu = _gpu_run(cfg, params, [tok], "serial")
+    _check_bf16(cfg, gpu, params, [tok])
+    _, again = _gpu_run(cfg, params, [tok], "overlap")
+    _bits_equal(gpu, again)
