@@ -330,6 +330,30 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
       }
   }
 
+  // fused Adam: the tile's parameters and moments are loaded now (they do not
+  // depend on the gradient), so their HBM latency hides behind the main loop
+  typedef float f32x4a_t __attribute__((ext_vector_type(4), aligned(4)));
+  typedef __attribute__((address_space(1))) f32x4a_t gvec;
+  constexpr int AQ = BN / 4;                                                  // items of 4 columns per row
+  constexpr int AIT = (KIND == GK_WGRAD && KG == 2) ? (BM * AQ + NT - 1) / NT : 1;  // items per thread
+  f32x4a_t apv[AIT], amv[AIT], avv[AIT];
+  bool afull[AIT];
+  int64_t afi[AIT];
+  if constexpr (KIND == GK_WGRAD && KG == 2) {
+#pragma unroll
+    for (int it = 0; it < AIT; ++it) {
+      const int c = tid + it * NT;
+      const int m = m0 + c / AQ, n = n0 + (c % AQ) * 4;
+      afull[it] = e.ap != nullptr && c < BM * AQ && m < g.M && n + 4 <= g.N;
+      afi[it] = (int64_t)m * g.N + n;
+      if (afull[it]) {
+        apv[it] = *reinterpret_cast<const gvec*>(gmem(e.ap) + afi[it]);
+        amv[it] = *reinterpret_cast<const gvec*>(gmem(e.am) + afi[it]);
+        avv[it] = *reinterpret_cast<const gvec*>(gmem(e.av) + afi[it]);
+      }
+    }
+  }
+
   const bool do_rows = (KIND == GK_WGRAD) && e.bpart != nullptr && by == 0 && wn == 0;
   float rs[TM];
 #pragma unroll
@@ -728,62 +752,47 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     if (e.ap) {
       // Fused Adam: the LDS tile holds this tile's finished gradient (the
       // contraction is not split).  Items of 4 consecutive columns of one
-      // row; every item's loads are issued before any store (16-byte
-      // accesses at 4-byte alignment: parameter rows start anywhere), a
-      // row's ragged end goes element by element.
-      typedef float f32x4a_t __attribute__((ext_vector_type(4), aligned(4)));
-      typedef __attribute__((address_space(1))) f32x4a_t gvec;
+      // row (16-byte accesses at 4-byte alignment: parameter rows start
+      // anywhere), whose parameters and moments were loaded before the main
+      // loop; a row's ragged end goes element by element.
       const float step = e.hyper[0], bc2s = e.hyper[1];
-      constexpr int Q = BN / 4;
-      constexpr int IT = (BM * Q + NT - 1) / NT;
+      constexpr int Q = AQ, IT = AIT;
       f32x4_t gv[IT];
-      f32x4a_t pv[IT], mv[IT], vv[IT];
-      bool full[IT];
-      int64_t fi[IT];
 #pragma unroll
       for (int it = 0; it < IT; ++it) {
         const int c = tid + it * NT;
-        const int ml = c / Q, nl = (c % Q) * 4;
-        const int m = m0 + ml, n = n0 + nl;
-        full[it] = c < BM * Q && m < M && n + 4 <= N;
-        fi[it] = (int64_t)m * N + n;
-        if (full[it]) {
-          gv[it] = *reinterpret_cast<const f32x4_t*>(&sc[ml * OPITCH + nl]);
-          pv[it] = *reinterpret_cast<const gvec*>(gmem(e.ap) + fi[it]);
-          mv[it] = *reinterpret_cast<const gvec*>(gmem(e.am) + fi[it]);
-          vv[it] = *reinterpret_cast<const gvec*>(gmem(e.av) + fi[it]);
-        }
+        if (afull[it]) gv[it] = *reinterpret_cast<const f32x4_t*>(&sc[(c / Q) * OPITCH + (c % Q) * 4]);
       }
 #pragma unroll
       for (int it = 0; it < IT; ++it) {
         const int c = tid + it * NT;
         const int ml = c / Q, nl = (c % Q) * 4;
         const int m = m0 + ml, n = n0 + nl;
-        if (full[it]) {
+        if (afull[it]) {
           float pp[4], mm[4], vq[4];
           T o[4];
 #pragma unroll
           for (int k = 0; k < 4; ++k) {
-            pp[k] = pv[it][k];
-            mm[k] = mv[it][k];
-            vq[k] = vv[it][k];
+            pp[k] = apv[it][k];
+            mm[k] = amv[it][k];
+            vq[k] = avv[it][k];
             adam_elem(pp[k], mm[k], vq[k], gv[it][k], e.b1, e.b2, step, bc2s, e.eps);
             o[k] = cvt<T>(pp[k]);
           }
-          if (e.ag) *reinterpret_cast<gvec*>(gmem(e.ag) + fi[it]) = f32x4a_t{gv[it][0], gv[it][1], gv[it][2], gv[it][3]};
-          *reinterpret_cast<gvec*>(gmem(e.am) + fi[it]) = f32x4a_t{mm[0], mm[1], mm[2], mm[3]};
-          *reinterpret_cast<gvec*>(gmem(e.av) + fi[it]) = f32x4a_t{vq[0], vq[1], vq[2], vq[3]};
-          *reinterpret_cast<gvec*>(gmem(e.ap) + fi[it]) = f32x4a_t{pp[0], pp[1], pp[2], pp[3]};
+          if (e.ag) *reinterpret_cast<gvec*>(gmem(e.ag) + afi[it]) = f32x4a_t{gv[it][0], gv[it][1], gv[it][2], gv[it][3]};
+          *reinterpret_cast<gvec*>(gmem(e.am) + afi[it]) = f32x4a_t{mm[0], mm[1], mm[2], mm[3]};
+          *reinterpret_cast<gvec*>(gmem(e.av) + afi[it]) = f32x4a_t{vq[0], vq[1], vq[2], vq[3]};
+          *reinterpret_cast<gvec*>(gmem(e.ap) + afi[it]) = f32x4a_t{pp[0], pp[1], pp[2], pp[3]};
           st4(static_cast<T*>(e.ash) + (int64_t)m * e.ldash + n, o);  // copy rows: 64-element multiples
         } else if (c < BM * Q && m < M && n < N) {
           for (int k = 0; k < N - n && k < 4; ++k) {
             const float gk = sc[ml * OPITCH + nl + k];
-            float pp = e.ap[fi[it] + k], mm = e.am[fi[it] + k], vq = e.av[fi[it] + k];
+            float pp = e.ap[afi[it] + k], mm = e.am[afi[it] + k], vq = e.av[afi[it] + k];
             adam_elem(pp, mm, vq, gk, e.b1, e.b2, step, bc2s, e.eps);
-            if (e.ag) e.ag[fi[it] + k] = gk;
-            e.am[fi[it] + k] = mm;
-            e.av[fi[it] + k] = vq;
-            e.ap[fi[it] + k] = pp;
+            if (e.ag) e.ag[afi[it] + k] = gk;
+            e.am[afi[it] + k] = mm;
+            e.av[afi[it] + k] = vq;
+            e.ap[afi[it] + k] = pp;
             static_cast<T*>(e.ash)[(int64_t)m * e.ldash + n + k] = cvt<T>(pp);
           }
         }
