@@ -47,7 +47,7 @@ METRIC = "train samples/s, 6-block CTR @1 MI355X; ERASE vs serial speedup; MFMA 
 KIND_SYMBOL = {"prologue": "erase_prologue", "fwd_gemm": "erase_fwd_gemm", "head_bce": "erase_head_bce",
                "wgrad_gemm": "erase_wgrad_gemm", "dgrad_gemm": "erase_dgrad_gemm", "adam": "erase_adam",
                "bwd_gemm": "erase_bwd_gemm", "fwd_head_gemm": "erase_fwd_head_gemm", "fwd_gemm_kg2": "erase_fwd_gemm_kg2",
-               "wgrad_gemm_kg2": "erase_wgrad_gemm_kg2"}
+               "wgrad_gemm_kg2": "erase_wgrad_gemm_kg2", "wgrad_adam_kg2": "erase_wgrad_adam_kg2"}
 
 
 def kernel_class(r, bf16=True):
@@ -264,7 +264,7 @@ def timed_records(tr, one_step, sched, n):
     return out
 
 
-BWD_KINDS = ("wgrad_gemm", "wgrad_gemm_kg2", "dgrad_gemm", "bwd_gemm", "adam")
+BWD_KINDS = ("wgrad_gemm", "wgrad_gemm_kg2", "wgrad_adam_kg2", "dgrad_gemm", "bwd_gemm", "adam")
 
 
 def conventional_comparison(args, log):

@@ -76,7 +76,10 @@ typedef enum { ERASE_IN_X = 0, ERASE_IN_PREV = 1 } erase_input_src;
 /* Schedules of one step.  All of them run the identical kernels on identical
  * inputs and produce bit-identical results.
  *   SERIAL:        everything on the forward stream: forward+loss of blocks
- *                  1..B, then backward of blocks B..1, then Adam of 1..B.
+ *                  1..B, then backward of blocks B..1, then Adam of 1..B
+ *                  (a block whose first-layer weight gradient carries its
+ *                  Adam update runs all of its Adam in that launch, at the
+ *                  end of its backward).
  *   OVERLAP:       ERASE early backward: forward+loss of block b on the
  *                  forward stream, then block b's backward and Adam on the
  *                  backward stream after an event, overlapping block b+1's
@@ -228,7 +231,12 @@ typedef struct {
                         forward launches of at most one workgroup per CU),
                         10 weight-grad GEMM of a block's first layer with two
                         k-groups and that layer's Adam update in its epilogue
-                        (kind 5 then updates the block's other parameters) */
+                        (kind 5 then updates the block's other parameters),
+                        11 the launch of kind 10 that also runs the Adam
+                        update of the block's other parameters in extra
+                        workgroups (used whenever a block's Adam directly
+                        follows its backward: every schedule but
+                        OVERLAP_ADAM_END; no kind 5 for the block then) */
   int32_t block;     /* block index, -1 for the step prologue */
   int32_t layer;     /* layer index within the block, -1 if none */
   int32_t stream;    /* 0 forward stream, 1 + k backward stream k */

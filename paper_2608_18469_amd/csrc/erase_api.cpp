@@ -421,10 +421,11 @@ void build_segments(Plan* P, const erase_block_buffers* bufs) {
     };
     for (int l = 0; l < B.L; ++l) {
       LayerRT& R = B.layer[l];
+      // a fused layer's weight and bias are updated by its weight-gradient launch
       fused = R.fused_adam;
       add(R.offW, R.N, R.K, R.part, R.pstride, (int)R.ldp, R.wgrad.split, R.wsh, R.ldwsh, R.wsht, R.ldwsht);
-      fused = false;
       add(R.offb, 1, R.N, R.bpart, R.N, R.N, R.wgrad.split, nullptr, 0, nullptr, 0);
+      fused = false;
     }
     const int NL = B.layer[B.L - 1].N;
     add(B.off_w, 1, NL, B.pdw, NL, NL, B.nhead, nullptr, 0, nullptr, 0);
@@ -814,8 +815,41 @@ erase_status enqueue_head(Ctx* c, Enqueuer& q, int b, const float* labels, hipSt
 // input gradient of the layer below; the block input is detached (Eq. 1), so
 // layer 0 has no input gradient.  When both GEMMs of a layer share a tile
 // they go out as one launch.
+// Arguments and cost of block b's Adam launch (the parameters not updated by
+// a fused weight-gradient launch).
+AdamArgs adam_args(const Ctx* c, int b, float* losses, int par, Cost* cost) {
+  const Plan& P = c->P;
+  const BlockRT& B = P.blk[b];
+  AdamArgs a{};
+  a.seg = B.segs_dev;
+  a.nseg = (int)B.segs.size();
+  for (int i = 0; i < a.nseg; ++i) a.chunk0[i] = B.segs[i].chunk0;
+  a.nchunks = B.nchunks;
+  a.hyper = reinterpret_cast<const float*>(P.t + 2) + 2 * par;
+  a.beta1 = c->cfg.beta1;
+  a.beta2 = c->cfg.beta2;
+  a.eps = c->cfg.eps;
+  a.ploss = B.ploss;
+  a.nloss = B.nhead;
+  a.inv_m = 1.0f / float(P.M);
+  a.loss_out = losses + b;
+  a.status = P.status;
+  cost->grid = (int)B.nchunks;
+  for (const AdamSeg& sg : B.segs) {
+    const double n = double(sg.rows) * sg.cols;
+    cost->flops += 12.0 * n;
+    cost->bytes += n * (4.0 * sg.nsplit + 24.0 + (sg.g ? 4.0 : 0.0) + (sg.sh ? P.esz : 0) + (sg.sht ? P.esz : 0));
+  }
+  return a;
+}
+
+// Block b's backward.  With `losses` set, a block whose first-layer weight
+// gradient carries the fused Adam update also runs the Adam update of its
+// other parameters in that launch (*adam_done = true); the caller then
+// launches no separate Adam for the block.
 erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStream_t s, int sid, int par,
-                              bool send = false) {
+                              bool send = false, float* losses = nullptr, bool* adam_done = nullptr) {
+  if (adam_done) *adam_done = false;
   const Plan& P = c->P;
   const BlockRT& B = P.blk[b];
   const int M = P.M, esz = P.esz, bf = P.bf16;
@@ -857,18 +891,32 @@ erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStre
       ew.ag = B.buf.grad ? B.buf.grad + R.offW : nullptr;
       ew.ash = R.wsh;
       ew.ldash = R.ldwsh;
+      ew.bp = B.buf.param + R.offb;
+      ew.bm = B.buf.m + R.offb;
+      ew.bv = B.buf.v + R.offb;
+      ew.bg = B.buf.grad ? B.buf.grad + R.offb : nullptr;
       ew.hyper = reinterpret_cast<const float*>(P.t + 2) + 2 * par;
       ew.b1 = c->cfg.beta1;
       ew.b2 = c->cfg.beta2;
       ew.eps = c->cfg.eps;
       // no partial slice is stored; Adam's per-parameter traffic moves here
-      const double n = double(R.N) * R.K;
+      const double n = double(R.N) * R.K + R.N;
       cw.flops += 12.0 * n;
-      cw.bytes += n * (24.0 + (ew.ag ? 4.0 : 0.0) + esz) - 4.0 * n;
+      cw.bytes += n * (24.0 + (ew.ag ? 4.0 : 0.0)) + double(R.N) * R.K * esz - 4.0 * n;
     }
     if (l == 0) {
-      RUN(gw.kgroups == 2 ? 10 : 3, b, l, sid, s, cw,
-          [&](const LaunchEv& ev) { return launch_gemm(bf, GK_WGRAD, gw, ew, s, ev); });
+      if (losses && R.fused_adam) {
+        Cost ca;
+        const AdamArgs aa = adam_args(c, b, losses, par, &ca);
+        cw.flops += ca.flops;
+        cw.bytes += ca.bytes;
+        cw.grid += (ca.grid + 1) / 2;
+        RUN(11, b, l, sid, s, cw, [&](const LaunchEv& ev) { return launch_wgrad_adam(bf, gw, ew, aa, s, ev); });
+        if (adam_done) *adam_done = true;
+      } else {
+        RUN(gw.kgroups == 2 ? 10 : 3, b, l, sid, s, cw,
+            [&](const LaunchEv& ev) { return launch_gemm(bf, GK_WGRAD, gw, ew, s, ev); });
+      }
       if (send && B.send) {
         // undetached: the gradient at the block input, dX = dH_0 W_0, is
         // added to the previous block's output gradient (its head's term,
@@ -956,28 +1004,8 @@ erase_status enqueue_backward(Ctx* c, Enqueuer& q, int b, const void* x, hipStre
 
 erase_status enqueue_adam(Ctx* c, Enqueuer& q, int b, float* losses, hipStream_t s, int sid, int par) {
   const Plan& P = c->P;
-  const BlockRT& B = P.blk[b];
-  AdamArgs a{};
-  a.seg = B.segs_dev;
-  a.nseg = (int)B.segs.size();
-  for (int i = 0; i < a.nseg; ++i) a.chunk0[i] = B.segs[i].chunk0;
-  a.nchunks = B.nchunks;
-  a.hyper = reinterpret_cast<const float*>(P.t + 2) + 2 * par;
-  a.beta1 = c->cfg.beta1;
-  a.beta2 = c->cfg.beta2;
-  a.eps = c->cfg.eps;
-  a.ploss = B.ploss;
-  a.nloss = B.nhead;
-  a.inv_m = 1.0f / float(P.M);
-  a.loss_out = losses + b;
-  a.status = P.status;
   Cost cost;
-  cost.grid = (int)B.nchunks;
-  for (const AdamSeg& sg : B.segs) {
-    const double n = double(sg.rows) * sg.cols;
-    cost.flops += 12.0 * n;
-    cost.bytes += n * (4.0 * sg.nsplit + 24.0 + (sg.g ? 4.0 : 0.0) + (sg.sh ? P.esz : 0) + (sg.sht ? P.esz : 0));
-  }
+  const AdamArgs a = adam_args(c, b, losses, par, &cost);
   const int bf = P.bf16;
   RUN(5, b, -1, sid, s, cost, [&](const LaunchEv& ev) { return launch_adam(bf, a, s, ev); });
   return ERASE_OK;
@@ -1057,9 +1085,10 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
           Enqueuer wq(c, false);
           erase_status s2 = head_b ? enqueue_head(c, wq, b, labels, sb, 1 + k) : ERASE_OK;
           if (s2 != ERASE_OK) return s2;
-          s2 = enqueue_backward(c, wq, b, x, sb, 1 + k, par);
+          bool done = false;
+          s2 = enqueue_backward(c, wq, b, x, sb, 1 + k, par, false, adam_end ? nullptr : losses, &done);
           if (s2 != ERASE_OK) return s2;
-          if (!adam_end) {
+          if (!adam_end && !done) {
             s2 = enqueue_adam(c, wq, b, losses, sb, 1 + k, par);
             if (s2 != ERASE_OK) return s2;
           }
@@ -1073,9 +1102,10 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
         st = enqueue_head(c, q, b, labels, sb, 1 + k);
         if (st != ERASE_OK) return st;
       }
-      st = enqueue_backward(c, q, b, x, sb, 1 + k, par);
+      bool done = false;
+      st = enqueue_backward(c, q, b, x, sb, 1 + k, par, false, adam_end ? nullptr : losses, &done);
       if (st != ERASE_OK) return st;
-      if (!adam_end) {
+      if (!adam_end && !done) {
         st = enqueue_adam(c, q, b, losses, sb, 1 + k, par);
         if (st != ERASE_OK) return st;
       }
@@ -1102,11 +1132,15 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
       erase_status st = enqueue_forward(c, q, b, x, labels, sf, 0);
       if (st != ERASE_OK) return st;
     }
+    std::vector<char> done(nb, 0);
     for (int b = nb - 1; b >= 0; --b) {
-      erase_status st = enqueue_backward(c, q, b, x, sf, 0, par, send);
+      bool d = false;
+      erase_status st = enqueue_backward(c, q, b, x, sf, 0, par, send, losses, &d);
       if (st != ERASE_OK) return st;
+      done[b] = d;
     }
     for (int b = 0; b < nb; ++b) {
+      if (done[b]) continue;
       erase_status st = enqueue_adam(c, q, b, losses, sf, 0, par);
       if (st != ERASE_OK) return st;
     }

@@ -98,6 +98,10 @@ struct EpiParams {
   void* ash; int64_t ldash;
   const float* hyper;  // lr / (1 - beta1^t), sqrt(1 - beta2^t) of this step
   float b1, b2, eps;
+  // and the bias's Adam update from the tiles' row sums of the A operand
+  // (bp non-null: the tiles of the first column block update bias entries
+  // [0, M), and no row sum is stored in bpart); gradient bg nullable
+  float* bp; float* bm; float* bv; float* bg;
   // logits (GK_FWD_LOGITS): lstat[m][2 t], lstat[m][2 t + 1] = max and sum
   // of exp(y - max) of row m over the columns of N-tile t (values as stored);
   // tlogit[m] = y[m][target[m]] (written by the tile holding that column)
@@ -187,6 +191,12 @@ struct AdamArgs {
   int* status;
 };
 hipError_t launch_adam(int bf16, const AdamArgs& a, hipStream_t s, const LaunchEv& ev = {});
+
+// A block's first-layer weight gradient with its fused Adam (g: 64x64, two
+// k-groups, unsplit; e.ap set) and the Adam launch `a` of the block's other
+// parameters in one launch (extra workgroups beside the GEMM tiles).
+hipError_t launch_wgrad_adam(int bf16, const GemmDesc& g, const EpiParams& e, const AdamArgs& a, hipStream_t s,
+                             const LaunchEv& ev = {});
 
 // Weight copies only (init / refresh): same segments, no update.
 hipError_t launch_refresh(int bf16, const AdamArgs& a, hipStream_t s);

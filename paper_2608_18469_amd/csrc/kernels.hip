@@ -602,7 +602,21 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
       sr += __shfl_xor(sr, 16, 64);
       sr += __shfl_xor(sr, 32, 64);
       const int m = m0 + wm * WM + i * 16 + lane;
-      if (lane < 16 && m < g.M) e.bpart[(int64_t)z * g.M + m] = sr;
+      if (lane < 16 && m < g.M) {
+        if constexpr (KIND == GK_WGRAD && KG == 2) {
+          if (e.bp) {
+            // fused Adam of the bias: this tile holds its rows' whole gradient
+            float p = e.bp[m], mo = e.bm[m], v = e.bv[m];
+            adam_elem(p, mo, v, sr, e.b1, e.b2, e.hyper[0], e.hyper[1], e.eps);
+            if (e.bg) e.bg[m] = sr;
+            e.bm[m] = mo;
+            e.bv[m] = v;
+            e.bp[m] = p;
+            continue;
+          }
+        }
+        e.bpart[(int64_t)z * g.M + m] = sr;
+      }
     }
   }
 
@@ -1281,14 +1295,25 @@ __device__ __forceinline__ int find_seg(const AdamArgs& a, int64_t chunk) {
 typedef float f32x4u_t __attribute__((ext_vector_type(4), aligned(4)));
 
 
+// One chunk of the Adam launch (ADAM_TR x ADAM_TC of a matrix segment, or
+// ADAM_TC elements of a vector) by 256 threads (tid 0..255) of a workgroup,
+// and the block loss with chunk 0.  s_o stages this chunk's transposed copy.
+// Every call executes exactly one __syncthreads (whatever the segment kind;
+// a negative chunk only takes part in it), so the two halves of a
+// 512-thread workgroup can each run a chunk.
 template <typename T>
-__global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
-  const int64_t chunk = blockIdx.x;
+__device__ __forceinline__ void adam_chunk(const AdamArgs& a, int64_t chunk, int tid, T (*s_o)[ADAM_TC]) {
+  if (chunk < 0) {
+    __syncthreads();
+    return;
+  }
   const AdamSeg sg = a.seg[find_seg(a, chunk)];
+  bool trans = false;  // the transposed copy is stored after the barrier
+  int r0 = 0, tile = 0;
   const float step = a.hyper[0];  // lr / (1 - beta1^t)
   const float bc2s = a.hyper[1];  // sqrt(1 - beta2^t)
   const float b1 = a.beta1, b2 = a.beta2, eps = a.eps;
-  const int tile = (int)(chunk - sg.chunk0);
+  tile = (int)(chunk - sg.chunk0);
   auto P = gmem(sg.p);
   auto Mo = gmem(sg.m);
   auto V = gmem(sg.v);
@@ -1298,7 +1323,7 @@ __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
     // a vector (bias or head parameter): one element per thread, possibly
     // many partials (one per head workgroup), 32 loads in flight per batch,
     // added in slice order
-    const int c = tile * ADAM_TC + (int)threadIdx.x;
+    const int c = tile * ADAM_TC + tid;
     const bool ok = c < sg.cols;
     const int cc = ok ? c : 0;  // clamped: loads stay in bounds
     float p = P[cc], m = Mo[cc], v = V[cc], g = 0.f;
@@ -1323,9 +1348,9 @@ __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
     // a matrix: a workgroup covers ADAM_TR (4) rows x ADAM_TC (256) columns,
     // a thread 4 consecutive columns of one row (16-byte loads and stores)
     static_assert(ADAM_TR == 4 && ADAM_TC == 256, "matrix tile is 4 rows x 64 threads x 4 columns");
-    const int r0 = (tile / sg.tcols) * ADAM_TR;
-    const int r = r0 + (int)(threadIdx.x >> 6);
-    const int c0 = (tile % sg.tcols) * ADAM_TC + (int)(threadIdx.x & 63) * 4;
+    r0 = (tile / sg.tcols) * ADAM_TR;
+    const int r = r0 + (tid >> 6);
+    const int c0 = (tile % sg.tcols) * ADAM_TC + (tid & 63) * 4;
     const bool any = r < sg.rows && c0 < sg.cols;
     const bool full = c0 + 4 <= sg.cols;
     const int rr = any ? r : 0, cc = any ? c0 : 0;  // clamped: loads stay in bounds
@@ -1413,14 +1438,18 @@ __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
     // transposed GEMM copy [cols][ldsht]: the 4 rows of each column, through
     // LDS (one 8- or 16-byte store per column)
     if (sg.sht) {
-      __shared__ T s_o[ADAM_TR][ADAM_TC];
-      const int cl = (int)(threadIdx.x & 63) * 4, rl = (int)(threadIdx.x >> 6);
+      const int cl = (tid & 63) * 4, rl = tid >> 6;
 #pragma unroll
       for (int k = 0; k < 4; ++k) s_o[rl][cl + k] = o[k];
-      __syncthreads();
-      const int c = (tile % sg.tcols) * ADAM_TC + (int)threadIdx.x;
+      trans = true;
+    }
+  }
+  __syncthreads();
+  if (trans) {
+    {
+      const int c = (tile % sg.tcols) * ADAM_TC + tid;
       if (c < sg.cols && r0 < sg.rows) {
-        T t4[4] = {s_o[0][threadIdx.x], s_o[1][threadIdx.x], s_o[2][threadIdx.x], s_o[3][threadIdx.x]};
+        T t4[4] = {s_o[0][tid], s_o[1][tid], s_o[2][tid], s_o[3][tid]};
         T* D = static_cast<T*>(sg.sht) + (int64_t)c * sg.ldsht + r0;
         if (r0 + 4 <= sg.rows) {
           st4(D, t4);
@@ -1432,17 +1461,60 @@ __global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
       }
     }
   }
-  if (chunk == 0 && threadIdx.x < 64 && a.ploss) {
+  if (chunk == 0 && tid < 64 && a.ploss) {
     // block loss: lane l sums partials l, l+64, ... in order, then a fixed
     // butterfly across the wave
     float L = 0.f;
-    for (int i = (int)threadIdx.x; i < a.nloss; i += 64) L += a.ploss[i];
+    for (int i = tid; i < a.nloss; i += 64) L += a.ploss[i];
     L = wave_sum(L) * a.inv_m;
-    if (threadIdx.x == 0) {
+    if (tid == 0) {
       a.loss_out[0] = L;
       if (!(fabsf(L) <= 3.4e38f)) a.status[0] = 1;
     }
   }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void erase_adam(AdamArgs a) {
+  __shared__ T s_o[ADAM_TR][ADAM_TC];
+  adam_chunk<T>(a, blockIdx.x, (int)threadIdx.x, s_o);
+}
+
+// A block's first-layer weight gradient with its fused Adam (two k-groups,
+// unsplit) and, in the same launch, the Adam update of the block's other
+// parameters: workgroups [0, ntiles) are the GEMM tiles (one per CU at
+// most), the rest run two Adam chunks each (one per half of the workgroup)
+// on the CUs the tiles leave free.  The two parts touch disjoint parameters,
+// and the Adam part reads only gradients finished by earlier launches.
+template <typename T, int BM, int BN>
+__global__ __launch_bounds__(512) void erase_wgrad_adam_kg2(GemmDesc g, EpiParams e, AdamArgs a, int ntiles) {
+  constexpr int BKK = sizeof(T) == 2 ? 128 : 0;
+  __shared__ __attribute__((aligned(16))) char smem[GemmSmem<T, BM, BN, GK_WGRAD, BKK>::BYTES];
+  static_assert(GemmSmem<T, BM, BN, GK_WGRAD, BKK>::BYTES >= 2 * ADAM_TR * ADAM_TC * (int)sizeof(T), "staging");
+  const int b = blockIdx.x;
+  if (b < ntiles) {
+    const int gm = (g.M + BM - 1) / BM, gn = (g.N + BN - 1) / BN;
+    const TileIdx ti = tile_from(xcd_linear(b, ntiles), gm, gn, g.group);
+    gemm_body<T, BM, BN, GK_WGRAD, 2, 2, BKK>(g, e, ti.m, ti.n, ti.z, smem);
+  } else {
+    const int half = (int)threadIdx.x >> 8;
+    T(*s_o)[ADAM_TC] = reinterpret_cast<T(*)[ADAM_TC]>(smem) + half * ADAM_TR;
+    const int64_t chunk = 2 * (int64_t)(b - ntiles) + half;
+    adam_chunk<T>(a, chunk < a.nchunks ? chunk : -1, (int)threadIdx.x & 255, s_o);
+  }
+}
+
+hipError_t launch_wgrad_adam(int bf16, const GemmDesc& g0, const EpiParams& e, const AdamArgs& a, hipStream_t s,
+                             const LaunchEv& ev) {
+  if (g0.bm != 64 || g0.bn != 64 || g0.kgroups != 2 || g0.split != 1 || !e.ap) return hipErrorInvalidValue;
+  const GemmDesc g = with_group(g0, 64, 64);
+  const int ntiles = ((g.M + 63) / 64) * ((g.N + 63) / 64);
+  const dim3 grid((unsigned)(ntiles + (a.nchunks + 1) / 2)), block(512);
+  if (bf16)
+    ERASE_LAUNCH((erase_wgrad_adam_kg2<uint16_t, 64, 64>), grid, block, 0, s, ev, g, e, a, ntiles);
+  else
+    ERASE_LAUNCH((erase_wgrad_adam_kg2<float, 64, 64>), grid, block, 0, s, ev, g, e, a, ntiles);
+  return hipGetLastError();
 }
 
 template <typename T>

@@ -31,7 +31,7 @@ DISPATCH_CALLER, DISPATCH_WORKER = 0, 1
 DISPATCH = {"caller": DISPATCH_CALLER, "worker": DISPATCH_WORKER}
 KERNEL_KINDS = {0: "prologue", 1: "fwd_gemm", 2: "head_bce", 3: "wgrad_gemm", 4: "dgrad_gemm", 5: "adam",
                 6: "bwd_gemm", 7: "empty", 8: "fwd_head_gemm", 9: "fwd_gemm_kg2",
-                10: "wgrad_gemm_kg2"}
+                10: "wgrad_gemm_kg2", 11: "wgrad_adam_kg2"}
 
 
 class LayerSpec(ctypes.Structure):
