@@ -2,4 +2,4 @@
 from .erase_oracle import *  # noqa: F401,F403
 from .erase_oracle import total_loss  # noqa: F401
 from . import transformer_oracle  # noqa: F401
-from .embed_oracle import embed_bags  # noqa: F401
+from .embed_oracle import embed_bags, embed_bags_backward  # noqa: F401

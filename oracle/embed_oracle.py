@@ -48,3 +48,24 @@ def embed_bags(dense, offsets, indices, tables):
             # of the bag's multiplicity vector with the table is the same)
             x[m, n_dense + t * dim: n_dense + (t + 1) * dim] = tab[ids].sum(axis=0)
     return x
+
+
+def embed_bags_backward(offsets, indices, dx, n_dense, rows, dim):
+    """Gradient of the tables given the gradient dx [M][>= n_dense + T*dim]
+    at x, in float64:
+
+        grad[t][r] = sum over the entries i of table t with indices[i] == r
+                     of dx[bag(i)][n_dense + t*dim : n_dense + (t+1)*dim]
+
+    where bag(i) is the bag (row of x) entry i belongs to.  The dense
+    features take no table gradient.  Returns [T][rows][dim]."""
+    offsets = np.asarray(offsets, dtype=np.int64)
+    indices = np.asarray(indices, dtype=np.int64)
+    dx = np.asarray(dx, dtype=np.float64)
+    T, M = offsets.shape[0], offsets.shape[1] - 1
+    g = np.zeros((T, rows, dim), dtype=np.float64)
+    for t in range(T):
+        for m in range(M):
+            for i in range(offsets[t, m], offsets[t, m + 1]):
+                g[t, indices[i]] += dx[m, n_dense + t * dim: n_dense + (t + 1) * dim]
+    return g

@@ -97,3 +97,38 @@ def test_generator_pooling_agrees():
     x = oracle.embed_bags(raw["dense"], raw["offsets"], raw["indices"], tabs.tables)
     # 20 terms of |v| <~ 0.05 each: float32 rounding well under 1e-7 absolute
     np.testing.assert_allclose(x32, x, rtol=1e-6, atol=2e-8)
+
+
+def test_backward_matches_torch_embedding_bag_autograd():
+    dense, offsets, indices, tables = _raw(7, rows=30)
+    M, n_dense, dim, T = dense.shape[0], dense.shape[1], tables[0].shape[1], len(tables)
+    rng = np.random.Generator(np.random.PCG64(8))
+    dx = rng.normal(size=(M, n_dense + T * dim + 3))
+    g = oracle.embed_bags_backward(offsets, indices, dx, n_dense, 30, dim)
+    for t, tab in enumerate(tables):
+        w = torch.tensor(tab, dtype=torch.float64, requires_grad=True)
+        o = offsets[t]
+        out = torch.nn.functional.embedding_bag(torch.from_numpy(indices[o[0]:o[-1]]), w,
+                                                torch.from_numpy(o[:-1] - o[0]), mode="sum")
+        out.backward(torch.from_numpy(dx[:, n_dense + t * dim: n_dense + (t + 1) * dim]))
+        np.testing.assert_allclose(g[t], w.grad.numpy(), rtol=1e-13, atol=1e-13)
+
+
+def test_backward_is_the_adjoint_of_the_forward():
+    """<embed_bags(tables), dx> over the pooled columns = <tables, backward(dx)>:
+    the forward is linear in the tables."""
+    dense, offsets, indices, tables = _raw(9, rows=21)
+    M, n_dense, dim, T = dense.shape[0], dense.shape[1], tables[0].shape[1], len(tables)
+    rng = np.random.Generator(np.random.PCG64(10))
+    dx = rng.normal(size=(M, n_dense + T * dim))
+    x = oracle.embed_bags(np.zeros_like(dense), offsets, indices, tables)
+    lhs = float(np.sum(x[:, n_dense:] * dx[:, n_dense:]))
+    g = oracle.embed_bags_backward(offsets, indices, dx, n_dense, 21, dim)
+    rhs = float(sum(np.sum(g[t] * tables[t]) for t in range(T)))
+    assert abs(lhs - rhs) <= 1e-12 * max(1.0, abs(lhs))
+    # rows no bag selects get zero
+    used = {(t, int(r)) for t in range(T) for r in indices[offsets[t, 0]:offsets[t, -1]]}
+    for t in range(T):
+        for r in range(21):
+            if (t, r) not in used:
+                assert np.all(g[t, r] == 0.0)
