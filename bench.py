@@ -372,8 +372,25 @@ def input_stage(args, log, tr, cfg, head, labels, losses):
     el = time.perf_counter() - t0
     tr.set_dispatch("caller")
     assert int(status.item()) == 0
+    # its backward (table gradients from a gradient at x), for the same bags
+    dx = torch.randn((M, tr.ncfg.x_ld), device="cuda").to(tr.act_dtype)
+    d0, o0, ix0 = feats[0]
+    tg = torch.empty((T, tabs.rows, dim), dtype=torch.float32, device="cuda")
+    g_, scratch = erase.embed_bags_backward(o0, ix0, dx, nd, tabs.rows, dim, table_grad=tg, stream=tr.sf)
+    torch.cuda.synchronize()
+    e0.record(tr.sf)
+    nb = 20
+    for _ in range(nb):
+        erase.embed_bags_backward(o0, ix0, dx, nd, tabs.rows, dim, table_grad=tg, stream=tr.sf)
+    e1.record(tr.sf)
+    torch.cuda.synchronize()
+    us_b = e0.elapsed_time(e1) / nb * 1e3
+    # algorithmic bytes: the ids, offsets and bucket bookkeeping, one dx row
+    # slice per entry, and the dense table gradient written once
+    bytes_b = nnz * (4 * 6 + dim * esz) + T * (M + 1) * 8 + T * tabs.rows * (dim * 4 + 16)
     log(f"[bench] input stage: {us:.1f} us per batch, {nbytes / us / 1e3:.0f} GB/s algorithmic; "
-        f"{head} from raw features {M * args.steps / el:.0f} samples/s")
+        f"{head} from raw features {M * args.steps / el:.0f} samples/s; backward {us_b:.0f} us "
+        f"({bytes_b / us_b / 1e3:.0f} GB/s algorithmic)")
     return {"kernel": "erase_embed_bags_k", "workload": f"{M} rows, {T} tables of {tabs.rows} x {dim} float32, "
                                                         f"bags of 1..20 Zipf(1.1) ids (mean nnz {nnz:.0f}), "
                                                         f"{nd} dense features, x in {tr.act_dtype}".replace("torch.", ""),
@@ -383,7 +400,10 @@ def input_stage(args, log, tr, cfg, head, labels, losses):
             "step_from_raw_features": {"schedule": head, "samples_per_s": M * args.steps / el,
                                        "ms_per_step": el / args.steps * 1e3},
             "note": "bytes count every gathered table row once per use; Zipf-skewed ids hit the caches, so HBM "
-                    "traffic is lower than the algorithmic bytes"}
+                    "traffic is lower than the algorithmic bytes",
+            "backward": {"entry": "erase_embed_bags_backward", "avg_us": us_b, "algorithmic_bytes": bytes_b,
+                         "achieved_gbs": bytes_b / us_b / 1e3,
+                         "note": "dense fp32 table gradient [26][100000][64] written in full (666 MB); six launches"}}
 
 
 def _merge(iv):

@@ -313,6 +313,30 @@ erase_status erase_embed_bags(const erase_bag_config* cfg, const float* dense, c
                               const int32_t* indices, const float* tables, void* x, int32_t* status,
                               void* stream);
 
+/* Backward of the embedding-bag stage: the gradient of the tables given the
+ * gradient dx at x (the part of a model the paper leaves to the usual
+ * end-of-step backward, Section 2.2, when it trains its tables from the
+ * gradient every block sends into the shared input; under this library's
+ * detached reading no block sends one):
+ *   table_grad[t][r][d] = sum over the entries i of the bags of table t with
+ *                         indices[i] == r of dx[m(i)][n_dense + t*dim + d]
+ * where m(i) is the bag (row of x) holding entry i.  Each row's entries are
+ * summed in fp32 in increasing entry order, so the result does not depend on
+ * scheduling; rows no entry selects are zero.  Bags must not overlap (each
+ * entry belongs to at most one bag; entries of no bag are ignored).
+ * Device pointers: offsets, indices as for erase_embed_bags; dx [batch][x_ld]
+ * of dtype (16-byte aligned); table_grad fp32 [n_tables][rows][dim]
+ * (16-byte aligned, fully written); scratch of
+ * erase_embed_bags_backward_scratch_bytes() bytes (16-byte aligned, any
+ * contents; the call clears what it needs); status as for erase_embed_bags
+ * (invalid offsets or ids set it to 1).  Six launches on `stream`, no wait.
+ * ERASE_ERR_SHAPE also when n_tables * rows >= 2^31; ERASE_ERR_WORKSPACE for
+ * a missing, misaligned or small scratch. */
+erase_status erase_embed_bags_backward_scratch_bytes(const erase_bag_config* cfg, size_t* bytes);
+erase_status erase_embed_bags_backward(const erase_bag_config* cfg, const int64_t* offsets, const int32_t* indices,
+                                       const void* dx, float* table_grad, void* scratch, size_t scratch_bytes,
+                                       int32_t* status, void* stream);
+
 /* Destroy the context: waits for its dispatch thread and streams, frees
  * events and graphs.  Never frees caller memory.  NULL is accepted. */
 erase_status erase_destroy(void* ctx);

@@ -127,4 +127,152 @@ hipError_t launch_embed_bags(int bf16, const EmbedArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Backward: table gradients from the gradient at x.  Entry i (an index
+// position) belongs to the bag (t, m) whose range holds it; its global row
+// is t * rows + indices[i].  Entries are bucketed by global row with integer
+// counters, and each row's entries are summed in increasing entry order, so
+// the result does not depend on scheduling.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void erase_bags_bwd_clear(EmbedBwdArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < a.trows) {
+    a.count[i] = 0;
+    a.fill[i] = 0;
+  }
+  if (i < a.nnz) a.owner[i] = -1;
+}
+
+// one thread per bag: its entries' owner
+__global__ __launch_bounds__(256) void erase_bags_bwd_owner(EmbedBwdArgs a) {
+  const int64_t bag = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (bag >= (int64_t)a.M * a.T) return;
+  const int t = (int)(bag / a.M), m = (int)(bag % a.M);
+  const int64_t beg = a.offsets[(int64_t)t * (a.M + 1) + m], end = a.offsets[(int64_t)t * (a.M + 1) + m + 1];
+  if (!(beg >= 0 && beg <= end && end <= a.nnz)) {
+    if (a.status) a.status[0] = 1;
+    return;
+  }
+  for (int64_t i = beg; i < end; ++i) a.owner[i] = (int32_t)bag;
+}
+
+// one thread per entry: global row and its count
+__global__ __launch_bounds__(256) void erase_bags_bwd_count(EmbedBwdArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= a.nnz) return;
+  const int32_t o = a.owner[i];
+  int32_t gid = -1;
+  if (o >= 0) {
+    const int32_t r = a.indices[i];
+    if (r >= 0 && r < a.rows) {
+      gid = (int32_t)((o / a.M) * a.rows + r);
+      atomicAdd(&a.count[gid], 1);
+    } else if (a.status) {
+      a.status[0] = 1;
+    }
+  }
+  a.gid[i] = gid;
+}
+
+// exclusive prefix sum of the counts (one workgroup of 1024 threads)
+__global__ __launch_bounds__(1024) void erase_bags_bwd_scan(EmbedBwdArgs a) {
+  __shared__ int part[1024];
+  const int tid = threadIdx.x;
+  const int64_t per = (a.trows + 1023) / 1024;
+  const int64_t lo = tid * per, hi = lo + per < a.trows ? lo + per : a.trows;
+  int s = 0;
+  for (int64_t v = lo; v < hi; ++v) s += a.count[v];
+  part[tid] = s;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int x = tid >= off ? part[tid - off] : 0;
+    __syncthreads();
+    part[tid] += x;
+    __syncthreads();
+  }
+  int run = part[tid] - s;
+  for (int64_t v = lo; v < hi; ++v) {
+    a.start[v] = run;
+    run += a.count[v];
+  }
+}
+
+__global__ __launch_bounds__(256) void erase_bags_bwd_scatter(EmbedBwdArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= a.nnz) return;
+  const int32_t gid = a.gid[i];
+  if (gid >= 0) a.bucket[a.start[gid] + atomicAdd(&a.fill[gid], 1)] = (int32_t)i;
+}
+
+// one wave per table row: the row's entries in increasing order (each step
+// the smallest entry above the last, a wave-wide minimum), their bags' dx
+// columns summed in fp32; rows no entry selects are zero.  dim / 4 lanes
+// (dim <= 256) own 4 columns each.
+template <typename T>
+__global__ __launch_bounds__(256) void erase_bags_bwd_rows(EmbedBwdArgs a) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t g = (int64_t)blockIdx.x * 4 + wave;
+  if (g >= a.trows) return;
+  const int t = (int)(g / a.rows);
+  const int s0 = a.start[g], c = a.count[g];
+  const int32_t mine = lane < c ? a.bucket[s0 + lane] : INT32_MAX;
+  const bool col = 4 * lane < a.dim;
+  const int64_t xc = a.n_dense + (int64_t)t * a.dim + 4 * lane;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  int32_t prev = -1;
+  for (int k = 0; k < c; ++k) {
+    int32_t cand = INT32_MAX;
+    if (c <= 64) {
+      if (mine > prev) cand = mine;
+    } else {
+      for (int j = lane; j < c; j += 64) {
+        const int32_t p = a.bucket[s0 + j];
+        if (p > prev && p < cand) cand = p;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) cand = min(cand, __shfl_xor(cand, o, 64));
+    prev = cand;
+    if (col) {
+      const int m = a.owner[cand] % a.M;
+      const T* src = static_cast<const T*>(a.dx) + (int64_t)m * a.lddx + xc;
+      if constexpr (sizeof(T) == 2) {
+        const u32x2s_t w = *reinterpret_cast<const u32x2s_t*>(src);
+        acc.x += __uint_as_float(w.x << 16);
+        acc.y += __uint_as_float(w.x & 0xffff0000u);
+        acc.z += __uint_as_float(w.y << 16);
+        acc.w += __uint_as_float(w.y & 0xffff0000u);
+      } else {
+        const f32x4s_t v = *reinterpret_cast<const f32x4s_t*>(src);
+        acc.x += v[0];
+        acc.y += v[1];
+        acc.z += v[2];
+        acc.w += v[3];
+      }
+    }
+  }
+  if (col) *reinterpret_cast<float4*>(a.grad + g * a.dim + 4 * lane) = acc;
+}
+
+hipError_t launch_embed_bags_backward(int bf16, const EmbedBwdArgs& a, hipStream_t s) {
+  if (a.dim % 4 || a.dim > 256 || a.trows <= 0) return hipErrorInvalidValue;
+  const int64_t nmax = a.trows > a.nnz ? a.trows : a.nnz;
+  hipLaunchKernelGGL(erase_bags_bwd_clear, dim3((unsigned)((nmax + 255) / 256)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(erase_bags_bwd_owner, dim3((unsigned)(((int64_t)a.M * a.T + 255) / 256)), dim3(256), 0, s, a);
+  if (a.nnz > 0) {
+    const dim3 ge((unsigned)((a.nnz + 255) / 256));
+    hipLaunchKernelGGL(erase_bags_bwd_count, ge, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(erase_bags_bwd_scan, dim3(1), dim3(1024), 0, s, a);
+    hipLaunchKernelGGL(erase_bags_bwd_scatter, ge, dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL(erase_bags_bwd_scan, dim3(1), dim3(1024), 0, s, a);
+  }
+  const dim3 gr((unsigned)((a.trows + 3) / 4));
+  if (bf16)
+    hipLaunchKernelGGL(erase_bags_bwd_rows<uint16_t>, gr, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(erase_bags_bwd_rows<float>, gr, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 }  // namespace erase

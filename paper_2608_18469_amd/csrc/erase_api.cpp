@@ -1549,6 +1549,64 @@ erase_status erase_embed_bags(const erase_bag_config* cfg, const float* dense, c
   return ERASE_OK;
 }
 
+erase_status erase_embed_bags_backward_scratch_bytes(const erase_bag_config* cfg, size_t* bytes) {
+  if (!cfg || !bytes) return ERASE_ERR_INVALID_ARG;
+  const erase_bag_config& b = *cfg;
+  if (b.n_tables < 1 || b.rows < 1 || b.nnz < 0 || int64_t(b.n_tables) * b.rows >= (int64_t(1) << 31) ||
+      b.nnz >= (int64_t(1) << 31))
+    return ERASE_ERR_SHAPE;
+  const int64_t tr = int64_t(b.n_tables) * b.rows;
+  *bytes = size_t(4) * size_t(3 * roundup(tr, 64) + 3 * roundup(std::max<int64_t>(b.nnz, 1), 64));
+  return ERASE_OK;
+}
+
+erase_status erase_embed_bags_backward(const erase_bag_config* cfg, const int64_t* offsets, const int32_t* indices,
+                                       const void* dx, float* table_grad, void* scratch, size_t scratch_bytes,
+                                       int32_t* status, void* stream) {
+  if (!cfg) return ERASE_ERR_INVALID_ARG;
+  const erase_bag_config& b = *cfg;
+  if (b.dtype != ERASE_F32 && b.dtype != ERASE_BF16) return ERASE_ERR_INVALID_ARG;
+  const int esz = b.dtype == ERASE_BF16 ? 2 : 4;
+  if (b.batch < 1 || b.batch > kMaxBatch || b.n_dense < 0 || b.n_dense > 4096 || b.n_tables < 1 ||
+      b.n_tables > 4096 || int64_t(b.n_tables) * b.batch >= (int64_t(1) << 31) || b.dim < 4 || b.dim > 256 ||
+      b.dim % 4 || b.rows < 1 || int64_t(b.n_tables) * b.rows >= (int64_t(1) << 31) || b.nnz < 0 ||
+      b.nnz >= (int64_t(1) << 31) || b.x_ld < int64_t(b.n_dense) + int64_t(b.n_tables) * b.dim ||
+      (b.x_ld * esz) % 16)
+    return ERASE_ERR_SHAPE;
+  size_t need = 0;
+  (void)erase_embed_bags_backward_scratch_bytes(cfg, &need);
+  auto mis = [](const void* p, uintptr_t a) { return reinterpret_cast<uintptr_t>(p) % a != 0; };
+  if (!offsets || mis(offsets, 8) || (b.nnz > 0 && (!indices || mis(indices, 4))) || !dx || mis(dx, 16) ||
+      !table_grad || mis(table_grad, 16) || (status && mis(status, 4)))
+    return ERASE_ERR_INVALID_ARG;
+  if (!scratch || mis(scratch, 16) || scratch_bytes < need) return ERASE_ERR_WORKSPACE;
+  const int64_t tr = int64_t(b.n_tables) * b.rows, trr = roundup(tr, 64), nr = roundup(std::max<int64_t>(b.nnz, 1), 64);
+  int32_t* w = static_cast<int32_t*>(scratch);
+  EmbedBwdArgs a{};
+  a.offsets = offsets;
+  a.indices = indices;
+  a.dx = dx;
+  a.lddx = b.x_ld;
+  a.grad = table_grad;
+  a.count = w;
+  a.start = w + trr;
+  a.fill = w + 2 * trr;
+  a.bucket = w + 3 * trr;
+  a.gid = w + 3 * trr + nr;
+  a.owner = w + 3 * trr + 2 * nr;
+  a.status = status;
+  a.nnz = b.nnz;
+  a.trows = tr;
+  a.rows = (int)b.rows;
+  a.M = b.batch;
+  a.n_dense = b.n_dense;
+  a.T = b.n_tables;
+  a.dim = b.dim;
+  if (launch_embed_bags_backward(b.dtype == ERASE_BF16, a, static_cast<hipStream_t>(stream)) != hipSuccess)
+    return ERASE_ERR_HIP;
+  return ERASE_OK;
+}
+
 erase_status erase_destroy(void* ctx) {
   Ctx* c = as_ctx(ctx);
   if (!c) return ERASE_OK;

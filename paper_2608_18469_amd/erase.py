@@ -82,6 +82,9 @@ SIGNATURES = {
     "erase_set_dispatch": (c_int32, [c_void_p, c_int32]),
     "erase_embed_bags": (c_int32, [POINTER(BagConfig), c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                    c_void_p]),
+    "erase_embed_bags_backward_scratch_bytes": (c_int32, [POINTER(BagConfig), POINTER(c_size_t)]),
+    "erase_embed_bags_backward": (c_int32, [POINTER(BagConfig), c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                            c_size_t, c_void_p, c_void_p]),
     "erase_read_timing": (c_int32, [c_void_p, POINTER(KernelTime), c_int32, POINTER(c_int32)]),
     "erase_destroy": (c_int32, [c_void_p]),
     "erase_status_str": (ctypes.c_char_p, [c_int32]),
@@ -214,6 +217,36 @@ def embed_bags(dense, offsets, indices, tables, x, status=None, stream=None):
     ptr = (lambda t: None if t is None or t.numel() == 0 else t.data_ptr())
     _check(lib().erase_embed_bags(ctypes.byref(cfg), ptr(dense), offsets.data_ptr(), ptr(indices),
                                   tables.data_ptr(), x.data_ptr(), ptr(status), s), "erase_embed_bags")
+
+
+def embed_bags_backward(offsets, indices, dx, n_dense, rows, dim, table_grad=None, status=None, stream=None):
+    """Backward of the embedding-bag stage (erase_embed_bags_backward) on device
+    tensors: offsets int64 [T][M+1], indices int32 [nnz], dx [M][x_ld] float32
+    or bfloat16 (the gradient at x), n_dense, rows, dim as in the forward.
+    Returns table_grad fp32 [T][rows][dim] (allocated unless given) and
+    allocates the scratch; enqueued on `stream` (default: the current one)."""
+    import torch
+    T = offsets.shape[0]
+    M, x_ld = dx.shape
+    for name, t, dt in (("offsets", offsets, torch.int64), ("indices", indices, torch.int32)):
+        if t.dtype != dt or not t.is_contiguous():
+            raise EraseError(ERR_INVALID_ARG, "embed_bags_backward", f"{name} must be a contiguous {dt} tensor")
+    if dx.dtype not in (torch.float32, torch.bfloat16) or dx.stride(1) != 1:
+        raise EraseError(ERR_INVALID_ARG, "embed_bags_backward", "dx must be float32 or bfloat16, unit column stride")
+    cfg = BagConfig(M, n_dense, T, dim, rows, indices.numel(), BF16 if dx.dtype == torch.bfloat16 else F32,
+                    dx.stride(0))
+    need = c_size_t(0)
+    _check(lib().erase_embed_bags_backward_scratch_bytes(ctypes.byref(cfg), ctypes.byref(need)),
+           "erase_embed_bags_backward_scratch_bytes")
+    scratch = torch.empty(need.value, dtype=torch.uint8, device=dx.device)
+    if table_grad is None:
+        table_grad = torch.empty((T, rows, dim), dtype=torch.float32, device=dx.device)
+    s = (stream or torch.cuda.current_stream()).cuda_stream
+    ptr = (lambda t: None if t is None or t.numel() == 0 else t.data_ptr())
+    _check(lib().erase_embed_bags_backward(ctypes.byref(cfg), offsets.data_ptr(), ptr(indices), dx.data_ptr(),
+                                           table_grad.data_ptr(), scratch.data_ptr(), need.value, ptr(status), s),
+           "erase_embed_bags_backward")
+    return table_grad, scratch
 
 
 class Trainer:

@@ -183,3 +183,39 @@ def test_embed_bags_validation():
     for bad in (dict(dense=None), dict(offsets=None), dict(offsets=516), dict(indices=None), dict(indices=770),
                 dict(tables=None), dict(tables=1032), dict(x=None), dict(x=2056), dict(status=258)):
         assert call(**bad) == erase.ERR_INVALID_ARG, bad
+
+
+def test_embed_bags_backward_validation():
+    """erase_embed_bags_backward: shape, pointer, alignment and scratch checks
+    on the host before anything is enqueued (fake pointers never dereferenced)."""
+    L = erase.lib()
+    good = dict(batch=8, n_dense=13, n_tables=2, dim=64, rows=100, nnz=10, dtype=erase.F32, x_ld=144)
+
+    def cfg_of(c):
+        return erase.BagConfig(c["batch"], c["n_dense"], c["n_tables"], c["dim"], c["rows"], c["nnz"], c["dtype"],
+                               c["x_ld"])
+
+    need = ctypes.c_size_t(0)
+    gc = cfg_of(good)
+    assert L.erase_embed_bags_backward_scratch_bytes(ctypes.byref(gc), ctypes.byref(need)) == erase.OK
+    # count, start, fill per table row, bucket, row id, owner per entry (int32, padded to 64)
+    assert need.value == 4 * (3 * 256 + 3 * 64)
+
+    def call(cfg=None, **ptrs):
+        c = dict(good)
+        c.update(cfg or {})
+        bc = cfg_of(c)
+        p = dict(offsets=512, indices=768, dx=2048, grad=4096, scratch=8192, nbytes=need.value, status=None)
+        p.update(ptrs)
+        return L.erase_embed_bags_backward(ctypes.byref(bc), p["offsets"], p["indices"], p["dx"], p["grad"],
+                                           p["scratch"], p["nbytes"], p["status"], None)
+
+    assert L.erase_embed_bags_backward(None, None, None, None, None, None, 0, None, None) == erase.ERR_INVALID_ARG
+    for bad in ({"batch": 0}, {"n_tables": 0}, {"dim": 6}, {"dim": 260}, {"rows": 0}, {"nnz": -1}, {"x_ld": 140},
+                {"rows": 1 << 30, "n_tables": 2}):
+        assert call(bad) == erase.ERR_SHAPE, bad
+    for bad in (dict(offsets=None), dict(offsets=516), dict(indices=None), dict(dx=None), dict(dx=2056),
+                dict(grad=None), dict(grad=4100), dict(status=258)):
+        assert call(**bad) == erase.ERR_INVALID_ARG, bad
+    for bad in (dict(scratch=None), dict(scratch=8200), dict(nbytes=need.value - 4)):
+        assert call(**bad) == erase.ERR_WORKSPACE, bad

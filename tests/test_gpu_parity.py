@@ -429,6 +429,102 @@ def test_embed_bags_invalid_entries_flagged():
             assert np.array_equal(x[m, :194], good_x[m, :194])
 
 
+def _run_bags_bwd(offsets, indices, dx, n_dense, rows, dim, dtype):
+    import torch
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    g = torch.full((offsets.shape[0], rows, dim), float("nan"), dtype=torch.float32, device="cuda")
+    erase.embed_bags_backward(torch.from_numpy(offsets).cuda(), torch.from_numpy(indices).cuda(),
+                              torch.from_numpy(dx).cuda().to(tdt), n_dense, rows, dim, table_grad=g, status=status)
+    torch.cuda.synchronize()
+    return g.cpu().numpy(), int(status.item())
+
+
+@pytest.mark.parametrize("dtype,dim,n_dense,M,T,rows,max_len", [("f32", 64, 13, 37, 5, 40, 7), ("bf16", 64, 13, 37, 5, 40, 7),
+                                                                ("f32", 4, 0, 5, 3, 9, 3), ("f32", 256, 1, 9, 2, 300, 7),
+                                                                ("bf16", 12, 3, 64, 2, 5, 90)])
+def test_embed_bags_backward_vs_oracle(dtype, dim, n_dense, M, T, rows, max_len):
+    """Table gradients against the float64 oracle: empty bags, rows selected
+    by no bag (zero), and with 5 rows and bags of up to 90 ids, rows selected
+    by well over 64 entries (the ordering path for long buckets); bit-identical
+    on a second run."""
+    _say(f"case: embed_bags_backward {dtype} dim={dim} M={M} T={T} rows={rows}")
+    _, offsets, indices, _ = _bags(M * 17 + dim, M, T, rows, dim, n_dense, max_len)
+    rng = np.random.Generator(np.random.PCG64(M + dim))
+    x_ld = (n_dense + T * dim + 7) // 8 * 8
+    dx = rng.normal(size=(M, x_ld)).astype(np.float32)
+    if dtype == "bf16":
+        dx = synth.round_to_bf16_values(dx)
+    g, st = _run_bags_bwd(offsets, indices, dx, n_dense, rows, dim, dtype)
+    assert st == 0
+    ref = oracle.embed_bags_backward(offsets, indices, dx.astype(np.float64), n_dense, rows, dim)
+    mag = oracle.embed_bags_backward(offsets, indices, np.abs(dx.astype(np.float64)), n_dense, rows, dim)
+    # fp32 sums of the same bf16/fp32 inputs: a few ulp of the sum of magnitudes
+    assert np.all(np.abs(g - ref) <= 1e-6 * mag + 1e-30)
+    used = {(t, int(r)) for t in range(T) for r in indices[offsets[t, 0]:offsets[t, -1]]}
+    for t in range(T):
+        for r in range(rows):
+            if (t, r) not in used:
+                assert np.all(g[t, r] == 0.0)
+    g2, _ = _run_bags_bwd(offsets, indices, dx, n_dense, rows, dim, dtype)
+    assert np.array_equal(g.view(np.uint32), g2.view(np.uint32))
+
+
+def test_embed_bags_backward_full_ctr_shape():
+    """The CTR input stage's backward at full size (4096 rows, 26 tables of
+    100000 x 64, Zipf(1.1) bags of 1..20 ids) with a bf16 dx: sampled rows
+    against their sums written out from the data, total mass per table, and
+    a bit-identical second run."""
+    _say("case: embed_bags_backward full CTR shape")
+    rng = np.random.Generator(np.random.PCG64(1))
+    tabs = synth.CtrTables(rng)
+    raw = synth.make_ctr_raw(tabs, 4096, rng)
+    offsets, indices = raw["offsets"], raw["indices"]
+    dx = synth.round_to_bf16_values(rng.normal(size=(4096, 1680)).astype(np.float32))
+    g, st = _run_bags_bwd(offsets, indices, dx, 13, synth.CTR_ROWS, 64, "bf16")
+    assert st == 0
+    T = offsets.shape[0]
+    bag_of = np.empty(int(offsets[-1, -1]), dtype=np.int64)
+    for t in range(T):
+        for m in range(4096):
+            bag_of[offsets[t, m]:offsets[t, m + 1]] = m
+    pick = np.random.Generator(np.random.PCG64(2))
+    for _ in range(40):
+        t = int(pick.integers(0, T))
+        seg = indices[offsets[t, 0]:offsets[t, -1]]
+        r = int(seg[pick.integers(0, seg.size)])            # a row some entry selects
+        ent = np.nonzero(seg == r)[0] + offsets[t, 0]
+        want = dx[bag_of[ent]][:, 13 + 64 * t: 13 + 64 * (t + 1)].astype(np.float64).sum(axis=0)
+        mag = np.abs(dx[bag_of[ent]][:, 13 + 64 * t: 13 + 64 * (t + 1)].astype(np.float64)).sum(axis=0)
+        assert np.all(np.abs(g[t, r] - want) <= 1e-6 * mag + 1e-30), (t, r)
+    for t in range(T):
+        lens = np.diff(offsets[t]).astype(np.float64)
+        want = (lens[:, None] * dx[:, 13 + 64 * t: 13 + 64 * (t + 1)].astype(np.float64)).sum(axis=0)
+        np.testing.assert_allclose(g[t].astype(np.float64).sum(axis=0), want, rtol=1e-4, atol=1e-2)
+    g2, _ = _run_bags_bwd(offsets, indices, dx, 13, synth.CTR_ROWS, 64, "bf16")
+    assert np.array_equal(g.view(np.uint32), g2.view(np.uint32))
+
+
+def test_embed_bags_backward_invalid_entries_flagged():
+    """Out-of-range ids and bag bounds are skipped and set the status word;
+    the rows of every other entry are exact."""
+    _say("case: embed_bags_backward invalid entries")
+    _, offsets, indices, _ = _bags(43, 16, 3, 50, 64, 2, 5, allow_empty=False)
+    rng = np.random.Generator(np.random.PCG64(44))
+    dx = rng.normal(size=(16, 200)).astype(np.float32)
+    bad_idx = indices.copy()
+    bad_idx[offsets[1, 3]] = 50
+    bad_idx[offsets[2, 7]] = -1
+    g, st = _run_bags_bwd(offsets, bad_idx, dx, 2, 50, 64, "f32")
+    assert st == 1
+    keep = np.ones(indices.size, dtype=bool)
+    keep[[offsets[1, 3], offsets[2, 7]]] = False
+    # the oracle with the two invalid entries pointed at a scratch row past the table
+    idx2 = np.where(keep, indices, 50)
+    ref = oracle.embed_bags_backward(offsets, idx2, dx.astype(np.float64), 2, 51, 64)[:, :50]
+    np.testing.assert_allclose(g, ref, rtol=1e-6, atol=1e-6)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_zero_lambda_block_is_frozen(dtype):
     """lambda_b = 0 (Eq. 2): the block's gradient is exactly zero, so Adam
