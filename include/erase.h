@@ -321,8 +321,12 @@ erase_status erase_embed_bags(const erase_bag_config* cfg, const float* dense, c
  *   table_grad[t][r][d] = sum over the entries i of the bags of table t with
  *                         indices[i] == r of dx[m(i)][n_dense + t*dim + d]
  * where m(i) is the bag (row of x) holding entry i.  Each row's entries are
- * summed in fp32 in increasing entry order, so the result does not depend on
- * scheduling; rows no entry selects are zero.  Bags must not overlap (each
+ * summed in fp32 in a fixed order: in increasing entry order for rows of at
+ * most 64 entries; rows of 65..16384 entries are sorted by entry, summed by
+ * dim-wide lane groups that each take every (256/dim)-th entry in order, and
+ * the groups added by a fixed butterfly; larger rows in increasing entry
+ * order (by repeated selection: correct but slow).  The result does not
+ * depend on scheduling; rows no entry selects are zero.  Bags must not overlap (each
  * entry belongs to at most one bag; entries of no bag are ignored).
  * Device pointers: offsets, indices as for erase_embed_bags; dx [batch][x_ld]
  * of dtype (16-byte aligned); table_grad fp32 [n_tables][rows][dim]

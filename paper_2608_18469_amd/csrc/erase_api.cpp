@@ -1556,7 +1556,8 @@ erase_status erase_embed_bags_backward_scratch_bytes(const erase_bag_config* cfg
       b.nnz >= (int64_t(1) << 31))
     return ERASE_ERR_SHAPE;
   const int64_t tr = int64_t(b.n_tables) * b.rows;
-  *bytes = size_t(4) * size_t(3 * roundup(tr, 64) + 3 * roundup(std::max<int64_t>(b.nnz, 1), 64));
+  const int64_t nr = roundup(std::max<int64_t>(b.nnz, 1), 64);
+  *bytes = size_t(4) * size_t(3 * roundup(tr, 64) + 5 * nr + 64 + roundup(tr / 4096 + 1, 64));
   return ERASE_OK;
 }
 
@@ -1594,6 +1595,10 @@ erase_status erase_embed_bags_backward(const erase_bag_config* cfg, const int64_
   a.bucket = w + 3 * trr;
   a.gid = w + 3 * trr + nr;
   a.owner = w + 3 * trr + 2 * nr;
+  a.large = w + 3 * trr + 3 * nr;
+  a.nlarge = w + 3 * trr + 4 * nr;
+  a.bsum = w + 3 * trr + 4 * nr + 64;
+  a.bagm = a.bsum + roundup(tr / 4096 + 1, 64);
   a.status = status;
   a.nnz = b.nnz;
   a.trows = tr;

@@ -221,13 +221,15 @@ hipError_t launch_embed_bags(int bf16, const EmbedArgs& a, hipStream_t s);
 // i of table t's bags with indices[i] == r of dx[bag m][n_dense + t dim + d],
 // entries in increasing order; rows no entry selects are zero.  Bags must
 // not overlap.  Scratch (all int32): count, start, fill [trows], bucket,
-// gid, owner [nnz].  Invalid offsets or ids set status[0] = 1 (nullable).
+// gid, owner, bagm [nnz], large [nnz / 65 + 1], nlarge [1], bsum [trows / 4096 + 1].
+// Invalid offsets or ids set status[0] = 1 (nullable).
 struct EmbedBwdArgs {
   const int64_t* offsets;  // [T][M+1]
   const int32_t* indices;  // [nnz]
   const void* dx; int64_t lddx;  // [M][lddx] of the activation dtype
   float* grad;             // [T][rows][dim]
   int32_t* count; int32_t* start; int32_t* fill; int32_t* bucket; int32_t* gid; int32_t* owner;
+  int32_t* large; int32_t* nlarge; int32_t* bsum; int32_t* bagm;
   int* status;
   int64_t nnz, trows;      // trows = T * rows < 2^31
   int rows, M, n_dense, T, dim;

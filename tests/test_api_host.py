@@ -198,8 +198,10 @@ def test_embed_bags_backward_validation():
     need = ctypes.c_size_t(0)
     gc = cfg_of(good)
     assert L.erase_embed_bags_backward_scratch_bytes(ctypes.byref(gc), ctypes.byref(need)) == erase.OK
-    # count, start, fill per table row, bucket, row id, owner per entry (int32, padded to 64)
-    assert need.value == 4 * (3 * 256 + 3 * 64)
+    # count, start, fill per table row; bucket, row id, owner, large-bucket
+    # list, bag of each sorted entry per entry (int32, padded to 64); the
+    # list's counter; one scan total per 4096 rows
+    assert need.value == 4 * (3 * 256 + 5 * 64 + 64 + 64)
 
     def call(cfg=None, **ptrs):
         c = dict(good)
