@@ -57,17 +57,64 @@ def kernel_class(r, bf16=True):
     return f"{KIND_SYMBOL[r['kind']]}<{t}>"
 
 
-def kernel_source_hash():
-    """Hash of the kernel sources and build flags: byte counters taken from
-    other sources are stale."""
+TF_SOURCES = ("csrc/transformer.hip", "csrc/tf_api.cpp")
+
+
+def kernel_source_hash(extra=()):
+    """Hash of the kernel sources and build flags: counters taken from other
+    sources are stale.  The transformer's figures also hash its own kernels
+    and launch plan (`extra`)."""
     h = hashlib.sha256()
-    for f in ("csrc/kernels.hip", "csrc/embed.hip", "csrc/internal.h", "build.py"):
+    for f in ("csrc/kernels.hip", "csrc/embed.hip", "csrc/internal.h", "build.py") + tuple(extra):
         with open(os.path.join(ROOT, "paper_2608_18469_amd", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ctr_mlp_hbm_traffic.md")
+MFMA_FILE = os.path.join(ROOT, "profiles", "mfma_busy_counters.md")
+
+
+def mfma_kind(kind):
+    """Kernel kinds whose launches run MFMA work (the GEMMs, and the first
+    layer's weight gradient with the block's Adam in the same launch)."""
+    return "gemm" in kind or kind == "wgrad_adam_kg2"
+
+
+def roofline_of(flops, nbytes, dur_s, peak_mfma):
+    """Roofline of one launch: the bound is the resource with the larger
+    minimum time (flops at the MFMA peak against bytes at the HBM peak)."""
+    t_mfma = flops / (peak_mfma * 1e12)
+    t_hbm = nbytes / (PEAK_HBM_GBS * 1e9)
+    if flops and t_mfma >= t_hbm:
+        r = {"bound": "mfma", "achieved": flops / dur_s / 1e12, "peak": peak_mfma, "unit": "TFLOP/s"}
+    else:
+        r = {"bound": "hbm", "achieved": nbytes / dur_s / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    r["frac"] = r["achieved"] / r["peak"]
+    return r
+
+
+def measured_mfma_busy(workload):
+    """Counter-based MFMA utilisation over every MFMA launch of `workload`,
+    from the committed summary of a rocprofv3 pass with
+    SQ_VALU_MFMA_BUSY_CYCLES and GRBM_GUI_ACTIVE: busy SIMD cycles over
+    (active cycles per XCD x 1024 SIMDs).  None when there is no summary or
+    the kernels changed since it was taken."""
+    try:
+        with open(MFMA_FILE) as f:
+            lines = f.read().splitlines()
+    except OSError:
+        return None
+    src = kernel_source_hash(TF_SOURCES if workload.startswith("tf_") else ())
+    for line in lines:
+        parts = line.split()
+        if len(parts) == 6 and parts[0] == "mfma_busy" and parts[1] == workload:
+            if parts[2] != src:
+                return None
+            busy, simd_cycles, n = float(parts[3]), float(parts[4]), int(parts[5])
+            return {"util": busy / simd_cycles, "busy_simd_cycles": busy, "active_simd_cycles": simd_cycles,
+                    "dispatches": n, "source": src}
+    return None
 
 
 def measured_traffic(kernel_class, workload):
@@ -524,7 +571,10 @@ def transformer_section(args, log):
         "steps": args.tf_steps, "warmup": args.tf_warmup,
         "flops_per_step": fl["total"],
         "mfma_util": {"gemm_kernels": gemm_util,
-                      "whole_step": fl["total"] / (res[best]["ms_per_step"] / 1e3) / 1e12 / PEAK_BF16_TFLOPS},
+                      "whole_step": fl["total"] / (res[best]["ms_per_step"] / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
+                      "counter_busy": (measured_mfma_busy("tf_c5") or {}).get("util"),
+                      "counter_busy_detail": measured_mfma_busy("tf_c5") or
+                      f"null: no MFMA busy counters of the current kernels ({kernel_source_hash(TF_SOURCES)})"},
         "bwd_fwd_overlap_fraction": ovl_all,
         "attention_bwd_overlap_fraction": float(np.mean([x for x in ovl_att if x is not None])) if any(
             x is not None for x in ovl_att) else None,
@@ -627,17 +677,11 @@ def main():
     nsteps = len(recs_all)
     ovl = float(np.mean([overlap_fraction(r) for r in recs_ovl]))
     dom_name, dom = max(classes.items(), key=lambda kv: kv[1]["ms"])
-    gemm_ms = sum(c["ms"] for c in classes.values() if c["kind"].find("gemm") >= 0)
-    gemm_flops = sum(c["flops"] for c in classes.values() if c["kind"].find("gemm") >= 0)
+    gemm_ms = sum(c["ms"] for c in classes.values() if mfma_kind(c["kind"]))
+    gemm_flops = sum(c["flops"] for c in classes.values() if mfma_kind(c["kind"]))
     peak_mfma = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
     avg_dur_s = dom["ms"] / dom["n"] / 1e3
-    if dom["kind"].find("gemm") >= 0:
-        achieved = dom["flops"] / dom["n"] / avg_dur_s / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": peak_mfma, "unit": "TFLOP/s"}
-    else:
-        achieved = dom["bytes"] / dom["n"] / avg_dur_s / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
-    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof = roofline_of(dom["flops"] / dom["n"], dom["bytes"] / dom["n"], avg_dur_s, peak_mfma)
     tr_meas = measured_traffic(dom_name, args.workload)
     roof["traffic"] = tr_meas["bytes"] if tr_meas else None  # HBM bytes per launch, counters
     roof["traffic_detail"] = tr_meas if tr_meas else f"null: no byte counters of the current kernels ({kernel_source_hash()})"
@@ -647,7 +691,7 @@ def main():
     roof["launches_per_step"] = dom["n"] / nsteps
     kernels = {k: {"avg_us": v["ms"] / v["n"] * 1e3, "launches_per_step": v["n"] / nsteps,
                    "us_per_step": v["ms"] / nsteps * 1e3,
-                   "tflops": (v["flops"] / (v["ms"] / 1e3) / 1e12) if v["kind"].find("gemm") >= 0 else None,
+                   "tflops": (v["flops"] / (v["ms"] / 1e3) / 1e12) if mfma_kind(v["kind"]) else None,
                    "gbs": v["bytes"] / (v["ms"] / 1e3) / 1e9}
                for k, v in sorted(classes.items(), key=lambda kv: -kv[1]["ms"])}
 
@@ -688,7 +732,10 @@ def main():
                                         if any(k in res for k in ("serial", "serial_graph")) else None)},
         "schedules": res,
         "mfma_util": {"gemm_kernels": gemm_flops / (gemm_ms / 1e3) / 1e12 / peak_mfma if gemm_ms else None,
-                      "whole_step": flops_step / (res[head]["ms_per_step"] / 1e3) / 1e12 / peak_mfma},
+                      "whole_step": flops_step / (res[head]["ms_per_step"] / 1e3) / 1e12 / peak_mfma,
+                      "counter_busy": (measured_mfma_busy(args.workload) or {}).get("util"),
+                      "counter_busy_detail": measured_mfma_busy(args.workload) or
+                      f"null: no MFMA busy counters of the current kernels ({kernel_source_hash()})"},
         "bwd_fwd_overlap_fraction": ovl,
         "kernel_timing": "per-kernel figures from a SERIAL pass (kernels alone), HIP events stamped at each "
                          "kernel's own start and end; overlap fraction from an OVERLAP pass",
