@@ -241,9 +241,7 @@ struct GemmSmem {
   // fused head: hw[BN], labels[BM], ds[BM], loss[BM], dw[2][BN], c (fp32),
   // past both the main-loop stages and the output tile
   static constexpr int HOFF = MAIN > TILE ? MAIN : TILE;
-  // logits: per wave column half, per row, (max, sum) pairs
-  static constexpr int BYTES = HOFF + (KIND == GK_FWD_HEAD ? (3 * BN + 3 * BM + 4) * 4
-                                       : KIND == GK_FWD_LOGITS ? 2 * BM * 2 * 4 : 0);
+  static constexpr int BYTES = HOFF + (KIND == GK_FWD_HEAD ? (3 * BN + 3 * BM + 4) * 4 : 0);
 };
 
 // KG k-groups of four waves (256 * KG threads): every k-group owns the whole
@@ -719,43 +717,43 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   }
 
   if constexpr (KIND == GK_FWD_LOGITS) {
-    // Row statistics of this tile's columns from the stored (rounded)
-    // values: every lane reduces its row over its TN columns, then the 16
-    // lanes sharing the row, then the two waves of a row half through LDS,
-    // all in a fixed order.
-    float* st = reinterpret_cast<float*>(smem + GemmSmem<T, BM, BN, KIND, BKX>::HOFF);  // [2][BM][2]
+    // Row statistics of this tile's columns from the stored (rounded) values
+    // in the LDS tile: NT / BM threads per row, each over a contiguous run
+    // of columns (16-byte LDS reads), then the row's threads combined by
+    // lane exchanges, in a fixed order.  The sums use exp2 of
+    // (x - max) log2(e).
+    constexpr int TPR = NT / BM, CPT = BN / TPR;  // threads per row, columns per thread
+    static_assert(TPR == 2 || TPR == 4, "logits statistics: 2 or 4 threads per row");
+    static_assert(CPT % 8 == 0, "logits statistics: whole 16-byte chunks per thread");
+    const int r = tid / TPR, c0 = (tid % TPR) * CPT;
+    const int nv = min(CPT, max(0, N - (n0 + c0)));  // valid columns of this thread
+    float x[CPT];
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int k = 0; k < CPT; k += 8) {
+      const u32x4_t w = *reinterpret_cast<const u32x4_t*>(&sc[r * OPITCH + c0 + k]);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int ml = wm * WM + i * 16 + (lane >> 4) * 4 + q;
-        float mx = -INFINITY;
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          if (n0 + wn * WN + j * 16 + (lane & 15) < N) mx = fmaxf(mx, acc[i][j][q]);
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-        float se = 0.f;
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          if (n0 + wn * WN + j * 16 + (lane & 15) < N) se += __expf(acc[i][j][q] - mx);
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) se += __shfl_xor(se, o, 64);
-        if ((lane & 15) == 0) {
-          st[(wn * BM + ml) * 2] = mx;
-          st[(wn * BM + ml) * 2 + 1] = se;
-        }
+      for (int h = 0; h < 4; ++h) {
+        x[k + 2 * h] = __uint_as_float(w[h] << 16);
+        x[k + 2 * h + 1] = __uint_as_float(w[h] & 0xffff0000u);
       }
-    __syncthreads();
-    for (int r = tid; r < BM; r += NT) {
-      const int m = m0 + r;
-      if (m >= M) continue;
-      const float ma = st[r * 2], sa = st[r * 2 + 1];
-      const float mb = st[(BM + r) * 2], sb = st[(BM + r) * 2 + 1];
-      const float mx = fmaxf(ma, mb);  // finite: every tile holds at least one column
-      const float se = (sa > 0.f ? sa * __expf(ma - mx) : 0.f) + (sb > 0.f ? sb * __expf(mb - mx) : 0.f);
-      e.lstat[(int64_t)m * e.ldlstat + 2 * by] = mx;
-      e.lstat[(int64_t)m * e.ldlstat + 2 * by + 1] = se;
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < CPT; ++k)
+      if (k < nv) mx = fmaxf(mx, x[k]);
+#pragma unroll
+    for (int o = 1; o < TPR; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+    // mx is finite: every tile holds at least one column of every row
+    const float l2e = 1.4426950408889634f, moff = mx * l2e;
+    float se = 0.f;
+#pragma unroll
+    for (int k = 0; k < CPT; ++k)
+      if (k < nv) se += __builtin_amdgcn_exp2f(fmaf(x[k], l2e, -moff));
+#pragma unroll
+    for (int o = 1; o < TPR; o <<= 1) se += __shfl_xor(se, o, 64);
+    if (tid % TPR == 0 && m0 + r < M) {
+      e.lstat[(int64_t)(m0 + r) * e.ldlstat + 2 * by] = mx;
+      e.lstat[(int64_t)(m0 + r) * e.ldlstat + 2 * by + 1] = se;
     }
   }
 
