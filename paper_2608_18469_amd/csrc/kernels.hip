@@ -315,17 +315,12 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     if constexpr (KIND == GK_FWD_RELU || KIND == GK_FWD_CROSS || KIND == GK_FWD_HEAD) bnv[j] = (n < g.N) ? e.bias[n] : 0.f;
   }
 
-  // logits: target column of each of the lane's rows, loaded now (latency
-  // hidden behind the main loop)
-  int tgt[KIND == GK_FWD_LOGITS ? TM : 1][4];
+  // logits: the target column of the row this thread takes in the
+  // statistics pass, loaded now (latency hidden behind the main loop)
+  int tgt1 = -1;
   if constexpr (KIND == GK_FWD_LOGITS) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + q;
-        tgt[i][q] = m < g.M ? e.target[m] : -1;
-      }
+    const int m = m0 + tid / (NT / BM);
+    if (m < g.M) tgt1 = e.target[m];
   }
 
   // fused Adam: the tile's parameters and moments are loaded now (they do not
@@ -656,9 +651,6 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
         } else {
           v = (m < M && n < N) ? epi_value<T, KIND>(e, m, n, acc[i][j][q], bn) : OT(0);
           if constexpr (KIND != GK_FWD_GELU) acc[i][j][q] = asf(v);  // GELU keeps the pre-activation
-          if constexpr (KIND == GK_FWD_LOGITS) {
-            if (m < M && n < N && n == tgt[i][q]) e.tlogit[m] = asf(v);
-          }
         }
         sc[ml * OPITCH + nl] = v;
       }
@@ -754,6 +746,8 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     if (tid % TPR == 0 && m0 + r < M) {
       e.lstat[(int64_t)(m0 + r) * e.ldlstat + 2 * by] = mx;
       e.lstat[(int64_t)(m0 + r) * e.ldlstat + 2 * by + 1] = se;
+      // the logit at the row's target column, when this tile holds it
+      if (tgt1 >= n0 && tgt1 < n0 + BN && tgt1 < N) e.tlogit[m0 + r] = asf(sc[r * OPITCH + (tgt1 - n0)]);
     }
   }
 
