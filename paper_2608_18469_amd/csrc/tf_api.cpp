@@ -310,7 +310,7 @@ void build_gemms(const erase_tf_config& c, Layout* P) {
     auto dgr = [&](int w, const void* A, int64_t lda, int kind, void* out, int64_t ldo) {
       Lin& L = B.dgr[w];
       L.kind = kind;
-      L.g = gdesc(A, lda, B.sht[w], D.rows[w], N, D.cols[w], D.rows[w], choose(N, D.cols[w], D.rows[w], false));
+      L.g = gdesc(A, lda, B.sht[w], D.rows[w], N, D.cols[w], D.rows[w], choose_fwd(N, D.cols[w], D.rows[w]));
       L.e = EpiParams{};
       L.e.dmn = out;
       L.e.lddmn = ldo;
