@@ -242,6 +242,10 @@ struct GemmSmem {
   // past both the main-loop stages and the output tile
   static constexpr int HOFF = MAIN > TILE ? MAIN : TILE;
   static constexpr int BYTES = HOFF + (KIND == GK_FWD_HEAD ? (3 * BN + 3 * BM + 4) * 4 : 0);
+  // two k-groups: k-group 1's partial tile and row sums, one 64-float row
+  // per accumulator register and wave, added by k-group 0 after the main loop
+  static constexpr int RED2 = 4 * ((BM / 32) * (BN / 32) * 4 + BM / 32) * 64 * 4;
+  static constexpr int BYTES_KG2 = BYTES > RED2 ? BYTES : RED2;
 };
 
 // KG k-groups of four waves (256 * KG threads): every k-group owns the whole
@@ -325,14 +329,17 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
 
   // fused Adam: the tile's parameters and moments are loaded now (they do not
   // depend on the gradient), so their HBM latency hides behind the main loop
+  // fused Adam: the 64x64 two k-group weight gradient only (a block's first
+  // layer); every other instantiation leaves these registers out
+  constexpr bool FADAM = KIND == GK_WGRAD && KG == 2 && BM == 64 && BN == 64;
   typedef float f32x4a_t __attribute__((ext_vector_type(4), aligned(4)));
   typedef __attribute__((address_space(1))) f32x4a_t gvec;
   constexpr int AQ = BN / 4;                                                  // items of 4 columns per row
-  constexpr int AIT = (KIND == GK_WGRAD && KG == 2) ? (BM * AQ + NT - 1) / NT : 1;  // items per thread
+  constexpr int AIT = FADAM ? (BM * AQ + NT - 1) / NT : 1;  // items per thread
   f32x4a_t apv[AIT], amv[AIT], avv[AIT];
   bool afull[AIT];
   int64_t afi[AIT];
-  if constexpr (KIND == GK_WGRAD && KG == 2) {
+  if constexpr (FADAM) {
 #pragma unroll
     for (int it = 0; it < AIT; ++it) {
       const int c = tid + it * NT;
@@ -557,7 +564,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     // memory, one 64-float row per accumulator register and wave; k-group 0
     // adds them
     float* red = reinterpret_cast<float*>(smem);
-    static_assert(4 * (TM * TN * 4 + TM) * 64 * 4 <= GemmSmem<T, BM, BN, KIND, BKX>::MAIN, "reduction buffer");
+    static_assert(4 * (TM * TN * 4 + TM) * 64 * 4 <= GemmSmem<T, BM, BN, KIND, BKX>::BYTES_KG2, "reduction buffer");
     const int sw = wave & 3;
     float* rrs = red + 4 * TM * TN * 4 * 64;
     if (kg == 1) {
@@ -596,7 +603,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
       sr += __shfl_xor(sr, 32, 64);
       const int m = m0 + wm * WM + i * 16 + lane;
       if (lane < 16 && m < g.M) {
-        if constexpr (KIND == GK_WGRAD && KG == 2) {
+        if constexpr (FADAM) {
           if (e.bp) {
             // fused Adam of the bias: this tile holds its rows' whole gradient
             float p = e.bp[m], mo = e.bm[m], v = e.bv[m];
@@ -659,7 +666,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   __syncthreads();
   bool store_tile = omn != nullptr;
   // fused Adam (two k-group weight gradients only) reads the LDS tile instead
-  if constexpr (KIND == GK_WGRAD && KG == 2) store_tile = store_tile && e.ap == nullptr;
+  if constexpr (FADAM) store_tile = store_tile && e.ap == nullptr;
   if (store_tile) {
     constexpr int CPRO = BN / OCH;
     for (int c = tid; c < BM * CPRO; c += NT) {
@@ -754,7 +761,7 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   // Only the two k-group kernels take the fused update: its per-thread item
   // arrays would otherwise hold a 128x128 tile's registers in every
   // weight-gradient instantiation (one wave per SIMD).
-  if constexpr (KIND == GK_WGRAD && KG == 2) {
+  if constexpr (FADAM) {
     if (e.ap) {
       // Fused Adam: the LDS tile holds this tile's finished gradient (the
       // contraction is not split).  Items of 4 consecutive columns of one
@@ -929,7 +936,7 @@ ERASE_GEMM_KERNEL(erase_fwd_logits_gemm, GK_FWD_LOGITS)
   template <typename T, int BM, int BN>                                                       \
   __global__ __launch_bounds__(512) void NAME(GemmDesc g, EpiParams e) {                      \
     constexpr int BKK = sizeof(T) == 2 ? BKX : 0;                                            \
-    __shared__ __attribute__((aligned(16))) char smem[GemmSmem<T, BM, BN, KIND, BKK>::BYTES]; \
+    __shared__ __attribute__((aligned(16))) char smem[GemmSmem<T, BM, BN, KIND, BKK>::BYTES_KG2]; \
     const int gm = (g.M + BM - 1) / BM, gn = (g.N + BN - 1) / BN;                             \
     const TileIdx ti = tile_from(xcd_linear(blockIdx.x, gridDim.x), gm, gn, g.group);        \
     gemm_body<T, BM, BN, KIND, 2, 2, BKK>(g, e, ti.m, ti.n, ti.z, smem);                      \
@@ -945,21 +952,38 @@ ERASE_GEMM_KERNEL_KG2(erase_wgrad_gemm_kg2, GK_WGRAD, 128)
 // activation gradient and are independent): workgroups [0, nw) compute the
 // weight-gradient tiles and slices (the longer contractions, so they start
 // first), the rest the input-gradient tiles.
-template <typename T, int BM, int BN>
-__global__ __launch_bounds__(256) void erase_bwd_gemm(GemmDesc gd, EpiParams ed, GemmDesc gw, EpiParams ew, int nw) {
-  constexpr int SD = GemmSmem<T, BM, BN, GK_DGRAD>::BYTES, SW = GemmSmem<T, BM, BN, GK_WGRAD>::BYTES;
-  __shared__ __attribute__((aligned(16))) char smem[SD > SW ? SD : SW];
+template <typename T, int BM, int BN, int KG>
+__device__ __forceinline__ void bwd_pair(const GemmDesc& gd, const EpiParams& ed, const GemmDesc& gw,
+                                         const EpiParams& ew, int nw, char* smem) {
   // each GEMM is renumbered on its own (workgroups b and b + 8 still share an
   // XCD after subtracting nw), so both spread evenly over the XCDs
   const int b = blockIdx.x;
   if (b < nw) {
     const TileIdx ti = tile_from(xcd_linear(b, nw), (gw.M + BM - 1) / BM, (gw.N + BN - 1) / BN, gw.group);
-    gemm_body<T, BM, BN, GK_WGRAD>(gw, ew, ti.m, ti.n, ti.z, smem);
+    gemm_body<T, BM, BN, GK_WGRAD, 2, KG>(gw, ew, ti.m, ti.n, ti.z, smem);
   } else {
     const int nd = gridDim.x - nw;
     const TileIdx ti = tile_from(xcd_linear(b - nw, nd), (gd.M + BM - 1) / BM, (gd.N + BN - 1) / BN, gd.group);
-    gemm_body<T, BM, BN, GK_DGRAD>(gd, ed, ti.m, ti.n, 0, smem);
+    gemm_body<T, BM, BN, GK_DGRAD, 2, KG>(gd, ed, ti.m, ti.n, 0, smem);
   }
+}
+
+template <typename T, int BM, int BN>
+__global__ __launch_bounds__(256) void erase_bwd_gemm(GemmDesc gd, EpiParams ed, GemmDesc gw, EpiParams ew, int nw) {
+  constexpr int SD = GemmSmem<T, BM, BN, GK_DGRAD>::BYTES, SW = GemmSmem<T, BM, BN, GK_WGRAD>::BYTES;
+  __shared__ __attribute__((aligned(16))) char smem[SD > SW ? SD : SW];
+  bwd_pair<T, BM, BN, 1>(gd, ed, gw, ew, nw, smem);
+}
+
+// The same pair with 512-thread workgroups: two k-groups of four waves, each
+// over half of every k-step of the whole tile, so every SIMD runs two waves
+// of one tile (the large 128x128 tiles, one workgroup per CU).
+template <typename T, int BM, int BN>
+__global__ __launch_bounds__(512) void erase_bwd_gemm_kg2(GemmDesc gd, EpiParams ed, GemmDesc gw, EpiParams ew,
+                                                          int nw) {
+  constexpr int SD = GemmSmem<T, BM, BN, GK_DGRAD>::BYTES_KG2, SW = GemmSmem<T, BM, BN, GK_WGRAD>::BYTES_KG2;
+  __shared__ __attribute__((aligned(16))) char smem[SD > SW ? SD : SW];
+  bwd_pair<T, BM, BN, 2>(gd, ed, gw, ew, nw, smem);
 }
 
 int xcd_group(int gm, int gn, int split, int bm, int bn) {
@@ -1058,7 +1082,7 @@ static hipError_t launch_gemm_t(int kind, const GemmDesc& g0, const EpiParams& e
   return hipGetLastError();
 }
 
-template <typename T, int BM, int BN>
+template <typename T, int BM, int BN, int KG = 1>
 static hipError_t launch_bwd_t(const GemmDesc& gd0, const EpiParams& ed, const GemmDesc& gw0, const EpiParams& ew,
                                hipStream_t s, const LaunchEv& ev) {
   const GemmDesc gd = with_group(gd0, BM, BN), gw = with_group(gw0, BM, BN);
@@ -1067,6 +1091,10 @@ static hipError_t launch_bwd_t(const GemmDesc& gd0, const EpiParams& ed, const G
   // 128x128: one workgroup per CU (an unused dynamic LDS reservation): two
   // co-resident 128x128 workgroups measured 20% slower on the vocabulary
   // head's backward (1.69 vs 1.41 ms)
+  if constexpr (KG == 2) {
+    ERASE_LAUNCH((erase_bwd_gemm_kg2<T, BM, BN>), dim3(nd + nw), dim3(512), 0, s, ev, gd, ed, gw, ew, nw);
+    return hipGetLastError();
+  }
   constexpr size_t kReserve = BM == 128 ? 40960 : 0;
   if constexpr (kReserve > 0) {
     static const hipError_t attr = hipFuncSetAttribute(
@@ -1081,6 +1109,10 @@ static hipError_t launch_bwd_t(const GemmDesc& gd0, const EpiParams& ed, const G
 hipError_t launch_bwd_gemm(int bf16, const GemmDesc& gd, const EpiParams& ed, const GemmDesc& gw, const EpiParams& ew,
                            hipStream_t s, const LaunchEv& ev) {
   if (gd.bm != gw.bm || gd.bn != gw.bn || gd.split != 1 || gw.split <= 0 || ew.ap) return hipErrorInvalidValue;
+  if (gd.kgroups == 2 || gw.kgroups == 2) {  // two k-groups: bf16 128x128 only
+    if (!bf16 || gd.kgroups != gw.kgroups || gd.bm != 128 || gd.bn != 128) return hipErrorInvalidValue;
+    return launch_bwd_t<uint16_t, 128, 128, 2>(gd, ed, gw, ew, s, ev);
+  }
   if (bf16) {
     if (gd.bm == 128 && gd.bn == 128) return launch_bwd_t<uint16_t, 128, 128>(gd, ed, gw, ew, s, ev);
     if (gd.bm == 64 && gd.bn == 64) return launch_bwd_t<uint16_t, 64, 64>(gd, ed, gw, ew, s, ev);

@@ -277,6 +277,8 @@ GemmDesc gdesc(const void* A, int64_t lda, const void* Bm, int64_t ldb, int64_t 
 }
 
 // GEMM launches of every block, fixed at init
+bool kg2_pair(int w) { return w == WH; }
+
 void build_gemms(const erase_tf_config& c, Layout* P) {
   const Dims& D = P->D;
   const int64_t N = D.N, d = D.d, V = D.V;
@@ -345,13 +347,15 @@ void build_gemms(const erase_tf_config& c, Layout* P) {
     for (int w = 0; w < NW; ++w) {
       if (B.dgr[w].g.M == 0 || B.dgr[w].kind != GK_DGRAD) continue;
       GemmDesc& gd = B.dgr[w].g;
-      const GemmDesc& gw = B.wgr[w].g;
+      GemmDesc& gw = B.wgr[w].g;
       if (gd.bm == gw.bm && gd.bn == gw.bn && (gd.bm == 128 || gd.bm == 64) && gd.bm == gd.bn) {
         B.grouped[w] = true;
       } else if (gw.bm == 64 && gw.bn == 64) {
         gd.bm = gd.bn = 64;
         B.grouped[w] = true;
       }
+      // 128x128 pairs: 512-thread workgroups, two k-groups of four waves
+      if (B.grouped[w] && gd.bm == 128 && kg2_pair(w)) gd.kgroups = gw.kgroups = 2;
     }
     (void)V;
     (void)c;

@@ -211,6 +211,56 @@ def test_tf_c5_full_size_sampled():
     assert np.max(np.abs(lse0 - ref)) < 5e-2, np.max(np.abs(lse0 - ref))
 
 
+def _bf16_view(tr, block, name, rows):
+    """Device view [rows][pitch] (bf16) of a stored tensor, without a copy."""
+    import ctypes
+    from paper_2608_18469_amd import erase_tf
+    torch = tr.torch
+    p, ld = ctypes.c_void_p(), ctypes.c_int64(0)
+    assert erase_tf.lib().erase_tf_tensor(tr.ctx, block, erase_tf.TENSORS[name], ctypes.byref(p),
+                                          ctypes.byref(ld)) == 0
+    tr.sync()
+    off = p.value - tr.ws.data_ptr()
+    assert 0 <= off and off + rows * ld.value * 2 <= tr.ws.numel()
+    return tr.ws[off:off + rows * ld.value * 2].view(torch.bfloat16).view(rows, ld.value)
+
+
+def test_tf_c5_head_backward_sampled():
+    """Both gradient GEMMs of the vocabulary head at the full shape, in the
+    launch configuration the benchmark times (one grouped launch of 128x128
+    tiles with two k-groups): sampled rows of the head's weight gradient and
+    sampled positions of the gradient at the block output, each recomputed in
+    float64 from the step's own stored logit gradient, head input and
+    weights."""
+    cfg = synth_tf.tf_config("tf_c5")
+    params, batches = synth_tf.make_workload(cfg, seed=0, n_batches=1)
+    print("[tf] c5 head backward", flush=True)
+    tr, rec = _gpu_run(cfg, params, batches, "serial")
+    N, d, V = cfg["batch"] * cfg["seq"], cfg["d"], cfg["vocab"]
+    rng = np.random.default_rng(11)
+    for b in (0, cfg["layers"] - 1):
+        dl = _bf16_view(tr, b, "logits", N)  # after the step: the logit gradient
+        hn = tr.tensor(b, "hn", N, d).astype(np.float64)
+        vs = np.concatenate([[0, V - 1], rng.choice(V, 6, replace=False)])
+        cols = dl[:, tr.torch.as_tensor(vs, device=tr.dev)].float().cpu().numpy().astype(np.float64)  # [N][8]
+        gwh = synth_tf.unpack_block(cfg, b, rec[0]["grads"][b])["wh"]
+        ref = cols.T @ hn
+        e = _rel(gwh[vs], ref)
+        print(f"[tf] c5 block {b} head weight gradient rows {[int(x) for x in vs]}: rel {e:.2e}", flush=True)
+        assert e < 1e-3, e
+        ns = np.concatenate([[0, N - 1], rng.choice(N, 6, replace=False)])
+        rows = dl[tr.torch.as_tensor(ns, device=tr.dev), :V].float().cpu().numpy().astype(np.float64)  # [8][V]
+        dhn = rows @ np.asarray(params[b]["wh"], np.float64)
+        z = tr.tensor(b, "z", N, d)[ns].astype(np.float64)
+        r = 1.0 / np.sqrt(np.mean(z * z, axis=-1, keepdims=True) + to.RMS_EPS)
+        dz_ref = to.rms_norm_backward(dhn, z, r)
+        dz = tr.tensor(b, "dz", N, d)[ns]
+        e = _rel(dz, dz_ref)
+        print(f"[tf] c5 block {b} output gradient at positions {[int(x) for x in ns]}: rel {e:.2e}", flush=True)
+        assert e < 2e-2, e
+    tr.close()
+
+
 def test_tf_checkpoint_resume_is_bit_identical():
     """Two steps in one run equal one step, a save of params / m / v / t, a
     fresh context resumed from them, and a second step; also after the
