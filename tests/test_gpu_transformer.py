@@ -173,6 +173,20 @@ def test_tf_invalid_token_is_reported():
     tr.close()
 
 
+def _bf16_view(tr, block, name, rows):
+    """Device view [rows][pitch] (bf16) of a stored tensor, without a copy."""
+    import ctypes
+    from paper_2608_18469_amd import erase_tf
+    torch = tr.torch
+    p, ld = ctypes.c_void_p(), ctypes.c_int64(0)
+    assert erase_tf.lib().erase_tf_tensor(tr.ctx, block, erase_tf.TENSORS[name], ctypes.byref(p),
+                                          ctypes.byref(ld)) == 0
+    tr.sync()
+    off = p.value - tr.ws.data_ptr()
+    assert 0 <= off and off + rows * ld.value * 2 <= tr.ws.numel()
+    return tr.ws[off:off + rows * ld.value * 2].view(torch.bfloat16).view(rows, ld.value)
+
+
 def test_tf_c5_full_size_sampled():
     """The full small-transformer shape (V 32768, d 512, 8 heads, 8 layers,
     T 1024, B 16) in the launch configuration the benchmark times: serial and
@@ -187,6 +201,8 @@ def test_tf_c5_full_size_sampled():
     z0 = tra.tensor(0, "z", T, d)
     o0 = tra.tensor(0, "o", T, d)
     lse0 = tra.tensor(0, "lse", cfg["heads"], T, dtype="f32")
+    V = cfg["vocab"]
+    dl0 = _bf16_view(tra, 0, "logits", T)[:, :V].float().cpu().numpy()  # after the step: the logit gradient
     tra.close()
     del tra
     print("[tf] c5 overlap", flush=True)
@@ -209,20 +225,16 @@ def test_tf_c5_full_size_sampled():
     mx = s.max(-1, keepdims=True)
     ref = (mx + np.log(np.exp(s - mx).sum(-1, keepdims=True)))[..., 0]
     assert np.max(np.abs(lse0 - ref)) < 5e-2, np.max(np.abs(lse0 - ref))
-
-
-def _bf16_view(tr, block, name, rows):
-    """Device view [rows][pitch] (bf16) of a stored tensor, without a copy."""
-    import ctypes
-    from paper_2608_18469_amd import erase_tf
-    torch = tr.torch
-    p, ld = ctypes.c_void_p(), ctypes.c_int64(0)
-    assert erase_tf.lib().erase_tf_tensor(tr.ctx, block, erase_tf.TENSORS[name], ctypes.byref(p),
-                                          ctypes.byref(ld)) == 0
-    tr.sync()
-    off = p.value - tr.ws.data_ptr()
-    assert 0 <= off and off + rows * ld.value * 2 <= tr.ws.numel()
-    return tr.ws[off:off + rows * ld.value * 2].view(torch.bfloat16).view(rows, ld.value)
+    # the head of block 1 on sequence 0: logits GEMM, statistics and
+    # cross-entropy, through the stored gradient lam (softmax - onehot) / N
+    x = c["logits"]
+    p = np.exp(x - x.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    p[np.arange(T), np.asarray(batches[0][0, 1:T + 1])] -= 1.0
+    p *= float(cfg.get("lam", 1.0)) / (cfg["batch"] * T)
+    e = _rel(dl0, p)
+    print(f"[tf] c5 sequence 0 logit gradient: rel {e:.2e}", flush=True)
+    assert e < 2e-2, e
 
 
 def test_tf_c5_head_backward_sampled():
