@@ -297,6 +297,7 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
         // one launch for both backward GEMMs when they can share a tile
         if (R.dgrad.bm != R.wgrad.bm || R.dgrad.bn != R.wgrad.bn) {
           GemmPlan d64 = choose_gemm(P->bf16, 1, 1, roundup(R.N, BK), false);  // 64x64, split 1
+          d64.kgroups = 1;  // the grouped launch runs 256-thread workgroups at 64x64
           GemmPlan w64 = d64;
           const int64_t w = cdiv(R.N, 64) * cdiv(R.K, 64);
           int sp = 1;
