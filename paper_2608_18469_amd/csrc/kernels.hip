@@ -133,12 +133,18 @@ __device__ __forceinline__ u32x4_t tr_frag(const T* p, int pitch) {
 // a = 0.044715, and its derivative
 // 0.5 (1 + t) + 0.5 u (1 - t^2) c (1 + 3 a u^2), t = tanh(c (u + a u^3)).
 constexpr float kGeluC = 0.7978845608028654f, kGeluA = 0.044715f;
+// tanh(y) = 1 - 2 / (exp(2y) + 1) with the hardware exp2 and reciprocal
+// (absolute error about 1e-7; +-1 in the limits, where exp2 gives inf or 0)
+__device__ __forceinline__ float tanh_hw(float y) {
+  const float e = __builtin_amdgcn_exp2f(y * 2.8853900817779268f);  // 2 log2(e)
+  return 1.f - 2.f * __builtin_amdgcn_rcpf(e + 1.f);
+}
 __device__ __forceinline__ float gelu_f(float u) {
-  const float t = tanhf(kGeluC * fmaf(kGeluA * u * u, u, u));
+  const float t = tanh_hw(kGeluC * fmaf(kGeluA * u * u, u, u));
   return 0.5f * u * (1.f + t);
 }
 __device__ __forceinline__ float gelu_grad_f(float u) {
-  const float t = tanhf(kGeluC * fmaf(kGeluA * u * u, u, u));
+  const float t = tanh_hw(kGeluC * fmaf(kGeluA * u * u, u, u));
   return 0.5f * (1.f + t) + 0.5f * u * (1.f - t * t) * kGeluC * fmaf(3.f * kGeluA, u * u, 1.f);
 }
 

@@ -315,7 +315,7 @@ __global__ __launch_bounds__(256) void tf_attn_fwd(TfAttnArgs a) {
     mb = fmaxf(mb, __shfl_xor(mb, 16, 64));
     mb = fmaxf(mb, __shfl_xor(mb, 32, 64));
     const float mnew = fmaxf(mrow, mb);
-    const float alpha = exp2f(mrow - mnew);
+    const float alpha = __builtin_amdgcn_exp2f(mrow - mnew);
     mrow = mnew;
     lpart *= alpha;
 #pragma unroll
@@ -328,7 +328,7 @@ __global__ __launch_bounds__(256) void tf_attn_fwd(TfAttnArgs a) {
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          p[4 * t + q] = exp2f(st4[st][t][q] - mnew);
+          p[4 * t + q] = __builtin_amdgcn_exp2f(st4[st][t][q] - mnew);
           lpart += p[4 * t + q];
         }
       pf[st] = u32x4_t{pack2(p[0], p[1]), pack2(p[2], p[3]), pack2(p[4], p[5]), pack2(p[6], p[7])};
@@ -457,7 +457,7 @@ __global__ __launch_bounds__(256) void tf_attn_bwd_dkdv(TfAttnArgs a) {
           const int ql = 32 * st + 8 * g + 4 * t + q;  // local query row
           const int qrow = q0 + ql;
           const bool ok = key <= qrow && qrow < a.T && key < a.T;
-          const float pv = ok ? exp2f(s4[t][q] * sc - sl[ql]) : 0.f;
+          const float pv = ok ? __builtin_amdgcn_exp2f(s4[t][q] * sc - sl[ql]) : 0.f;
           p[4 * t + q] = pv;
           ds[4 * t + q] = pv * (p4[t][q] - sd[ql]);
         }
@@ -546,7 +546,7 @@ __global__ __launch_bounds__(256) void tf_attn_bwd_dq(TfAttnArgs a) {
         for (int q = 0; q < 4; ++q) {
           const int key = k0 + 32 * st + 8 * g + 4 * t + q;
           const bool ok = key <= qrow && key < a.T && qrow < a.T;
-          const float pv = ok ? exp2f(s4[t][q] * sc - lq) : 0.f;
+          const float pv = ok ? __builtin_amdgcn_exp2f(s4[t][q] * sc - lq) : 0.f;
           ds[4 * t + q] = pv * (p4[t][q] - dq);
         }
       const u32x4_t dsf = {pack2(ds[0], ds[1]), pack2(ds[2], ds[3]), pack2(ds[4], ds[5]), pack2(ds[6], ds[7])};
