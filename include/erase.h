@@ -35,6 +35,10 @@
 #include <stddef.h>
 #include <stdint.h>
 
+/* The entry points below are the only symbols the library exports (it is
+ * built with hidden visibility). */
+#define ERASE_API __attribute__((visibility("default")))
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -163,12 +167,12 @@ typedef struct {
 } erase_block_buffers;
 
 /* Number of fp32 parameters of block `block`.  Host only; no HIP call. */
-erase_status erase_param_count(const erase_config* cfg, int32_t block, int64_t* count);
+ERASE_API erase_status erase_param_count(const erase_config* cfg, int32_t block, int64_t* count);
 
 /* Bytes of device workspace erase_init() needs for `cfg` (activations in both
  * row- and feature-major layouts, activation gradients, GEMM copies of the
  * weights, split-reduction partials, counters).  Host only; no HIP call. */
-erase_status erase_workspace_bytes(const erase_config* cfg, size_t* bytes);
+ERASE_API erase_status erase_workspace_bytes(const erase_config* cfg, size_t* bytes);
 
 /* Validate `cfg`, carve `workspace` (device, 256-byte aligned, ws_bytes >=
  * erase_workspace_bytes) and create the context with its events.  Enqueues on
@@ -176,7 +180,7 @@ erase_status erase_workspace_bytes(const erase_config* cfg, size_t* bytes);
  * and resets the step counter to 0; does not synchronize.  `bufs` is a host
  * array of n_blocks entries whose device buffers must stay valid for the
  * context's life.  The config is copied; `cfg` may be freed afterwards. */
-erase_status erase_init(const erase_config* cfg, const erase_block_buffers* bufs,
+ERASE_API erase_status erase_init(const erase_config* cfg, const erase_block_buffers* bufs,
                         void* workspace, size_t ws_bytes, void* s_fwd, void* s_bwd,
                         void** ctx_out);
 
@@ -185,7 +189,7 @@ erase_status erase_init(const erase_config* cfg, const erase_block_buffers* bufs
  * backward and Adam run on s_bwd[b % n_bwd], so the backwards of different
  * blocks may also overlap one another (the paper's CTR model used four side
  * streams, Section 3.2).  erase_init() is this call with n_bwd = 1. */
-erase_status erase_init_streams(const erase_config* cfg, const erase_block_buffers* bufs,
+ERASE_API erase_status erase_init_streams(const erase_config* cfg, const erase_block_buffers* bufs,
                                 void* workspace, size_t ws_bytes, void* s_fwd, void* const* s_bwd,
                                 int32_t n_bwd, void** ctx_out);
 
@@ -196,22 +200,22 @@ erase_status erase_init_streams(const erase_config* cfg, const erase_block_buffe
  *   losses: device fp32 [n_blocks], receives the unweighted l_b.
  * x, labels and losses must stay unmodified and valid until erase_sync().
  * The step increments the device step counter before its Adam updates. */
-erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t schedule,
+ERASE_API erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t schedule,
                         float* losses);
 
 /* Wait for all enqueued work of the context, then report deferred errors
  * (HIP errors, non-finite loss: ERASE_ERR_NONFINITE, sticky). */
-erase_status erase_sync(void* ctx);
+ERASE_API erase_status erase_sync(void* ctx);
 
 /* Read / overwrite the device step counter t (Adam bias correction uses t+1
  * at the next step).  Both synchronize the forward stream.  Used for
  * checkpoint/resume together with the caller-owned param/m/v buffers. */
-erase_status erase_get_step(void* ctx, int64_t* t);
-erase_status erase_set_step(void* ctx, int64_t t);
+ERASE_API erase_status erase_get_step(void* ctx, int64_t* t);
+ERASE_API erase_status erase_set_step(void* ctx, int64_t t);
 
 /* Re-derive the GEMM weight copies after the caller changed `param` (e.g. a
  * checkpoint load).  Enqueued on s_fwd. */
-erase_status erase_refresh_weights(void* ctx);
+ERASE_API erase_status erase_refresh_weights(void* ctx);
 
 /* Per-launch kernel timing, for measurement.  When enabled, non-graph
  * schedules bracket every kernel launch with timing events on the launch's
@@ -250,8 +254,8 @@ typedef struct {
   double bytes;      /* algorithmic HBM bytes of the launch */
 } erase_kernel_time;
 
-erase_status erase_set_timing(void* ctx, int32_t enable);
-erase_status erase_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, int32_t* n);
+ERASE_API erase_status erase_set_timing(void* ctx, int32_t enable);
+ERASE_API erase_status erase_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, int32_t* n);
 
 /* Host dispatch of the ERASE schedules (Section 2.2: blocking dispatch on
  * the main thread vs non-blocking dispatch on a thread pool).
@@ -272,7 +276,7 @@ erase_status erase_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, i
  * calling thread's current device must be the context's) and joined by
  * erase_destroy().  ERASE_ERR_INVALID_ARG for an unknown mode. */
 typedef enum { ERASE_DISPATCH_CALLER = 0, ERASE_DISPATCH_WORKER = 1 } erase_dispatch;
-erase_status erase_set_dispatch(void* ctx, int32_t mode);
+ERASE_API erase_status erase_set_dispatch(void* ctx, int32_t mode);
 
 /* Embedding-bag input stage of the CTR workload.  The paper feeds its CTR
  * model (Section 3.2) an input embedding x (Section 2.1) without describing
@@ -309,7 +313,7 @@ typedef struct {
   int64_t x_ld;
 } erase_bag_config;
 
-erase_status erase_embed_bags(const erase_bag_config* cfg, const float* dense, const int64_t* offsets,
+ERASE_API erase_status erase_embed_bags(const erase_bag_config* cfg, const float* dense, const int64_t* offsets,
                               const int32_t* indices, const float* tables, void* x, int32_t* status,
                               void* stream);
 
@@ -336,20 +340,20 @@ erase_status erase_embed_bags(const erase_bag_config* cfg, const float* dense, c
  * (invalid offsets or ids set it to 1).  Six launches on `stream`, no wait.
  * ERASE_ERR_SHAPE also when n_tables * rows >= 2^31; ERASE_ERR_WORKSPACE for
  * a missing, misaligned or small scratch. */
-erase_status erase_embed_bags_backward_scratch_bytes(const erase_bag_config* cfg, size_t* bytes);
-erase_status erase_embed_bags_backward(const erase_bag_config* cfg, const int64_t* offsets, const int32_t* indices,
+ERASE_API erase_status erase_embed_bags_backward_scratch_bytes(const erase_bag_config* cfg, size_t* bytes);
+ERASE_API erase_status erase_embed_bags_backward(const erase_bag_config* cfg, const int64_t* offsets, const int32_t* indices,
                                        const void* dx, float* table_grad, void* scratch, size_t scratch_bytes,
                                        int32_t* status, void* stream);
 
 /* Destroy the context: waits for its dispatch thread and streams, frees
  * events and graphs.  Never frees caller memory.  NULL is accepted. */
-erase_status erase_destroy(void* ctx);
+ERASE_API erase_status erase_destroy(void* ctx);
 
 /* Static description of a status code. */
-const char* erase_status_str(int32_t status);
+ERASE_API const char* erase_status_str(int32_t status);
 
 /* Last error message recorded on the context ("" if none). */
-const char* erase_last_error(void* ctx);
+ERASE_API const char* erase_last_error(void* ctx);
 
 #ifdef __cplusplus
 }

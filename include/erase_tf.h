@@ -51,20 +51,20 @@ typedef struct {
  * order: block 0 only: E[V][d]; then every block: Wqkv[3d][d], Wo[d][d],
  * W1[4d][d], W2[d][4d], Wh[V][d] (row-major, torch nn.Linear layout).
  * Host only; no HIP call. */
-erase_status erase_tf_param_count(const erase_tf_config* cfg, int32_t block, int64_t* count);
+ERASE_API erase_status erase_tf_param_count(const erase_tf_config* cfg, int32_t block, int64_t* count);
 
 /* Bytes of device workspace for `cfg`: per block the activations, the
  * vocabulary logits [B T][V] (bf16, overwritten in place by their
  * gradient), softmax statistics, activation gradients, weight-gradient
  * partials and the bf16 weight copies.  Host only; no HIP call. */
-erase_status erase_tf_workspace_bytes(const erase_tf_config* cfg, size_t* bytes);
+ERASE_API erase_status erase_tf_workspace_bytes(const erase_tf_config* cfg, size_t* bytes);
 
 /* Validate, carve `workspace` (device, 256-byte aligned) and create the
  * context.  Enqueues on s_fwd the zeroing of the workspace and the weight
  * copies; resets the step counter to 0; does not synchronize.  `bufs` is a
  * host array of n_layers entries (param, m, v required, grad optional; all
  * 4-byte aligned) that must stay valid for the context's life. */
-erase_status erase_tf_init(const erase_tf_config* cfg, const erase_block_buffers* bufs, void* workspace,
+ERASE_API erase_status erase_tf_init(const erase_tf_config* cfg, const erase_block_buffers* bufs, void* workspace,
                            size_t ws_bytes, void* s_fwd, void* s_bwd, void** ctx_out);
 
 /* Enqueue one training step and return without waiting.
@@ -82,18 +82,18 @@ erase_status erase_tf_init(const erase_tf_config* cfg, const erase_block_buffers
  *           Other schedules: ERASE_ERR_UNSUPPORTED.
  *   losses: device fp32 [n_layers], receives the unweighted l_b.
  * tokens and losses must stay valid and unmodified until erase_tf_sync(). */
-erase_status erase_tf_step(void* ctx, const int32_t* tokens, int32_t schedule, float* losses);
+ERASE_API erase_status erase_tf_step(void* ctx, const int32_t* tokens, int32_t schedule, float* losses);
 
 /* Wait for the context's work; report deferred errors (HIP errors,
  * ERASE_ERR_NONFINITE for a non-finite loss, ERASE_ERR_INVALID_ARG for an
  * out-of-range token id), all sticky. */
-erase_status erase_tf_sync(void* ctx);
+ERASE_API erase_status erase_tf_sync(void* ctx);
 
 /* Step counter (synchronizes s_fwd), weight-copy refresh after the caller
  * changed `param`, as in erase.h. */
-erase_status erase_tf_get_step(void* ctx, int64_t* t);
-erase_status erase_tf_set_step(void* ctx, int64_t t);
-erase_status erase_tf_refresh_weights(void* ctx);
+ERASE_API erase_status erase_tf_get_step(void* ctx, int64_t* t);
+ERASE_API erase_status erase_tf_set_step(void* ctx, int64_t t);
+ERASE_API erase_status erase_tf_refresh_weights(void* ctx);
 
 /* Per-launch timing as in erase.h (erase_kernel_time records; record 0 is
  * the empty interval, kind 7).  Kinds of this step: 0 prologue, 1 forward
@@ -104,8 +104,8 @@ erase_status erase_tf_refresh_weights(void* ctx);
  * 14 attention forward, 15 attention backward (layer 1 row sums, 2 dK/dV,
  * 3 dQ), 16 softmax cross-entropy, 17 embedding gradient (four launches,
  * bracketed by stream events rather than kernel-stamped ones). */
-erase_status erase_tf_set_timing(void* ctx, int32_t enable);
-erase_status erase_tf_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, int32_t* n);
+ERASE_API erase_status erase_tf_set_timing(void* ctx, int32_t enable);
+ERASE_API erase_status erase_tf_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, int32_t* n);
 
 /* Device address and row pitch (elements) of a stored tensor of block
  * `block`, for inspection after erase_tf_sync():
@@ -114,13 +114,13 @@ erase_status erase_tf_read_timing(void* ctx, erase_kernel_time* out, int32_t cap
  *   [.][V] (bf16; after a step, the gradient), 11 lse (fp32 [B][H][T],
  *   pitch T), 12 dqkv, 13 dz (bf16 unless noted; rows are positions
  *   b T + t).  ERASE_ERR_INVALID_ARG for an unknown id or block. */
-erase_status erase_tf_tensor(void* ctx, int32_t block, int32_t which, void** ptr, int64_t* ld);
+ERASE_API erase_status erase_tf_tensor(void* ctx, int32_t block, int32_t which, void** ptr, int64_t* ld);
 
 /* Destroy (waits for the streams; frees events).  NULL is accepted. */
-erase_status erase_tf_destroy(void* ctx);
+ERASE_API erase_status erase_tf_destroy(void* ctx);
 
 /* Last error message recorded on the context ("" if none). */
-const char* erase_tf_last_error(void* ctx);
+ERASE_API const char* erase_tf_last_error(void* ctx);
 
 #ifdef __cplusplus
 }
