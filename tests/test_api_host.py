@@ -28,6 +28,16 @@ def test_library_exports_every_declared_symbol():
     assert set(names) == set(erase.SIGNATURES), set(names) ^ set(erase.SIGNATURES)
 
 
+def test_library_hides_its_internal_host_functions():
+    """Built with hidden visibility: the host-side launchers and planners are
+    not exported, only the C entry points (and the kernels, which the HIP
+    runtime registers)."""
+    L = erase.lib()
+    for internal in ("_ZN5erase11launch_gemmEiiRKNS_8GemmDescERKNS_9EpiParamsEP12ihipStream_tRKNS_8LaunchEvE",
+                     "_ZN5erase11launch_adamEiRKNS_8AdamArgsEP12ihipStream_tRKNS_8LaunchEvE"):
+        assert not hasattr(L, internal), internal
+
+
 def test_status_strings():
     L = erase.lib()
     for s in range(0, -8, -1):
