@@ -99,7 +99,8 @@ def block_forward(blk: dict, p: dict, a0: np.ndarray, emulate_bf16: bool = False
 
 
 def block_backward(blk: dict, p: dict, cache: dict, y: np.ndarray,
-                   emulate_bf16: bool = False, g_out=None, want_input_grad: bool = False):
+                   emulate_bf16: bool = False, g_out=None, want_input_grad: bool = False,
+                   trace: dict | None = None):
     """Local loss and exact gradient of lam_b * l_b w.r.t. theta_b only.
 
     l_b = mean_i BCE(s_i, y_i).  With g_s = lam (sigma(s) - y) / M:
@@ -111,6 +112,11 @@ def block_backward(blk: dict, p: dict, cache: dict, y: np.ndarray,
                    gradient at a_{l-1} = u W_l + g         (only if l > 1)
     No gradient is formed for the block input a_0: it is detached (Eq. 1).
     Returns (loss, grads) with grads shaped like p.
+
+    ``trace`` (a dict, optional) receives the activation gradients the step
+    stores per layer -- "u" (the GEMM operand u above), "g" (a cross layer's
+    gradient at its output) and "wcopy" (the weight matrix as the GEMMs
+    read it) -- for checks of where emulation rounds; nothing else changes.
 
     For the undetached baseline (conventional backpropagation through the
     cuts, the comparison of Section 3): ``g_out`` is added to g at z (the
@@ -144,6 +150,11 @@ def block_backward(blk: dict, p: dict, cache: dict, y: np.ndarray,
             u = rnd(g * a0)
             if want_input_grad:
                 g_in = g_in + g * cache["pre"][l - 1]
+        if trace is not None:
+            trace.setdefault("u", {})[l] = u
+            trace.setdefault("wcopy", {})[l] = rnd(W)
+            if kinds[l - 1] == "cross":
+                trace.setdefault("g", {})[l] = g
         grads[l - 1] = (u.T @ acts[l - 1], u.sum(axis=0))
         if l > 1 or want_input_grad:
             g_below = u @ rnd(W)

@@ -172,10 +172,14 @@ def tf_block_forward(cfg: dict, p: dict, a0: np.ndarray, emulate_bf16: bool = Fa
 
 
 def tf_block_backward(cfg: dict, c: dict, target: np.ndarray, lam: float, emulate_bf16: bool = False,
-                      g_out: np.ndarray | None = None, need_input_grad: bool = False):
+                      g_out: np.ndarray | None = None, need_input_grad: bool = False,
+                      trace: dict | None = None):
     """Local loss and the gradient of lam * loss (+ <g_out, z> when the
     undetached baseline sends a gradient into z) at the block's weights, and
-    at its input a0 when ``need_input_grad``.  Returns (loss, grads, g_a0)."""
+    at its input a0 when ``need_input_grad``.  Returns (loss, grads, g_a0).
+    ``trace`` (a dict, optional) receives the activation gradients the step
+    stores (dlog, dhn, dz, du, dn2, da1, do, dqkv, and dn1 when formed), for
+    checks of where emulation rounds; nothing else changes."""
     rb = _bf16 if emulate_bf16 else _ident
     B, T = cfg["batch"], cfg["seq"]
     N = B * T
@@ -201,9 +205,14 @@ def tf_block_backward(cfg: dict, c: dict, target: np.ndarray, lam: float, emulat
     dqkv = rb(np.concatenate([_unheads(dq), _unheads(dk), _unheads(dv)], axis=1))
     gr["wqkv"] = dqkv.T @ c["n1"]
     g_a0 = None
+    dn1 = None
     if need_input_grad:
         dn1 = rb(dqkv @ W["wqkv"])
         g_a0 = da1 + rms_norm_backward(dn1, c["a0"], c["r1"])
+    if trace is not None:
+        trace.update(dlog=dlog, dhn=dhn, dz=dz, du=du, dn2=dn2, da1=da1, do=do, dqkv=dqkv)
+        if dn1 is not None:
+            trace["dn1"] = dn1
     return loss, gr, g_a0
 
 

@@ -362,3 +362,75 @@ def test_bf16_emulation_rounding_agrees_with_input_rounding():
     for b in range(2):
         for A, B in zip(_leaves(r0["grads"][b]), _leaves(r1["grads"][b])):
             assert np.linalg.norm(A - B) <= 2e-2 * np.linalg.norm(A) + 1e-12
+
+
+def _is_bf16(a):
+    """Elementwise: the value is a bf16 number (a float32 whose low 16 bits
+    are zero), by definition of the format rather than by a rounding routine."""
+    a = np.asarray(a, dtype=np.float64)
+    f = a.astype(np.float32)
+    return (f.astype(np.float64) == a) & ((f.view(np.uint32) & np.uint32(0xFFFF)) == 0)
+
+
+def _nonzero_bf16_share(a):
+    a = np.asarray(a, dtype=np.float64)
+    nz = a != 0
+    return float(np.mean(_is_bf16(a[nz]))) if np.any(nz) else 0.0
+
+
+def test_bf16_rounding_is_nearest_even():
+    """The oracle's bf16 rounding against values fixed by the format: bf16
+    keeps 7 fraction bits, so at 1 the spacing is 2^-7 and 1 + 2^-8 is a tie
+    (to the even 1), 1 + 3 * 2^-8 a tie (to the even 1 + 2^-6), and
+    1 + 2^-8 + 2^-20 rounds up; negative values mirror them."""
+    r = oracle.erase_oracle._bf16
+    cases = {1 + 2 ** -8: 1.0, 1 + 3 * 2 ** -8: 1 + 2 ** -6, 1 + 2 ** -8 + 2 ** -20: 1 + 2 ** -7,
+             1 + 2 ** -9: 1.0, 3.0: 3.0, 2.0 ** -130: 2.0 ** -130, 65504.0: 65536.0}
+    for v, want in cases.items():
+        got = r(np.array([v, -v], dtype=np.float64))
+        assert got.tolist() == [want, -want], (v, got, want)
+
+
+def test_bf16_emulation_rounds_exactly_the_stored_tensors():
+    """emulate_bf16 rounds what the GPU stores in bf16 and nothing else: the
+    layer outputs, the activation gradients u (and a cross layer's g) and the
+    weight copies the GEMMs read are bf16 numbers; the pre-activations, the
+    logits, the weight and bias gradients and the updated fp32 parameters and
+    moments are not.  Without emulation the stored tensors are not bf16 either
+    (so the first half is not vacuous)."""
+    blocks = [
+        {"input": "x", "layers": [("cross", 24, 24), ("cross", 24, 24), ("linear_relu", 24, 20),
+                                  ("linear_relu", 20, 16)], "lam": 1.0},
+        {"input": "prev", "layers": [("linear_relu", 16, 12), ("linear_relu", 12, 8)], "lam": 0.5},
+    ]
+    cfg = synth.custom("bf16", batch=300, in_dim=24, blocks=blocks, label_p=0.4)
+    params, batches = synth.make_workload(cfg, 3, 1)
+    x, y = batches[0]
+    assert np.all(_is_bf16(x))
+    # parameters after one exact step: no longer bf16 numbers, so the weight
+    # copies are rounded only if emulation rounds them
+    m0 = synth.zero_state(params)
+    params = oracle.step(cfg, params, m0, m0, 0, x, y)["params"]
+    assert all(_nonzero_bf16_share(W) < 0.3 for p in params for (W, _b) in p["layers"])
+    for emulate in (True, False):
+        caches = oracle.forward_all(cfg, params, x, emulate_bf16=emulate)
+        for b, (blk, c) in enumerate(zip(cfg["blocks"], caches)):
+            tr = {}
+            p = {"layers": [(np.asarray(W, F64), np.asarray(bb, F64)) for (W, bb) in params[b]["layers"]],
+                 "head": (np.asarray(params[b]["head"][0], F64), np.asarray(params[b]["head"][1], F64))}
+            _loss, gr = oracle.block_backward(blk, p, c, y.astype(F64), emulate_bf16=emulate, trace=tr)
+            stored = list(c["acts"][1:]) + list(tr["u"].values()) + list(tr.get("g", {}).values())
+            if emulate:
+                for a in stored + list(tr["wcopy"].values()):
+                    assert np.all(_is_bf16(a))
+            else:
+                assert all(_nonzero_bf16_share(a) < 0.2 for a in stored)
+            # kept in fp32 / fp64: never rounded to bf16
+            kept = list(c["pre"]) + [c["s"]] + [t for (gW, gb) in gr["layers"] for t in (gW, gb)] + list(gr["head"])
+            assert _nonzero_bf16_share(np.concatenate([np.ravel(a) for a in kept])) < 0.05
+    m, v = synth.zero_state(params), synth.zero_state(params)
+    r = oracle.step(cfg, params, m, v, 1, x, y, emulate_bf16=True)
+    for b in range(2):
+        for tree in (r["params"][b], r["m"][b], r["v"][b]):
+            for (W, bb) in tree["layers"]:
+                assert _nonzero_bf16_share(W) < 0.3

@@ -232,3 +232,47 @@ def test_emulated_bf16_is_close():
         assert abs(a["losses"][blk] - b["losses"][blk]) < 2e-2 * a["losses"][blk]
         for k in a["grads"][blk]:
             assert _rel(b["grads"][blk][k], a["grads"][blk][k]) < 0.1
+
+
+def _is_bf16(a):
+    """Elementwise: a bf16 number (a float32 whose low 16 bits are zero)."""
+    a = np.asarray(a, dtype=np.float64)
+    f = a.astype(np.float32)
+    return (f.astype(np.float64) == a) & ((f.view(np.uint32) & np.uint32(0xFFFF)) == 0)
+
+
+def _share(arrays):
+    a = np.concatenate([np.ravel(np.asarray(x, dtype=np.float64)) for x in arrays])
+    a = a[a != 0]
+    return float(np.mean(_is_bf16(a))) if a.size else 0.0
+
+
+def test_bf16_emulation_rounds_exactly_the_stored_tensors():
+    """emulate_bf16 rounds what the GPU stores in bf16 -- the weight copies,
+    the block's activations (n1, q/k/v, o, a1, n2, u, g, z, hn) and the stored
+    activation gradients (logit gradient, dhn, dz, du, dn2, da1, do, dqkv,
+    dn1) -- and leaves the fp32 ones alone: the RMSNorm statistics, the
+    attention probabilities, the logits and the weight gradients.  Without
+    emulation the stored tensors are not bf16 (the check is not vacuous)."""
+    cfg = _cfg(vocab=64, d=32, heads=2, layers=2, seq=16, batch=3)
+    params, tokens = _work(cfg, seed=21)
+    inp, tgt = tokens[:, :-1].reshape(-1), tokens[:, 1:].reshape(-1)
+    acts = ("n1", "q", "k", "v", "o", "a1", "n2", "u", "g", "z", "hn")
+    grads = ("dlog", "dhn", "dz", "du", "dn2", "da1", "do", "dqkv", "dn1")
+    for emulate in (True, False):
+        rb = to._bf16 if emulate else (lambda a: a)
+        a0 = rb(np.asarray(params[0]["emb"], np.float64))[inp]
+        c = to.tf_block_forward(cfg, {k: np.asarray(a, np.float64) for k, a in params[0].items()}, a0, emulate)
+        tr = {}
+        _loss, gr, _ga0 = to.tf_block_backward(cfg, c, tgt, 1.0, emulate, None, True, trace=tr)
+        stored = [c[k] for k in acts] + [tr[k] for k in grads]
+        if emulate:
+            for k in acts:
+                assert np.all(_is_bf16(c[k])), k
+            for k in grads:
+                assert np.all(_is_bf16(tr[k])), k
+            for k, Wc in c["W"].items():
+                assert np.all(_is_bf16(Wc)), k
+        else:
+            assert _share(stored) < 0.05
+        assert _share([c["r1"], c["r2"], c["r3"], c["P"], c["logits"]] + list(gr.values())) < 0.05
