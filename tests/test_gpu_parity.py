@@ -600,13 +600,34 @@ def test_deep_chain_multi_stream_matches_serial():
 
 
 def test_ctr_mlp_full_size_vs_oracle():
-    """The benchmarked workload itself: 6 blocks, batch 4096, bf16, 2 steps,
-    in the overlapped-graph schedule the benchmark times."""
-    _say("case: ctr_mlp full size, overlap_graph")
+    """The benchmarked workload itself (6 blocks, batch 4096, bf16), 2 steps,
+    in the benchmark's headline schedule: PIPELINE with the backward work
+    enqueued by the library's worker thread on 2 backward streams."""
+    _say("case: ctr_mlp full size, pipeline+worker, 2 backward streams")
     cfg = synth.config("ctr_mlp")
     params, batches = synth.make_workload(cfg, 0, 2)
-    _, g = run_gpu(cfg, params, batches, "overlap_graph")
+    tr = erase.Trainer(cfg, params, keep_grads=True, bwd_streams=2)
+    tr.set_dispatch("worker")
+    _, g = run_gpu(cfg, params, batches, "pipeline", trainer=tr)
+    tr.close()
     _say("  ", check_bf16(cfg, g, params, batches))
+
+
+def test_ctr_mlp_full_size_headline_schedule_bit_identical():
+    """At the benchmarked size (6 blocks, batch 4096, bf16, 2 backward
+    streams, worker dispatch), 6 PIPELINE steps enqueued back to back -- so
+    the zero-padded input copies and the events of one step are reused while
+    the previous step's backward may still run -- and a mix with
+    OVERLAP_GRAPH and OVERLAP give the same bits as 6 SERIAL steps: losses of
+    every step, and the final gradients, parameters and moments."""
+    _say("case: ctr_mlp full size, pipeline+worker back to back vs serial")
+    cfg = synth.config("ctr_mlp")
+    params, batches = synth.make_workload(cfg, 19, 6)
+    ref_l, ref = run_gpu_nosync(cfg, params, batches, ["serial"])
+    for scheds in (["pipeline"], ["pipeline", "overlap_graph", "pipeline", "pipeline", "overlap", "pipeline"]):
+        got_l, got = run_gpu_nosync(cfg, params, batches, scheds, bwd_streams=2, dispatch="worker")
+        assert np.array_equal(ref_l.view(np.uint32), got_l.view(np.uint32)), scheds
+        assert_bit_identical([ref], [got])
 
 
 def test_deep_chain_full_size_vs_oracle():
