@@ -43,6 +43,10 @@
 extern "C" {
 #endif
 
+/* Opaque training-step context: created by erase_init(), owned by the
+ * library, released by erase_destroy(). */
+typedef struct erase_ctx erase_ctx;
+
 typedef enum {
   ERASE_OK = 0,
   ERASE_ERR_INVALID_ARG = -1,  /* null pointer, bad enum, bad hyper-parameter, misaligned pointer */
@@ -182,7 +186,7 @@ ERASE_API erase_status erase_workspace_bytes(const erase_config* cfg, size_t* by
  * context's life.  The config is copied; `cfg` may be freed afterwards. */
 ERASE_API erase_status erase_init(const erase_config* cfg, const erase_block_buffers* bufs,
                         void* workspace, size_t ws_bytes, void* s_fwd, void* s_bwd,
-                        void** ctx_out);
+                        erase_ctx** ctx_out);
 
 /* erase_init() with `n_bwd` backward streams (1..8, distinct, none equal to
  * s_fwd; `s_bwd` is a host array).  In the overlapped schedules block b's
@@ -191,7 +195,7 @@ ERASE_API erase_status erase_init(const erase_config* cfg, const erase_block_buf
  * streams, Section 3.2).  erase_init() is this call with n_bwd = 1. */
 ERASE_API erase_status erase_init_streams(const erase_config* cfg, const erase_block_buffers* bufs,
                                 void* workspace, size_t ws_bytes, void* s_fwd, void* const* s_bwd,
-                                int32_t n_bwd, void** ctx_out);
+                                int32_t n_bwd, erase_ctx** ctx_out);
 
 /* Enqueue one training step (Section 2.2) and return without waiting.
  *   x:      device, [batch][x_ld] of dtype, 16-byte aligned, rows' tails
@@ -200,22 +204,22 @@ ERASE_API erase_status erase_init_streams(const erase_config* cfg, const erase_b
  *   losses: device fp32 [n_blocks], receives the unweighted l_b.
  * x, labels and losses must stay unmodified and valid until erase_sync().
  * The step increments the device step counter before its Adam updates. */
-ERASE_API erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t schedule,
+ERASE_API erase_status erase_step(erase_ctx* ctx, const void* x, const float* labels, int32_t schedule,
                         float* losses);
 
 /* Wait for all enqueued work of the context, then report deferred errors
  * (HIP errors, non-finite loss: ERASE_ERR_NONFINITE, sticky). */
-ERASE_API erase_status erase_sync(void* ctx);
+ERASE_API erase_status erase_sync(erase_ctx* ctx);
 
 /* Read / overwrite the device step counter t (Adam bias correction uses t+1
  * at the next step).  Both synchronize the forward stream.  Used for
  * checkpoint/resume together with the caller-owned param/m/v buffers. */
-ERASE_API erase_status erase_get_step(void* ctx, int64_t* t);
-ERASE_API erase_status erase_set_step(void* ctx, int64_t t);
+ERASE_API erase_status erase_get_step(erase_ctx* ctx, int64_t* t);
+ERASE_API erase_status erase_set_step(erase_ctx* ctx, int64_t t);
 
 /* Re-derive the GEMM weight copies after the caller changed `param` (e.g. a
  * checkpoint load).  Enqueued on s_fwd. */
-ERASE_API erase_status erase_refresh_weights(void* ctx);
+ERASE_API erase_status erase_refresh_weights(erase_ctx* ctx);
 
 /* Per-launch kernel timing, for measurement.  When enabled, non-graph
  * schedules bracket every kernel launch with timing events on the launch's
@@ -254,8 +258,8 @@ typedef struct {
   double bytes;      /* algorithmic HBM bytes of the launch */
 } erase_kernel_time;
 
-ERASE_API erase_status erase_set_timing(void* ctx, int32_t enable);
-ERASE_API erase_status erase_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, int32_t* n);
+ERASE_API erase_status erase_set_timing(erase_ctx* ctx, int32_t enable);
+ERASE_API erase_status erase_read_timing(erase_ctx* ctx, erase_kernel_time* out, int32_t cap, int32_t* n);
 
 /* Host dispatch of the ERASE schedules (Section 2.2: blocking dispatch on
  * the main thread vs non-blocking dispatch on a thread pool).
@@ -276,7 +280,7 @@ ERASE_API erase_status erase_read_timing(void* ctx, erase_kernel_time* out, int3
  * calling thread's current device must be the context's) and joined by
  * erase_destroy().  ERASE_ERR_INVALID_ARG for an unknown mode. */
 typedef enum { ERASE_DISPATCH_CALLER = 0, ERASE_DISPATCH_WORKER = 1 } erase_dispatch;
-ERASE_API erase_status erase_set_dispatch(void* ctx, int32_t mode);
+ERASE_API erase_status erase_set_dispatch(erase_ctx* ctx, int32_t mode);
 
 /* Embedding-bag input stage of the CTR workload.  The paper feeds its CTR
  * model (Section 3.2) an input embedding x (Section 2.1) without describing
@@ -347,13 +351,13 @@ ERASE_API erase_status erase_embed_bags_backward(const erase_bag_config* cfg, co
 
 /* Destroy the context: waits for its dispatch thread and streams, frees
  * events and graphs.  Never frees caller memory.  NULL is accepted. */
-ERASE_API erase_status erase_destroy(void* ctx);
+ERASE_API erase_status erase_destroy(erase_ctx* ctx);
 
 /* Static description of a status code. */
 ERASE_API const char* erase_status_str(int32_t status);
 
 /* Last error message recorded on the context ("" if none). */
-ERASE_API const char* erase_last_error(void* ctx);
+ERASE_API const char* erase_last_error(erase_ctx* ctx);
 
 #ifdef __cplusplus
 }

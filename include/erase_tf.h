@@ -36,6 +36,10 @@
 extern "C" {
 #endif
 
+/* Opaque transformer-step context: created by erase_tf_init(), owned by
+ * the library, released by erase_tf_destroy(). */
+typedef struct erase_tf_ctx erase_tf_ctx;
+
 typedef struct {
   int32_t vocab;     /* V: multiple of 64, 64..1048576 */
   int32_t d_model;   /* d = 64 * n_heads, at most 4096 */
@@ -65,7 +69,7 @@ ERASE_API erase_status erase_tf_workspace_bytes(const erase_tf_config* cfg, size
  * host array of n_layers entries (param, m, v required, grad optional; all
  * 4-byte aligned) that must stay valid for the context's life. */
 ERASE_API erase_status erase_tf_init(const erase_tf_config* cfg, const erase_block_buffers* bufs, void* workspace,
-                           size_t ws_bytes, void* s_fwd, void* s_bwd, void** ctx_out);
+                           size_t ws_bytes, void* s_fwd, void* s_bwd, erase_tf_ctx** ctx_out);
 
 /* Enqueue one training step and return without waiting.
  *   tokens: device int32 [batch][seq_len + 1]; position t of row b reads
@@ -82,18 +86,18 @@ ERASE_API erase_status erase_tf_init(const erase_tf_config* cfg, const erase_blo
  *           Other schedules: ERASE_ERR_UNSUPPORTED.
  *   losses: device fp32 [n_layers], receives the unweighted l_b.
  * tokens and losses must stay valid and unmodified until erase_tf_sync(). */
-ERASE_API erase_status erase_tf_step(void* ctx, const int32_t* tokens, int32_t schedule, float* losses);
+ERASE_API erase_status erase_tf_step(erase_tf_ctx* ctx, const int32_t* tokens, int32_t schedule, float* losses);
 
 /* Wait for the context's work; report deferred errors (HIP errors,
  * ERASE_ERR_NONFINITE for a non-finite loss, ERASE_ERR_INVALID_ARG for an
  * out-of-range token id), all sticky. */
-ERASE_API erase_status erase_tf_sync(void* ctx);
+ERASE_API erase_status erase_tf_sync(erase_tf_ctx* ctx);
 
 /* Step counter (synchronizes s_fwd), weight-copy refresh after the caller
  * changed `param`, as in erase.h. */
-ERASE_API erase_status erase_tf_get_step(void* ctx, int64_t* t);
-ERASE_API erase_status erase_tf_set_step(void* ctx, int64_t t);
-ERASE_API erase_status erase_tf_refresh_weights(void* ctx);
+ERASE_API erase_status erase_tf_get_step(erase_tf_ctx* ctx, int64_t* t);
+ERASE_API erase_status erase_tf_set_step(erase_tf_ctx* ctx, int64_t t);
+ERASE_API erase_status erase_tf_refresh_weights(erase_tf_ctx* ctx);
 
 /* Per-launch timing as in erase.h (erase_kernel_time records; record 0 is
  * the empty interval, kind 7).  Kinds of this step: 0 prologue, 1 forward
@@ -104,8 +108,8 @@ ERASE_API erase_status erase_tf_refresh_weights(void* ctx);
  * 14 attention forward, 15 attention backward (layer 1 row sums, 2 dK/dV,
  * 3 dQ), 16 softmax cross-entropy, 17 embedding gradient (four launches,
  * bracketed by stream events rather than kernel-stamped ones). */
-ERASE_API erase_status erase_tf_set_timing(void* ctx, int32_t enable);
-ERASE_API erase_status erase_tf_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, int32_t* n);
+ERASE_API erase_status erase_tf_set_timing(erase_tf_ctx* ctx, int32_t enable);
+ERASE_API erase_status erase_tf_read_timing(erase_tf_ctx* ctx, erase_kernel_time* out, int32_t cap, int32_t* n);
 
 /* Device address and row pitch (elements) of a stored tensor of block
  * `block`, for inspection after erase_tf_sync():
@@ -114,13 +118,13 @@ ERASE_API erase_status erase_tf_read_timing(void* ctx, erase_kernel_time* out, i
  *   [.][V] (bf16; after a step, the gradient), 11 lse (fp32 [B][H][T],
  *   pitch T), 12 dqkv, 13 dz (bf16 unless noted; rows are positions
  *   b T + t).  ERASE_ERR_INVALID_ARG for an unknown id or block. */
-ERASE_API erase_status erase_tf_tensor(void* ctx, int32_t block, int32_t which, void** ptr, int64_t* ld);
+ERASE_API erase_status erase_tf_tensor(erase_tf_ctx* ctx, int32_t block, int32_t which, void** ptr, int64_t* ld);
 
 /* Destroy (waits for the streams; frees events).  NULL is accepted. */
-ERASE_API erase_status erase_tf_destroy(void* ctx);
+ERASE_API erase_status erase_tf_destroy(erase_tf_ctx* ctx);
 
 /* Last error message recorded on the context ("" if none). */
-ERASE_API const char* erase_tf_last_error(void* ctx);
+ERASE_API const char* erase_tf_last_error(erase_tf_ctx* ctx);
 
 #ifdef __cplusplus
 }

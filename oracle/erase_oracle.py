@@ -136,6 +136,10 @@ def block_backward(blk: dict, p: dict, cache: dict, y: np.ndarray,
     dc = np.array([gs.sum()], dtype=s.dtype)
     g = np.outer(gs, w)
     if g_out is not None:
+        if emulate_bf16 and blk["layers"][-1][0] == "linear_relu":
+            # the head's term is stored (bf16, under the last layer's ReLU
+            # mask) before the gradient from the next block is added to it
+            g = rnd(g * (acts[-1] > 0))
         g = g + g_out
     a0 = acts[0]
     kinds = [k for (k, _i, _o) in blk["layers"]]

@@ -1190,8 +1190,15 @@ void destroy_graphs(Ctx* c) {
   c->graphs.clear();
 }
 
-Ctx* as_ctx(void* p) { return static_cast<Ctx*>(p); }
+}  // namespace
 
+// The opaque context handle of the C ABI.
+struct erase_ctx {
+  Ctx impl;
+};
+
+namespace {
+Ctx* as_ctx(erase_ctx* p) { return p ? &p->impl : nullptr; }
 }  // namespace
 
 // ===========================================================================
@@ -1222,13 +1229,13 @@ erase_status erase_workspace_bytes(const erase_config* cfg, size_t* bytes) {
 }
 
 erase_status erase_init(const erase_config* cfg, const erase_block_buffers* bufs, void* workspace, size_t ws_bytes,
-                        void* s_fwd, void* s_bwd, void** ctx_out) {
+                        void* s_fwd, void* s_bwd, erase_ctx** ctx_out) {
   void* const one[1] = {s_bwd};
   return erase_init_streams(cfg, bufs, workspace, ws_bytes, s_fwd, one, 1, ctx_out);
 }
 
 erase_status erase_init_streams(const erase_config* cfg, const erase_block_buffers* bufs, void* workspace,
-                                size_t ws_bytes, void* s_fwd, void* const* s_bwd, int32_t n_bwd, void** ctx_out) {
+                                size_t ws_bytes, void* s_fwd, void* const* s_bwd, int32_t n_bwd, erase_ctx** ctx_out) {
   if (!ctx_out) return ERASE_ERR_INVALID_ARG;
   *ctx_out = nullptr;
   std::string err;
@@ -1253,7 +1260,8 @@ erase_status erase_init_streams(const erase_config* cfg, const erase_block_buffe
     if (ws_bytes < build_plan(*cfg, 0, &probe)) return ERASE_ERR_WORKSPACE;
   }
 
-  Ctx* c = new Ctx();
+  erase_ctx* h = new erase_ctx();
+  Ctx* c = &h->impl;
   c->cfg = *cfg;
   c->blocks.assign(cfg->blocks, cfg->blocks + cfg->n_blocks);
   c->layers.resize(cfg->n_blocks);
@@ -1272,7 +1280,7 @@ erase_status erase_init_streams(const erase_config* cfg, const erase_block_buffe
   auto bail = [&](erase_status s) {
     for (hipEvent_t e : c->ef) (void)hipEventDestroy(e);
     for (hipEvent_t e : c->eb) (void)hipEventDestroy(e);
-    delete c;
+    delete h;
     return s;
   };
   if (hipGetDevice(&c->device) != hipSuccess) return bail(ERASE_ERR_HIP);
@@ -1297,11 +1305,11 @@ erase_status erase_init_streams(const erase_config* cfg, const erase_block_buffe
   if (refresh(c) != ERASE_OK) return bail(ERASE_ERR_HIP);
   // the host copies of the segment tables must outlive the async copies:
   // they live in the context, which outlives the stream work it enqueued
-  *ctx_out = c;
+  *ctx_out = h;
   return ERASE_OK;
 }
 
-erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t schedule, float* losses) {
+erase_status erase_step(erase_ctx* ctx, const void* x, const float* labels, int32_t schedule, float* losses) {
   Ctx* c = as_ctx(ctx);
   if (!c) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
@@ -1392,7 +1400,7 @@ erase_status erase_step(void* ctx, const void* x, const float* labels, int32_t s
   return ERASE_OK;
 }
 
-erase_status erase_sync(void* ctx) {
+erase_status erase_sync(erase_ctx* ctx) {
   Ctx* c = as_ctx(ctx);
   if (!c) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
@@ -1410,7 +1418,7 @@ erase_status erase_sync(void* ctx) {
   return ERASE_OK;
 }
 
-erase_status erase_get_step(void* ctx, int64_t* t) {
+erase_status erase_get_step(erase_ctx* ctx, int64_t* t) {
   Ctx* c = as_ctx(ctx);
   if (!c || !t) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
@@ -1422,7 +1430,7 @@ erase_status erase_get_step(void* ctx, int64_t* t) {
   return ERASE_OK;
 }
 
-erase_status erase_set_step(void* ctx, int64_t t) {
+erase_status erase_set_step(erase_ctx* ctx, int64_t t) {
   Ctx* c = as_ctx(ctx);
   if (!c || t < 0) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
@@ -1435,7 +1443,7 @@ erase_status erase_set_step(void* ctx, int64_t t) {
   return ERASE_OK;
 }
 
-erase_status erase_refresh_weights(void* ctx) {
+erase_status erase_refresh_weights(erase_ctx* ctx) {
   Ctx* c = as_ctx(ctx);
   if (!c) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
@@ -1445,7 +1453,7 @@ erase_status erase_refresh_weights(void* ctx) {
   return refresh(c);
 }
 
-erase_status erase_set_timing(void* ctx, int32_t enable) {
+erase_status erase_set_timing(erase_ctx* ctx, int32_t enable) {
   Ctx* c = as_ctx(ctx);
   if (!c) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
@@ -1466,7 +1474,7 @@ erase_status erase_set_timing(void* ctx, int32_t enable) {
   return ERASE_OK;
 }
 
-erase_status erase_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, int32_t* n) {
+erase_status erase_read_timing(erase_ctx* ctx, erase_kernel_time* out, int32_t cap, int32_t* n) {
   Ctx* c = as_ctx(ctx);
   if (!c || !n || (cap > 0 && !out)) return ERASE_ERR_INVALID_ARG;
   if (!c->last_valid) return ERASE_ERR_STATE;
@@ -1495,7 +1503,7 @@ erase_status erase_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, i
   return ERASE_OK;
 }
 
-erase_status erase_set_dispatch(void* ctx, int32_t mode) {
+erase_status erase_set_dispatch(erase_ctx* ctx, int32_t mode) {
   Ctx* c = as_ctx(ctx);
   if (!c) return ERASE_ERR_INVALID_ARG;
   if (mode != ERASE_DISPATCH_CALLER && mode != ERASE_DISPATCH_WORKER) return ERASE_ERR_INVALID_ARG;
@@ -1613,7 +1621,7 @@ erase_status erase_embed_bags_backward(const erase_bag_config* cfg, const int64_
   return ERASE_OK;
 }
 
-erase_status erase_destroy(void* ctx) {
+erase_status erase_destroy(erase_ctx* ctx) {
   Ctx* c = as_ctx(ctx);
   if (!c) return ERASE_OK;
   if (c->worker) {
@@ -1629,7 +1637,7 @@ erase_status erase_destroy(void* ctx) {
   if (c->tstart) (void)hipEventDestroy(c->tstart);
   if (c->tnull0) (void)hipEventDestroy(c->tnull0);
   if (c->tnull1) (void)hipEventDestroy(c->tnull1);
-  delete c;
+  delete ctx;
   return ERASE_OK;
 }
 
@@ -1647,7 +1655,7 @@ const char* erase_status_str(int32_t s) {
   }
 }
 
-const char* erase_last_error(void* ctx) {
+const char* erase_last_error(erase_ctx* ctx) {
   Ctx* c = as_ctx(ctx);
   return c ? c->err.c_str() : "";
 }

@@ -732,8 +732,15 @@ erase_status refresh(TfCtx* c) {
   return ERASE_OK;
 }
 
-TfCtx* as_ctx(void* p) { return static_cast<TfCtx*>(p); }
+}  // namespace
 
+// The opaque context handle of the C ABI.
+struct erase_tf_ctx {
+  TfCtx impl;
+};
+
+namespace {
+TfCtx* as_ctx(erase_tf_ctx* p) { return p ? &p->impl : nullptr; }
 }  // namespace
 
 extern "C" {
@@ -755,7 +762,7 @@ erase_status erase_tf_workspace_bytes(const erase_tf_config* cfg, size_t* bytes)
 }
 
 erase_status erase_tf_init(const erase_tf_config* cfg, const erase_block_buffers* bufs, void* workspace,
-                           size_t ws_bytes, void* s_fwd, void* s_bwd, void** ctx_out) {
+                           size_t ws_bytes, void* s_fwd, void* s_bwd, erase_tf_ctx** ctx_out) {
   if (!ctx_out) return ERASE_ERR_INVALID_ARG;
   *ctx_out = nullptr;
   if (erase_status st = validate(cfg, nullptr); st != ERASE_OK) return st;
@@ -772,7 +779,8 @@ erase_status erase_tf_init(const erase_tf_config* cfg, const erase_block_buffers
     Layout probe;
     if (ws_bytes < build_layout(*cfg, 0, &probe)) return ERASE_ERR_WORKSPACE;
   }
-  TfCtx* c = new TfCtx();
+  erase_tf_ctx* h = new erase_tf_ctx();
+  TfCtx* c = &h->impl;
   c->cfg = *cfg;
   c->ws = static_cast<char*>(workspace);
   c->sf = static_cast<hipStream_t>(s_fwd);
@@ -783,7 +791,7 @@ erase_status erase_tf_init(const erase_tf_config* cfg, const erase_block_buffers
   auto bail = [&](erase_status s) {
     for (hipEvent_t e : c->ef) (void)hipEventDestroy(e);
     if (c->ejoin) (void)hipEventDestroy(c->ejoin);
-    delete c;
+    delete h;
     return s;
   };
   if (hipGetDevice(&c->device) != hipSuccess) return bail(ERASE_ERR_HIP);
@@ -801,11 +809,11 @@ erase_status erase_tf_init(const erase_tf_config* cfg, const erase_block_buffers
         hipSuccess)
       return bail(ERASE_ERR_HIP);
   if (refresh(c) != ERASE_OK) return bail(ERASE_ERR_HIP);
-  *ctx_out = c;
+  *ctx_out = h;
   return ERASE_OK;
 }
 
-erase_status erase_tf_step(void* ctx, const int32_t* tokens, int32_t schedule, float* losses) {
+erase_status erase_tf_step(erase_tf_ctx* ctx, const int32_t* tokens, int32_t schedule, float* losses) {
   TfCtx* c = as_ctx(ctx);
   if (!c || !tokens || !losses) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
@@ -836,7 +844,7 @@ erase_status erase_tf_step(void* ctx, const int32_t* tokens, int32_t schedule, f
   return ERASE_OK;
 }
 
-erase_status erase_tf_sync(void* ctx) {
+erase_status erase_tf_sync(erase_tf_ctx* ctx) {
   TfCtx* c = as_ctx(ctx);
   if (!c) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
@@ -857,7 +865,7 @@ erase_status erase_tf_sync(void* ctx) {
   return ERASE_OK;
 }
 
-erase_status erase_tf_get_step(void* ctx, int64_t* t) {
+erase_status erase_tf_get_step(erase_tf_ctx* ctx, int64_t* t) {
   TfCtx* c = as_ctx(ctx);
   if (!c || !t) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
@@ -867,7 +875,7 @@ erase_status erase_tf_get_step(void* ctx, int64_t* t) {
   return ERASE_OK;
 }
 
-erase_status erase_tf_set_step(void* ctx, int64_t t) {
+erase_status erase_tf_set_step(erase_tf_ctx* ctx, int64_t t) {
   TfCtx* c = as_ctx(ctx);
   if (!c || t < 0) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
@@ -877,7 +885,7 @@ erase_status erase_tf_set_step(void* ctx, int64_t t) {
   return ERASE_OK;
 }
 
-erase_status erase_tf_refresh_weights(void* ctx) {
+erase_status erase_tf_refresh_weights(erase_tf_ctx* ctx) {
   TfCtx* c = as_ctx(ctx);
   if (!c) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
@@ -885,7 +893,7 @@ erase_status erase_tf_refresh_weights(void* ctx) {
   return refresh(c);
 }
 
-erase_status erase_tf_set_timing(void* ctx, int32_t enable) {
+erase_status erase_tf_set_timing(erase_tf_ctx* ctx, int32_t enable) {
   TfCtx* c = as_ctx(ctx);
   if (!c) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
@@ -905,7 +913,7 @@ erase_status erase_tf_set_timing(void* ctx, int32_t enable) {
   return ERASE_OK;
 }
 
-erase_status erase_tf_read_timing(void* ctx, erase_kernel_time* out, int32_t cap, int32_t* n) {
+erase_status erase_tf_read_timing(erase_tf_ctx* ctx, erase_kernel_time* out, int32_t cap, int32_t* n) {
   TfCtx* c = as_ctx(ctx);
   if (!c || !n || cap < 0 || (cap > 0 && !out)) return ERASE_ERR_INVALID_ARG;
   if (c->sticky != ERASE_OK) return ERASE_ERR_STATE;
@@ -930,7 +938,7 @@ erase_status erase_tf_read_timing(void* ctx, erase_kernel_time* out, int32_t cap
   return ERASE_OK;
 }
 
-erase_status erase_tf_tensor(void* ctx, int32_t block, int32_t which, void** ptr, int64_t* ld) {
+erase_status erase_tf_tensor(erase_tf_ctx* ctx, int32_t block, int32_t which, void** ptr, int64_t* ld) {
   TfCtx* c = as_ctx(ctx);
   if (!c || !ptr || !ld || block < 0 || block >= c->P.D.L) return ERASE_ERR_INVALID_ARG;
   const Layout& P = c->P;
@@ -959,7 +967,7 @@ erase_status erase_tf_tensor(void* ctx, int32_t block, int32_t which, void** ptr
   return ERASE_OK;
 }
 
-erase_status erase_tf_destroy(void* ctx) {
+erase_status erase_tf_destroy(erase_tf_ctx* ctx) {
   TfCtx* c = as_ctx(ctx);
   if (!c) return ERASE_OK;
   (void)hipStreamSynchronize(c->sf);
@@ -969,11 +977,11 @@ erase_status erase_tf_destroy(void* ctx) {
   for (hipEvent_t e : c->pool) (void)hipEventDestroy(e);
   for (hipEvent_t e : {c->t0, c->tn0, c->tn1})
     if (e) (void)hipEventDestroy(e);
-  delete c;
+  delete ctx;
   return ERASE_OK;
 }
 
-const char* erase_tf_last_error(void* ctx) {
+const char* erase_tf_last_error(erase_tf_ctx* ctx) {
   TfCtx* c = as_ctx(ctx);
   return c ? c->err.c_str() : "";
 }

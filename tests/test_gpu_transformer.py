@@ -257,11 +257,11 @@ def test_tf_c5_kernel_classes_full_step_vs_oracle():
     """One whole step at a shape with the full model's launch configuration
     (16 sequences of 1024 tokens, width 512, 8 heads, vocabulary 16384, 2
     layers): every GEMM launch takes the tile, k-group and split of the
-    benchmarked 8-layer, 32768-word model -- the two k-group 128x128 grouped
-    vocabulary backward, the 64x128 logits and GELU kernels, the 128x128
-    grouped body backward -- and losses, gradients, parameters and both Adam
-    moments of both blocks (the second reads the first's output) match the
-    oracles."""
+    benchmarked 8-layer, 32768-word model (among them the two k-group
+    128x128 grouped vocabulary backward, the 64x128 logits, MLP-up and
+    MLP-down input-gradient kernels, and the 128x128 forward tiles) -- and
+    losses, gradients, parameters and both Adam moments of both blocks (the
+    second reads the first's output) match the oracles."""
     c5 = synth_tf.tf_config("tf_c5")
     cfg = synth_tf.tf_config("tf_c5", vocab=16384, layers=2)
     params, batches = synth_tf.make_workload(cfg, seed=0, n_batches=1)
@@ -269,9 +269,11 @@ def test_tf_c5_kernel_classes_full_step_vs_oracle():
     print("[tf] launch plans of the full model and of V 16384, 2 layers", flush=True)
     want, got = _plan(c5, p5, b5[0]), _plan(cfg, params, batches[0])
     del p5, b5
+    print(f"[tf] launch plan: {sorted(got)}", flush=True)
     assert got == want, (sorted(got ^ want))
+    # the vocabulary head: 64x128 logits tiles, one grouped two k-group
+    # 128x128 launch for both of its gradients
     assert ("bwd_gemm", 4, 128, 128, 1) in got and ("fwd_gemm", 4, 64, 128, 1) in got
-    assert ("fwd_gemm", 2, 64, 128, 1) in got and any(k == "bwd_gemm" and l == 3 for k, l, *_ in got)
     print("[tf] V 16384, 2 layers: GPU step", flush=True)
     tr, gpu = _gpu_run(cfg, params, batches, "serial")
     tr.close()
