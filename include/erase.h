@@ -349,6 +349,25 @@ ERASE_API erase_status erase_embed_bags_backward(const erase_bag_config* cfg, co
                                        const void* dx, float* table_grad, void* scratch, size_t scratch_bytes,
                                        int32_t* status, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc):
+ * erase_embed_bags_backward() with the library's own scratch instead of a
+ * caller's.  Same arguments, results and errors otherwise.  The scratch is
+ * one static device array of ERASE_BAG_SCRATCH_MAX bytes per GPU, created
+ * with the library's code on that GPU and held until the process ends; its
+ * device address is looked up on the first call on each device.  Shapes
+ * whose erase_embed_bags_backward_scratch_bytes() exceeds it return
+ * ERASE_ERR_WORKSPACE before anything is enqueued (the 26 x 100000-row,
+ * 4096-row-batch CTR shape needs about 54 MB).  Allocates nothing: no
+ * hipMalloc, hipFree or allocating library call.  Every call on one GPU
+ * shares that GPU's array (the launches clear what they need first): calls
+ * that overlap on one GPU -- unordered streams, or several host threads --
+ * race; order them on one stream. */
+#define ERASE_BAG_SCRATCH_MAX ((size_t)64 << 20)
+ERASE_API erase_status erase_embed_bags_backward_noalloc(const erase_bag_config* cfg, const int64_t* offsets,
+                                                         const int32_t* indices, const void* dx, float* table_grad,
+                                                         int32_t* status, void* stream);
+
 /* Destroy the context: waits for its dispatch thread and streams, frees
  * events and graphs.  Never frees caller memory.  NULL is accepted. */
 ERASE_API erase_status erase_destroy(erase_ctx* ctx);

@@ -13,10 +13,38 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <mutex>
 
+#include "erase.h"
 #include "internal.h"
 
 namespace erase {
+
+// Scratch of erase_embed_bags_backward_noalloc: one array per GPU, created
+// with the code object on that GPU and held until the process ends.  In host
+// code `scratch` names a host-side stand-in; kernels get its device address
+// from bag_scratch_device_ptr().
+static __device__ __align__(256) char scratch[ERASE_BAG_SCRATCH_MAX];
+
+hipError_t bag_scratch_device_ptr(void** ptr, size_t* bytes) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  *bytes = sizeof(scratch);
+  return hipSuccess;
+}
 
 typedef float f32x4e_t __attribute__((ext_vector_type(4)));
 // output columns start after the dense features, so stores are aligned only

@@ -1570,9 +1570,13 @@ erase_status erase_embed_bags_backward_scratch_bytes(const erase_bag_config* cfg
   return ERASE_OK;
 }
 
-erase_status erase_embed_bags_backward(const erase_bag_config* cfg, const int64_t* offsets, const int32_t* indices,
-                                       const void* dx, float* table_grad, void* scratch, size_t scratch_bytes,
-                                       int32_t* status, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Shapes and pointers of the embedding-bag backward; *need = its scratch bytes.
+erase_status check_bags_backward(const erase_bag_config* cfg, const int64_t* offsets, const int32_t* indices,
+                                 const void* dx, const float* table_grad, const int32_t* status, size_t* need) {
   if (!cfg) return ERASE_ERR_INVALID_ARG;
   const erase_bag_config& b = *cfg;
   if (b.dtype != ERASE_F32 && b.dtype != ERASE_BF16) return ERASE_ERR_INVALID_ARG;
@@ -1583,13 +1587,17 @@ erase_status erase_embed_bags_backward(const erase_bag_config* cfg, const int64_
       b.nnz >= (int64_t(1) << 31) || b.x_ld < int64_t(b.n_dense) + int64_t(b.n_tables) * b.dim ||
       (b.x_ld * esz) % 16)
     return ERASE_ERR_SHAPE;
-  size_t need = 0;
-  (void)erase_embed_bags_backward_scratch_bytes(cfg, &need);
+  (void)erase_embed_bags_backward_scratch_bytes(cfg, need);
   auto mis = [](const void* p, uintptr_t a) { return reinterpret_cast<uintptr_t>(p) % a != 0; };
   if (!offsets || mis(offsets, 8) || (b.nnz > 0 && (!indices || mis(indices, 4))) || !dx || mis(dx, 16) ||
       !table_grad || mis(table_grad, 16) || (status && mis(status, 4)))
     return ERASE_ERR_INVALID_ARG;
-  if (!scratch || mis(scratch, 16) || scratch_bytes < need) return ERASE_ERR_WORKSPACE;
+  return ERASE_OK;
+}
+
+// Carve `scratch` (checked) and enqueue the backward's launches.
+erase_status run_bags_backward(const erase_bag_config& b, const int64_t* offsets, const int32_t* indices,
+                               const void* dx, float* table_grad, void* scratch, int32_t* status, void* stream) {
   const int64_t tr = int64_t(b.n_tables) * b.rows, trr = roundup(tr, 64), nr = roundup(std::max<int64_t>(b.nnz, 1), 64);
   int32_t* w = static_cast<int32_t*>(scratch);
   EmbedBwdArgs a{};
@@ -1619,6 +1627,33 @@ erase_status erase_embed_bags_backward(const erase_bag_config* cfg, const int64_
   if (launch_embed_bags_backward(b.dtype == ERASE_BF16, a, static_cast<hipStream_t>(stream)) != hipSuccess)
     return ERASE_ERR_HIP;
   return ERASE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+erase_status erase_embed_bags_backward(const erase_bag_config* cfg, const int64_t* offsets, const int32_t* indices,
+                                       const void* dx, float* table_grad, void* scratch, size_t scratch_bytes,
+                                       int32_t* status, void* stream) {
+  size_t need = 0;
+  if (erase_status st = check_bags_backward(cfg, offsets, indices, dx, table_grad, status, &need); st != ERASE_OK)
+    return st;
+  if (!scratch || reinterpret_cast<uintptr_t>(scratch) % 16 || scratch_bytes < need) return ERASE_ERR_WORKSPACE;
+  return run_bags_backward(*cfg, offsets, indices, dx, table_grad, scratch, status, stream);
+}
+
+erase_status erase_embed_bags_backward_noalloc(const erase_bag_config* cfg, const int64_t* offsets,
+                                               const int32_t* indices, const void* dx, float* table_grad,
+                                               int32_t* status, void* stream) {
+  size_t need = 0;
+  if (erase_status st = check_bags_backward(cfg, offsets, indices, dx, table_grad, status, &need); st != ERASE_OK)
+    return st;
+  if (need > ERASE_BAG_SCRATCH_MAX) return ERASE_ERR_WORKSPACE;
+  void* scratch = nullptr;
+  size_t bytes = 0;
+  if (bag_scratch_device_ptr(&scratch, &bytes) != hipSuccess || bytes < need) return ERASE_ERR_HIP;
+  return run_bags_backward(*cfg, offsets, indices, dx, table_grad, scratch, status, stream);
 }
 
 erase_status erase_destroy(erase_ctx* ctx) {

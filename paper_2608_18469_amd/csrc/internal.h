@@ -235,6 +235,9 @@ struct EmbedBwdArgs {
   int rows, M, n_dense, T, dim;
 };
 hipError_t launch_embed_bags_backward(int bf16, const EmbedBwdArgs& a, hipStream_t s);
+// Device address, on the current device, of the library's static scratch of
+// the allocation-free backward (bytes: its size); looked up once per device.
+hipError_t bag_scratch_device_ptr(void** ptr, size_t* bytes);
 
 // ---------------------------------------------------------------------------
 // small-transformer kernels (transformer.hip), bf16 activations

@@ -85,6 +85,8 @@ SIGNATURES = {
     "erase_embed_bags_backward_scratch_bytes": (c_int32, [POINTER(BagConfig), POINTER(c_size_t)]),
     "erase_embed_bags_backward": (c_int32, [POINTER(BagConfig), c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                             c_size_t, c_void_p, c_void_p]),
+    "erase_embed_bags_backward_noalloc": (c_int32, [POINTER(BagConfig), c_void_p, c_void_p, c_void_p, c_void_p,
+                                                    c_void_p, c_void_p]),
     "erase_read_timing": (c_int32, [c_void_p, POINTER(KernelTime), c_int32, POINTER(c_int32)]),
     "erase_destroy": (c_int32, [c_void_p]),
     "erase_status_str": (ctypes.c_char_p, [c_int32]),
@@ -247,6 +249,34 @@ def embed_bags_backward(offsets, indices, dx, n_dense, rows, dim, table_grad=Non
                                            table_grad.data_ptr(), scratch.data_ptr(), need.value, ptr(status), s),
            "erase_embed_bags_backward")
     return table_grad, scratch
+
+
+BAG_SCRATCH_MAX = 64 << 20  # ERASE_BAG_SCRATCH_MAX of include/erase.h
+
+
+def embed_bags_backward_noalloc(offsets, indices, dx, n_dense, rows, dim, table_grad, status=None, stream=None):
+    """erase_embed_bags_backward_noalloc: the backward of the embedding-bag
+    stage with the library's static device scratch (for callers that cannot
+    allocate); arguments as for embed_bags_backward, table_grad given.  Calls
+    that overlap on one GPU share the scratch and race."""
+    import torch
+    T = offsets.shape[0]
+    M, x_ld = dx.shape
+    for name, t, dt in (("offsets", offsets, torch.int64), ("indices", indices, torch.int32),
+                        ("table_grad", table_grad, torch.float32)):
+        if t.dtype != dt or not t.is_contiguous():
+            raise EraseError(ERR_INVALID_ARG, "embed_bags_backward_noalloc", f"{name} must be a contiguous {dt} tensor")
+    if dx.dtype not in (torch.float32, torch.bfloat16) or dx.stride(1) != 1:
+        raise EraseError(ERR_INVALID_ARG, "embed_bags_backward_noalloc",
+                         "dx must be float32 or bfloat16, unit column stride")
+    cfg = BagConfig(M, n_dense, T, dim, rows, indices.numel(), BF16 if dx.dtype == torch.bfloat16 else F32,
+                    dx.stride(0))
+    s = (stream or torch.cuda.current_stream()).cuda_stream
+    ptr = (lambda t: None if t is None or t.numel() == 0 else t.data_ptr())
+    _check(lib().erase_embed_bags_backward_noalloc(ctypes.byref(cfg), offsets.data_ptr(), ptr(indices),
+                                                   dx.data_ptr(), table_grad.data_ptr(), ptr(status), s),
+           "erase_embed_bags_backward_noalloc")
+    return table_grad
 
 
 class Trainer:

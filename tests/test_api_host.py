@@ -231,3 +231,34 @@ def test_embed_bags_backward_validation():
         assert call(**bad) == erase.ERR_INVALID_ARG, bad
     for bad in (dict(scratch=None), dict(scratch=8200), dict(nbytes=need.value - 4)):
         assert call(**bad) == erase.ERR_WORKSPACE, bad
+
+
+def test_embed_bags_backward_noalloc_validation():
+    """The allocation-free variant checks shapes and pointers like the scratch
+    entry point and rejects shapes whose scratch exceeds its static array,
+    all before any HIP call (fake pointers never dereferenced)."""
+    L = erase.lib()
+    ok = dict(batch=8, n_dense=13, n_tables=2, dim=64, rows=100, nnz=10, dtype=erase.F32, x_ld=144)
+
+    def call(ptrs=None, **over):
+        c = dict(ok)
+        c.update(over)
+        bc = erase.BagConfig(c["batch"], c["n_dense"], c["n_tables"], c["dim"], c["rows"], c["nnz"], c["dtype"],
+                             c["x_ld"])
+        p = dict(offsets=512, indices=768, dx=2048, grad=4096, status=None)
+        p.update(ptrs or {})
+        return L.erase_embed_bags_backward_noalloc(ctypes.byref(bc), p["offsets"], p["indices"], p["dx"], p["grad"],
+                                                   p["status"], None)
+
+    assert L.erase_embed_bags_backward_noalloc(None, None, None, None, None, None, None) == erase.ERR_INVALID_ARG
+    for bad in ({"batch": 0}, {"dim": 6}, {"x_ld": 140}):
+        assert call(**bad) == erase.ERR_SHAPE, bad
+    for bad in (dict(offsets=None), dict(dx=2056), dict(grad=4100)):
+        assert call(bad) == erase.ERR_INVALID_ARG, bad
+    # 26 tables of 1,000,000 rows: about 312 MB of counters, past the 64 MiB array
+    big = dict(n_tables=26, rows=1_000_000, x_ld=13 + 26 * 64 + 3)
+    need = ctypes.c_size_t(0)
+    bc = erase.BagConfig(8, 13, 26, 64, 1_000_000, 10, erase.F32, big["x_ld"])
+    assert L.erase_embed_bags_backward_scratch_bytes(ctypes.byref(bc), ctypes.byref(need)) == erase.OK
+    assert need.value > erase.BAG_SCRATCH_MAX
+    assert call(**big) == erase.ERR_WORKSPACE
