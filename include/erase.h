@@ -329,19 +329,23 @@ ERASE_API erase_status erase_embed_bags(const erase_bag_config* cfg, const float
  *   table_grad[t][r][d] = sum over the entries i of the bags of table t with
  *                         indices[i] == r of dx[m(i)][n_dense + t*dim + d]
  * where m(i) is the bag (row of x) holding entry i.  Each row's entries are
- * summed in fp32 in a fixed order: in increasing entry order for rows of at
- * most 64 entries; rows of 65..16384 entries are sorted by entry, summed by
- * dim-wide lane groups that each take every (256/dim)-th entry in order, and
- * the groups added by a fixed butterfly; larger rows in increasing entry
- * order (by repeated selection: correct but slow).  The result does not
- * depend on scheduling; rows no entry selects are zero.  Bags must not overlap (each
- * entry belongs to at most one bag; entries of no bag are ignored).
+ * summed in fp32 in a fixed order of increasing entry index: rows of at most
+ * 64 entries by the lane groups of one wave (G = dim/4 rounded up to a
+ * power of two lanes each; entry k to group k mod 64/G, each group in order,
+ * the groups then added by a fixed butterfly); rows of 65..1024 entries by
+ * the lane groups of a 256-thread workgroup and rows of 1025..16384 entries
+ * by those of a 1024-thread one (entry k to group k mod threads/G, the
+ * groups' partial rows then added in group order); larger rows
+ * in increasing entry order (by repeated selection: correct but slow).  The
+ * result does not depend on scheduling; rows no entry selects are zero.
+ * Bags must not overlap (each entry belongs to at most one bag; entries of
+ * no bag are ignored).
  * Device pointers: offsets, indices as for erase_embed_bags; dx [batch][x_ld]
  * of dtype (16-byte aligned); table_grad fp32 [n_tables][rows][dim]
  * (16-byte aligned, fully written); scratch of
  * erase_embed_bags_backward_scratch_bytes() bytes (16-byte aligned, any
  * contents; the call clears what it needs); status as for erase_embed_bags
- * (invalid offsets or ids set it to 1).  Six launches on `stream`, no wait.
+ * (invalid offsets or ids set it to 1).  Eleven launches on `stream`, no wait.
  * ERASE_ERR_SHAPE also when n_tables * rows >= 2^31; ERASE_ERR_WORKSPACE for
  * a missing, misaligned or small scratch. */
 ERASE_API erase_status erase_embed_bags_backward_scratch_bytes(const erase_bag_config* cfg, size_t* bytes);
@@ -358,7 +362,7 @@ ERASE_API erase_status erase_embed_bags_backward(const erase_bag_config* cfg, co
  * device address is looked up on the first call on each device.  Shapes
  * whose erase_embed_bags_backward_scratch_bytes() exceeds it return
  * ERASE_ERR_WORKSPACE before anything is enqueued (the 26 x 100000-row,
- * 4096-row-batch CTR shape needs about 54 MB).  Allocates nothing: no
+ * 4096-row-batch CTR shape needs about 48 MB).  Allocates nothing: no
  * hipMalloc, hipFree or allocating library call.  Every call on one GPU
  * shares that GPU's array (the launches clear what they need first): calls
  * that overlap on one GPU -- unordered streams, or several host threads --

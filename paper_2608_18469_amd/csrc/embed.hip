@@ -156,23 +156,35 @@ hipError_t launch_embed_bags(int bf16, const EmbedArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-constexpr int kSmallBucket = 64;  // entries a wave orders from its registers
+constexpr int kSmallBucket = 64;  // entries a wave sorts in its registers
 constexpr int kSortCap = 16384;   // largest bucket sorted in LDS (64 KB)
 
 // ---------------------------------------------------------------------------
 // Backward: table gradients from the gradient at x.  Entry i (an index
 // position) belongs to the bag (t, m) whose range holds it; its global row
-// is t * rows + indices[i].  Entries are bucketed by global row with integer
-// counters, and each row's entries are summed in increasing entry order, so
-// the result does not depend on scheduling.
+// is t * rows + indices[i].  Entries are bucketed by global row (counts,
+// an exclusive scan, then each entry to its slot), every bucket is put in
+// increasing entry order, and each row is summed in a fixed order of its
+// entries, so the result does not depend on scheduling:
+//  * rows of at most 64 entries: one wave; entries sorted across its lanes,
+//    entry k to lane group k mod (64/G) (G lanes of 4 columns cover a row),
+//    each group adding its entries in order, the groups then combined by a
+//    fixed butterfly;
+//  * rows of 65..1024 entries: one workgroup of 256 threads, and rows of
+//    1025..16384 entries one of 1024 threads; entries sorted in LDS, entry
+//    k to lane group k mod (threads/G), the groups' partial rows then added
+//    in group order;
+//  * larger rows: increasing entry order, by repeated selection (correct but
+//    slow; no workload here has such a row);
+//  * rows no entry selects: zero, written by the waves that scan the counts.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void erase_bags_bwd_clear(EmbedBwdArgs a) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i == 0) a.nlarge[0] = 0;
-  if (i < a.trows) {
-    a.count[i] = 0;
-    a.fill[i] = 0;
+  if (i == 0) {
+    a.nlarge[0] = 0;  // rows listed for the large-bucket kernels
+    a.nlarge[1] = 0;  // rows of 1..kSmallBucket entries (set by the scans)
   }
+  if (i < a.trows) a.count[i] = 0;
   if (i < a.nnz) a.owner[i] = -1;
 }
 
@@ -189,30 +201,63 @@ __global__ __launch_bounds__(256) void erase_bags_bwd_owner(EmbedBwdArgs a) {
   for (int64_t i = beg; i < end; ++i) a.owner[i] = (int32_t)bag;
 }
 
-// one thread per entry: global row and its count
+// One thread per entry: its global row, and its slot in the row's bucket
+// from the row's counter.  The lanes of a wave that share a row add to its
+// counter once (a leader per row: Zipf-skewed ids repeat the hot rows many
+// times per wave, and every increment of one counter is serialised).
 __global__ __launch_bounds__(256) void erase_bags_bwd_count(EmbedBwdArgs a) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= a.nnz) return;
-  const int32_t o = a.owner[i];
+  const int lane = threadIdx.x & 63;
   int32_t gid = -1;
-  if (o >= 0) {
-    const int32_t r = a.indices[i];
-    if (r >= 0 && r < a.rows) {
-      gid = (int32_t)((o / a.M) * a.rows + r);
-      // a row whose count passes kSmallBucket is listed once for sorting
-      if (atomicAdd(&a.count[gid], 1) == kSmallBucket) a.large[atomicAdd(a.nlarge, 1)] = gid;
-    } else if (a.status) {
-      a.status[0] = 1;
+  if (i < a.nnz) {
+    const int32_t o = a.owner[i];
+    if (o >= 0) {
+      const int32_t r = a.indices[i];
+      if (r >= 0 && r < a.rows) {
+        gid = (int32_t)((o / a.M) * a.rows + r);
+      } else if (a.status) {
+        a.status[0] = 1;
+      }
     }
   }
-  a.gid[i] = gid;
+  // group the lanes by row: each lane learns its row's leader (the lowest
+  // lane of the row) and its rank among the row's lanes; each leader counts
+  int leader = 0, rank = 0, k = 0;
+  uint64_t pending = __ballot(gid >= 0);
+  while (pending) {
+    const int l0 = __ffsll((unsigned long long)pending) - 1;
+    const int32_t lg = __shfl(gid, l0, 64);
+    const uint64_t same = __ballot(gid == lg) & pending;
+    if (lane == l0) k = __popcll(same);
+    if ((same >> lane) & 1ull) {
+      leader = l0;
+      rank = __popcll(same & ((1ull << lane) - 1ull));
+    }
+    pending &= ~same;
+  }
+  // every leader adds to its row's counter at once (one round trip)
+  int32_t base = 0;
+  if (k > 0) {
+    base = atomicAdd(&a.count[gid], k);
+    // a row whose count passes kSmallBucket is listed once (exactly one
+    // addition crosses the threshold)
+    if (base <= kSmallBucket && base + k > kSmallBucket) a.large[atomicAdd(a.nlarge, 1)] = gid;
+  }
+  base = __shfl(base, leader, 64);
+  const int32_t slot = base + rank;
+  if (i < a.nnz) {
+    a.gid[i] = gid;
+    a.slot[i] = slot;
+  }
 }
 
-// Exclusive prefix sum of the counts in three passes: each workgroup scans
-// a block of kScanBlock counts (local offsets into start, the block total
-// into bsum), one workgroup scans the block totals, and the block offsets
-// are added.
-constexpr int kScanBlock = 4096;  // 256 threads x 16 counts
+// Exclusive prefix sums over the table rows in three passes, of the counts
+// (each bucket's start) and of the flags of rows with 1..kSmallBucket
+// entries (each such row's place in the list the row-sum kernel walks):
+// each workgroup sums a block of kScanBlock rows (count offsets into start,
+// block totals into bsum and bsum2), one workgroup scans the block totals,
+// and a last pass adds the block offsets and writes the list.
+constexpr int kScanBlock = 4096;  // 256 threads x 16 rows
 
 __device__ __forceinline__ int block_exclusive_scan(int v, int* part) {
   // exclusive scan of one value per thread over 256 threads (Hillis-Steele in LDS)
@@ -230,14 +275,17 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* part) {
   return incl - v;
 }
 
+__device__ __forceinline__ bool small_row(int c) { return c > 0 && c <= kSmallBucket; }
+
 __global__ __launch_bounds__(256) void erase_bags_bwd_scan_local(EmbedBwdArgs a) {
   __shared__ int part[256];
   const int64_t base = (int64_t)blockIdx.x * kScanBlock + threadIdx.x * 16;
-  int v[16], s = 0;
+  int v[16], s = 0, f = 0;
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
     v[k] = base + k < a.trows ? a.count[base + k] : 0;
     s += v[k];
+    f += small_row(v[k]) ? 1 : 0;
   }
   int run = block_exclusive_scan(s, part);
 #pragma unroll
@@ -245,77 +293,67 @@ __global__ __launch_bounds__(256) void erase_bags_bwd_scan_local(EmbedBwdArgs a)
     if (base + k < a.trows) a.start[base + k] = run;
     run += v[k];
   }
-  if (threadIdx.x == 255) a.bsum[blockIdx.x] = run;
+  const int fx = block_exclusive_scan(f, part);
+  if (threadIdx.x == 255) {
+    a.bsum[blockIdx.x] = run;
+    a.bsum2[blockIdx.x] = fx + f;
+  }
 }
 
-__global__ __launch_bounds__(256) void erase_bags_bwd_scan_blocks(EmbedBwdArgs a) {
-  __shared__ int part[256];
-  const int nb = (int)((a.trows + kScanBlock - 1) / kScanBlock);
+__device__ __forceinline__ int scan_totals(int* t, int nb, int* part) {
+  // exclusive scan of t[0..nb) in place; returns the total
   int carry = 0;
   for (int b0 = 0; b0 < nb; b0 += 256) {
     const int b = b0 + (int)threadIdx.x;
-    const int v = b < nb ? a.bsum[b] : 0;
+    const int v = b < nb ? t[b] : 0;
     const int ex = block_exclusive_scan(v, part);
-    if (b < nb) a.bsum[b] = carry + ex;
+    if (b < nb) t[b] = carry + ex;
     // the chunk's total, from the last thread's inclusive value
     if (threadIdx.x == 255) part[0] = ex + v;
     __syncthreads();
     carry += part[0];
     __syncthreads();
   }
+  return carry;
+}
+
+__global__ __launch_bounds__(256) void erase_bags_bwd_scan_blocks(EmbedBwdArgs a) {
+  __shared__ int part[256];
+  const int nb = (int)((a.trows + kScanBlock - 1) / kScanBlock);
+  (void)scan_totals(a.bsum, nb, part);
+  const int nsmall = scan_totals(a.bsum2, nb, part);
+  if (threadIdx.x == 0) a.nlarge[1] = nsmall;
 }
 
 __global__ __launch_bounds__(256) void erase_bags_bwd_scan_add(EmbedBwdArgs a) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < a.trows) a.start[i] += a.bsum[i / kScanBlock];
+  __shared__ int part[256];
+  const int64_t base = (int64_t)blockIdx.x * kScanBlock + threadIdx.x * 16;
+  const int off = a.bsum[blockIdx.x];
+  int f = 0;
+  bool fl[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    fl[k] = false;
+    if (base + k < a.trows) {
+      a.start[base + k] += off;
+      fl[k] = small_row(a.count[base + k]);
+    }
+    f += fl[k] ? 1 : 0;
+  }
+  int pos = a.bsum2[blockIdx.x] + block_exclusive_scan(f, part);
+#pragma unroll
+  for (int k = 0; k < 16; ++k)
+    if (fl[k]) a.small[pos++] = (int32_t)(base + k);
 }
 
+// one thread per entry: into its slot of its row's bucket (no atomics)
 __global__ __launch_bounds__(256) void erase_bags_bwd_scatter(EmbedBwdArgs a) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= a.nnz) return;
   const int32_t gid = a.gid[i];
-  if (gid >= 0) a.bucket[a.start[gid] + atomicAdd(&a.fill[gid], 1)] = (int32_t)i;
+  if (gid >= 0) a.bucket[a.start[gid] + a.slot[i]] = (int32_t)i;
 }
 
-// Buckets of more than kSmallBucket entries are sorted by entry index: one
-// workgroup of 1024 threads per listed bucket, a bitonic sort in LDS of up
-// to kSortCap entries (larger buckets keep the selection order below).
-__global__ __launch_bounds__(1024) void erase_bags_bwd_sort(EmbedBwdArgs a) {
-  __shared__ int32_t key[kSortCap];
-  if ((int)blockIdx.x >= a.nlarge[0]) return;  // uniform per workgroup
-  const int32_t g = a.large[blockIdx.x];
-  const int c = a.count[g], s0 = a.start[g];
-  if (c > kSortCap) return;
-  int n2 = 1;
-  while (n2 < c) n2 <<= 1;
-  for (int i = threadIdx.x; i < n2; i += 1024) key[i] = i < c ? a.bucket[s0 + i] : INT32_MAX;
-  __syncthreads();
-  for (int k = 2; k <= n2; k <<= 1)
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int i = threadIdx.x; i < n2; i += 1024) {
-        const int l = i ^ j;
-        if (l > i) {
-          const int32_t x = key[i], y = key[l];
-          if (((i & k) == 0) == (x > y)) {
-            key[i] = y;
-            key[l] = x;
-          }
-        }
-      }
-      __syncthreads();
-    }
-  for (int i = threadIdx.x; i < c; i += 1024) {
-    a.bucket[s0 + i] = key[i];
-    a.bagm[s0 + i] = a.owner[key[i]] % a.M;  // the entry's bag (row of dx)
-  }
-}
-
-// waves walk the table rows (grid-stride); per row the entries in increasing order, their
-// bags' dx columns summed in fp32; rows no entry selects are zero.  Small
-// buckets: each step the smallest entry above the last (a wave-wide
-// minimum over the entries held in registers); sorted buckets: in bucket
-// order; buckets too large to sort: the selection over the bucket.  dim / 4
-// lanes (dim <= 256) own 4 columns each.
 // 4 consecutive dx columns of bag row m, as fp32
 template <typename T>
 __device__ __forceinline__ float4 dx4(const EmbedBwdArgs& a, int m, int64_t xc) {
@@ -336,60 +374,179 @@ __device__ __forceinline__ void add4(float4& a, const float4& b) {
   a.w += b.w;
 }
 
+// Buckets of more than kSmallBucket entries (the listed rows): one workgroup
+// of NT threads per bucket of LO < c <= HI entries sorts it by entry in LDS
+// (bitonic, up to CAP entries), turns the entries into their bag rows, and
+// sums the row: lane group q (G lanes, 4 columns each) takes entries q,
+// q + NG, ... in order, then the NG partial rows are added in group order.
+// Buckets beyond CAP are summed in increasing entry order by repeated
+// selection.  Instances: 256 threads for 65..1024 entries, 1024 threads
+// above (kSortCap, 16384, sorted).
+constexpr int kMidBucket = 1024;
+template <typename T, int G, int NT, int CAP>
+__global__ __launch_bounds__(NT) void erase_bags_bwd_large(EmbedBwdArgs a, int lo, int hi) {
+  constexpr int NG = NT / G;  // lane groups of the workgroup
+  static_assert(NG * 4 * G <= CAP, "partial rows fit in the key array");
+  __shared__ int32_t key[CAP];
+  __shared__ int32_t sel[NT / 64];
+  if ((int)blockIdx.x >= a.nlarge[0]) return;  // uniform per workgroup
+  const int32_t g = a.large[blockIdx.x];
+  const int c = a.count[g], s0 = a.start[g];
+  if (c <= lo || c > hi) return;  // the other instance's bucket
+  const int tid = threadIdx.x;
+  const int q = tid / G, cq = tid % G;
+  const bool col = 4 * cq < a.dim;
+  const int t = g / a.rows;
+  const int64_t xc = a.n_dense + (int64_t)t * a.dim + 4 * cq;
+  float* out = a.grad + (int64_t)g * a.dim + 4 * cq;
+  if (c > CAP) {
+    // increasing entry order by repeated selection: a workgroup-wide minimum
+    // of the entries above the last one; group 0 adds
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    int32_t prev = -1;
+    for (int k = 0; k < c; ++k) {
+      int32_t cand = INT32_MAX;
+      for (int j = tid; j < c; j += NT) {
+        const int32_t p = a.bucket[s0 + j];
+        if (p > prev && p < cand) cand = p;
+      }
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) cand = min(cand, __shfl_xor(cand, o, 64));
+      if ((tid & 63) == 0) sel[tid >> 6] = cand;
+      __syncthreads();
+      cand = sel[0];
+      for (int w = 1; w < NT / 64; ++w) cand = min(cand, sel[w]);
+      __syncthreads();
+      prev = cand;
+      if (q == 0 && col) add4(acc, dx4<T>(a, a.owner[cand] % a.M, xc));
+    }
+    if (q == 0 && col) *reinterpret_cast<float4*>(out) = acc;
+    return;
+  }
+  int n2 = 1;
+  while (n2 < c) n2 <<= 1;
+  constexpr int PER = CAP / NT;  // keys per thread
+  {
+    int32_t tmp[PER];  // every load in flight before the LDS stores
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int i = tid + u * NT;
+      tmp[u] = i < c ? a.bucket[s0 + i] : INT32_MAX;
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u)
+      if (tid + u * NT < n2) key[tid + u * NT] = tmp[u];
+  }
+  __syncthreads();
+  for (int k = 2; k <= n2; k <<= 1)
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = tid; i < n2; i += NT) {
+        const int l = i ^ j;
+        if (l > i) {
+          const int32_t x = key[i], y = key[l];
+          if (((i & k) == 0) == (x > y)) {
+            key[i] = y;
+            key[l] = x;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  // entries -> their bag rows (rows of dx), in place (each thread its own keys)
+  {
+    int32_t tmp[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int i = tid + u * NT;
+      tmp[u] = i < c ? a.owner[key[i]] % a.M : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u)
+      if (tid + u * NT < c) key[tid + u * NT] = tmp[u];
+  }
+  __syncthreads();
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (col) {
+    int k = q;
+    for (; k + 15 * NG < c; k += 16 * NG) {
+      float4 v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) v[u] = dx4<T>(a, key[k + u * NG], xc);
+#pragma unroll
+      for (int u = 0; u < 16; ++u) add4(acc, v[u]);
+    }
+    for (; k < c; k += NG) add4(acc, dx4<T>(a, key[k], xc));
+  }
+  __syncthreads();  // key[] is reused for the partial rows
+  float* part = reinterpret_cast<float*>(key);  // [NG][4 G] floats
+  if (col) *reinterpret_cast<float4*>(part + q * 4 * G + 4 * cq) = acc;
+  __syncthreads();
+  if (tid < a.dim) {
+    float sum = 0.f;
+    for (int w = 0; w < NG; ++w) sum += part[w * 4 * G + tid];
+    a.grad[(int64_t)g * a.dim + tid] = sum;
+  }
+}
+
+// Bitonic sort (ascending) of one value per lane across a wave.
+__device__ __forceinline__ int32_t wave_sort(int32_t v, int lane) {
+#pragma unroll
+  for (int k = 2; k <= 64; k <<= 1)
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const int32_t o = __shfl_xor(v, j, 64);
+      const bool lower = (lane & j) == 0, up = (lane & k) == 0;
+      v = (lower == up) ? min(v, o) : max(v, o);
+    }
+  return v;
+}
+
+// Rows no entry selects: zeros, one 16-byte chunk per thread.
+__global__ __launch_bounds__(256) void erase_bags_bwd_zero(EmbedBwdArgs a) {
+  const int cpr = a.dim / 4;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= a.trows * cpr) return;
+  if (a.count[i / cpr] == 0) *reinterpret_cast<float4*>(a.grad + 4 * i) = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+// One wave per listed row of 1..kSmallBucket entries (grid-stride): its
+// entries sorted across the lanes, their bag rows looked up in parallel,
+// lane group q adding entries q, q + 64/G, ... in order (eight loads in
+// flight), the groups combined by a fixed butterfly.  (Loading the next
+// row's list entry, count and bucket during the current row's sums measured
+// slower: 146 against 131 us on the CTR shape.)
 template <typename T, int G>
 __global__ __launch_bounds__(256) void erase_bags_bwd_rows(EmbedBwdArgs a) {
-  constexpr int E = 64 / G;  // entries summed side by side by the lane groups of a sorted bucket
+  constexpr int NGW = 64 / G;  // lane groups per wave
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int q = lane / G, cq = lane % G;  // lane group, column quad
   const bool col = 4 * cq < a.dim;
-  const int64_t nw = (int64_t)gridDim.x * 4;
-  for (int64_t g = (int64_t)blockIdx.x * 4 + wave; g < a.trows; g += nw) {
+  const int n = a.nlarge[1];
+  for (int idx = (int)blockIdx.x * 4 + wave; idx < n; idx += (int)gridDim.x * 4) {
+    const int64_t g = a.small[idx];
+    const int c = a.count[g], s0 = a.start[g];
+    const int32_t e = wave_sort(lane < c ? a.bucket[s0 + lane] : INT32_MAX, lane);
+    const int m = lane < c ? a.owner[e] % a.M : 0;  // bag row of the lane's entry
     const int t = (int)(g / a.rows);
-    const int s0 = a.start[g], c = a.count[g];
     const int64_t xc = a.n_dense + (int64_t)t * a.dim + 4 * cq;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (c > kSmallBucket && c <= kSortCap) {
-      // sorted bucket, bag rows alongside: group q sums entries q, q + E,
-      // ... in increasing order, then the groups are added by a fixed butterfly
-      // eight entries' loads in flight, added in entry order
-      int k = q;
-      for (; k + 7 * E < c; k += 8 * E) {
-        float4 v[8];
+    for (int k0 = 0; k0 < c; k0 += 8 * NGW) {
+      float4 v[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = col ? dx4<T>(a, a.bagm[s0 + k + u * E], xc) : make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-        for (int u = 0; u < 8; ++u) add4(acc, v[u]);
+      for (int u = 0; u < 8; ++u) {
+        const int k = k0 + u * NGW + q;
+        const int mk = __shfl(m, k & 63, 64);
+        v[u] = (k < c && col) ? dx4<T>(a, mk, xc) : make_float4(0.f, 0.f, 0.f, 0.f);
       }
-      for (; k < c; k += E)
-        if (col) add4(acc, dx4<T>(a, a.bagm[s0 + k], xc));
 #pragma unroll
-      for (int o = G; o < 64; o <<= 1) {
-        acc.x += __shfl_xor(acc.x, o, 64);
-        acc.y += __shfl_xor(acc.y, o, 64);
-        acc.z += __shfl_xor(acc.z, o, 64);
-        acc.w += __shfl_xor(acc.w, o, 64);
-      }
-    } else {
-      // small buckets (and buckets too large to sort): each step the smallest
-      // entry above the last, a wave-wide minimum; entries held in
-      // registers when there are at most 64
-      const int32_t mine = lane < c ? a.bucket[s0 + lane] : INT32_MAX;
-      int32_t prev = -1;
-      for (int k = 0; k < c; ++k) {
-        int32_t cand = INT32_MAX;
-        if (c <= kSmallBucket) {
-          if (mine > prev) cand = mine;
-        } else {
-          for (int j = lane; j < c; j += 64) {
-            const int32_t p = a.bucket[s0 + j];
-            if (p > prev && p < cand) cand = p;
-          }
-        }
+      for (int u = 0; u < 8; ++u) add4(acc, v[u]);
+    }
 #pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) cand = min(cand, __shfl_xor(cand, o, 64));
-        prev = cand;
-        if (col) add4(acc, dx4<T>(a, a.owner[cand] % a.M, xc));
-      }
+    for (int o = G; o < 64; o <<= 1) {
+      acc.x += __shfl_xor(acc.x, o, 64);
+      acc.y += __shfl_xor(acc.y, o, 64);
+      acc.z += __shfl_xor(acc.z, o, 64);
+      acc.w += __shfl_xor(acc.w, o, 64);
     }
     if (col && q == 0) *reinterpret_cast<float4*>(a.grad + g * a.dim + 4 * cq) = acc;
   }
@@ -406,21 +563,37 @@ hipError_t launch_embed_bags_backward(int bf16, const EmbedBwdArgs& a, hipStream
     const unsigned nsb = (unsigned)((a.trows + kScanBlock - 1) / kScanBlock);
     hipLaunchKernelGGL(erase_bags_bwd_scan_local, dim3(nsb), dim3(256), 0, s, a);
     hipLaunchKernelGGL(erase_bags_bwd_scan_blocks, dim3(1), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(erase_bags_bwd_scan_add, dim3((unsigned)((a.trows + 255) / 256)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(erase_bags_bwd_scan_add, dim3(nsb), dim3(256), 0, s, a);
     hipLaunchKernelGGL(erase_bags_bwd_scatter, ge, dim3(256), 0, s, a);
-    // at most nnz / (kSmallBucket + 1) rows pass the small-bucket count
-    hipLaunchKernelGGL(erase_bags_bwd_sort, dim3((unsigned)(a.nnz / (kSmallBucket + 1) + 1)), dim3(1024), 0, s, a);
   }
-  // no entries: the counts are zero and no row reads start
-  const dim3 gr((unsigned)std::min<int64_t>((a.trows + 3) / 4, 8192));
-  int G = 1;  // lanes per entry: dim / 4 rounded up to a power of two
+  // rows no entry selects (every row when there are no entries): zeros
+  hipLaunchKernelGGL(erase_bags_bwd_zero, dim3((unsigned)((a.trows * (a.dim / 4) + 255) / 256)), dim3(256), 0, s, a);
+  int G = 1;  // lanes per row: dim / 4 rounded up to a power of two
   while (G < a.dim / 4) G *= 2;
-#define ERASE_BAG_ROWS(GG)                                                                   \
-  case GG:                                                                                   \
-    if (bf16)                                                                                \
-      hipLaunchKernelGGL((erase_bags_bwd_rows<uint16_t, GG>), gr, dim3(256), 0, s, a);       \
-    else                                                                                     \
-      hipLaunchKernelGGL((erase_bags_bwd_rows<float, GG>), gr, dim3(256), 0, s, a);          \
+  // listed rows of 1..kSmallBucket entries: at most min(rows, entries)
+  const int64_t nsmall_max = std::min<int64_t>(a.trows, std::max<int64_t>(a.nnz, 1));
+  const dim3 gr((unsigned)std::min<int64_t>((nsmall_max + 3) / 4, 16384));
+  // at most nnz / (kSmallBucket + 1) rows pass the small-bucket count
+  const dim3 gl((unsigned)(a.nnz / (kSmallBucket + 1) + 1));
+#define ERASE_BAG_ROWS(GG)                                                                                \
+  case GG:                                                                                                \
+    if (bf16) {                                                                                           \
+      if (a.nnz > 0) {                                                                                    \
+        hipLaunchKernelGGL((erase_bags_bwd_large<uint16_t, GG, 256, kMidBucket>), gl, dim3(256), 0, s, a,  \
+                           kSmallBucket, kMidBucket);                                                     \
+        hipLaunchKernelGGL((erase_bags_bwd_large<uint16_t, GG, 1024, kSortCap>), gl, dim3(1024), 0, s, a,  \
+                           kMidBucket, INT32_MAX);                                                        \
+      }                                                                                                   \
+      hipLaunchKernelGGL((erase_bags_bwd_rows<uint16_t, GG>), gr, dim3(256), 0, s, a);                    \
+    } else {                                                                                              \
+      if (a.nnz > 0) {                                                                                    \
+        hipLaunchKernelGGL((erase_bags_bwd_large<float, GG, 256, kMidBucket>), gl, dim3(256), 0, s, a,     \
+                           kSmallBucket, kMidBucket);                                                     \
+        hipLaunchKernelGGL((erase_bags_bwd_large<float, GG, 1024, kSortCap>), gl, dim3(1024), 0, s, a,     \
+                           kMidBucket, INT32_MAX);                                                        \
+      }                                                                                                   \
+      hipLaunchKernelGGL((erase_bags_bwd_rows<float, GG>), gr, dim3(256), 0, s, a);                       \
+    }                                                                                                     \
     break;
   switch (G) {
     ERASE_BAG_ROWS(1)

@@ -1566,7 +1566,7 @@ erase_status erase_embed_bags_backward_scratch_bytes(const erase_bag_config* cfg
     return ERASE_ERR_SHAPE;
   const int64_t tr = int64_t(b.n_tables) * b.rows;
   const int64_t nr = roundup(std::max<int64_t>(b.nnz, 1), 64);
-  *bytes = size_t(4) * size_t(3 * roundup(tr, 64) + 5 * nr + 64 + roundup(tr / 4096 + 1, 64));
+  *bytes = size_t(4) * size_t(2 * roundup(tr, 64) + 6 * nr + 64 + 2 * roundup(tr / 4096 + 1, 64));
   return ERASE_OK;
 }
 
@@ -1606,16 +1606,20 @@ erase_status run_bags_backward(const erase_bag_config& b, const int64_t* offsets
   a.dx = dx;
   a.lddx = b.x_ld;
   a.grad = table_grad;
+  // count and start per table row; bucket, row, owner, slot, and the lists
+  // of large and of small rows per entry; the lists' counters; two scan
+  // totals per 4096 rows
   a.count = w;
   a.start = w + trr;
-  a.fill = w + 2 * trr;
-  a.bucket = w + 3 * trr;
-  a.gid = w + 3 * trr + nr;
-  a.owner = w + 3 * trr + 2 * nr;
-  a.large = w + 3 * trr + 3 * nr;
-  a.nlarge = w + 3 * trr + 4 * nr;
-  a.bsum = w + 3 * trr + 4 * nr + 64;
-  a.bagm = a.bsum + roundup(tr / 4096 + 1, 64);
+  a.bucket = w + 2 * trr;
+  a.gid = w + 2 * trr + nr;
+  a.owner = w + 2 * trr + 2 * nr;
+  a.large = w + 2 * trr + 3 * nr;
+  a.slot = w + 2 * trr + 4 * nr;
+  a.small = w + 2 * trr + 5 * nr;
+  a.nlarge = w + 2 * trr + 6 * nr;
+  a.bsum = a.nlarge + 64;
+  a.bsum2 = a.bsum + roundup(tr / 4096 + 1, 64);
   a.status = status;
   a.nnz = b.nnz;
   a.trows = tr;

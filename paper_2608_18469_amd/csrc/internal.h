@@ -228,8 +228,8 @@ struct EmbedBwdArgs {
   const int32_t* indices;  // [nnz]
   const void* dx; int64_t lddx;  // [M][lddx] of the activation dtype
   float* grad;             // [T][rows][dim]
-  int32_t* count; int32_t* start; int32_t* fill; int32_t* bucket; int32_t* gid; int32_t* owner;
-  int32_t* large; int32_t* nlarge; int32_t* bsum; int32_t* bagm;
+  int32_t* count; int32_t* start; int32_t* bucket; int32_t* gid; int32_t* owner; int32_t* slot;
+  int32_t* large; int32_t* small; int32_t* nlarge; int32_t* bsum; int32_t* bsum2;
   int* status;
   int64_t nnz, trows;      // trows = T * rows < 2^31
   int rows, M, n_dense, T, dim;

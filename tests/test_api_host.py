@@ -208,10 +208,10 @@ def test_embed_bags_backward_validation():
     need = ctypes.c_size_t(0)
     gc = cfg_of(good)
     assert L.erase_embed_bags_backward_scratch_bytes(ctypes.byref(gc), ctypes.byref(need)) == erase.OK
-    # count, start, fill per table row; bucket, row id, owner, large-bucket
-    # list, bag of each sorted entry per entry (int32, padded to 64); the
-    # list's counter; one scan total per 4096 rows
-    assert need.value == 4 * (3 * 256 + 5 * 64 + 64 + 64)
+    # count, start per table row; bucket, row id, owner, slot, large- and
+    # small-row lists per entry (int32, padded to 64); the lists' counters;
+    # two scan totals per 4096 rows
+    assert need.value == 4 * (2 * 256 + 6 * 64 + 64 + 2 * 64)
 
     def call(cfg=None, **ptrs):
         c = dict(good)
