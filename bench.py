@@ -56,6 +56,8 @@ KIND_SYMBOL = {"prologue": "erase_prologue", "fwd_gemm": "erase_fwd_gemm", "head
 
 def kernel_class(r, bf16=True):
     t = "bf16" if bf16 else "f32"
+    if r["kind"] == "fwd_head_gemm" and bf16 and r["tile_m"] == 16:
+        return "erase_fwd_head16"  # the bf16 16-row last layer + head kernel
     if r["tile_m"]:
         return f"{KIND_SYMBOL[r['kind']]}<{t},{r['tile_m']},{r['tile_n']}>"
     return f"{KIND_SYMBOL[r['kind']]}<{t}>"
@@ -338,7 +340,8 @@ def conventional_comparison(args, log):
     cfg = synth.config("deep_chain")
     M = cfg["batch"]
     params, batches = synth.make_workload(cfg, 0, 8)
-    tr = erase.Trainer(cfg, params, keep_grads=True, bwd_streams=args.bwd_streams)
+    tr = erase.Trainer(cfg, params, keep_grads=True, bwd_streams=args.bwd_streams,
+                       x_in_place=not args.x_copy and M % 128 == 0)
     dev = [tr.device_batch(x, y) for (x, y) in batches]
     losses = torch.zeros(len(cfg["blocks"]), device="cuda")
     scheds = ["undetached", "undetached_graph", "serial", "serial_graph", "overlap", "overlap_graph", "pipeline",
@@ -628,8 +631,12 @@ def ctr_section(args, workload, log, scheds, headline, steps, warmup, timing_ste
     cfg = synth.config(workload)
     bf16 = cfg["dtype"] == "bf16"
     log(f"[bench] generating {workload} (batch {cfg['batch']}, {len(cfg['blocks'])} blocks, {n_batches} batches)")
-    params, batches = synth.make_workload(cfg, 0, n_batches)
-    tr = erase.Trainer(cfg, params, keep_grads=True, bwd_streams=args.bwd_streams)
+    # one more batch than the timed steps cycle over: held out, for the
+    # normalized entropy of data the heads have not trained on
+    params, batches = synth.make_workload(cfg, 0, n_batches + 1)
+    held = batches.pop()
+    in_place = not args.x_copy and cfg["batch"] % 128 == 0
+    tr = erase.Trainer(cfg, params, keep_grads=True, bwd_streams=args.bwd_streams, x_in_place=in_place)
     dev = [tr.device_batch(x, y) for (x, y) in batches]
     losses = torch.zeros(len(cfg["blocks"]), device="cuda")
     flops_step = synth.gemm_flops_per_step(cfg)
@@ -689,10 +696,15 @@ def ctr_section(args, workload, log, scheds, headline, steps, warmup, timing_ste
                    "tflops": (v["flops"] / (v["ms"] / 1e3) / 1e12) if mfma_kind(v["kind"]) else None,
                    "gbs": v["bytes"] / (v["ms"] / 1e3) / 1e9}
                for k, v in sorted(classes.items(), key=lambda kv: -kv[1]["ms"])}
-    # the heads after the run: one more serial step on batch 0
+    # the heads after the run: the loss of a step is taken before its update,
+    # so a step on batch 0 gives the training NE, one on the held-out batch
+    # the NE on unseen data
     tr.step(*dev[0], "serial", losses, wait_current=False)
     tr.sync()
     ne1 = normalized_entropy(losses.cpu().numpy(), batches[0][1])
+    tr.step(*tr.device_batch(*held), "serial", losses, wait_current=False)
+    tr.sync()
+    ne_held = normalized_entropy(losses.cpu().numpy(), held[1])
     best_serial = max((k for k in ("serial", "serial_graph") if k in res), key=lambda k: res[k]["samples_per_s"],
                       default=None)
     sp = lambda a, b: res[a]["samples_per_s"] / res[b]["samples_per_s"] if a in res and b in res else None
@@ -714,11 +726,15 @@ def ctr_section(args, workload, log, scheds, headline, steps, warmup, timing_ste
                       "counter_busy_detail": measured_mfma_busy(workload) or
                       f"null: no MFMA busy counters of the current kernels ({kernel_source_hash()})"},
         "flops_per_step": flops_step,
+        "x_layout": (f"read in place: [{M}][{tr.ncfg.x_ld}] with zero row tails (no per-step copy)" if in_place
+                     else f"[{M}][{tr.ncfg.x_ld}], copied into a zero-padded workspace buffer every step"),
         "bwd_fwd_overlap_fraction": ovl,
         "bwd_fwd_overlap_trace": measured_trace_overlap(workload),
-        "normalized_entropy": {"first_step": ne0, "after_run": ne1,
-                               "note": "mean BCE of each head over the base-rate entropy of batch 0's labels, at the "
-                                       "first step and after the timed steps (8 synthetic batches cycled)"},
+        "normalized_entropy": {"first_step": ne0, "after_run_train": ne1, "after_run_held_out": ne_held,
+                               "note": "mean BCE of each head over the base-rate entropy of the batch's labels: batch "
+                                       "0 at the first step and after the timed steps (the steps cycle over "
+                                       f"{n_batches} synthetic batches, which the heads memorise: the labels are "
+                                       "random), and a held-out batch after them"},
         "kernel_timing": "per-kernel figures from a SERIAL pass (kernels alone), HIP events stamped at each "
                          "kernel's own start and end; overlap fraction from an OVERLAP pass, over every "
                          "backward stream",
@@ -831,6 +847,10 @@ def main():
     ap.add_argument("--bwd-streams", type=int, default=2,
                     help="backward streams of the ERASE schedules (block b uses stream b %% n); 2 measured "
                          "fastest on ctr_mlp (1 leaves the backward chain serial, 3+ exceed the 4 hardware queues)")
+    ap.add_argument("--x-copy", action="store_true",
+                    help="hand x over in its plain layout, copied into a padded workspace buffer every step (by "
+                         "default x is resident with rows of a multiple of 128 elements and zero tails, read in "
+                         "place)")
     ap.add_argument("--no-dcn", action="store_true", help="skip the CTR-DCNv2 (batch 16384) measurement")
     ap.add_argument("--dcn-steps", type=int, default=40)
     ap.add_argument("--dcn-warmup", type=int, default=5)

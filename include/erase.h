@@ -156,6 +156,10 @@ typedef struct {
   int32_t dtype;                    /* erase_dtype */
   float lr, beta1, beta2, eps;      /* Adam (bias-corrected, eps outside the sqrt); lr >= 0,
                                        0 <= beta < 1, eps >= 0 */
+  int32_t x_in_place;               /* 0: every step copies x into a zero-padded buffer of the
+                                       workspace.  1: the GEMMs read x where it is; the caller
+                                       guarantees that x's row tails [in_dim, x_ld) are zero, and
+                                       x_ld and batch must be multiples of 128 (ERASE_ERR_SHAPE) */
 } erase_config;
 
 /* Per-block fp32 device buffers, each of erase_param_count() elements, in

@@ -59,6 +59,9 @@ erase_status validate(const erase_config* c, std::string* err) {
   const int esz = c->dtype == ERASE_BF16 ? 2 : 4;
   if (c->x_ld < c->in_dim || (int64_t(c->x_ld) * esz) % 16 != 0)
     return fail(ERASE_ERR_SHAPE, "x_ld must be >= in_dim and a multiple of 16 bytes");
+  if (c->x_in_place != 0 && c->x_in_place != 1) return fail(ERASE_ERR_INVALID_ARG, "x_in_place must be 0 or 1");
+  if (c->x_in_place && (c->x_ld % 128 != 0 || c->batch % 128 != 0))
+    return fail(ERASE_ERR_SHAPE, "x read in place: x_ld and batch must be multiples of 128");
   if (!(std::isfinite(c->lr) && c->lr >= 0.f)) return fail(ERASE_ERR_INVALID_ARG, "lr must be finite and >= 0");
   if (!(c->beta1 >= 0.f && c->beta1 < 1.f && c->beta2 >= 0.f && c->beta2 < 1.f))
     return fail(ERASE_ERR_INVALID_ARG, "betas must be in [0, 1)");
@@ -159,6 +162,7 @@ struct Plan {
   // zero-padded and feature-major copies of x, one pair per step parity so a
   // step's prologue never overwrites what the previous step's backward reads
   void* xp[2] = {nullptr, nullptr}; int64_t ldxp = 0;
+  bool x_in_place = false;  // the GEMMs read the caller's (zero-padded) x; no copy
 
   std::vector<BlockRT> blk;
   size_t bytes = 0;
@@ -234,7 +238,8 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
   P->status = reinterpret_cast<int*>(base + 8);
   bool any_x = false;
   for (int b = 0; b < c.n_blocks; ++b) any_x |= c.blocks[b].input_src == ERASE_IN_X;
-  if (any_x) {
+  P->x_in_place = c.x_in_place != 0;
+  if (any_x && !P->x_in_place) {
     // zero-padded copy of x, one per step parity; 128-column rows (the
     // weight gradient reads k-major tiles up to 128 columns wide)
     P->ldxp = roundup(c.in_dim, 128);
@@ -359,14 +364,15 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
     off += 1;
     B.nparam = off;
     // Head+loss fused into the last forward GEMM when one tile spans the
-    // whole width: 32 x 128 (bf16) or 64 x 64 (fp32) workgroups over M.  The
-    // head epilogue is a chain of short dependent steps per workgroup, so
-    // 32-row tiles (twice the workgroups) beat 64-row ones (9.0 vs 12.1 us on
-    // the 4096 x 128 CTR layer).
+    // whole width: 16 x 128 (bf16, a kernel of its own) or 64 x 64 (fp32,
+    // the GEMM core) workgroups over M.  The layer is a few k-steps and the
+    // head a chain of short dependent steps per workgroup, so shorter tiles
+    // (more workgroups) win: 64-row GEMM-core tiles 12.1 us, 32-row 9.0 us
+    // on the 4096 x 128 CTR layer.
     LayerRT& RL = B.layer[B.L - 1];
     B.head_fused = RL.kind == ERASE_LAYER_LINEAR_RELU && NL <= (P->bf16 ? 128 : 64);
     if (B.head_fused) {
-      RL.fwd.bm = P->bf16 ? 32 : 64;
+      RL.fwd.bm = P->bf16 ? 16 : 64;
       RL.fwd.bn = P->bf16 ? 128 : 64;
       RL.fwd.kgroups = 1;
       RL.fwd.group = xcd_group((int)cdiv(M, RL.fwd.bm), 1, 1, RL.fwd.bm, RL.fwd.bn);
@@ -697,9 +703,13 @@ void layer_input(const Ctx* c, int b, int l, const void* x, int par, const void*
     *mn = B.layer[l - 1].y;
     *ldmn = B.layer[l - 1].ldy;
   } else if (B.input_src == ERASE_IN_X) {
-    (void)x;
-    *mn = P.xp[par];
-    *ldmn = P.ldxp;
+    if (P.x_in_place) {
+      *mn = x;
+      *ldmn = c->cfg.x_ld;
+    } else {
+      *mn = P.xp[par];
+      *ldmn = P.ldxp;
+    }
   } else {
     const BlockRT& A = P.blk[b - 1];
     const LayerRT& R = A.layer[A.L - 1];

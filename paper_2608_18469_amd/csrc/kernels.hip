@@ -1128,8 +1128,151 @@ hipError_t launch_bwd_gemm(int bf16, const GemmDesc& gd, const EpiParams& ed, co
   return hipErrorInvalidValue;
 }
 
+// The last layer of a block with its local head and loss (Section 2.1,
+// Eq. 2) for bf16 outputs at most 128 wide, in 16-row tiles: twice as many
+// workgroups as the 32-row GEMM-core tile, for a layer whose work is a few
+// k-steps.  Four waves of 32 output columns each; the MFMA operands come
+// straight from global memory (the rows of the activation and of the weight
+// copy are contiguous along the contraction, and every load of the
+// contraction is in flight at once, up to 256 per pass).  Per tile:
+//   z = relu(acc + b) (as stored, bf16),  s_m = sum_n z_mn w_n + c,
+//   loss_m = max(s,0) - s y_m + log1p(e^-|s|),  ds_m = lam (sigmoid(s_m) - y_m) / M,
+//   dz_mn = ds_m w_n [z_mn > 0],  partials dw_n = sum_m z_mn ds_m, dc, loss,
+// every sum in a fixed order.
+__global__ __launch_bounds__(256) void erase_fwd_head16(GemmDesc g, EpiParams e) {
+  constexpr int TR = 16, TC = 128, OP = TC + 8;  // tile rows, columns, LDS pitch (bf16)
+  __shared__ float s_part[4][TR];
+  __shared__ float s_ds[TR], s_l[TR];
+  __shared__ __attribute__((aligned(16))) uint16_t s_z[TR][OP];
+  __shared__ __attribute__((aligned(16))) uint16_t s_dz[TR][OP];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int M = g.M, N = g.N, K = g.K;
+  const int m0 = (int)blockIdx.x * TR;
+  const int fr = lane & 15, kq = (lane >> 4) * 8;
+  const int c0 = wave * 32 + fr, c1 = c0 + 16;  // this lane's two output columns
+  const uint16_t* A = static_cast<const uint16_t*>(g.A);
+  const uint16_t* W = static_cast<const uint16_t*>(g.B);
+  const uint16_t* pa = A + (int64_t)(m0 + fr) * g.lda + kq;
+  const uint16_t* pb0 = W + (int64_t)c0 * g.ldb + kq;
+  const uint16_t* pb1 = W + (int64_t)c1 * g.ldb + kq;
+  // head inputs first: their latency hides behind the operand loads
+  const float b0 = c0 < N ? e.bias[c0] : 0.f, b1 = c1 < N ? e.bias[c1] : 0.f;
+  const float w0 = c0 < N ? e.hw[c0] : 0.f, w1 = c1 < N ? e.hw[c1] : 0.f;
+  const float hc = e.hc[0];
+  float yl = 0.f;
+  if (tid < TR && m0 + tid < M) yl = e.labels[m0 + tid];
+  f32x4_t acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  for (int k0 = 0; k0 < K; k0 += 8 * 32) {
+    u32x4_t fa[8], f0[8], f1[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (k0 + 32 * u < K) {
+        fa[u] = *reinterpret_cast<const u32x4_t*>(pa + k0 + 32 * u);
+        f0[u] = *reinterpret_cast<const u32x4_t*>(pb0 + k0 + 32 * u);
+        f1[u] = *reinterpret_cast<const u32x4_t*>(pb1 + k0 + 32 * u);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (k0 + 32 * u < K) {
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, fa[u]),
+                                                       __builtin_bit_cast(bf16x8_t, f0[u]), acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, fa[u]),
+                                                       __builtin_bit_cast(bf16x8_t, f1[u]), acc1, 0, 0, 0);
+      }
+    }
+  }
+  // lane holds rows 4 (lane >> 4) + q of columns c0 and c1
+  const int rb = (lane >> 4) * 4;
+  float z0[4], z1[4], part[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const bool live = m0 + rb + q < M;
+    const float v0 = acc0[q] + b0, v1 = acc1[q] + b1;
+    z0[q] = (live && c0 < N) ? bf2f(f2bf(v0 < 0.f ? 0.f : v0)) : 0.f;  // keeps NaN, like max(h, 0)
+    z1[q] = (live && c1 < N) ? bf2f(f2bf(v1 < 0.f ? 0.f : v1)) : 0.f;
+    part[q] = fmaf(z1[q], w1, z0[q] * w0);
+  }
+  // the row's partial logit over the wave's 32 columns: lanes of one row
+  // group (16 lanes) combined by a fixed butterfly
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) part[q] += __shfl_xor(part[q], o, 64);
+    if (fr == 0) s_part[wave][rb + q] = part[q];
+  }
+  __syncthreads();
+  if (tid < TR) {
+    float ds = 0.f, l = 0.f;
+    if (m0 + tid < M) {
+      const float sv = ((s_part[0][tid] + s_part[1][tid]) + (s_part[2][tid] + s_part[3][tid])) + hc;
+      const float en = __expf(-fabsf(sv));
+      const float sig = sv >= 0.f ? 1.f / (1.f + en) : en / (1.f + en);
+      ds = e.lam * (sig - yl) * e.inv_m;
+      l = fmaxf(sv, 0.f) - sv * yl + log1pf(en);
+    }
+    s_ds[tid] = ds;
+    s_l[tid] = l;
+  }
+  __syncthreads();
+  float dw0 = 0.f, dw1 = 0.f;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float ds = s_ds[rb + q];
+    s_z[rb + q][c0] = f2bf(z0[q]);
+    s_z[rb + q][c1] = f2bf(z1[q]);
+    s_dz[rb + q][c0] = f2bf(z0[q] > 0.f ? ds * w0 : 0.f);
+    s_dz[rb + q][c1] = f2bf(z1[q] > 0.f ? ds * w1 : 0.f);
+    dw0 = fmaf(z0[q], ds, dw0);
+    dw1 = fmaf(z1[q], ds, dw1);
+  }
+  // column sums over the tile's 16 rows: the four row groups (lanes 16 apart)
+  dw0 += __shfl_xor(dw0, 16, 64);
+  dw0 += __shfl_xor(dw0, 32, 64);
+  dw1 += __shfl_xor(dw1, 16, 64);
+  dw1 += __shfl_xor(dw1, 32, 64);
+  if (lane < 16) {
+    if (c0 < N) e.pdw[(int64_t)blockIdx.x * N + c0] = dw0;
+    if (c1 < N) e.pdw[(int64_t)blockIdx.x * N + c1] = dw1;
+  }
+  if (tid == 0) {
+    float d = 0.f, l = 0.f;
+    for (int r = 0; r < TR; ++r) {
+      d += s_ds[r];
+      l += s_l[r];
+    }
+    e.pdc[blockIdx.x] = d;
+    e.ploss[blockIdx.x] = l;
+  }
+  __syncthreads();
+  // 16-byte row-major stores of dz (and of z when a later block reads it)
+  const int r = tid >> 4, n = (tid & 15) * 8;
+  if (m0 + r < M && n < N) {
+    if (e.dmn) {
+      uint16_t* dst = static_cast<uint16_t*>(e.dmn) + (int64_t)(m0 + r) * e.lddmn + n;
+      if (n + 8 <= N)
+        *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(&s_dz[r][n]);
+      else
+        for (int k = 0; k < N - n; ++k) dst[k] = s_dz[r][n + k];
+    }
+    if (e.y) {
+      uint16_t* dst = static_cast<uint16_t*>(e.y) + (int64_t)(m0 + r) * e.ldy + n;
+      if (n + 8 <= N)
+        *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(&s_z[r][n]);
+      else
+        for (int k = 0; k < N - n; ++k) dst[k] = s_z[r][n + k];
+    }
+  }
+}
+
 hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s, const LaunchEv& ev) {
   if (g.M <= 0 || g.N <= 0 || g.split <= 0) return hipErrorInvalidValue;
+  if (bf16 && kind == GK_FWD_HEAD && g.bm == 16) {
+    // 16-row tiles: outputs at most 128 wide, contraction a multiple of 32
+    if (g.N > 128 || g.K % 32 || g.split != 1) return hipErrorInvalidValue;
+    ERASE_LAUNCH(erase_fwd_head16, dim3((unsigned)((g.M + 15) / 16)), dim3(256), 0, s, ev, g, e);
+    return hipGetLastError();
+  }
   if (bf16) {
     if (g.bm == 128 && g.bn == 128) return launch_gemm_t<uint16_t, 128, 128>(kind, g, e, s, ev);
     if (g.bm == 128 && g.bn == 64) return launch_gemm_t<uint16_t, 128, 64>(kind, g, e, s, ev);

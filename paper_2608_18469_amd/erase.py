@@ -46,7 +46,7 @@ class BlockSpec(ctypes.Structure):
 class Config(ctypes.Structure):
     _fields_ = [("n_blocks", c_int32), ("blocks", POINTER(BlockSpec)), ("batch", c_int32), ("in_dim", c_int32),
                 ("x_ld", c_int32), ("dtype", c_int32), ("lr", c_float), ("beta1", c_float), ("beta2", c_float),
-                ("eps", c_float)]
+                ("eps", c_float), ("x_in_place", c_int32)]
 
 
 class BlockBuffers(ctypes.Structure):
@@ -129,7 +129,7 @@ class NativeConfig:
     """ctypes view of a model description (see ``synth.config``), kept alive
     together with the arrays it points to."""
 
-    def __init__(self, cfg: dict, x_ld: int | None = None):
+    def __init__(self, cfg: dict, x_ld: int | None = None, x_in_place: bool = False):
         esz = 2 if cfg["dtype"] == "bf16" else 4
         per16 = 16 // esz
         if x_ld is None:
@@ -148,7 +148,7 @@ class NativeConfig:
         ad = cfg["adam"]
         self.c = Config(len(cfg["blocks"]), ctypes.cast(blocks, POINTER(BlockSpec)), cfg["batch"], cfg["in_dim"],
                         self.x_ld, BF16 if cfg["dtype"] == "bf16" else F32, ad["lr"], ad["beta1"], ad["beta2"],
-                        ad["eps"])
+                        ad["eps"], 1 if x_in_place else 0)
 
     def ptr(self):
         return ctypes.byref(self.c)
@@ -284,7 +284,7 @@ class Trainer:
 
     def __init__(self, cfg: dict, params: list, x_ld: int | None = None, keep_grads: bool = True,
                  m: list | None = None, v: list | None = None, step: int = 0, bwd_streams: int = 1,
-                 streams=None):
+                 streams=None, x_in_place: bool = False):
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("no HIP device available: the ERASE step runs only on the GPU")
@@ -292,7 +292,11 @@ class Trainer:
         self.torch = torch
         self.cfg = cfg
         self.dev = torch.device("cuda", torch.cuda.current_device())
-        self.ncfg = NativeConfig(cfg, x_ld)
+        # x read in place: rows of a multiple of 128 elements (zero tails, as
+        # device_batch and erase_embed_bags write them)
+        if x_in_place and x_ld is None:
+            x_ld = (cfg["in_dim"] + 127) // 128 * 128
+        self.ncfg = NativeConfig(cfg, x_ld, x_in_place)
         self.act_dtype = torch.bfloat16 if cfg["dtype"] == "bf16" else torch.float32
         nb = len(cfg["blocks"])
         self.param, self.m, self.v, self.grad = [], [], [], []

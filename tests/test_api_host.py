@@ -262,3 +262,21 @@ def test_embed_bags_backward_noalloc_validation():
     assert L.erase_embed_bags_backward_scratch_bytes(ctypes.byref(bc), ctypes.byref(need)) == erase.OK
     assert need.value > erase.BAG_SCRATCH_MAX
     assert call(**big) == erase.ERR_WORKSPACE
+
+
+def test_x_in_place_validation_and_workspace():
+    """x read in place: x_ld and batch must be multiples of 128, the flag 0 or
+    1, and the workspace has no padded copy of x."""
+    L = erase.lib()
+    cfg = synth.config("ctr_mlp")
+    copy = _ncfg(cfg)
+    inplace = _ncfg(cfg, x_ld=1792, x_in_place=True)
+    assert erase.workspace_bytes(inplace) < erase.workspace_bytes(copy)
+    for over in (dict(x_ld=1680), dict(batch=4000)):
+        nc = _ncfg(dict(cfg, batch=over.get("batch", cfg["batch"])), x_ld=over.get("x_ld", 1792), x_in_place=True)
+        n = ctypes.c_size_t(0)
+        assert L.erase_workspace_bytes(nc.ptr(), ctypes.byref(n)) == erase.ERR_SHAPE, over
+    bad = _ncfg(cfg, x_ld=1792, x_in_place=True)
+    bad.c.x_in_place = 2
+    n = ctypes.c_size_t(0)
+    assert L.erase_workspace_bytes(bad.ptr(), ctypes.byref(n)) == erase.ERR_INVALID_ARG

@@ -638,6 +638,35 @@ def test_ctr_mlp_full_size_headline_schedule_bit_identical():
         assert_bit_identical([ref], [got])
 
 
+def test_x_in_place_matches_the_padded_copy():
+    """The GEMMs reading the caller's zero-padded x in place give the same
+    bits as the step that copies x into its workspace, in the serial and
+    the headline schedule (pipeline, worker dispatch, 2 backward streams),
+    over 3 back-to-back steps; cross layers read x0 in place too."""
+    _say("case: x read in place vs padded copy")
+    cfg = _ctr_small(batch=512, blocks=3)
+    dcn = synth.config("ctr_dcn", batch=256, ctr_rows=5000)
+    dcn["blocks"] = dcn["blocks"][:1]
+    for c in (cfg, dcn):
+        params, batches = synth.make_workload(c, 27, 3)
+        ref_l, ref = run_gpu_nosync(c, params, batches, ["serial"])
+        for scheds, disp in ((["serial"], "caller"), (["pipeline"], "worker")):
+            import torch
+            tr = erase.Trainer(c, params, keep_grads=True, bwd_streams=2, x_in_place=True)
+            assert tr.ncfg.x_ld % 128 == 0
+            tr.set_dispatch(disp)
+            dev = [tr.device_batch(x, y) for (x, y) in batches]
+            outs = [torch.zeros(len(c["blocks"]), dtype=torch.float32, device="cuda") for _ in batches]
+            for i, (xd, yd) in enumerate(dev):
+                tr.step(xd, yd, scheds[0], losses=outs[i], wait_current=(i == 0))
+            tr.sync()
+            p, m, v, g = tr.flat_state()
+            tr.close()
+            got_l = np.stack([o.cpu().numpy() for o in outs])
+            assert np.array_equal(ref_l.view(np.uint32), got_l.view(np.uint32)), scheds
+            assert_bit_identical([ref], [{"losses": got_l[-1], "params": p, "m": m, "v": v, "grads": g}])
+
+
 def test_deep_chain_full_size_vs_oracle():
     _say("case: deep_chain full size")
     cfg = synth.config("deep_chain")
