@@ -897,7 +897,7 @@ def main():
         print(f"--headline {args.headline} is not among --schedules {args.schedules}", file=sys.stderr)
         sys.exit(2)
     cfg, sec = ctr_section(args, args.workload, log, scheds, args.headline, args.steps, args.warmup,
-                           args.timing_steps)
+                           args.timing_steps, n_batches=8 if args.workload == "ctr_mlp" else 2)
     bf16 = cfg["dtype"] == "bf16"
     M = cfg["batch"]
     out = {
