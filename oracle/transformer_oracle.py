@@ -31,7 +31,8 @@ positions; lam_b = 1.
 
 Arithmetic is float64 unless ``dtype`` says otherwise.  ``emulate_bf16=True``
 rounds to bf16 the tensors the GPU stores in bf16 (weight copies, block
-activations, stored activation gradients and the logit gradient); it is a
+activations, stored activation gradients, and the head's exponentials and
+row-scaled input, which stand in for a stored logit gradient); it is a
 diagnostic for tighter comparisons, not the reference.
 
 Pins (tests/test_oracle_transformer.py): torch CPU autograd of the same
@@ -178,7 +179,8 @@ def tf_block_backward(cfg: dict, c: dict, target: np.ndarray, lam: float, emulat
     undetached baseline sends a gradient into z) at the block's weights, and
     at its input a0 when ``need_input_grad``.  Returns (loss, grads, g_a0).
     ``trace`` (a dict, optional) receives the activation gradients the step
-    stores (dlog, dhn, dz, du, dn2, da1, do, dqkv, and dn1 when formed), for
+    stores (dhn, dz, du, dn2, da1, do, dqkv, and dn1 when formed; the head's
+    pexp and hns under emulation, the logit gradient dlog otherwise), for
     checks of where emulation rounds; nothing else changes."""
     rb = _bf16 if emulate_bf16 else _ident
     B, T = cfg["batch"], cfg["seq"]
@@ -186,10 +188,31 @@ def tf_block_backward(cfg: dict, c: dict, target: np.ndarray, lam: float, emulat
     W = c["W"]
     rows, dlog = softmax_xent(c["logits"], target)
     loss = float(np.mean(rows))
-    dlog = rb(dlog * (lam / N))
-    gr = {"wh": dlog.T @ c["hn"]}
-    dhn = rb(dlog @ W["wh"])
-    dz = rms_norm_backward(dhn, c["z"], c["r3"])
+    head = {}
+    if emulate_bf16:
+        # The head as the GPU stores it in bf16: exponentials relative to the
+        # target logit, e = exp(x - x_target), with row sums S; the target
+        # entry replaced by e - S; the head input scaled per row by
+        # s = lam / (N S).  Then lam (softmax - onehot) / N = s (e - S onehot),
+        # so dWh = e^T (s hn) and dhn = s (e Wh), the row scale applied after
+        # the stored product.
+        x = c["logits"]
+        idx = np.arange(N)
+        e = rb(np.exp(x - x[idx, target][:, None]))
+        S = e.sum(axis=1)
+        e[idx, target] = rb(e[idx, target] - S)
+        s = (lam / N) / S
+        hns = rb(s[:, None] * c["hn"])
+        gr = {"wh": e.T @ hns}
+        dhn = rb(e @ W["wh"])
+        dz = rms_norm_backward(s[:, None] * dhn, c["z"], c["r3"])
+        head = {"pexp": e, "hns": hns}
+    else:
+        dlog = dlog * (lam / N)
+        gr = {"wh": dlog.T @ c["hn"]}
+        dhn = dlog @ W["wh"]
+        dz = rms_norm_backward(dhn, c["z"], c["r3"])
+        head = {"dlog": dlog}
     if g_out is not None:
         dz = dz + g_out
     dz = rb(dz)
@@ -210,7 +233,7 @@ def tf_block_backward(cfg: dict, c: dict, target: np.ndarray, lam: float, emulat
         dn1 = rb(dqkv @ W["wqkv"])
         g_a0 = da1 + rms_norm_backward(dn1, c["a0"], c["r1"])
     if trace is not None:
-        trace.update(dlog=dlog, dhn=dhn, dz=dz, du=du, dn2=dn2, da1=da1, do=do, dqkv=dqkv)
+        trace.update(head, dhn=dhn, dz=dz, du=du, dn2=dn2, da1=da1, do=do, dqkv=dqkv)
         if dn1 is not None:
             trace["dn1"] = dn1
     return loss, gr, g_a0

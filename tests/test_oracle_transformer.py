@@ -234,6 +234,32 @@ def test_emulated_bf16_is_close():
             assert _rel(b["grads"][blk][k], a["grads"][blk][k]) < 0.1
 
 
+def test_emulated_head_reproduces_the_logit_gradient():
+    """The emulated head (exponentials relative to the target logit, the
+    target entry minus the row sum, the row scale on the head input and after
+    the input-gradient product) gives the head weight gradient and dz of the
+    float64 logit gradient lam (softmax - onehot) / N up to bf16 rounding; a
+    dropped one-hot entry or a wrong scale would be off by O(1)."""
+    cfg = _cfg(vocab=96, d=32, heads=2, layers=1, seq=24, batch=3)
+    params, tokens = _work(cfg, seed=5)
+    inp, tgt = tokens[:, :-1].reshape(-1), tokens[:, 1:].reshape(-1)
+    p = {k: np.asarray(a, np.float64) for k, a in params[0].items()}
+    a0 = np.asarray(params[0]["emb"], np.float64)[inp]
+    c = to.tf_block_forward(cfg, p, a0, False)
+    out = {}
+    for emulate in (False, True):
+        tr = {}
+        _loss, gr, _ga0 = to.tf_block_backward(cfg, c, tgt, 0.7, emulate, trace=tr)
+        out[emulate] = (gr["wh"], tr["dz"])
+    assert _rel(out[True][0], out[False][0]) < 1e-2
+    assert _rel(out[True][1], out[False][1]) < 2e-2
+    # the stored head tensors: the target entries are the only negatives
+    tr = {}
+    to.tf_block_backward(cfg, c, tgt, 0.7, True, trace=tr)
+    neg = tr["pexp"] < 0
+    assert np.array_equal(np.argwhere(neg)[:, 1], tgt) and neg.sum() == tgt.size
+
+
 def _is_bf16(a):
     """Elementwise: a bf16 number (a float32 whose low 16 bits are zero)."""
     a = np.asarray(a, dtype=np.float64)
@@ -249,17 +275,19 @@ def _share(arrays):
 
 def test_bf16_emulation_rounds_exactly_the_stored_tensors():
     """emulate_bf16 rounds what the GPU stores in bf16 -- the weight copies,
-    the block's activations (n1, q/k/v, o, a1, n2, u, g, z, hn) and the stored
-    activation gradients (logit gradient, dhn, dz, du, dn2, da1, do, dqkv,
-    dn1) -- and leaves the fp32 ones alone: the RMSNorm statistics, the
-    attention probabilities, the logits and the weight gradients.  Without
-    emulation the stored tensors are not bf16 (the check is not vacuous)."""
+    the block's activations (n1, q/k/v, o, a1, n2, u, g, z, hn), the head's
+    exponentials and row-scaled input, and the stored activation gradients
+    (dhn, dz, du, dn2, da1, do, dqkv, dn1) -- and leaves the fp32 ones alone:
+    the RMSNorm statistics, the attention probabilities, the logits and the
+    weight gradients.  Without emulation the stored tensors are not bf16
+    (the check is not vacuous)."""
     cfg = _cfg(vocab=64, d=32, heads=2, layers=2, seq=16, batch=3)
     params, tokens = _work(cfg, seed=21)
     inp, tgt = tokens[:, :-1].reshape(-1), tokens[:, 1:].reshape(-1)
     acts = ("n1", "q", "k", "v", "o", "a1", "n2", "u", "g", "z", "hn")
-    grads = ("dlog", "dhn", "dz", "du", "dn2", "da1", "do", "dqkv", "dn1")
+    body = ("dhn", "dz", "du", "dn2", "da1", "do", "dqkv", "dn1")
     for emulate in (True, False):
+        grads = (("pexp", "hns") if emulate else ("dlog",)) + body
         rb = to._bf16 if emulate else (lambda a: a)
         a0 = rb(np.asarray(params[0]["emb"], np.float64))[inp]
         c = to.tf_block_forward(cfg, {k: np.asarray(a, np.float64) for k, a in params[0].items()}, a0, emulate)
