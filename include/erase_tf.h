@@ -106,18 +106,22 @@ ERASE_API erase_status erase_tf_refresh_weights(erase_tf_ctx* ctx);
  * 1), 6 both gradient GEMMs of one weight in one launch (layer as for 1),
  * 5 Adam, 11 embedding gather, 12 RMSNorm forward, 13 RMSNorm backward,
  * 14 attention forward, 15 attention backward (layer 1 row sums, 2 dK/dV,
- * 3 dQ), 16 softmax cross-entropy, 17 embedding gradient (four launches,
- * bracketed by stream events rather than kernel-stamped ones). */
+ * 3 dQ), 16 softmax normaliser of the vocabulary head (layer 0 every row,
+ * 1 the recomputation of out-of-range rows), 17 embedding gradient (four
+ * launches, bracketed by stream events rather than kernel-stamped ones). */
 ERASE_API erase_status erase_tf_set_timing(erase_tf_ctx* ctx, int32_t enable);
 ERASE_API erase_status erase_tf_read_timing(erase_tf_ctx* ctx, erase_kernel_time* out, int32_t cap, int32_t* n);
 
 /* Device address and row pitch (elements) of a stored tensor of block
  * `block`, for inspection after erase_tf_sync():
  *   0 a0, 1 n1, 2 qkv [.][3d], 3 o, 4 a1, 5 n2, 6 u [.][4d] (MLP
- *   pre-activation), 7 gelu(u), 8 z, 9 hn, 10 logits / logit gradient
- *   [.][V] (bf16; after a step, the gradient), 11 lse (fp32 [B][H][T],
- *   pitch T), 12 dqkv, 13 dz (bf16 unless noted; rows are positions
- *   b T + t).  ERASE_ERR_INVALID_ARG for an unknown id or block. */
+ *   pre-activation), 7 gelu(u), 8 z, 9 hn, 10 the head's exponentials
+ *   e[n][v] = exp(logit - target logit) [.][V] (bf16; after a step the
+ *   target entry holds e - S_n, S_n the row's sum, so that rowscale[n] e[n]
+ *   is the logit gradient lam (softmax - onehot) / N), 11 lse (fp32
+ *   [B][H][T], pitch T), 12 dqkv, 13 dz, 14 rowscale (fp32 [B T], pitch
+ *   B T: lam / (N S_n)), 15 hns = rowscale hn (bf16 unless noted; rows are
+ *   positions b T + t).  ERASE_ERR_INVALID_ARG for an unknown id or block. */
 ERASE_API erase_status erase_tf_tensor(erase_tf_ctx* ctx, int32_t block, int32_t which, void** ptr, int64_t* ld);
 
 /* Destroy (waits for the streams; frees events).  NULL is accepted. */

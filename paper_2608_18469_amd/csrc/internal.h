@@ -48,9 +48,9 @@ int xcd_group(int gm, int gn, int split, int bm, int bn);
 //   GK_FWD_LIN     y = acc (+ res)                       (projections, residual adds)
 //   GK_FWD_GELU    y = gelu(acc), and acc itself into gout (the MLP up-projection)
 //   GK_DGRAD_GELU  g = acc * gelu'(u), u read from mask  (input gradient below the GELU)
-//   GK_FWD_LOGITS  y = acc, plus per row the maximum and the sum of exp(y - max)
-//                  over this tile's columns into lstat, and y at the row's target
-//                  column into tlogit                     (vocabulary head)
+//   GK_FWD_LOGITS  y = exp(acc - xref[m]) (the row's exponentials relative to a
+//                  reference logit), plus per row the sum of the stored values
+//                  over this tile's columns into lstat    (vocabulary head)
 // GK_DGRAD with neither mask nor below_cross stores g = acc (+ res) as is.
 enum GemmKind {
   GK_FWD_RELU = 0, GK_FWD_CROSS = 1, GK_WGRAD = 2, GK_DGRAD = 3, GK_FWD_HEAD = 4,
@@ -102,12 +102,10 @@ struct EpiParams {
   // (bp non-null: the tiles of the first column block update bias entries
   // [0, M), and no row sum is stored in bpart); gradient bg nullable
   float* bp; float* bm; float* bv; float* bg;
-  // logits (GK_FWD_LOGITS): lstat[m][2 t], lstat[m][2 t + 1] = max and sum
-  // of exp(y - max) of row m over the columns of N-tile t (values as stored);
-  // tlogit[m] = y[m][target[m]] (written by the tile holding that column)
+  // logits (GK_FWD_LOGITS): lstat[m][t] = sum over the columns of N-tile t
+  // of the stored (bf16) values exp(acc - xref[m]) of row m
   float* lstat; int64_t ldlstat;
-  const int32_t* target;
-  float* tlogit;
+  const float* xref;
 };
 
 hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s,
@@ -256,17 +254,24 @@ struct TfEmbedArgs {
 };
 hipError_t launch_tf_embed(const TfEmbedArgs& a, hipStream_t s, const LaunchEv& ev = {});
 
-// Forward: y = x r, r = 1 / sqrt(mean(x^2) + eps) per row (r written).
-// Backward: dx = r (dy - y mean(dy y)) + res (res nullable), y = x r, into
-// out_f32 (fp32) when set, else y (bf16).  N rows of width d (d % 8 == 0,
-// d <= 4096).
+// Forward: y = x r, r = 1 / sqrt(mean(x^2) + eps) per row (r written); with
+// hw set (the vocabulary head's bf16 weight [V][ldhw]), also the target
+// logit xref[n] = y[n] . hw[target[n]] of the stored row (0 where the target
+// is invalid).
+// Backward: dx = r (s dy - y mean(s dy y)) + res (res nullable), y = x r,
+// s = dyscale[n] (1 when dyscale is null), into out_f32 (fp32) when set,
+// else y (bf16).  N rows of width d (d % 8 == 0, d <= 4096).
 struct TfRmsArgs {
   const uint16_t* x; int64_t ldx;
   uint16_t* y; int64_t ldy;
   float* r;
   const uint16_t* dy; int64_t lddy;
+  const float* dyscale;
   const uint16_t* res; int64_t ldres;
   float* out_f32; int64_t ldout;
+  const uint16_t* hw; int64_t ldhw;
+  const int32_t* target;
+  float* xref;
   int64_t N;
   int d;
   float eps;
@@ -289,22 +294,42 @@ struct TfAttnArgs {
 };
 hipError_t launch_tf_attn(int part, const TfAttnArgs& a, hipStream_t s, const LaunchEv& ev = {});
 
-// Softmax cross-entropy of N rows of V logits (bf16, in place): lse from the
-// per-tile statistics of the logits GEMM, loss_n = lse - tlogit[n], and
-// logits[n][v] <- scale (exp(logit - lse) - [v == target[n]]); ploss[w] = sum
-// of the losses of rows 4 w .. 4 w + 3.
-struct TfXentArgs {
-  uint16_t* logits; int64_t ldlog;
+// Softmax cross-entropy of the vocabulary head without a pass over the
+// logits.  The logits GEMM stores e[n][v] = exp(x[n][v] - xref[n]) (bf16),
+// xref[n] the target logit, and per-tile sums of e.  With S_n = sum_v e[n][v]
+// the loss is lse - x_target = log S_n and the logit gradient is
+// scale (e / S_n - onehot) = (scale / S_n) (e - S_n onehot).  So the head's
+// gradient GEMMs take e with its target entry replaced by e - S_n as the
+// output gradient, the input gradient is scaled per row afterwards
+// (rowscale[n] = scale / S_n, applied by the RMSNorm backward), and the
+// weight gradient takes hns[n] = rowscale[n] hn[n] as its second operand.
+//   part 0 (one wave per row, four rows per workgroup): S_n from lstat, the
+//     loss, rowscale, the target entry, hns; a row whose S_n falls outside
+//     [2^-60, 2^60] (exponentials relative to the target logit out of range)
+//     is flagged instead;
+//   part 1 (one workgroup per four rows): every flagged row recomputed from
+//     hn and w with the row's exact maximum as the reference, then the same
+//     outputs; flags cleared.  Nothing to do for a row that is not flagged.
+// ploss[g] = sum of the losses of rows 4 g .. 4 g + 3 (rowloss keeps each).
+// flag [N] must be zero on entry to part 0 (part 1 leaves it zero).
+struct TfHeadArgs {
+  uint16_t* e; int64_t lde;         // [N][lde] exponentials (bf16), in place
   const float* lstat; int64_t ldlstat;
   int ntiles;
-  const float* tlogit;
+  const float* xref;
   const int32_t* target;
+  const uint16_t* hn; int64_t ldhn;  // head input (bf16)
+  uint16_t* hns; int64_t ldhns;      // scaled head input (bf16)
+  const uint16_t* w; int64_t ldw;    // head weight [V][ldw] (bf16)
+  float* rowscale;
+  float* rowloss;
+  int32_t* flag;
   int64_t N;
-  int V;
-  float scale;
+  int V, d;
+  float scale;  // lam / N
   float* ploss;
 };
-hipError_t launch_tf_xent(const TfXentArgs& a, hipStream_t s, const LaunchEv& ev = {});
+hipError_t launch_tf_head(int part, const TfHeadArgs& a, hipStream_t s, const LaunchEv& ev = {});
 
 // Embedding gradient: grad[v] = sum over positions n with input[n] == v, in
 // increasing n, of dx[n] (fp32); zero rows for absent tokens.  count and

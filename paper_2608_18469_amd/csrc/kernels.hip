@@ -243,7 +243,9 @@ struct GemmSmem {
   static constexpr int STAGE = KMAJ ? BK * (BM + BN + 2 * PAD) : (BM + BN) * PITCH;
   using OT = typename std::conditional<KIND == GK_WGRAD, float, T>::type;
   static constexpr int MAIN = 2 * STAGE * (int)sizeof(T);
-  static constexpr int TILE = BM * (BN + 16 / (int)sizeof(OT)) * (int)sizeof(OT);
+  // the logits epilogue stages the fp32 accumulators ([BM][BN + 4] floats)
+  static constexpr int TILE = KIND == GK_FWD_LOGITS ? BM * (BN + 4) * 4
+                                                    : BM * (BN + 16 / (int)sizeof(OT)) * (int)sizeof(OT);
   // fused head: hw[BN], labels[BM], ds[BM], loss[BM], dw[2][BN], c (fp32),
   // past both the main-loop stages and the output tile
   static constexpr int HOFF = MAIN > TILE ? MAIN : TILE;
@@ -325,12 +327,20 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     if constexpr (KIND == GK_FWD_RELU || KIND == GK_FWD_CROSS || KIND == GK_FWD_HEAD) bnv[j] = (n < g.N) ? e.bias[n] : 0.f;
   }
 
-  // logits: the target column of the row this thread takes in the
-  // statistics pass, loaded now (latency hidden behind the main loop)
-  int tgt1 = -1;
+  // logits: the epilogue's store pass gives each row LTPR threads of 8
+  // consecutive columns; the reference
+  // logit of each of the thread's rows (in units of log2) is loaded now,
+  // its latency hidden behind the main loop
+  constexpr float kL2e = 1.4426950408889634f;
+  constexpr int LTPR = BN / 8, LRPP = NT / LTPR, LPASS = BM / LRPP;  // threads per row, rows per pass, passes
+  float xrl[KIND == GK_FWD_LOGITS ? LPASS : 1];
   if constexpr (KIND == GK_FWD_LOGITS) {
-    const int m = m0 + tid / (NT / BM);
-    if (m < g.M) tgt1 = e.target[m];
+    static_assert(sizeof(T) == 2 && LPASS * LRPP == BM && LTPR <= 64, "logits: bf16, store pass matching the tile");
+#pragma unroll
+    for (int p = 0; p < LPASS; ++p) {
+      const int m = m0 + tid / LTPR + p * LRPP;
+      xrl[p] = m < g.M ? e.xref[m] * kL2e : 0.f;
+    }
   }
 
   // fused Adam: the tile's parameters and moments are loaded now (they do not
@@ -658,6 +668,11 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
       for (int q = 0; q < 4; ++q) {
         const int ml = wm * WM + i * 16 + (lane >> 4) * 4 + q;
         const int m = m0 + ml;
+        if constexpr (KIND == GK_FWD_LOGITS) {
+          // the fp32 accumulators as they are; the store pass exponentiates
+          reinterpret_cast<float*>(smem)[ml * (BN + 4) + nl] = acc[i][j][q];
+          continue;
+        }
         OT v;
         if constexpr (KIND == GK_WGRAD) {
           v = acc[i][j][q];
@@ -673,6 +688,8 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   bool store_tile = omn != nullptr;
   // fused Adam (two k-group weight gradients only) reads the LDS tile instead
   if constexpr (FADAM) store_tile = store_tile && e.ap == nullptr;
+  // logits: the store pass below exponentiates as it stores
+  if constexpr (KIND == GK_FWD_LOGITS) store_tile = false;
   if (store_tile) {
     constexpr int CPRO = BN / OCH;
     for (int c = tid; c < BM * CPRO; c += NT) {
@@ -722,45 +739,53 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
   }
 
   if constexpr (KIND == GK_FWD_LOGITS) {
-    // Row statistics of this tile's columns from the stored (rounded) values
-    // in the LDS tile: NT / BM threads per row, each over a contiguous run
-    // of columns (16-byte LDS reads), then the row's threads combined by
-    // lane exchanges, in a fixed order.  The sums use exp2 of
-    // (x - max) log2(e).
-    constexpr int TPR = NT / BM, CPT = BN / TPR;  // threads per row, columns per thread
-    static_assert(TPR == 2 || TPR == 4, "logits statistics: 2 or 4 threads per row");
-    static_assert(CPT % 8 == 0, "logits statistics: whole 16-byte chunks per thread");
-    const int r = tid / TPR, c0 = (tid % TPR) * CPT;
-    const int nv = min(CPT, max(0, N - (n0 + c0)));  // valid columns of this thread
-    float x[CPT];
+    // Store pass: y = exp(acc - xref) rounded to bf16 (pairs converted by
+    // one instruction), one 16-byte store of 8 consecutive columns per
+    // thread and row, and the row's sum of the stored values: the thread's
+    // 8 in column order, then a butterfly over the row's LTPR lanes (the
+    // same sum in every lane), so the order is fixed.  Columns past N are
+    // neither stored nor summed (only the last column tile has any).
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    typedef float f32x2_t __attribute__((ext_vector_type(2)));
+    const float* scf = reinterpret_cast<const float*>(smem);
+    uint16_t* Y = static_cast<uint16_t*>(e.y);
+    const int tq = tid % LTPR, r0 = tid / LTPR, c0 = 8 * tq;
+    const bool full = n0 + BN <= N;
 #pragma unroll
-    for (int k = 0; k < CPT; k += 8) {
-      const u32x4_t w = *reinterpret_cast<const u32x4_t*>(&sc[r * OPITCH + c0 + k]);
+    for (int p = 0; p < LPASS; ++p) {
+      const int ml = r0 + p * LRPP, m = m0 + ml, n = n0 + c0;
+      const f32x4_t xa = *reinterpret_cast<const f32x4_t*>(&scf[ml * (BN + 4) + c0]);
+      const f32x4_t xb = *reinterpret_cast<const f32x4_t*>(&scf[ml * (BN + 4) + c0 + 4]);
+      float ev[8];
 #pragma unroll
-      for (int h = 0; h < 4; ++h) {
-        x[k + 2 * h] = __uint_as_float(w[h] << 16);
-        x[k + 2 * h + 1] = __uint_as_float(w[h] & 0xffff0000u);
+      for (int k = 0; k < 4; ++k) {
+        ev[k] = __builtin_amdgcn_exp2f(fmaf(xa[k], kL2e, -xrl[p]));
+        ev[4 + k] = __builtin_amdgcn_exp2f(fmaf(xb[k], kL2e, -xrl[p]));
       }
-    }
-    float mx = -INFINITY;
+      if (!full) {
 #pragma unroll
-    for (int k = 0; k < CPT; ++k)
-      if (k < nv) mx = fmaxf(mx, x[k]);
+        for (int k = 0; k < 8; ++k)
+          if (n + k >= N) ev[k] = 0.f;
+      }
+      u32x4_t o;
+      float se = 0.f;
 #pragma unroll
-    for (int o = 1; o < TPR; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-    // mx is finite: every tile holds at least one column of every row
-    const float l2e = 1.4426950408889634f, moff = mx * l2e;
-    float se = 0.f;
+      for (int k = 0; k < 4; ++k) {
+        o[k] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{ev[2 * k], ev[2 * k + 1]}), bf16x2_t));
+        se += __uint_as_float(o[k] << 16);
+        se += __uint_as_float(o[k] & 0xffff0000u);
+      }
+      if (m < M) {
+        uint16_t* dst = Y + (int64_t)m * e.ldy + n;
+        if (full || n + 8 <= N) {
+          *reinterpret_cast<u32x4_t*>(dst) = o;
+        } else {
+          for (int k = 0; k < 8 && n + k < N; ++k) dst[k] = (uint16_t)(k & 1 ? o[k / 2] >> 16 : o[k / 2] & 0xffffu);
+        }
+      }
 #pragma unroll
-    for (int k = 0; k < CPT; ++k)
-      if (k < nv) se += __builtin_amdgcn_exp2f(fmaf(x[k], l2e, -moff));
-#pragma unroll
-    for (int o = 1; o < TPR; o <<= 1) se += __shfl_xor(se, o, 64);
-    if (tid % TPR == 0 && m0 + r < M) {
-      e.lstat[(int64_t)(m0 + r) * e.ldlstat + 2 * by] = mx;
-      e.lstat[(int64_t)(m0 + r) * e.ldlstat + 2 * by + 1] = se;
-      // the logit at the row's target column, when this tile holds it
-      if (tgt1 >= n0 && tgt1 < n0 + BN && tgt1 < N) e.tlogit[m0 + r] = asf(sc[r * OPITCH + (tgt1 - n0)]);
+      for (int q = 1; q < LTPR; q <<= 1) se += __shfl_xor(se, q, 64);
+      if (tq == 0 && m < M) e.lstat[(int64_t)m * e.ldlstat + by] = se;
     }
   }
 

@@ -152,9 +152,12 @@ struct Block {
   float* part[NW] = {};
   Plan1 wp[NW];
   // activations (rows Np, pitch: multiples of 128 elements)
-  uint16_t *a0 = nullptr, *n1, *qkv, *o, *a1, *n2, *u, *g, *z, *hn, *logits;
+  // logits: the head's exponentials relative to the target logit, then
+  // (after tf_head_norm) the head's output gradient up to a row scale
+  uint16_t *a0 = nullptr, *n1, *qkv, *o, *a1, *n2, *u, *g, *z, *hn, *logits, *hns;
   uint16_t *dhn, *dz, *du, *dn2, *da1, *dout, *dqkv, *dn1 = nullptr;
-  float *r1, *r2, *r3, *lse, *dsum, *lstat, *tlogit, *ploss, *da0 = nullptr, *gemb = nullptr;
+  float *r1, *r2, *r3, *lse, *dsum, *lstat, *xref, *rowscale, *rowloss, *ploss, *da0 = nullptr, *gemb = nullptr;
+  int32_t* flag = nullptr;
   int ntiles = 0, nloss = 0;
   Lin fwd[NW], dgr[NW], wgr[NW];
   bool grouped[NW] = {};  // input- and weight-gradient GEMMs of the weight in one launch
@@ -229,6 +232,7 @@ size_t build_layout(const erase_tf_config& c, uintptr_t base, Layout* P) {
     B.z = bf(Np, P->ldd);
     B.hn = bf(Np, P->ldd);
     B.logits = bf(Np, P->ldv);
+    B.hns = bf(Np, P->ldd);
     B.dhn = bf(Np, P->ldd);
     B.dz = bf(Np, P->ldd);
     B.du = bf(Np, P->ld4);
@@ -243,8 +247,11 @@ size_t build_layout(const erase_tf_config& c, uintptr_t base, Layout* P) {
     B.dsum = f32(BHT);
     const Plan1 ph = choose_fwd(D.N, D.V, d);
     B.ntiles = (int)cdv(D.V, ph.bn);
-    B.lstat = f32(Np * 2 * B.ntiles);
-    B.tlogit = f32(Np);
+    B.lstat = f32(Np * B.ntiles);
+    B.xref = f32(Np);
+    B.rowscale = f32(Np);
+    B.rowloss = f32(Np);
+    B.flag = i32(Np);  // zero from init; tf_head_fix clears what it sets
     B.nloss = (int)cdv(D.N, 4);
     B.ploss = f32(B.nloss);
     for (int i = 0; i < NW; ++i) {
@@ -304,9 +311,8 @@ void build_gemms(const erase_tf_config& c, Layout* P) {
     B.fwd[W2].e.ldres = P->ldd;
     fwd(WH, B.hn, P->ldd, GK_FWD_LOGITS, B.logits, P->ldv);
     B.fwd[WH].e.lstat = B.lstat;
-    B.fwd[WH].e.ldlstat = 2 * B.ntiles;
-    B.fwd[WH].e.target = P->target;
-    B.fwd[WH].e.tlogit = B.tlogit;
+    B.fwd[WH].e.ldlstat = B.ntiles;
+    B.fwd[WH].e.xref = B.xref;
 
     // input gradients: A = the output gradient [N][rows], B = transposed copy [cols][rows]
     auto dgr = [&](int w, const void* A, int64_t lda, int kind, void* out, int64_t ldo) {
@@ -335,7 +341,7 @@ void build_gemms(const erase_tf_config& c, Layout* P) {
       L.e.ldp = D.cols[w];
       L.e.pstride = D.rows[w] * D.cols[w];
     };
-    wgr(WH, B.logits, P->ldv, B.hn, P->ldd);
+    wgr(WH, B.logits, P->ldv, B.hns, P->ldd);  // hns: the row-scaled head input
     wgr(W2, B.dz, P->ldd, B.g, P->ld4);
     wgr(W1, B.du, P->ld4, B.n2, P->ldd);
     wgr(WO, B.da1, P->ldd, B.o, P->ldd);
@@ -560,28 +566,48 @@ erase_status enqueue_body(TfCtx* c, int b, const int32_t* tokens, hipStream_t s,
   return ERASE_OK;
 }
 
-// local head: norm, logits with per-tile statistics, cross-entropy and the
-// logit gradient
+// local head: norm (and the target logit), the logits GEMM storing the
+// exponentials relative to the target logit with per-tile sums, then per row
+// the loss and the scales of the head's gradient (Section 2.1: the block's
+// own objective)
 erase_status enqueue_head(TfCtx* c, int b, hipStream_t s, int sid) {
   const Layout& P = c->P;
   const Dims& D = P.D;
   const Block& B = P.blk[b];
-  if (auto st = rms(c, 0, rms_args(P, B.z, B.r3, B.hn), b, 2, sid, s); st != ERASE_OK) return st;
+  TfRmsArgs ra = rms_args(P, B.z, B.r3, B.hn);
+  ra.hw = B.sh[WH];
+  ra.ldhw = D.cols[WH];
+  ra.target = P.target;
+  ra.xref = B.xref;
+  if (auto st = rms(c, 0, ra, b, 2, sid, s); st != ERASE_OK) return st;
   if (auto st = gemm(c, B.fwd[WH], 1, b, WH, sid, s); st != ERASE_OK) return st;
-  TfXentArgs x{};
-  x.logits = B.logits;
-  x.ldlog = P.ldv;
+  TfHeadArgs x{};
+  x.e = B.logits;
+  x.lde = P.ldv;
   x.lstat = B.lstat;
-  x.ldlstat = 2 * B.ntiles;
+  x.ldlstat = B.ntiles;
   x.ntiles = B.ntiles;
-  x.tlogit = B.tlogit;
+  x.xref = B.xref;
   x.target = P.target;
+  x.hn = B.hn;
+  x.ldhn = P.ldd;
+  x.hns = B.hns;
+  x.ldhns = P.ldd;
+  x.w = B.sh[WH];
+  x.ldw = D.cols[WH];
+  x.rowscale = B.rowscale;
+  x.rowloss = B.rowloss;
+  x.flag = B.flag;
   x.N = D.N;
   x.V = D.V;
+  x.d = D.d;
   x.scale = c->cfg.lambda / float(D.N);
   x.ploss = B.ploss;
-  TFRUN(c, 16, b, -1, sid, 0.0, double(D.N) * D.V * 4.0, (int)cdv(D.N, 4),
-        [&](const LaunchEv& ev) { return launch_tf_xent(x, s, ev); });
+  // bytes: per-tile sums, and the head input read and written scaled
+  TFRUN(c, 16, b, 0, sid, 0.0, double(D.N) * (4.0 * B.ntiles + 4.0 * D.d + 16.0), (int)cdv(D.N, 4),
+        [&](const LaunchEv& ev) { return launch_tf_head(0, x, s, ev); });
+  TFRUN(c, 16, b, 1, sid, 0.0, double(D.N) * 4.0, (int)cdv(D.N, 4),
+        [&](const LaunchEv& ev) { return launch_tf_head(1, x, s, ev); });
   return ERASE_OK;
 }
 
@@ -605,10 +631,11 @@ erase_status enqueue_backward(TfCtx* c, int b, hipStream_t s, int sid) {
   };
   erase_status st;
   if ((st = G2(WH)) != ERASE_OK) return st;
-  {  // dz = rms'(z) dhn
+  {  // dz = rms'(z) (rowscale dhn): the head's input gradient takes its row scale here
     TfRmsArgs a = rms_args(P, B.z, B.r3, B.dz);
     a.dy = B.dhn;
     a.lddy = P.ldd;
+    a.dyscale = B.rowscale;
     if ((st = rms(c, 1, a, b, 2, sid, s)) != ERASE_OK) return st;
   }
   if ((st = G(B.dgr[W2], 4, W2)) != ERASE_OK) return st;
@@ -960,6 +987,8 @@ erase_status erase_tf_tensor(erase_tf_ctx* ctx, int32_t block, int32_t which, vo
     case 11: p = B.lse; l = P.D.T; break;
     case 12: p = B.dqkv; l = P.ld3; break;
     case 13: p = B.dz; break;
+    case 14: p = B.rowscale; l = P.D.N; break;
+    case 15: p = B.hns; break;
     default: return ERASE_ERR_INVALID_ARG;
   }
   *ptr = p;

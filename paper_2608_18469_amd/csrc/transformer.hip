@@ -12,9 +12,12 @@
 //                   log-sum-exp.
 //  * tf_attn_bwd_*: D = rowsum(do * o), then dK/dV per key block and dQ per
 //                   query block (no atomics: every output has one writer).
-//  * tf_xent:       log-sum-exp per row from the logits GEMM's per-tile
-//                   statistics, the row loss, and the logit gradient
-//                   lam (softmax - onehot) / N in place of the logits.
+//  * tf_head_norm:  the softmax normaliser of every row from the logits
+//                   GEMM's per-tile sums of exponentials relative to the
+//                   target logit: the row loss, the row's gradient scale,
+//                   the target entry of the gradient and the scaled head
+//                   input; tf_head_fix recomputes the rare rows whose
+//                   exponentials were out of range.
 //  * tf_emb_*:      embedding gradient: positions bucketed by token (integer
 //                   counters), each bucket ordered by position, rows summed in
 //                   that order, so the result does not depend on scheduling.
@@ -183,6 +186,8 @@ __global__ __launch_bounds__(256) void tf_rms_fwd(TfRmsArgs a) {
   ss = wsum(ss);
   const float r = 1.f / sqrtf(ss / (float)a.d + a.eps);
   if (lane == 0) a.r[n] = r;
+  const int32_t tg = a.hw ? a.target[n] : -1;
+  float xt = 0.f;
 #pragma unroll
   for (int i = 0; i < kRmsChunks; ++i) {
     const int c = lane + 64 * i;
@@ -191,6 +196,19 @@ __global__ __launch_bounds__(256) void tf_rms_fwd(TfRmsArgs a) {
 #pragma unroll
     for (int k = 0; k < 4; ++k) o[k] = pack2(lo16(v[i][k]) * r, hi16(v[i][k]) * r);
     *reinterpret_cast<u32x4_t*>(a.y + n * a.ldy + c * 8) = o;
+    if (tg >= 0) {
+      // the target logit of the stored (rounded) row
+      const u32x4_t w = *reinterpret_cast<const u32x4_t*>(a.hw + (int64_t)tg * a.ldhw + c * 8);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        xt = fmaf(lo16(o[k]), lo16(w[k]), xt);
+        xt = fmaf(hi16(o[k]), hi16(w[k]), xt);
+      }
+    }
+  }
+  if (a.hw) {
+    xt = wsum(xt);
+    if (lane == 0) a.xref[n] = xt;
   }
 }
 
@@ -200,6 +218,7 @@ __global__ __launch_bounds__(256) void tf_rms_bwd(TfRmsArgs a) {
   if (n >= a.N) return;
   const int nc = a.d / 8;
   const float r = a.r[n];
+  const float gs = a.dyscale ? a.dyscale[n] : 1.f;
   u32x4_t xv[kRmsChunks], gv[kRmsChunks];
   float dot = 0.f;
 #pragma unroll
@@ -212,8 +231,8 @@ __global__ __launch_bounds__(256) void tf_rms_bwd(TfRmsArgs a) {
     }
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      dot = fmaf(lo16(gv[i][k]), lo16(xv[i][k]) * r, dot);
-      dot = fmaf(hi16(gv[i][k]), hi16(xv[i][k]) * r, dot);
+      dot = fmaf(lo16(gv[i][k]) * gs, lo16(xv[i][k]) * r, dot);
+      dot = fmaf(hi16(gv[i][k]) * gs, hi16(xv[i][k]) * r, dot);
     }
   }
   const float mdot = wsum(dot) / (float)a.d;
@@ -224,8 +243,8 @@ __global__ __launch_bounds__(256) void tf_rms_bwd(TfRmsArgs a) {
     float o[8];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      o[2 * k] = r * (lo16(gv[i][k]) - lo16(xv[i][k]) * r * mdot);
-      o[2 * k + 1] = r * (hi16(gv[i][k]) - hi16(xv[i][k]) * r * mdot);
+      o[2 * k] = r * (lo16(gv[i][k]) * gs - lo16(xv[i][k]) * r * mdot);
+      o[2 * k + 1] = r * (hi16(gv[i][k]) * gs - hi16(xv[i][k]) * r * mdot);
     }
     if (a.res) {
       const u32x4_t rv = *reinterpret_cast<const u32x4_t*>(a.res + n * a.ldres + c * 8);
@@ -566,53 +585,133 @@ __global__ __launch_bounds__(256) void tf_attn_bwd_dq(TfAttnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// softmax cross-entropy rows: one wave per row
+// vocabulary head: softmax normaliser, loss and gradient scale per row
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void tf_xent(TfXentArgs a) {
+// Range of S_n (the sum of a row's exponentials relative to the target logit)
+// the fast path accepts: S_n >= e^0 up to rounding whenever the target is
+// valid, and S_n <= 2^60 keeps rowscale and hns far from underflow.
+constexpr float kHeadLo = 0x1p-60f, kHeadHi = 0x1p60f;
+
+// rowscale, the target entry of the gradient (pt: its stored exponential)
+// and hns = rowscale hn of row n, by the lanes of one wave
+__device__ __forceinline__ void head_finish(const TfHeadArgs& a, int64_t n, float se, int tg, float pt, int lane) {
+  const float s = a.scale / se;
+  if (lane == 0) {
+    a.rowscale[n] = s;
+    if (tg >= 0) a.e[n * a.lde + tg] = tobf(pt - se);
+  }
+  for (int c = lane; c < a.d / 8; c += 64) {
+    const u32x4_t h = *reinterpret_cast<const u32x4_t*>(a.hn + n * a.ldhn + c * 8);
+    u32x4_t o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) o[k] = pack2(lo16(h[k]) * s, hi16(h[k]) * s);
+    *reinterpret_cast<u32x4_t*>(a.hns + n * a.ldhns + c * 8) = o;
+  }
+}
+
+__global__ __launch_bounds__(256) void tf_head_norm(TfHeadArgs a) {
   __shared__ float sloss[4];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t n = (int64_t)blockIdx.x * 4 + wave;
   float loss = 0.f;
   if (n < a.N) {
     const float* st = a.lstat + n * a.ldlstat;
-    float mx = -INFINITY;
-    for (int t = lane; t < a.ntiles; t += 64) mx = fmaxf(mx, st[2 * t]);
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
     float se = 0.f;
-    for (int t = lane; t < a.ntiles; t += 64) se += st[2 * t + 1] * __expf(st[2 * t] - mx);
+    for (int t = lane; t < a.ntiles; t += 64) se += st[t];
     se = wsum(se);
-    const float lse = mx + __logf(se);
     const int tg = a.target[n];
-    loss = tg >= 0 ? lse - a.tlogit[n] : 0.f;
-    uint16_t* row = a.logits + n * a.ldlog;
-    const int nch = a.V / 8;
-    // four 16-byte chunks per lane in flight: all loads, then all stores
-    for (int c0 = lane; c0 < nch; c0 += 256) {
-      u32x4_t v[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (c0 + 64 * u < nch) v[u] = *reinterpret_cast<const u32x4_t*>(row + (c0 + 64 * u) * 8);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int c = c0 + 64 * u;
-        if (c >= nch) continue;
-        u32x4_t o;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const int col = c * 8 + 2 * k;
-          float p0 = __expf(lo16(v[u][k]) - lse), p1 = __expf(hi16(v[u][k]) - lse);
-          if (col == tg) p0 -= 1.f;
-          if (col + 1 == tg) p1 -= 1.f;
-          o[k] = pack2(p0 * a.scale, p1 * a.scale);
-        }
-        *reinterpret_cast<u32x4_t*>(row + c * 8) = o;
-      }
+    if (se >= kHeadLo && se <= kHeadHi) {  // false for NaN
+      loss = tg >= 0 ? __logf(se) : 0.f;
+      const float pt = tg >= 0 ? bf(a.e[n * a.lde + tg]) : 0.f;
+      head_finish(a, n, se, tg, pt, lane);
+    } else if (lane == 0) {
+      a.flag[n] = 1;
     }
+    if (lane == 0) a.rowloss[n] = loss;
   }
   if (lane == 0) sloss[wave] = loss;
   __syncthreads();
   if (threadIdx.x == 0) a.ploss[blockIdx.x] = (sloss[0] + sloss[1]) + (sloss[2] + sloss[3]);
+}
+
+// logit of vocabulary row v from the head input held in LDS (fp32)
+__device__ __forceinline__ float head_logit(const TfHeadArgs& a, const float* h, int v) {
+  const uint16_t* w = a.w + (int64_t)v * a.ldw;
+  float x = 0.f;
+  for (int c = 0; c < a.d; c += 8) {
+    const u32x4_t q = *reinterpret_cast<const u32x4_t*>(w + c);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      x = fmaf(h[c + 2 * k], lo16(q[k]), x);
+      x = fmaf(h[c + 2 * k + 1], hi16(q[k]), x);
+    }
+  }
+  return x;
+}
+
+// Flagged rows of a group of four: the row's logits recomputed (one thread
+// per vocabulary row, fp32 dot products), their exact maximum as the
+// reference, then the exponentials, their sum and the same outputs as the
+// fast path.  Sums in a fixed order (per thread over its rows, a wave
+// butterfly, then the four waves).
+constexpr int kHeadMaxD = 4096;
+__global__ __launch_bounds__(256) void tf_head_fix(TfHeadArgs a) {
+  __shared__ int fl[4];
+  __shared__ float hrow[kHeadMaxD];
+  __shared__ float red[3][4];
+  __shared__ float spt;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int64_t n0 = (int64_t)blockIdx.x * 4;
+  if (tid < 4) fl[tid] = n0 + tid < a.N ? a.flag[n0 + tid] : 0;
+  __syncthreads();
+  if (!(fl[0] | fl[1] | fl[2] | fl[3])) return;
+  for (int j = 0; j < 4; ++j) {
+    if (!fl[j]) continue;
+    const int64_t n = n0 + j;
+    const int tg = a.target[n];
+    for (int c = tid; c < a.d; c += 256) hrow[c] = bf(a.hn[n * a.ldhn + c]);
+    if (tid == 0) spt = 0.f;
+    __syncthreads();
+    float mx = -INFINITY;
+    for (int v = tid; v < a.V; v += 256) mx = fmaxf(mx, head_logit(a, hrow, v));
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+    if (lane == 0) red[0][wave] = mx;
+    __syncthreads();
+    mx = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
+    float se = 0.f, xt = 0.f;
+    for (int v = tid; v < a.V; v += 256) {
+      const float x = head_logit(a, hrow, v);
+      const uint16_t p = tobf(__expf(x - mx));
+      a.e[n * a.lde + v] = p;
+      se += bf(p);
+      if (v == tg) {
+        xt = x;
+        spt = bf(p);
+      }
+    }
+    se = wsum(se);
+    xt = wsum(xt);  // one thread holds the target logit, the others zero
+    if (lane == 0) {
+      red[1][wave] = se;
+      red[2][wave] = xt;
+    }
+    __syncthreads();
+    se = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+    xt = (red[2][0] + red[2][1]) + (red[2][2] + red[2][3]);
+    if (wave == 0) head_finish(a, n, se, tg, spt, lane);
+    if (tid == 0) {
+      a.rowloss[n] = tg >= 0 ? mx + __logf(se) - xt : 0.f;
+      a.flag[n] = 0;
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    float l[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) l[q] = n0 + q < a.N ? a.rowloss[n0 + q] : 0.f;
+    a.ploss[blockIdx.x] = (l[0] + l[1]) + (l[2] + l[3]);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -747,9 +846,13 @@ hipError_t launch_tf_attn(int part, const TfAttnArgs& a, hipStream_t s, const La
   return hipGetLastError();
 }
 
-hipError_t launch_tf_xent(const TfXentArgs& a, hipStream_t s, const LaunchEv& ev) {
-  if (a.V % 8) return hipErrorInvalidValue;
-  ERASE_TF_LAUNCH(tf_xent, dim3((unsigned)((a.N + 3) / 4)), dim3(256), s, ev, a);
+hipError_t launch_tf_head(int part, const TfHeadArgs& a, hipStream_t s, const LaunchEv& ev) {
+  if (a.d % 8 || a.d > kHeadMaxD || a.N < 1) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)((a.N + 3) / 4));
+  if (part == 0)
+    ERASE_TF_LAUNCH(tf_head_norm, grid, dim3(256), s, ev, a);
+  else
+    ERASE_TF_LAUNCH(tf_head_fix, grid, dim3(256), s, ev, a);
   return hipGetLastError();
 }
 

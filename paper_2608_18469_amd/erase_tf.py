@@ -16,12 +16,12 @@ from . import erase, synth_tf
 from .erase import BlockBuffers, EraseError, KernelTime, OK
 
 TF_KERNEL_KINDS = {0: "prologue", 1: "fwd_gemm", 3: "wgrad_gemm", 4: "dgrad_gemm", 5: "adam", 6: "bwd_gemm", 7: "empty",
-                   11: "embed", 12: "rms_fwd", 13: "rms_bwd", 14: "attn_fwd", 15: "attn_bwd", 16: "xent",
+                   11: "embed", 12: "rms_fwd", 13: "rms_bwd", 14: "attn_fwd", 15: "attn_bwd", 16: "head_norm",
                    17: "emb_grad"}
 GEMM_NAMES = {0: "qkv", 1: "proj", 2: "mlp_up", 3: "mlp_down", 4: "vocab"}
 SCHEDULES = {"serial": erase.SERIAL, "overlap": erase.OVERLAP}
 TENSORS = {"a0": 0, "n1": 1, "qkv": 2, "o": 3, "a1": 4, "n2": 5, "u": 6, "g": 7, "z": 8, "hn": 9,
-           "logits": 10, "lse": 11, "dqkv": 12, "dz": 13}
+           "logits": 10, "lse": 11, "dqkv": 12, "dz": 13, "rowscale": 14, "hns": 15}
 
 
 class TfConfig(ctypes.Structure):

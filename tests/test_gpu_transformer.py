@@ -204,7 +204,10 @@ def test_tf_c5_full_size_sampled():
     o0 = tra.tensor(0, "o", T, d)
     lse0 = tra.tensor(0, "lse", cfg["heads"], T, dtype="f32")
     V = cfg["vocab"]
-    dl0 = _bf16_view(tra, 0, "logits", T)[:, :V].float().cpu().numpy()  # after the step: the logit gradient
+    # after the step: the head's exponentials with the target entry minus the
+    # row sum, and the row scale; their product is the logit gradient
+    dl0 = _bf16_view(tra, 0, "logits", T)[:, :V].float().cpu().numpy()
+    dl0 = dl0 * tra.tensor(0, "rowscale", 1, T, dtype="f32")[0][:, None]
     tra.close()
     del tra
     print("[tf] c5 overlap", flush=True)
@@ -227,8 +230,8 @@ def test_tf_c5_full_size_sampled():
     mx = s.max(-1, keepdims=True)
     ref = (mx + np.log(np.exp(s - mx).sum(-1, keepdims=True)))[..., 0]
     assert np.max(np.abs(lse0 - ref)) < 5e-2, np.max(np.abs(lse0 - ref))
-    # the head of block 1 on sequence 0: logits GEMM, statistics and
-    # cross-entropy, through the stored gradient lam (softmax - onehot) / N
+    # the head of block 1 on sequence 0: logits GEMM, row sums and
+    # normaliser, through the logit gradient lam (softmax - onehot) / N
     x = c["logits"]
     p = np.exp(x - x.max(axis=1, keepdims=True))
     p /= p.sum(axis=1, keepdims=True)
@@ -340,7 +343,7 @@ def test_tf_timing_records():
         recs = tr.read_timing()
         assert recs[0]["kind"] == "empty"
         kinds = {r["kind"] for r in recs[1:]}
-        assert {"prologue", "embed", "rms_fwd", "fwd_gemm", "attn_fwd", "xent", "rms_bwd", "attn_bwd",
+        assert {"prologue", "embed", "rms_fwd", "fwd_gemm", "attn_fwd", "head_norm", "rms_bwd", "attn_bwd",
                 "adam", "emb_grad"} <= kinds, kinds
         assert any(k in kinds for k in ("bwd_gemm", "wgrad_gemm"))
         for r in recs[1:]:
@@ -348,10 +351,37 @@ def test_tf_timing_records():
         streams = {r["stream"] for r in recs[1:]}
         assert streams == ({0} if sched == "serial" else {0, 1}), streams
         # per block: the forward body on stream 0, the head on the backward stream when overlapped
-        heads = [r for r in recs[1:] if r["kind"] == "xent"]
-        assert len(heads) == cfg["layers"] and all(r["stream"] == (0 if sched == "serial" else 1) for r in heads)
+        # the normaliser and the recomputation of out-of-range rows: two launches per block
+        heads = [r for r in recs[1:] if r["kind"] == "head_norm"]
+        assert len(heads) == 2 * cfg["layers"] and all(r["stream"] == (0 if sched == "serial" else 1) for r in heads)
+        assert sorted(r["layer"] for r in heads) == [0] * cfg["layers"] + [1] * cfg["layers"]
     tr.set_timing(False)
     tr.close()
+
+
+def test_tf_head_rows_out_of_range():
+    """Rows whose exponentials relative to the target logit sum past 2^60
+    (row loss above 60 ln 2) take the recomputation with the row's exact
+    maximum; the others the fast path.  A head weight 32 times its initial
+    scale gives logits spread over about +-60, so both kinds of rows occur
+    (checked on the oracle's row losses).  Compared with the float64 oracle:
+    the bf16 emulation's exponentials relative to the target logit overflow
+    bf16 on such rows, so it does not model them."""
+    cfg = synth_tf.tf_config("tf_small", layers=1, seq=64)
+    params, batches = synth_tf.make_workload(cfg, seed=12, n_batches=1)
+    params[0]["wh"] = np.asarray(params[0]["wh"]) * 32.0  # a power of two: still bf16 values
+    tok = batches[0]
+    caches, _, tgt = to._forward(cfg, params, tok, False, np.float64)
+    rows, _ = to.softmax_xent(caches[0]["logits"], tgt)
+    far = int(np.sum(rows > 42.0))
+    near = int(np.sum(rows < 40.0))
+    print(f"[tf] head out-of-range rows: {far} above, {near} below of {rows.size}", flush=True)
+    assert far > 0 and near > 0
+    _, gpu = _gpu_run(cfg, params, batches, "serial")
+    r64 = _oracle_run(cfg, params, batches)
+    w = _worst(cfg, gpu, r64)
+    print(f"[tf] head out-of-range rows vs float64: {w}", flush=True)
+    assert all(w[k] < 2e-2 for k in FIELDS), w
 
 
 def test_tf_widest_model():
