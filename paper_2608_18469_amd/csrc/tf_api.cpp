@@ -310,6 +310,12 @@ void build_gemms(const erase_tf_config& c, Layout* P) {
     B.fwd[W2].e.res = B.a1;
     B.fwd[W2].e.ldres = P->ldd;
     fwd(WH, B.hn, P->ldd, GK_FWD_LOGITS, B.logits, P->ldv);
+    // tile order: groups of 8 M-tiles (512 positions), each walking every
+    // vocabulary tile, keep the tiles an XCD runs at once on about 2 MB of
+    // operands (its L2 holds 4 MB).  Measured at 16384 x 32768 x 512: 0.89
+    // ms, against 0.99 ms for the generic choice (groups of 128 M-tiles, 6 MB
+    // of head input in flight per XCD), 0.91 for 16, 0.93 for 2, 1.20 for 1.
+    B.fwd[WH].g.group = 8;
     B.fwd[WH].e.lstat = B.lstat;
     B.fwd[WH].e.ldlstat = B.ntiles;
     B.fwd[WH].e.xref = B.xref;
