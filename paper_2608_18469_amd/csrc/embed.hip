@@ -171,7 +171,8 @@ constexpr int kSortCap = 16384;   // largest bucket sorted in LDS (64 KB)
 //    each group adding its entries in order, the groups then combined by a
 //    fixed butterfly;
 //  * rows of 65..1024 entries: one workgroup of 256 threads, and rows of
-//    1025..16384 entries one of 1024 threads; entries sorted in LDS, entry
+//    1025..16384 entries one of 1024 threads; entries sorted in LDS (a
+//    bitmap over their range, or a bitonic sort), entry
 //    k to lane group k mod (threads/G), the groups' partial rows then added
 //    in group order;
 //  * larger rows: increasing entry order, by repeated selection (correct but
@@ -201,53 +202,76 @@ __global__ __launch_bounds__(256) void erase_bags_bwd_owner(EmbedBwdArgs a) {
   for (int64_t i = beg; i < end; ++i) a.owner[i] = (int32_t)bag;
 }
 
-// One thread per entry: its global row, and its slot in the row's bucket
-// from the row's counter.  The lanes of a wave that share a row add to its
-// counter once (a leader per row: Zipf-skewed ids repeat the hot rows many
-// times per wave, and every increment of one counter is serialised).
+// Each entry's global row, and its slot in the row's bucket.  A workgroup
+// takes kCountTile entries (kCountPer per thread) and first counts their
+// rows in an LDS hash table, so each row it holds takes one addition to its
+// global counter per workgroup (Zipf-hot rows occur in most workgroups, and
+// the additions to one counter are serialised).  Slots need only be distinct
+// within a bucket (every bucket is sorted by entry before it is summed): an
+// entry's slot is its row's base from that addition plus its rank from the
+// LDS count.
+constexpr int kCountPer = 8, kCountTile = 256 * kCountPer, kHashSlots = 2 * kCountTile;
 __global__ __launch_bounds__(256) void erase_bags_bwd_count(EmbedBwdArgs a) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int lane = threadIdx.x & 63;
-  int32_t gid = -1;
-  if (i < a.nnz) {
-    const int32_t o = a.owner[i];
-    if (o >= 0) {
-      const int32_t r = a.indices[i];
-      if (r >= 0 && r < a.rows) {
-        gid = (int32_t)((o / a.M) * a.rows + r);
-      } else if (a.status) {
-        a.status[0] = 1;
+  __shared__ int32_t hkey[kHashSlots];  // global row, -1: empty
+  __shared__ int32_t hval[kHashSlots];  // the row's entries in this tile, then its base
+  const int tid = threadIdx.x;
+  for (int h = tid; h < kHashSlots; h += 256) {
+    hkey[h] = -1;
+    hval[h] = 0;
+  }
+  __syncthreads();
+  const int64_t i0 = (int64_t)blockIdx.x * kCountTile + tid;
+  int32_t gid[kCountPer], hs[kCountPer], rk[kCountPer];
+#pragma unroll
+  for (int u = 0; u < kCountPer; ++u) {
+    const int64_t i = i0 + u * 256;
+    gid[u] = -1;
+    hs[u] = 0;
+    rk[u] = 0;
+    if (i < a.nnz) {
+      const int32_t o = a.owner[i];
+      if (o >= 0) {
+        const int32_t r = a.indices[i];
+        if (r >= 0 && r < a.rows) {
+          gid[u] = (int32_t)((o / a.M) * a.rows + r);
+        } else if (a.status) {
+          a.status[0] = 1;
+        }
       }
     }
   }
-  // group the lanes by row: each lane learns its row's leader (the lowest
-  // lane of the row) and its rank among the row's lanes; each leader counts
-  int leader = 0, rank = 0, k = 0;
-  uint64_t pending = __ballot(gid >= 0);
-  while (pending) {
-    const int l0 = __ffsll((unsigned long long)pending) - 1;
-    const int32_t lg = __shfl(gid, l0, 64);
-    const uint64_t same = __ballot(gid == lg) & pending;
-    if (lane == l0) k = __popcll(same);
-    if ((same >> lane) & 1ull) {
-      leader = l0;
-      rank = __popcll(same & ((1ull << lane) - 1ull));
+#pragma unroll
+  for (int u = 0; u < kCountPer; ++u) {
+    if (gid[u] < 0) continue;
+    // open addressing: at most kCountTile keys in 2 kCountTile slots
+    int h = (int)(((uint32_t)gid[u] * 0x9E3779B1u) >> 20) & (kHashSlots - 1);
+    while (true) {
+      const int32_t prev = atomicCAS(&hkey[h], -1, gid[u]);
+      if (prev == -1 || prev == gid[u]) break;
+      h = (h + 1) & (kHashSlots - 1);
     }
-    pending &= ~same;
+    hs[u] = h;
+    rk[u] = atomicAdd(&hval[h], 1);
   }
-  // every leader adds to its row's counter at once (one round trip)
-  int32_t base = 0;
-  if (k > 0) {
-    base = atomicAdd(&a.count[gid], k);
+  __syncthreads();
+  for (int h = tid; h < kHashSlots; h += 256) {
+    const int32_t g = hkey[h];
+    if (g < 0) continue;
+    const int k = hval[h];
+    const int32_t base = atomicAdd(&a.count[g], k);
     // a row whose count passes kSmallBucket is listed once (exactly one
     // addition crosses the threshold)
-    if (base <= kSmallBucket && base + k > kSmallBucket) a.large[atomicAdd(a.nlarge, 1)] = gid;
+    if (base <= kSmallBucket && base + k > kSmallBucket) a.large[atomicAdd(a.nlarge, 1)] = g;
+    hval[h] = base;
   }
-  base = __shfl(base, leader, 64);
-  const int32_t slot = base + rank;
-  if (i < a.nnz) {
-    a.gid[i] = gid;
-    a.slot[i] = slot;
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < kCountPer; ++u) {
+    const int64_t i = i0 + u * 256;
+    if (i < a.nnz) {
+      a.gid[i] = gid[u];
+      a.slot[i] = gid[u] >= 0 ? hval[hs[u]] + rk[u] : 0;
+    }
   }
 }
 
@@ -260,39 +284,70 @@ __global__ __launch_bounds__(256) void erase_bags_bwd_count(EmbedBwdArgs a) {
 constexpr int kScanBlock = 4096;  // 256 threads x 16 rows
 
 __device__ __forceinline__ int block_exclusive_scan(int v, int* part) {
-  // exclusive scan of one value per thread over 256 threads (Hillis-Steele in LDS)
-  const int tid = threadIdx.x;
-  part[tid] = v;
-  __syncthreads();
-  for (int off = 1; off < 256; off <<= 1) {
-    const int x = tid >= off ? part[tid - off] : 0;
-    __syncthreads();
-    part[tid] += x;
-    __syncthreads();
+  // exclusive scan of one value per thread over 256 threads: inclusive scans
+  // within the waves (lane shifts), then the wave totals through LDS
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
   }
-  const int incl = part[tid];
+  if (lane == 63) part[w] = x;
   __syncthreads();
-  return incl - v;
+  int base = 0;
+  for (int k = 0; k < w; ++k) base += part[k];
+  __syncthreads();
+  return base + x - v;
 }
 
 __device__ __forceinline__ bool small_row(int c) { return c > 0 && c <= kSmallBucket; }
 
+// a thread's 16 consecutive rows: four 16-byte accesses when all exist
+__device__ __forceinline__ void load16(const int32_t* p, int64_t base, int64_t n, int v[16]) {
+  if (base + 16 <= n) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int4 x = reinterpret_cast<const int4*>(p + base)[q];
+      v[4 * q] = x.x;
+      v[4 * q + 1] = x.y;
+      v[4 * q + 2] = x.z;
+      v[4 * q + 3] = x.w;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = base + k < n ? p[base + k] : 0;
+  }
+}
+__device__ __forceinline__ void store16(int32_t* p, int64_t base, int64_t n, const int v[16]) {
+  if (base + 16 <= n) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      reinterpret_cast<int4*>(p + base)[q] = make_int4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+      if (base + k < n) p[base + k] = v[k];
+  }
+}
+
 __global__ __launch_bounds__(256) void erase_bags_bwd_scan_local(EmbedBwdArgs a) {
   __shared__ int part[256];
   const int64_t base = (int64_t)blockIdx.x * kScanBlock + threadIdx.x * 16;
-  int v[16], s = 0, f = 0;
+  int v[16], st[16], s = 0, f = 0;
+  load16(a.count, base, a.trows, v);
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
-    v[k] = base + k < a.trows ? a.count[base + k] : 0;
     s += v[k];
     f += small_row(v[k]) ? 1 : 0;
   }
   int run = block_exclusive_scan(s, part);
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
-    if (base + k < a.trows) a.start[base + k] = run;
+    st[k] = run;
     run += v[k];
   }
+  store16(a.start, base, a.trows, st);
   const int fx = block_exclusive_scan(f, part);
   if (threadIdx.x == 255) {
     a.bsum[blockIdx.x] = run;
@@ -329,17 +384,17 @@ __global__ __launch_bounds__(256) void erase_bags_bwd_scan_add(EmbedBwdArgs a) {
   __shared__ int part[256];
   const int64_t base = (int64_t)blockIdx.x * kScanBlock + threadIdx.x * 16;
   const int off = a.bsum[blockIdx.x];
-  int f = 0;
+  int f = 0, st[16], c[16];
   bool fl[16];
+  load16(a.start, base, a.trows, st);
+  load16(a.count, base, a.trows, c);
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
-    fl[k] = false;
-    if (base + k < a.trows) {
-      a.start[base + k] += off;
-      fl[k] = small_row(a.count[base + k]);
-    }
+    st[k] += off;
+    fl[k] = base + k < a.trows && small_row(c[k]);
     f += fl[k] ? 1 : 0;
   }
+  store16(a.start, base, a.trows, st);
   int pos = a.bsum2[blockIdx.x] + block_exclusive_scan(f, part);
 #pragma unroll
   for (int k = 0; k < 16; ++k)
@@ -376,12 +431,45 @@ __device__ __forceinline__ void add4(float4& a, const float4& b) {
 
 // Buckets of more than kSmallBucket entries (the listed rows): one workgroup
 // of NT threads per bucket of LO < c <= HI entries sorts it by entry in LDS
-// (bitonic, up to CAP entries), turns the entries into their bag rows, and
+// (up to CAP entries: a bitmap over the bucket's entry range when it spans
+// at most 32 kBitWords entries, as on the CTR shape, else a bitonic sort),
+// turns the entries into their bag rows, and
 // sums the row: lane group q (G lanes, 4 columns each) takes entries q,
 // q + NG, ... in order, then the NG partial rows are added in group order.
 // Buckets beyond CAP are summed in increasing entry order by repeated
 // selection.  Instances: 256 threads for 65..1024 entries, 1024 threads
 // above (kSortCap, 16384, sorted).
+constexpr int kBitWords = 2048;  // bitmap of the bitmap sort: buckets whose entries span <= 64 Ki
+
+// Minimum over the NT threads of a workgroup (every thread gets it).
+template <int NT>
+__device__ __forceinline__ int32_t block_min_nt(int32_t v, int32_t* sel) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
+  if ((threadIdx.x & 63) == 0) sel[threadIdx.x >> 6] = v;
+  __syncthreads();
+  v = sel[0];
+  for (int w = 1; w < NT / 64; ++w) v = min(v, sel[w]);
+  __syncthreads();
+  return v;
+}
+// Exclusive prefix sum of one value per thread over the NT threads.
+template <int NT>
+__device__ __forceinline__ int block_exclusive_scan_nt(int v, int32_t* sel) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) sel[w] = x;
+  __syncthreads();
+  int base = 0;
+  for (int k = 0; k < w; ++k) base += sel[k];
+  __syncthreads();
+  return base + x - v;
+}
 constexpr int kMidBucket = 1024;
 template <typename T, int G, int NT, int CAP>
 __global__ __launch_bounds__(NT) void erase_bags_bwd_large(EmbedBwdArgs a, int lo, int hi) {
@@ -389,6 +477,7 @@ __global__ __launch_bounds__(NT) void erase_bags_bwd_large(EmbedBwdArgs a, int l
   static_assert(NG * 4 * G <= CAP, "partial rows fit in the key array");
   __shared__ int32_t key[CAP];
   __shared__ int32_t sel[NT / 64];
+  __shared__ uint32_t bits[kBitWords];
   if ((int)blockIdx.x >= a.nlarge[0]) return;  // uniform per workgroup
   const int32_t g = a.large[blockIdx.x];
   const int c = a.count[g], s0 = a.start[g];
@@ -423,35 +512,72 @@ __global__ __launch_bounds__(NT) void erase_bags_bwd_large(EmbedBwdArgs a, int l
     if (q == 0 && col) *reinterpret_cast<float4*>(out) = acc;
     return;
   }
-  int n2 = 1;
-  while (n2 < c) n2 <<= 1;
   constexpr int PER = CAP / NT;  // keys per thread
-  {
-    int32_t tmp[PER];  // every load in flight before the LDS stores
-#pragma unroll
-    for (int u = 0; u < PER; ++u) {
-      const int i = tid + u * NT;
-      tmp[u] = i < c ? a.bucket[s0 + i] : INT32_MAX;
-    }
-#pragma unroll
-    for (int u = 0; u < PER; ++u)
-      if (tid + u * NT < n2) key[tid + u * NT] = tmp[u];
+  // the bucket's entry range
+  int32_t e_lo = INT32_MAX, e_hi = -1;
+  for (int i = tid; i < c; i += NT) {
+    const int32_t p = a.bucket[s0 + i];
+    e_lo = min(e_lo, p);
+    e_hi = max(e_hi, p);
   }
-  __syncthreads();
-  for (int k = 2; k <= n2; k <<= 1)
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int i = tid; i < n2; i += NT) {
-        const int l = i ^ j;
-        if (l > i) {
-          const int32_t x = key[i], y = key[l];
-          if (((i & k) == 0) == (x > y)) {
-            key[i] = y;
-            key[l] = x;
+  e_lo = block_min_nt<NT>(e_lo, sel);
+  e_hi = -block_min_nt<NT>(-e_hi, sel);
+  const int64_t range = (int64_t)e_hi - e_lo + 1;
+  if (range <= 32 * (int64_t)kBitWords) {
+    // Bitmap sort (the entries of a bucket are distinct): one bit per entry
+    // of the range, then every thread lists the set bits of its run of
+    // words, in order, at its place from a scan of the runs' bit counts.
+    const int nw = (int)((range + 31) / 32);
+    for (int w = tid; w < nw; w += NT) bits[w] = 0u;
+    __syncthreads();
+    for (int i = tid; i < c; i += NT) {
+      const int32_t p = a.bucket[s0 + i] - e_lo;
+      atomicOr(&bits[p >> 5], 1u << (p & 31));
+    }
+    __syncthreads();
+    const int per = (nw + NT - 1) / NT, w0 = min(nw, tid * per), w1 = min(nw, w0 + per);
+    int cnt = 0;
+    for (int w = w0; w < w1; ++w) cnt += __popc(bits[w]);
+    int pos = block_exclusive_scan_nt<NT>(cnt, sel);
+    for (int w = w0; w < w1; ++w) {
+      uint32_t b = bits[w];
+      while (b) {
+        key[pos++] = e_lo + 32 * w + (__ffs(b) - 1);
+        b &= b - 1u;
+      }
+    }
+    __syncthreads();
+  } else {
+    // bitonic sort of the bucket in LDS
+    int n2 = 1;
+    while (n2 < c) n2 <<= 1;
+    {
+      int32_t tmp[PER];  // every load in flight before the LDS stores
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int i = tid + u * NT;
+        tmp[u] = i < c ? a.bucket[s0 + i] : INT32_MAX;
+      }
+#pragma unroll
+      for (int u = 0; u < PER; ++u)
+        if (tid + u * NT < n2) key[tid + u * NT] = tmp[u];
+    }
+    __syncthreads();
+    for (int k = 2; k <= n2; k <<= 1)
+      for (int j = k >> 1; j > 0; j >>= 1) {
+        for (int i = tid; i < n2; i += NT) {
+          const int l = i ^ j;
+          if (l > i) {
+            const int32_t x = key[i], y = key[l];
+            if (((i & k) == 0) == (x > y)) {
+              key[i] = y;
+              key[l] = x;
+            }
           }
         }
+        __syncthreads();
       }
-      __syncthreads();
-    }
+  }
   // entries -> their bag rows (rows of dx), in place (each thread its own keys)
   {
     int32_t tmp[PER];
@@ -509,12 +635,26 @@ __global__ __launch_bounds__(256) void erase_bags_bwd_zero(EmbedBwdArgs a) {
   if (a.count[i / cpr] == 0) *reinterpret_cast<float4*>(a.grad + 4 * i) = make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
-// One wave per listed row of 1..kSmallBucket entries (grid-stride): its
-// entries sorted across the lanes, their bag rows looked up in parallel,
-// lane group q adding entries q, q + 64/G, ... in order (eight loads in
-// flight), the groups combined by a fixed butterfly.  (Loading the next
+// Listed rows of 1..kSmallBucket entries, in groups of 64 / G consecutive
+// rows per wave (grid-stride), one row per lane group of G lanes.
+//  * When every row of the group has at most 4 entries (92% of the rows
+//    with entries on the CTR shape, 73% have one), each lane group sums its
+//    own row: its entries sorted in registers, their bag rows and dx slices
+//    loaded by the group's lanes, added as (0 + v0 + 0 + v1) ... exactly as
+//    the wave path below associates at most 4 entries:
+//    ((0 + v0) + (0 + v1)) + ((0 + v2) + (0 + v3)).
+//  * Otherwise the group's rows go one after another through the wave path:
+//    the row's entries sorted across the lanes, their bag rows looked up in
+//    parallel, lane group q adding entries q, q + 64/G, ... in order (eight
+//    loads in flight), the groups combined by a fixed butterfly.
+// Either way a row's sum depends only on its own entries.  (Loading the next
 // row's list entry, count and bucket during the current row's sums measured
-// slower: 146 against 131 us on the CTR shape.)
+// slower: 146 against 131 us on the CTR shape, before the per-group path.)
+__device__ __forceinline__ void sort2(int32_t& x, int32_t& y) {
+  const int32_t lo = min(x, y), hi = max(x, y);
+  x = lo;
+  y = hi;
+}
 template <typename T, int G>
 __global__ __launch_bounds__(256) void erase_bags_bwd_rows(EmbedBwdArgs a) {
   constexpr int NGW = 64 / G;  // lane groups per wave
@@ -522,33 +662,71 @@ __global__ __launch_bounds__(256) void erase_bags_bwd_rows(EmbedBwdArgs a) {
   const int q = lane / G, cq = lane % G;  // lane group, column quad
   const bool col = 4 * cq < a.dim;
   const int n = a.nlarge[1];
-  for (int idx = (int)blockIdx.x * 4 + wave; idx < n; idx += (int)gridDim.x * 4) {
-    const int64_t g = a.small[idx];
-    const int c = a.count[g], s0 = a.start[g];
-    const int32_t e = wave_sort(lane < c ? a.bucket[s0 + lane] : INT32_MAX, lane);
-    const int m = lane < c ? a.owner[e] % a.M : 0;  // bag row of the lane's entry
-    const int t = (int)(g / a.rows);
-    const int64_t xc = a.n_dense + (int64_t)t * a.dim + 4 * cq;
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int k0 = 0; k0 < c; k0 += 8 * NGW) {
-      float4 v[8];
+  const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int grp = (int)blockIdx.x * 4 + wave; grp * NGW < n; grp += (int)gridDim.x * 4) {
+    if constexpr (NGW >= 4) {
+      const int idx = grp * NGW + q;
+      const bool has = idx < n;
+      const int64_t gq = has ? a.small[idx] : 0;
+      const int cn = has ? a.count[gq] : 0, sq = has ? a.start[gq] : 0;
+      if (__all(cn <= 4)) {  // wave-uniform
+        int32_t e[4];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int k = k0 + u * NGW + q;
-        const int mk = __shfl(m, k & 63, 64);
-        v[u] = (k < c && col) ? dx4<T>(a, mk, xc) : make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int k = 0; k < 4; ++k) e[k] = k < cn ? a.bucket[sq + k] : INT32_MAX;
+        sort2(e[0], e[1]);
+        sort2(e[2], e[3]);
+        sort2(e[0], e[2]);
+        sort2(e[1], e[3]);
+        sort2(e[1], e[2]);
+        const int64_t xc = a.n_dense + (gq / a.rows) * a.dim + 4 * cq;
+        float4 v[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int m = k < cn ? a.owner[e[k]] % a.M : 0;
+          v[k] = (k < cn && col) ? dx4<T>(a, m, xc) : zero;
+        }
+        float4 s01 = zero, s1 = zero, s23 = zero, s3 = zero;
+        add4(s01, v[0]);
+        add4(s1, v[1]);
+        add4(s01, s1);
+        add4(s23, v[2]);
+        add4(s3, v[3]);
+        add4(s23, s3);
+        add4(s01, s23);
+        if (has && col) *reinterpret_cast<float4*>(a.grad + gq * a.dim + 4 * cq) = s01;
+        continue;
+      }
+    }
+    for (int j = 0; j < NGW; ++j) {
+      const int idx = grp * NGW + j;
+      if (idx >= n) break;
+      const int64_t g = a.small[idx];
+      const int c = a.count[g], s0 = a.start[g];
+      const int32_t e = wave_sort(lane < c ? a.bucket[s0 + lane] : INT32_MAX, lane);
+      const int m = lane < c ? a.owner[e] % a.M : 0;  // bag row of the lane's entry
+      const int t = (int)(g / a.rows);
+      const int64_t xc = a.n_dense + (int64_t)t * a.dim + 4 * cq;
+      float4 acc = zero;
+      for (int k0 = 0; k0 < c; k0 += 8 * NGW) {
+        float4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int k = k0 + u * NGW + q;
+          const int mk = __shfl(m, k & 63, 64);
+          v[u] = (k < c && col) ? dx4<T>(a, mk, xc) : zero;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) add4(acc, v[u]);
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) add4(acc, v[u]);
+      for (int o = G; o < 64; o <<= 1) {
+        acc.x += __shfl_xor(acc.x, o, 64);
+        acc.y += __shfl_xor(acc.y, o, 64);
+        acc.z += __shfl_xor(acc.z, o, 64);
+        acc.w += __shfl_xor(acc.w, o, 64);
+      }
+      if (col && q == 0) *reinterpret_cast<float4*>(a.grad + g * a.dim + 4 * cq) = acc;
     }
-#pragma unroll
-    for (int o = G; o < 64; o <<= 1) {
-      acc.x += __shfl_xor(acc.x, o, 64);
-      acc.y += __shfl_xor(acc.y, o, 64);
-      acc.z += __shfl_xor(acc.z, o, 64);
-      acc.w += __shfl_xor(acc.w, o, 64);
-    }
-    if (col && q == 0) *reinterpret_cast<float4*>(a.grad + g * a.dim + 4 * cq) = acc;
   }
 }
 
@@ -559,7 +737,8 @@ hipError_t launch_embed_bags_backward(int bf16, const EmbedBwdArgs& a, hipStream
   hipLaunchKernelGGL(erase_bags_bwd_owner, dim3((unsigned)(((int64_t)a.M * a.T + 255) / 256)), dim3(256), 0, s, a);
   if (a.nnz > 0) {
     const dim3 ge((unsigned)((a.nnz + 255) / 256));
-    hipLaunchKernelGGL(erase_bags_bwd_count, ge, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(erase_bags_bwd_count, dim3((unsigned)((a.nnz + kCountTile - 1) / kCountTile)), dim3(256), 0,
+                       s, a);
     const unsigned nsb = (unsigned)((a.trows + kScanBlock - 1) / kScanBlock);
     hipLaunchKernelGGL(erase_bags_bwd_scan_local, dim3(nsb), dim3(256), 0, s, a);
     hipLaunchKernelGGL(erase_bags_bwd_scan_blocks, dim3(1), dim3(256), 0, s, a);

@@ -443,13 +443,18 @@ def _run_bags_bwd(offsets, indices, dx, n_dense, rows, dim, dtype):
 @pytest.mark.parametrize("dtype,dim,n_dense,M,T,rows,max_len", [("f32", 64, 13, 37, 5, 40, 7), ("bf16", 64, 13, 37, 5, 40, 7),
                                                                 ("f32", 4, 0, 5, 3, 9, 3), ("f32", 256, 1, 9, 2, 300, 7),
                                                                 ("bf16", 12, 3, 64, 2, 5, 90),
-                                                                ("f32", 8, 0, 400, 1, 1, 90)])
+                                                                ("f32", 8, 0, 400, 1, 1, 90),
+                                                                ("f32", 8, 0, 30000, 1, 30, 20),
+                                                                ("bf16", 8, 0, 30000, 1, 500, 20)])
 def test_embed_bags_backward_vs_oracle(dtype, dim, n_dense, M, T, rows, max_len):
     """Table gradients against the float64 oracle: empty bags, rows selected
     by no bag (zero), and with 5 rows and bags of up to 90 ids, rows selected
-    by well over 64 entries (sorted in LDS); with one row and 400 bags of up
-    to 90 ids, a row of over 16384 entries (the selection path);
-    bit-identical on a second run."""
+    by well over 64 entries (sorted in LDS by a bitmap over their entry
+    range); with one row and 400 bags of up to 90 ids, a row of over 16384
+    entries (the selection path); with 30000 bags of up to 20 ids over 30 or
+    500 rows, buckets of 1025..16384 and of 65..1024 entries whose entries
+    span more than the bitmap's 64 Ki (the bitonic sort); bit-identical on
+    a second run."""
     _say(f"case: embed_bags_backward {dtype} dim={dim} M={M} T={T} rows={rows}")
     _, offsets, indices, _ = _bags(M * 17 + dim, M, T, rows, dim, n_dense, max_len)
     rng = np.random.Generator(np.random.PCG64(M + dim))
