@@ -632,7 +632,11 @@ __global__ __launch_bounds__(256) void erase_bags_bwd_zero(EmbedBwdArgs a) {
   const int cpr = a.dim / 4;
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= a.trows * cpr) return;
-  if (a.count[i / cpr] == 0) *reinterpret_cast<float4*>(a.grad + 4 * i) = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (a.count[i / cpr] == 0) {
+    // streaming stores: the zeros are not read again by this launch sequence
+    typedef float f32x4v_t __attribute__((ext_vector_type(4)));
+    __builtin_nontemporal_store(f32x4v_t{0.f, 0.f, 0.f, 0.f}, reinterpret_cast<f32x4v_t*>(a.grad + 4 * i));
+  }
 }
 
 // Listed rows of 1..kSmallBucket entries, in groups of 64 / G consecutive
