@@ -315,13 +315,15 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
         R.grouped = (R.dgrad.bm == 64 && R.dgrad.bn == 64) || (R.dgrad.bm == 128 && R.dgrad.bn == 128);
         if (R.grouped && R.wgrad.split > 1) {
           // the input-gradient tiles of the same launch fill the chip: the
-          // weight gradient keeps slices of >= 1024 batch rows, so Adam reads
-          // fewer fp32 partial slices (CTR layers 2 and 3: 4 slices instead
-          // of 16; the launch alone is longer, 10.6 vs 8.3 us, but leaves
-          // CUs to the overlapped kernels: 11.96M vs 11.0M samples/s)
+          // weight gradient keeps slices of >= 512 batch rows, so Adam reads
+          // fewer fp32 partial slices.  CTR layers 2 and 3, same-box A/B of
+          // 4, 8 and 16 slices: the launch 10.9, 9.2, 9.2 us; SERIAL 9.36M,
+          // 9.78M, 9.51M samples/s; PIPELINE+worker 12.85M, 12.94M, 12.38M
+          // (16 slices: the first layer's launch, whose extra workgroups run
+          // the other layers' Adam, 22.1 -> 23.5 us)
           const int64_t Kc = roundup(M, BK);
           int sp = R.wgrad.split;
-          while (sp > 1 && Kc / sp < 1024) sp /= 2;
+          while (sp > 1 && Kc / sp < 512) sp /= 2;
           R.wgrad.kps = (int)roundup(cdiv(Kc, sp), BK);
           R.wgrad.split = (int)cdiv(Kc, R.wgrad.kps);
         }

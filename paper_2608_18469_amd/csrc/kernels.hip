@@ -1614,7 +1614,7 @@ __device__ __forceinline__ void adam_chunk(const AdamArgs& a, int64_t chunk, int
       if (full) {
         auto st = [&](float* base, const float* x) {
           f32x4u_t w = {x[0], x[1], x[2], x[3]};
-          *reinterpret_cast<__attribute__((address_space(1))) f32x4u_t*>(gmem(base) + fi) = w;
+          __builtin_nontemporal_store(w, reinterpret_cast<__attribute__((address_space(1))) f32x4u_t*>(gmem(base) + fi));
         };
         if (sg.g) st(sg.g, g);
         st(sg.m, m);
@@ -1924,10 +1924,12 @@ __device__ __forceinline__ void wgrad_adam_w4_tile(const GemmDesc& g, const EpiP
         adam_elem(pp[k], mm[k], vq[k], gv[it][k], e.b1, e.b2, step, bc2s, e.eps);
         o[k] = f2bf(pp[k]);
       }
-      if (e.ag) *reinterpret_cast<gvec*>(gmem(e.ag) + afi[it]) = f32x4a_t{gv[it][0], gv[it][1], gv[it][2], gv[it][3]};
-      *reinterpret_cast<gvec*>(gmem(e.am) + afi[it]) = f32x4a_t{mm[0], mm[1], mm[2], mm[3]};
-      *reinterpret_cast<gvec*>(gmem(e.av) + afi[it]) = f32x4a_t{vq[0], vq[1], vq[2], vq[3]};
-      *reinterpret_cast<gvec*>(gmem(e.ap) + afi[it]) = f32x4a_t{pp[0], pp[1], pp[2], pp[3]};
+      if (e.ag)
+        __builtin_nontemporal_store(f32x4a_t{gv[it][0], gv[it][1], gv[it][2], gv[it][3]},
+                                    reinterpret_cast<gvec*>(gmem(e.ag) + afi[it]));
+      __builtin_nontemporal_store(f32x4a_t{mm[0], mm[1], mm[2], mm[3]}, reinterpret_cast<gvec*>(gmem(e.am) + afi[it]));
+      __builtin_nontemporal_store(f32x4a_t{vq[0], vq[1], vq[2], vq[3]}, reinterpret_cast<gvec*>(gmem(e.av) + afi[it]));
+      __builtin_nontemporal_store(f32x4a_t{pp[0], pp[1], pp[2], pp[3]}, reinterpret_cast<gvec*>(gmem(e.ap) + afi[it]));
       st4(static_cast<uint16_t*>(e.ash) + (int64_t)m * e.ldash + n, o);  // copy rows: 64-element multiples
     } else if (m < g.M && n < g.N) {
       for (int k = 0; k < g.N - n && k < 4; ++k) {
