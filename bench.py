@@ -58,6 +58,10 @@ def kernel_class(r, bf16=True):
     t = "bf16" if bf16 else "f32"
     if r["kind"] == "fwd_head_gemm" and bf16 and r["tile_m"] == 16:
         return "erase_fwd_head16"  # the bf16 16-row last layer + head kernel
+    if r["kind"] in ("wgrad_adam_kg2", "wgrad_gemm_kg2") and bf16:
+        # the bf16 first-layer weight gradient with its Adam update: four
+        # waves per 64x64 tile, direct-to-LDS slices (one kernel for both)
+        return "erase_wgrad_adam_w4"
     if r["tile_m"]:
         return f"{KIND_SYMBOL[r['kind']]}<{t},{r['tile_m']},{r['tile_n']}>"
     return f"{KIND_SYMBOL[r['kind']]}<{t}>"
