@@ -1299,8 +1299,14 @@ __global__ __launch_bounds__(256) void erase_fwd_head16(GemmDesc g, EpiParams e)
   }
 }
 
+// bf16 vocabulary logits in 128x256 tiles; false when the shape does not fit
+static bool logits_wide_fits(const GemmDesc& g, const EpiParams& e);
+static hipError_t launch_logits_wide(const GemmDesc& g, const EpiParams& e, hipStream_t s, const LaunchEv& ev);
+
 hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s, const LaunchEv& ev) {
   if (g.M <= 0 || g.N <= 0 || g.split <= 0) return hipErrorInvalidValue;
+  if (bf16 && kind == GK_FWD_LOGITS && g.bm == 128 && g.bn == 256)
+    return logits_wide_fits(g, e) ? launch_logits_wide(g, e, s, ev) : hipErrorInvalidValue;
   if (bf16 && kind == GK_FWD_HEAD && g.bm == 16) {
     // 16-row tiles: outputs at most 128 wide, contraction a multiple of 32
     if (g.N > 128 || g.K % 32 || g.split != 1) return hipErrorInvalidValue;
@@ -1966,6 +1972,159 @@ static hipError_t launch_wgrad_w8(const GemmDesc& g0, const EpiParams& e, const 
   const int ntiles = ((g.M + 63) / 64) * ((g.N + 63) / 64);
   const dim3 grid((unsigned)(ntiles + a.nchunks)), block(256);
   ERASE_LAUNCH(erase_wgrad_adam_w4, grid, block, 0, s, ev, g, e, a, ntiles);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Vocabulary logits in wide tiles (bf16): e[m][n] = exp(sum_k h[m][k] w[n][k]
+// - xref[m]) rounded to bf16, and per row and 128-column tile the sum of the
+// stored values (the epilogue of GK_FWD_LOGITS).  A workgroup computes 128
+// positions x 256 vocabulary rows with four waves of 64 x 128, so a wave
+// reads 6 KB of MFMA fragments from LDS per 64 x 128 x 32 slab (the GEMM
+// core's 2 x 2 waves of 32 x 64 read 3 KB per slab of a quarter of that
+// work).  The operand rows of a 32-wide k-step go straight from global
+// memory into one of three LDS stages (global_load_lds_dwordx4; chunk c of
+// row r at slot c ^ ((r >> 1) & 3): conflict-free 16-byte fragment reads),
+// two k-steps in flight, one barrier per k-step.  72 KB of LDS and 171
+// VGPRs let two workgroups share a CU, so one's epilogue and operand waits
+// overlap the other's MFMAs.  The MFMA computes the transposed tile
+// (vocabulary rows as the A operand): a lane holds 4 consecutive vocabulary
+// columns of one position, stored as 8 bytes; a row's sum over a 128-column
+// tile adds the lane's 32 values, then the 4 lane groups, in a fixed order.
+// ---------------------------------------------------------------------------
+namespace lgw {
+constexpr int BM = 128, BN = 256, BK = 32;  // positions, vocabulary rows per workgroup; k-step
+constexpr int NST = 3;                      // LDS stages
+constexpr int STAGE = (BM + BN) * BK * 2;   // 24 KB: rows of 64 bytes
+constexpr int LOADS = (BM + BN) / 16 / 4;   // loads of 16 rows per wave and k-step
+// M-tiles per group of the tile order (each group walks every vocabulary
+// tile).  Same-box sweep at 16384 x 32768 x 512: groups of 2 M-tiles 765 and
+// 800 us on two boxes, against 818 (4), 840 (8), 861 (16), 932 (32), 1002 (1),
+// and N-tile groups of 2, 8, 32: 815, 856, 995 us; the GEMM core's 64 x 128
+// tiles 874-934 us on the same boxes.
+constexpr int GROUP = 2;
+}  // namespace lgw
+
+__global__ __launch_bounds__(256) void erase_fwd_logits_wide(GemmDesc g, EpiParams e) {
+  using namespace lgw;
+  __shared__ __attribute__((aligned(16))) char smem[NST * STAGE];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wv & 1, wn = wv >> 1;  // the wave's 64 positions and 128 vocabulary rows
+  const int gm = (g.M + BM - 1) / BM, gn = g.N / BN;
+  const TileIdx ti = tile_from(xcd_linear((int)blockIdx.x, (int)gridDim.x), gm, gn, GROUP);
+  const int m0 = ti.m * BM, n0 = ti.n * BN;
+  const int nk = g.K / BK;
+  const int fr = lane & 15, fg = lane >> 4;
+  constexpr float kL2e = 1.4426950408889634f;
+
+  // the reference logits of the lane's 4 positions (log2 units), loaded
+  // before the operand loads so the first wait covers them (rows up to the
+  // next multiple of 128 positions exist; those past M are not stored)
+  float xl[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) xl[j] = e.xref[m0 + 64 * wm + 16 * j + fr] * kL2e;
+
+  // direct-to-LDS loads: load u of wave wv fills stage rows 16 ui .. 16 ui +
+  // 15, ui = LOADS wv + u (rows [0, BM) positions, then vocabulary rows);
+  // lane l writes row 16 ui + (l >> 2), slot l & 3, which holds chunk
+  // (l & 3) ^ ((l >> 3) & 3)
+  const int ch = (lane & 3) ^ ((lane >> 3) & 3);
+  const uint16_t* pa = static_cast<const uint16_t*>(g.A) + (int64_t)(m0 + (lane >> 2)) * g.lda + ch * 8;
+  const uint16_t* pw = static_cast<const uint16_t*>(g.B) + (int64_t)(n0 + (lane >> 2)) * g.ldb + ch * 8;
+  const uint32_t lbase = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) char*)smem);
+  auto dma = [&](int ks, int st) {
+    const uint32_t l0 = lbase + st * STAGE;
+#pragma unroll
+    for (int u = 0; u < LOADS; ++u) {
+      const int ui = LOADS * wv + u;
+      const uint16_t* src = ui < BM / 16 ? pa + (int64_t)(16 * ui) * g.lda : pw + (int64_t)(16 * (ui - BM / 16)) * g.ldb;
+      lds_dma16(src + ks * BK, l0 + ui * 1024);
+    }
+  };
+  static_assert(LOADS == 6, "the waits below count 6 loads per k-step");
+
+  // fragment reads: row block at stage row R0 (a multiple of 16): lane reads
+  // row R0 + (l & 15), chunk l >> 4, at slot chunk ^ (((l & 15) >> 1) & 3)
+  const int fo = fr * 64 + (fg ^ ((fr >> 1) & 3)) * 16;
+  f32x4_t acc[8][4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  if (nk > 0) dma(0, 0);
+  if (nk > 1) dma(1, 1);
+  for (int ks = 0; ks < nk; ++ks) {
+    // this wave's loads of k-step ks have landed (those of ks + 1 may not);
+    // after the barrier every wave's have, and every wave is done reading
+    // k-step ks - 1, whose stage the loads of ks + 2 overwrite
+    if (ks + 1 < nk)
+      asm volatile("s_waitcnt vmcnt(6)" ::: "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (ks + 2 < nk) dma(ks + 2, (ks + 2) % NST);
+    const char* st = smem + (ks % NST) * STAGE;
+    u32x4_t fw[8], fh[4];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) fw[i] = *reinterpret_cast<const u32x4_t*>(st + (BM + 128 * wn + 16 * i) * 64 + fo);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) fh[j] = *reinterpret_cast<const u32x4_t*>(st + (64 * wm + 16 * j) * 64 + fo);
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, fw[i]),
+                                                            __builtin_bit_cast(bf16x8_t, fh[j]), acc[i][j], 0, 0, 0);
+  }
+
+  // The reference logits are needed from here on: taken now, the compiler's
+  // wait for them lies before the first store (stores count in the same
+  // counter, and a wait between stores would wait for them too)
+  asm volatile("" ::"v"(xl[0]), "v"(xl[1]), "v"(xl[2]), "v"(xl[3]));
+
+  // acc[i][j][q]: vocabulary row n0 + 128 wn + 16 i + 4 (l >> 4) + q of
+  // position m0 + 64 wm + 16 j + (l & 15)
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  uint16_t* Y = static_cast<uint16_t*>(e.y);
+  const int tcol = (n0 + 128 * wn) / 128;  // the row-sum tile
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int p = m0 + 64 * wm + 16 * j + fr;
+    float se = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      float ev[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) ev[q] = __builtin_amdgcn_exp2f(fmaf(acc[i][j][q], kL2e, -xl[j]));
+      const uint32_t o0 = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{ev[0], ev[1]}), bf16x2_t));
+      const uint32_t o1 = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{ev[2], ev[3]}), bf16x2_t));
+      se += __uint_as_float(o0 << 16);
+      se += __uint_as_float(o0 & 0xffff0000u);
+      se += __uint_as_float(o1 << 16);
+      se += __uint_as_float(o1 & 0xffff0000u);
+      if (p < g.M)
+        *reinterpret_cast<uint2*>(Y + (int64_t)p * e.ldy + n0 + 128 * wn + 16 * i + 4 * fg) = uint2{o0, o1};
+    }
+    se += __shfl_xor(se, 16, 64);
+    se += __shfl_xor(se, 32, 64);
+    if (fg == 0 && p < g.M) e.lstat[(int64_t)p * e.ldlstat + tcol] = se;
+  }
+}
+
+static bool logits_wide_fits(const GemmDesc& g, const EpiParams& e) {
+  // whole 256-row vocabulary tiles and 32-wide k-steps within both operand
+  // rows; operand rows up to the next multiple of 128 positions must be
+  // readable (activation buffers are padded to that); 8-byte output stores
+  return g.split == 1 && g.N % lgw::BN == 0 && g.K % lgw::BK == 0 && g.K > 0 && g.K <= g.lda && g.K <= g.ldb &&
+         e.ldy % 4 == 0 && (reinterpret_cast<uintptr_t>(e.y) & 7) == 0;
+}
+
+static hipError_t launch_logits_wide(const GemmDesc& g, const EpiParams& e, hipStream_t s, const LaunchEv& ev) {
+  const int tiles = ((g.M + lgw::BM - 1) / lgw::BM) * (g.N / lgw::BN);
+  ERASE_LAUNCH(erase_fwd_logits_wide, dim3((unsigned)tiles), dim3(256), 0, s, ev, g, e);
   return hipGetLastError();
 }
 

@@ -126,6 +126,11 @@ Plan1 choose_fwd(int64_t M, int64_t N, int64_t K) {
   return p;
 }
 
+// The vocabulary logits run in 128 x 256 tiles with per-128-column row sums
+// when the vocabulary is a multiple of 256 and the width a multiple of 64
+// (the k-step); otherwise in the GEMM core's tiles.
+bool logits_wide(const Dims& D) { return D.V % 256 == 0 && D.d % 64 == 0; }
+
 struct Carver {
   uintptr_t base;
   size_t off = kAlign;  // header: step counter, status word, Adam factors
@@ -246,7 +251,7 @@ size_t build_layout(const erase_tf_config& c, uintptr_t base, Layout* P) {
     B.lse = f32(BHT);
     B.dsum = f32(BHT);
     const Plan1 ph = choose_fwd(D.N, D.V, d);
-    B.ntiles = (int)cdv(D.V, ph.bn);
+    B.ntiles = (int)cdv(D.V, logits_wide(D) ? 128 : ph.bn);
     B.lstat = f32(Np * B.ntiles);
     B.xref = f32(Np);
     B.rowscale = f32(Np);
@@ -310,12 +315,17 @@ void build_gemms(const erase_tf_config& c, Layout* P) {
     B.fwd[W2].e.res = B.a1;
     B.fwd[W2].e.ldres = P->ldd;
     fwd(WH, B.hn, P->ldd, GK_FWD_LOGITS, B.logits, P->ldv);
-    // tile order: groups of 8 M-tiles (512 positions), each walking every
-    // vocabulary tile, keep the tiles an XCD runs at once on about 2 MB of
-    // operands (its L2 holds 4 MB).  Measured at 16384 x 32768 x 512: 0.89
-    // ms, against 0.99 ms for the generic choice (groups of 128 M-tiles, 6 MB
-    // of head input in flight per XCD), 0.91 for 16, 0.93 for 2, 1.20 for 1.
+    // GEMM-core tiles (64 x 128): groups of 8 M-tiles (512 positions), each
+    // walking every vocabulary tile, keep the tiles an XCD runs at once on
+    // about 2 MB of operands (its L2 holds 4 MB).  Measured at 16384 x 32768
+    // x 512: 0.89 ms, against 0.99 ms for the generic choice (groups of 128
+    // M-tiles, 6 MB of head input in flight per XCD), 0.91 for 16, 0.93 for
+    // 2, 1.20 for 1.
     B.fwd[WH].g.group = 8;
+    if (logits_wide(D)) {
+      B.fwd[WH].g.bm = 128;
+      B.fwd[WH].g.bn = 256;
+    }
     B.fwd[WH].e.lstat = B.lstat;
     B.fwd[WH].e.ldlstat = B.ntiles;
     B.fwd[WH].e.xref = B.xref;
