@@ -2014,7 +2014,7 @@ __global__ __launch_bounds__(256) void erase_fwd_logits_wide(GemmDesc g, EpiPara
   const int gm = (g.M + BM - 1) / BM, gn = g.N / BN;
   const TileIdx ti = tile_from(xcd_linear((int)blockIdx.x, (int)gridDim.x), gm, gn, GROUP);
   const int m0 = ti.m * BM, n0 = ti.n * BN;
-  const int nk = g.K / BK;
+  const int nk = g.K / BK, M = g.M;
   const int fr = lane & 15, fg = lane >> 4;
   constexpr float kL2e = 1.4426950408889634f;
 
@@ -2033,12 +2033,16 @@ __global__ __launch_bounds__(256) void erase_fwd_logits_wide(GemmDesc g, EpiPara
   const uint16_t* pa = static_cast<const uint16_t*>(g.A) + (int64_t)(m0 + (lane >> 2)) * g.lda + ch * 8;
   const uint16_t* pw = static_cast<const uint16_t*>(g.B) + (int64_t)(n0 + (lane >> 2)) * g.ldb + ch * 8;
   const uint32_t lbase = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) char*)smem);
+  // row strides of 16 rows, in registers: the loads' asm statements clobber
+  // memory, so values read from the kernel arguments inside the loop would
+  // be loaded again (scalar loads and a full wait) before every load
+  const int64_t sa = 16 * g.lda, sw = 16 * g.ldb;
   auto dma = [&](int ks, int st) {
     const uint32_t l0 = lbase + st * STAGE;
 #pragma unroll
     for (int u = 0; u < LOADS; ++u) {
       const int ui = LOADS * wv + u;
-      const uint16_t* src = ui < BM / 16 ? pa + (int64_t)(16 * ui) * g.lda : pw + (int64_t)(16 * (ui - BM / 16)) * g.ldb;
+      const uint16_t* src = ui < BM / 16 ? pa + ui * sa : pw + (ui - BM / 16) * sw;
       lds_dma16(src + ks * BK, l0 + ui * 1024);
     }
   };
@@ -2089,6 +2093,7 @@ __global__ __launch_bounds__(256) void erase_fwd_logits_wide(GemmDesc g, EpiPara
   typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
   typedef float f32x2_t __attribute__((ext_vector_type(2)));
   uint16_t* Y = static_cast<uint16_t*>(e.y);
+  const int64_t ldy = e.ldy;
   const int tcol = (n0 + 128 * wn) / 128;  // the row-sum tile
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -2105,12 +2110,11 @@ __global__ __launch_bounds__(256) void erase_fwd_logits_wide(GemmDesc g, EpiPara
       se += __uint_as_float(o0 & 0xffff0000u);
       se += __uint_as_float(o1 << 16);
       se += __uint_as_float(o1 & 0xffff0000u);
-      if (p < g.M)
-        *reinterpret_cast<uint2*>(Y + (int64_t)p * e.ldy + n0 + 128 * wn + 16 * i + 4 * fg) = uint2{o0, o1};
+      if (p < M) *reinterpret_cast<uint2*>(Y + (int64_t)p * ldy + n0 + 128 * wn + 16 * i + 4 * fg) = uint2{o0, o1};
     }
     se += __shfl_xor(se, 16, 64);
     se += __shfl_xor(se, 32, 64);
-    if (fg == 0 && p < g.M) e.lstat[(int64_t)p * e.ldlstat + tcol] = se;
+    if (fg == 0 && p < M) e.lstat[(int64_t)p * e.ldlstat + tcol] = se;
   }
 }
 
