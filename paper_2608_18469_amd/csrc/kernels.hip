@@ -1299,13 +1299,13 @@ __global__ __launch_bounds__(256) void erase_fwd_head16(GemmDesc g, EpiParams e)
   }
 }
 
-// bf16 vocabulary logits in 128x256 tiles; false when the shape does not fit
+// bf16 vocabulary logits in 256x256 tiles; false when the shape does not fit
 static bool logits_wide_fits(const GemmDesc& g, const EpiParams& e);
 static hipError_t launch_logits_wide(const GemmDesc& g, const EpiParams& e, hipStream_t s, const LaunchEv& ev);
 
 hipError_t launch_gemm(int bf16, int kind, const GemmDesc& g, const EpiParams& e, hipStream_t s, const LaunchEv& ev) {
   if (g.M <= 0 || g.N <= 0 || g.split <= 0) return hipErrorInvalidValue;
-  if (bf16 && kind == GK_FWD_LOGITS && g.bm == 128 && g.bn == 256)
+  if (bf16 && kind == GK_FWD_LOGITS && g.bm == 256 && g.bn == 256)
     return logits_wide_fits(g, e) ? launch_logits_wide(g, e, s, ev) : hipErrorInvalidValue;
   if (bf16 && kind == GK_FWD_HEAD && g.bm == 16) {
     // 16-row tiles: outputs at most 128 wide, contraction a multiple of 32
@@ -1978,79 +1978,78 @@ static hipError_t launch_wgrad_w8(const GemmDesc& g0, const EpiParams& e, const 
 // ---------------------------------------------------------------------------
 // Vocabulary logits in wide tiles (bf16): e[m][n] = exp(sum_k h[m][k] w[n][k]
 // - xref[m]) rounded to bf16, and per row and 128-column tile the sum of the
-// stored values (the epilogue of GK_FWD_LOGITS).  A workgroup computes 128
-// positions x 256 vocabulary rows with four waves of 64 x 128, so a wave
-// reads 6 KB of MFMA fragments from LDS per 64 x 128 x 32 slab (the GEMM
-// core's 2 x 2 waves of 32 x 64 read 3 KB per slab of a quarter of that
-// work).  The operand rows of a 32-wide k-step go straight from global
-// memory into one of three LDS stages (global_load_lds_dwordx4; chunk c of
-// row r at slot c ^ ((r >> 1) & 3): conflict-free 16-byte fragment reads),
-// two k-steps in flight, one barrier per k-step.  72 KB of LDS and 171
-// VGPRs let two workgroups share a CU, so one's epilogue and operand waits
-// overlap the other's MFMAs.  The MFMA computes the transposed tile
-// (vocabulary rows as the A operand): a lane holds 4 consecutive vocabulary
-// columns of one position, stored as 8 bytes; a row's sum over a 128-column
-// tile adds the lane's 32 values, then the 4 lane groups, in a fixed order.
+// stored values (the epilogue of GK_FWD_LOGITS).  A workgroup of eight waves
+// computes 256 positions x 256 vocabulary rows, each wave 64 x 128, so a
+// wave reads 12 KB of MFMA fragments from LDS per 64 x 128 x 64 slab (the
+// GEMM core's 2 x 2 waves of 32 x 64 read 6 KB per slab of a quarter of
+// that work), and the operands cross L2 once per 256 x 256 tile.  The
+// operand rows of a 64-wide k-step (one 128-byte line per row) go straight
+// from global memory into one of two 64 KB LDS stages
+// (global_load_lds_dwordx4; chunk c of row r at slot c ^ (r & 7):
+// conflict-free 16-byte fragment reads), the next k-step in flight, one
+// barrier per k-step; two waves per SIMD.  The MFMA computes the transposed
+// tile (vocabulary rows as the A operand): a lane holds 4 consecutive
+// vocabulary columns of one position, stored as 8 bytes; a row's sum over a
+// 128-column tile adds the lane's 32 values, then the 4 lane groups, in a
+// fixed order.
 // ---------------------------------------------------------------------------
 namespace lgw {
-constexpr int BM = 128, BN = 256, BK = 32;  // positions, vocabulary rows per workgroup; k-step
-constexpr int NST = 3;                      // LDS stages
-constexpr int STAGE = (BM + BN) * BK * 2;   // 24 KB: rows of 64 bytes
-constexpr int LOADS = (BM + BN) / 16 / 4;   // loads of 16 rows per wave and k-step
+constexpr int BM = 256, BN = 256, BK = 64;  // positions, vocabulary rows per workgroup; k-step
+constexpr int NW = 8, NT = 64 * NW;         // waves and threads
+constexpr int NST = 2;                      // LDS stages
+constexpr int STAGE = (BM + BN) * BK * 2;   // 64 KB: rows of 128 bytes
+constexpr int LOADS = (BM + BN) / 8 / NW;   // loads of 8 rows per wave and k-step
 // M-tiles per group of the tile order (each group walks every vocabulary
-// tile).  Same-box sweep at 16384 x 32768 x 512: groups of 2 M-tiles 765 and
-// 800 us on two boxes, against 818 (4), 840 (8), 861 (16), 932 (32), 1002 (1),
-// and N-tile groups of 2, 8, 32: 815, 856, 995 us; the GEMM core's 64 x 128
-// tiles 874-934 us on the same boxes.
-constexpr int GROUP = 2;
+// tile).  Measured at 16384 x 32768 x 512 (kernel alone, same box): 818-821
+// us; the 128 x 256 form of this kernel (four waves, 32-wide k-steps in
+// three 24 KB stages, two workgroups per CU) 857-881 us, the GEMM core's 64
+// x 128 tiles about 1 ms.
+constexpr int GROUP = 1;
 }  // namespace lgw
 
-__global__ __launch_bounds__(256) void erase_fwd_logits_wide(GemmDesc g, EpiParams e) {
+__global__ __launch_bounds__(lgw::NT) void erase_fwd_logits_wide(GemmDesc g, EpiParams e) {
   using namespace lgw;
   __shared__ __attribute__((aligned(16))) char smem[NST * STAGE];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wv & 1, wn = wv >> 1;  // the wave's 64 positions and 128 vocabulary rows
-  const int gm = (g.M + BM - 1) / BM, gn = g.N / BN;
+  const int wm = wv & 3, wn = wv >> 2;  // the wave's 64 positions and 128 vocabulary rows
+  const int gm = g.M / BM, gn = g.N / BN;
   const TileIdx ti = tile_from(xcd_linear((int)blockIdx.x, (int)gridDim.x), gm, gn, GROUP);
   const int m0 = ti.m * BM, n0 = ti.n * BN;
-  const int nk = g.K / BK, M = g.M;
+  const int nk = g.K / BK;
   const int fr = lane & 15, fg = lane >> 4;
   constexpr float kL2e = 1.4426950408889634f;
 
   // the reference logits of the lane's 4 positions (log2 units), loaded
-  // before the operand loads so the first wait covers them (rows up to the
-  // next multiple of 128 positions exist; those past M are not stored)
+  // before the operand loads so the first wait covers them
   float xl[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) xl[j] = e.xref[m0 + 64 * wm + 16 * j + fr] * kL2e;
 
-  // direct-to-LDS loads: load u of wave wv fills stage rows 16 ui .. 16 ui +
-  // 15, ui = LOADS wv + u (rows [0, BM) positions, then vocabulary rows);
-  // lane l writes row 16 ui + (l >> 2), slot l & 3, which holds chunk
-  // (l & 3) ^ ((l >> 3) & 3)
-  const int ch = (lane & 3) ^ ((lane >> 3) & 3);
-  const uint16_t* pa = static_cast<const uint16_t*>(g.A) + (int64_t)(m0 + (lane >> 2)) * g.lda + ch * 8;
-  const uint16_t* pw = static_cast<const uint16_t*>(g.B) + (int64_t)(n0 + (lane >> 2)) * g.ldb + ch * 8;
+  // direct-to-LDS loads: load u of wave wv fills stage rows 8 ui .. 8 ui + 7,
+  // ui = LOADS wv + u (rows [0, BM) positions, then vocabulary rows); lane l
+  // writes row 8 ui + (l >> 3), slot l & 7, which holds chunk (l & 7) ^ (l >> 3)
+  const int ch = (lane & 7) ^ (lane >> 3);
+  const uint16_t* pa = static_cast<const uint16_t*>(g.A) + (int64_t)(m0 + (lane >> 3)) * g.lda + ch * 8;
+  const uint16_t* pw = static_cast<const uint16_t*>(g.B) + (int64_t)(n0 + (lane >> 3)) * g.ldb + ch * 8;
   const uint32_t lbase = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) char*)smem);
-  // row strides of 16 rows, in registers: the loads' asm statements clobber
+  // row strides of 8 rows, in registers: the loads' asm statements clobber
   // memory, so values read from the kernel arguments inside the loop would
   // be loaded again (scalar loads and a full wait) before every load
-  const int64_t sa = 16 * g.lda, sw = 16 * g.ldb;
+  const int64_t sa = 8 * g.lda, sw = 8 * g.ldb;
   auto dma = [&](int ks, int st) {
     const uint32_t l0 = lbase + st * STAGE;
 #pragma unroll
     for (int u = 0; u < LOADS; ++u) {
       const int ui = LOADS * wv + u;
-      const uint16_t* src = ui < BM / 16 ? pa + ui * sa : pw + (ui - BM / 16) * sw;
+      const uint16_t* src = ui < BM / 8 ? pa + ui * sa : pw + (ui - BM / 8) * sw;
       lds_dma16(src + ks * BK, l0 + ui * 1024);
     }
   };
-  static_assert(LOADS == 6, "the waits below count 6 loads per k-step");
 
-  // fragment reads: row block at stage row R0 (a multiple of 16): lane reads
-  // row R0 + (l & 15), chunk l >> 4, at slot chunk ^ (((l & 15) >> 1) & 3)
-  const int fo = fr * 64 + (fg ^ ((fr >> 1) & 3)) * 16;
+  // fragment reads: row block at stage row R0 (a multiple of 16), k half h:
+  // lane reads row R0 + (l & 15), chunk 4 h + (l >> 4), at slot chunk ^ (l & 7)
+  const int fo0 = fr * 128 + ((0 + fg) ^ (lane & 7)) * 16, fo1 = fr * 128 + ((4 + fg) ^ (lane & 7)) * 16;
   f32x4_t acc[8][4];
 #pragma unroll
   for (int i = 0; i < 8; ++i)
@@ -2058,29 +2057,29 @@ __global__ __launch_bounds__(256) void erase_fwd_logits_wide(GemmDesc g, EpiPara
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   if (nk > 0) dma(0, 0);
-  if (nk > 1) dma(1, 1);
   for (int ks = 0; ks < nk; ++ks) {
-    // this wave's loads of k-step ks have landed (those of ks + 1 may not);
-    // after the barrier every wave's have, and every wave is done reading
-    // k-step ks - 1, whose stage the loads of ks + 2 overwrite
-    if (ks + 1 < nk)
-      asm volatile("s_waitcnt vmcnt(6)" ::: "memory");
-    else
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // this wave's loads of k-step ks have landed; after the barrier every
+    // wave's have, and every wave is done reading k-step ks - 1, whose stage
+    // the loads of ks + 1 overwrite
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    if (ks + 2 < nk) dma(ks + 2, (ks + 2) % NST);
+    if (ks + 1 < nk) dma(ks + 1, (ks + 1) % NST);
     const char* st = smem + (ks % NST) * STAGE;
-    u32x4_t fw[8], fh[4];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) fw[i] = *reinterpret_cast<const u32x4_t*>(st + (BM + 128 * wn + 16 * i) * 64 + fo);
+    for (int h = 0; h < 2; ++h) {
+      const int fo = h ? fo1 : fo0;
+      u32x4_t fw[8], fh[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) fh[j] = *reinterpret_cast<const u32x4_t*>(st + (64 * wm + 16 * j) * 64 + fo);
+      for (int i = 0; i < 8; ++i) fw[i] = *reinterpret_cast<const u32x4_t*>(st + (BM + 128 * wn + 16 * i) * 128 + fo);
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+      for (int j = 0; j < 4; ++j) fh[j] = *reinterpret_cast<const u32x4_t*>(st + (64 * wm + 16 * j) * 128 + fo);
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, fw[i]),
-                                                            __builtin_bit_cast(bf16x8_t, fh[j]), acc[i][j], 0, 0, 0);
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, fw[i]),
+                                                              __builtin_bit_cast(bf16x8_t, fh[j]), acc[i][j], 0, 0, 0);
+    }
   }
 
   // The reference logits are needed from here on: taken now, the compiler's
@@ -2110,25 +2109,24 @@ __global__ __launch_bounds__(256) void erase_fwd_logits_wide(GemmDesc g, EpiPara
       se += __uint_as_float(o0 & 0xffff0000u);
       se += __uint_as_float(o1 << 16);
       se += __uint_as_float(o1 & 0xffff0000u);
-      if (p < M) *reinterpret_cast<uint2*>(Y + (int64_t)p * ldy + n0 + 128 * wn + 16 * i + 4 * fg) = uint2{o0, o1};
+      *reinterpret_cast<uint2*>(Y + (int64_t)p * ldy + n0 + 128 * wn + 16 * i + 4 * fg) = uint2{o0, o1};
     }
     se += __shfl_xor(se, 16, 64);
     se += __shfl_xor(se, 32, 64);
-    if (fg == 0 && p < M) e.lstat[(int64_t)p * e.ldlstat + tcol] = se;
+    if (fg == 0) e.lstat[(int64_t)p * e.ldlstat + tcol] = se;
   }
 }
 
 static bool logits_wide_fits(const GemmDesc& g, const EpiParams& e) {
-  // whole 256-row vocabulary tiles and 32-wide k-steps within both operand
-  // rows; operand rows up to the next multiple of 128 positions must be
-  // readable (activation buffers are padded to that); 8-byte output stores
-  return g.split == 1 && g.N % lgw::BN == 0 && g.K % lgw::BK == 0 && g.K > 0 && g.K <= g.lda && g.K <= g.ldb &&
-         e.ldy % 4 == 0 && (reinterpret_cast<uintptr_t>(e.y) & 7) == 0;
+  // whole 256 x 256 tiles and 64-wide k-steps within both operand rows;
+  // 8-byte output stores
+  return g.split == 1 && g.M > 0 && g.M % lgw::BM == 0 && g.N % lgw::BN == 0 && g.K % lgw::BK == 0 && g.K > 0 &&
+         g.K <= g.lda && g.K <= g.ldb && e.ldy % 4 == 0 && (reinterpret_cast<uintptr_t>(e.y) & 7) == 0;
 }
 
 static hipError_t launch_logits_wide(const GemmDesc& g, const EpiParams& e, hipStream_t s, const LaunchEv& ev) {
-  const int tiles = ((g.M + lgw::BM - 1) / lgw::BM) * (g.N / lgw::BN);
-  ERASE_LAUNCH(erase_fwd_logits_wide, dim3((unsigned)tiles), dim3(256), 0, s, ev, g, e);
+  const int tiles = (g.M / lgw::BM) * (g.N / lgw::BN);
+  ERASE_LAUNCH(erase_fwd_logits_wide, dim3((unsigned)tiles), dim3(lgw::NT), 0, s, ev, g, e);
   return hipGetLastError();
 }
 

@@ -126,10 +126,10 @@ Plan1 choose_fwd(int64_t M, int64_t N, int64_t K) {
   return p;
 }
 
-// The vocabulary logits run in 128 x 256 tiles with per-128-column row sums
-// when the vocabulary is a multiple of 256 and the width a multiple of 64
-// (the k-step); otherwise in the GEMM core's tiles.
-bool logits_wide(const Dims& D) { return D.V % 256 == 0 && D.d % 64 == 0; }
+// The vocabulary logits run in 256 x 256 tiles with per-128-column row sums
+// when the positions and the vocabulary are multiples of 256 and the width a
+// multiple of 64 (the k-step); otherwise in the GEMM core's tiles.
+bool logits_wide(const Dims& D) { return D.N % 256 == 0 && D.V % 256 == 0 && D.d % 64 == 0; }
 
 struct Carver {
   uintptr_t base;
@@ -323,7 +323,7 @@ void build_gemms(const erase_tf_config& c, Layout* P) {
     // 2, 1.20 for 1.
     B.fwd[WH].g.group = 8;
     if (logits_wide(D)) {
-      B.fwd[WH].g.bm = 128;
+      B.fwd[WH].g.bm = 256;
       B.fwd[WH].g.bn = 256;
     }
     B.fwd[WH].e.lstat = B.lstat;

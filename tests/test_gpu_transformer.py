@@ -261,7 +261,7 @@ def test_tf_c5_kernel_classes_full_step_vs_oracle():
     (16 sequences of 1024 tokens, width 512, 8 heads, vocabulary 16384, 2
     layers): every GEMM launch takes the tile, k-group and split of the
     benchmarked 8-layer, 32768-word model (among them the two k-group
-    128x128 grouped vocabulary backward, the 128x256 logits kernel, the
+    128x128 grouped vocabulary backward, the 256x256 logits kernel, the
     64x128 MLP-up and MLP-down input-gradient kernels, and the 128x128
     forward tiles) -- and
     losses, gradients, parameters and both Adam moments of both blocks (the
@@ -275,9 +275,9 @@ def test_tf_c5_kernel_classes_full_step_vs_oracle():
     del p5, b5
     print(f"[tf] launch plan: {sorted(got)}", flush=True)
     assert got == want, (sorted(got ^ want))
-    # the vocabulary head: 128x256 logits tiles, one grouped two k-group
+    # the vocabulary head: 256x256 logits tiles, one grouped two k-group
     # 128x128 launch for both of its gradients
-    assert ("bwd_gemm", 4, 128, 128, 1) in got and ("fwd_gemm", 4, 128, 256, 1) in got
+    assert ("bwd_gemm", 4, 128, 128, 1) in got and ("fwd_gemm", 4, 256, 256, 1) in got
     print("[tf] V 16384, 2 layers: GPU step", flush=True)
     tr, gpu = _gpu_run(cfg, params, batches, "serial")
     tr.close()
