@@ -1296,11 +1296,15 @@ erase_status erase_init_streams(const erase_config* cfg, const erase_block_buffe
     return s;
   };
   if (hipGetDevice(&c->device) != hipSuccess) return bail(ERASE_ERR_HIP);
+  // The ordering events only order streams of this device (no host waits on
+  // them): recorded without the system-scope fence, which writes back and
+  // invalidates the caches at every record
+  const unsigned evflags = hipEventDisableTiming | hipEventDisableSystemFence;
   for (int b = 0; b < cfg->n_blocks; ++b) {
     hipEvent_t e1, e2;
-    if (hipEventCreateWithFlags(&e1, hipEventDisableTiming) != hipSuccess) return bail(ERASE_ERR_HIP);
+    if (hipEventCreateWithFlags(&e1, evflags) != hipSuccess) return bail(ERASE_ERR_HIP);
     c->ef.push_back(e1);
-    if (hipEventCreateWithFlags(&e2, hipEventDisableTiming) != hipSuccess) return bail(ERASE_ERR_HIP);
+    if (hipEventCreateWithFlags(&e2, evflags) != hipSuccess) return bail(ERASE_ERR_HIP);
     c->eb.push_back(e2);
   }
   // zero the workspace once (counters, and the padding every GEMM operand

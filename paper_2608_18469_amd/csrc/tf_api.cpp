@@ -838,12 +838,15 @@ erase_status erase_tf_init(const erase_tf_config* cfg, const erase_block_buffers
     return s;
   };
   if (hipGetDevice(&c->device) != hipSuccess) return bail(ERASE_ERR_HIP);
+  // ordering events between this device's streams only (no host waits on
+  // them): recorded without the system-scope fence
+  const unsigned evflags = hipEventDisableTiming | hipEventDisableSystemFence;
   for (int b = 0; b < cfg->n_layers; ++b) {
     hipEvent_t e;
-    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return bail(ERASE_ERR_HIP);
+    if (hipEventCreateWithFlags(&e, evflags) != hipSuccess) return bail(ERASE_ERR_HIP);
     c->ef.push_back(e);
   }
-  if (hipEventCreateWithFlags(&c->ejoin, hipEventDisableTiming) != hipSuccess) return bail(ERASE_ERR_HIP);
+  if (hipEventCreateWithFlags(&c->ejoin, evflags) != hipSuccess) return bail(ERASE_ERR_HIP);
   // zero the workspace once: counters, and the padding rows and columns every
   // GEMM operand relies on (nothing writes outside the logical extents)
   if (hipMemsetAsync(c->ws, 0, c->P.bytes, c->sf) != hipSuccess) return bail(ERASE_ERR_HIP);
