@@ -665,6 +665,10 @@ class Enqueuer {
       lev.e1 = tl.e1;
     }
     (void)s;
+    if (!timed_ && end_) {
+      lev.e1 = end_;  // recorded at this kernel's end (the last such launch wins)
+      end_used_ = true;
+    }
     hipError_t e = fn(lev);
     if (!hip_ok(c_, e, "kernel launch")) return ERASE_ERR_HIP;
     if (timed_) {
@@ -683,10 +687,23 @@ class Enqueuer {
     return ERASE_OK;
   }
   std::vector<TimedLaunch>& launches() { return out_; }
+  // Stream-ordering event to be recorded by the launches that follow, at
+  // each kernel's end (in place of a record after them, which costs a packet
+  // of its own on the stream); none while timing (the launches carry their
+  // timing events) or under graph capture.  end_recorded() tells whether a
+  // launch took it since set_end.
+  void set_end(hipEvent_t e) {
+    end_ = ends_ok_ ? e : nullptr;
+    end_used_ = false;
+  }
+  bool end_recorded() const { return end_used_; }
+  void no_end_events() { ends_ok_ = false; }
 
  private:
   Ctx* c_;
   bool timed_;
+  bool ends_ok_ = true, end_used_ = false;
+  hipEvent_t end_ = nullptr;
   size_t ev_ = 0;
   std::vector<TimedLaunch> out_;
 };
@@ -1084,9 +1101,11 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
       // a standalone head goes to the backward stream, in front of the
       // block's backward: the next block's forward waits only for the body
       const bool head_b = !P.blk[b].head_fused;
+      q.set_end(c->ef[b]);
       erase_status st = enqueue_forward(c, q, b, x, labels, sf, 0, !head_b);
       if (st != ERASE_OK) return st;
-      HIPCHK(c, hipEventRecord(c->ef[b], sf));
+      if (!q.end_recorded()) HIPCHK(c, hipEventRecord(c->ef[b], sf));
+      q.set_end(nullptr);
       if (threaded) {
         // ef[b] is recorded again only in a later step, after this job has
         // finished (the waits above, or the join below), so the job's wait
@@ -1096,6 +1115,7 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
                                         ebb]() -> erase_status {
           HIPCHK(c, hipStreamWaitEvent(sb, efb, 0));
           Enqueuer wq(c, false);
+          wq.set_end(ebb);
           erase_status s2 = head_b ? enqueue_head(c, wq, b, labels, sb, 1 + k) : ERASE_OK;
           if (s2 != ERASE_OK) return s2;
           bool done = false;
@@ -1105,12 +1125,13 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
             s2 = enqueue_adam(c, wq, b, losses, sb, 1 + k, par);
             if (s2 != ERASE_OK) return s2;
           }
-          HIPCHK(c, hipEventRecord(ebb, sb));
+          if (!wq.end_recorded()) HIPCHK(c, hipEventRecord(ebb, sb));
           return ERASE_OK;
         });
         continue;
       }
       HIPCHK(c, hipStreamWaitEvent(sb, c->ef[b], 0));
+      q.set_end(c->eb[b]);
       if (head_b) {
         st = enqueue_head(c, q, b, labels, sb, 1 + k);
         if (st != ERASE_OK) return st;
@@ -1122,7 +1143,8 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
         st = enqueue_adam(c, q, b, losses, sb, 1 + k, par);
         if (st != ERASE_OK) return st;
       }
-      HIPCHK(c, hipEventRecord(c->eb[b], sb));
+      if (!q.end_recorded()) HIPCHK(c, hipEventRecord(c->eb[b], sb));
+      q.set_end(nullptr);
     }
     if (threaded && !pipeline) {
       erase_status st = quiesce(c);
@@ -1395,6 +1417,7 @@ erase_status erase_step(erase_ctx* ctx, const void* x, const float* labels, int3
     GraphEntry g{x, labels, losses, schedule, c->par, nullptr, nullptr};
     HIPCHK(c, hipStreamBeginCapture(c->sf, hipStreamCaptureModeThreadLocal));
     Enqueuer q(c, false);
+    q.no_end_events();
     erase_status st = enqueue_step(c, q, x, labels, schedule, losses);
     hipGraph_t graph_h = nullptr;
     hipError_t ee = hipStreamEndCapture(c->sf, &graph_h);

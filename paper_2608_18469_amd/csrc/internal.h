@@ -57,9 +57,10 @@ enum GemmKind {
   GK_FWD_LIN = 5, GK_FWD_GELU = 6, GK_DGRAD_GELU = 7, GK_FWD_LOGITS = 8
 };
 
-// Optional timing events of one launch: when set, the kernel is dispatched
+// Optional events of one launch: when either is set, the kernel is dispatched
 // with hipExtLaunchKernelGGL, which stamps e0/e1 at the kernel's own start
-// and end on the device.
+// and end on the device (timing: both; e1 alone: a stream-ordering event
+// recorded by the launch itself, with no packet of its own).
 struct LaunchEv {
   hipEvent_t e0 = nullptr, e1 = nullptr;
 };

@@ -42,7 +42,7 @@ namespace erase {
 
 #define ERASE_LAUNCH(KERNEL, GRID, BLOCK, SHMEM, STREAM, EV, ...)                                   \
   do {                                                                                             \
-    if ((EV).e0)                                                                                   \
+    if ((EV).e0 || (EV).e1)                                                                        \
       hipExtLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, (EV).e0, (EV).e1, 0, __VA_ARGS__); \
     else                                                                                           \
       hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, __VA_ARGS__);                        \
