@@ -1980,9 +1980,13 @@ static hipError_t launch_wgrad_w8(const GemmDesc& g0, const EpiParams& e, const 
 // - xref[m]) rounded to bf16, and per row and 128-column tile the sum of the
 // stored values (the epilogue of GK_FWD_LOGITS).  A workgroup of eight waves
 // computes 256 positions x 256 vocabulary rows, each wave 64 x 128, so a
-// wave reads 12 KB of MFMA fragments from LDS per 64 x 128 x 64 slab (the
-// GEMM core's 2 x 2 waves of 32 x 64 read 6 KB per slab of a quarter of
-// that work), and the operands cross L2 once per 256 x 256 tile.  The
+// wave reads 24 KB of MFMA fragments from LDS per 64 x 128 x 64 slab (the
+// GEMM core's 2 x 2 waves of 32 x 64 read 12 KB per slab of a quarter of
+// that work), and the operands cross L2 once per 256 x 256 tile.  Measured
+// at 16384 x 32768 x 512 (kernel alone, same box): 818-821 us, against
+// 857-881 us for a 128 x 256 form (four waves, 32-wide k-steps in three 24
+// KB stages, two workgroups per CU: each operand line fetched in two halves)
+// and about 1 ms for the GEMM core's 64 x 128 tiles.  The
 // operand rows of a 64-wide k-step (one 128-byte line per row) go straight
 // from global memory into one of two 64 KB LDS stages
 // (global_load_lds_dwordx4; chunk c of row r at slot c ^ (r & 7):
@@ -2000,10 +2004,8 @@ constexpr int NST = 2;                      // LDS stages
 constexpr int STAGE = (BM + BN) * BK * 2;   // 64 KB: rows of 128 bytes
 constexpr int LOADS = (BM + BN) / 8 / NW;   // loads of 8 rows per wave and k-step
 // M-tiles per group of the tile order (each group walks every vocabulary
-// tile).  Measured at 16384 x 32768 x 512 (kernel alone, same box): 818-821
-// us; the 128 x 256 form of this kernel (four waves, 32-wide k-steps in
-// three 24 KB stages, two workgroups per CU) 857-881 us, the GEMM core's 64
-// x 128 tiles about 1 ms.
+// tile): one, 256 positions, the group size that measured best for the
+// 128 x 256 form (two of its tiles)
 constexpr int GROUP = 1;
 }  // namespace lgw
 
