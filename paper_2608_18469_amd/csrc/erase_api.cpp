@@ -742,18 +742,22 @@ erase_status enqueue_head(Ctx* c, Enqueuer& q, int b, const float* labels, hipSt
 // Block b's forward GEMMs and, unless it is fused into the last GEMM or
 // `with_head` is false, its local head and loss.
 erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const float* labels, hipStream_t s, int sid,
-                             bool with_head = true) {
+                             bool with_head = true, int l_begin = 0, int l_end = -1, int par = -1) {
   const Plan& P = c->P;
   const BlockRT& B = P.blk[b];
   const int M = P.M, esz = P.esz;
+  // (the worker thread passes the step parity it was given; c->par may
+  // already belong to the next step)
+  if (par < 0) par = c->par;
   const void* x0;
   int64_t ldx0;
-  layer_input(c, b, 0, x, c->par, &x0, &ldx0);
-  for (int l = 0; l < B.L; ++l) {
+  layer_input(c, b, 0, x, par, &x0, &ldx0);
+  if (l_end < 0) l_end = B.L;
+  for (int l = l_begin; l < l_end; ++l) {
     const LayerRT& R = B.layer[l];
     const void* a;
     int64_t lda;
-    layer_input(c, b, l, x, c->par, &a, &lda);
+    layer_input(c, b, l, x, par, &a, &lda);
     GemmDesc g{};
     g.A = a;
     g.lda = lda;
@@ -805,7 +809,7 @@ erase_status enqueue_forward(Ctx* c, Enqueuer& q, int b, const void* x, const fl
     RUN(fused ? 8 : g.kgroups == 2 ? 9 : 1, b, l, sid, s, cost,
         [&](const LaunchEv& ev) { return launch_gemm(bf, kind, g, e, s, ev); });
   }
-  if (B.head_fused || !with_head) return ERASE_OK;
+  if (B.head_fused || !with_head || l_end < B.L) return ERASE_OK;
   return enqueue_head(c, q, b, labels, s, sid);
 }
 
@@ -1099,10 +1103,14 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
         if (chained_next) HIPCHK(c, hipStreamWaitEvent(sf, c->eb[b + 1], 0));
       }
       // a standalone head goes to the backward stream, in front of the
-      // block's backward: the next block's forward waits only for the body
+      // block's backward: the next block's forward waits only for the body.
+      // A head fused into the last layer takes that layer with it when no
+      // later block reads the block's output.
       const bool head_b = !P.blk[b].head_fused;
+      const int L = P.blk[b].L;
+      const bool last_b = !head_b && L >= 2 && !chained_next;
       q.set_end(c->ef[b]);
-      erase_status st = enqueue_forward(c, q, b, x, labels, sf, 0, !head_b);
+      erase_status st = enqueue_forward(c, q, b, x, labels, sf, 0, !head_b, 0, last_b ? L - 1 : L);
       if (st != ERASE_OK) return st;
       if (!q.end_recorded()) HIPCHK(c, hipEventRecord(c->ef[b], sf));
       q.set_end(nullptr);
@@ -1111,12 +1119,14 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
         // finished (the waits above, or the join below), so the job's wait
         // always binds to this step's record
         hipEvent_t efb = c->ef[b], ebb = c->eb[b];
-        c->job_of[b] = c->worker->push([c, b, x, labels, losses, sb, k, par, adam_end, head_b, efb,
+        c->job_of[b] = c->worker->push([c, b, x, labels, losses, sb, k, par, adam_end, head_b, last_b, L, efb,
                                         ebb]() -> erase_status {
           HIPCHK(c, hipStreamWaitEvent(sb, efb, 0));
           Enqueuer wq(c, false);
           wq.set_end(ebb);
-          erase_status s2 = head_b ? enqueue_head(c, wq, b, labels, sb, 1 + k) : ERASE_OK;
+          erase_status s2 = head_b ? enqueue_head(c, wq, b, labels, sb, 1 + k)
+                            : last_b ? enqueue_forward(c, wq, b, x, labels, sb, 1 + k, true, L - 1, L, par)
+                                     : ERASE_OK;
           if (s2 != ERASE_OK) return s2;
           bool done = false;
           s2 = enqueue_backward(c, wq, b, x, sb, 1 + k, par, false, adam_end ? nullptr : losses, &done);
@@ -1134,6 +1144,9 @@ erase_status enqueue_step(Ctx* c, Enqueuer& q, const void* x, const float* label
       q.set_end(c->eb[b]);
       if (head_b) {
         st = enqueue_head(c, q, b, labels, sb, 1 + k);
+        if (st != ERASE_OK) return st;
+      } else if (last_b) {
+        st = enqueue_forward(c, q, b, x, labels, sb, 1 + k, true, L - 1, L, par);
         if (st != ERASE_OK) return st;
       }
       bool done = false;

@@ -787,7 +787,14 @@ def test_kernel_timing_records():
     tr2.sync()
     r2 = tr2.read_timing()[1:]
     assert {r["stream"] for r in r2 if r["kind"] == "wgrad_adam_kg2"} == {1, 2}
-    assert {r["stream"] for r in recs if r["kind"] in ("fwd_gemm", "fwd_gemm_kg2", "fwd_head_gemm", "prologue")} == {0}
+    assert {r["stream"] for r in recs if r["kind"] in ("fwd_gemm", "fwd_gemm_kg2", "prologue")} == {0}
+    # the last layer with its fused head runs on the backward stream in the
+    # ERASE order (no later block reads the block's output), on the forward
+    # stream in the serial one
+    assert {r["stream"] for r in recs if r["kind"] == "fwd_head_gemm"} == {1}
+    tr.step(xd, yd, "serial")
+    tr.sync()
+    assert {r["stream"] for r in tr.read_timing()[1:] if r["kind"] == "fwd_head_gemm"} == {0}
     with pytest.raises(erase.EraseError):
         tr.step(xd, yd, "overlap_graph")
     # a standalone head (256-wide chain blocks) runs on the backward stream in
