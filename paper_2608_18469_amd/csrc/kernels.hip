@@ -1757,6 +1757,11 @@ __device__ __forceinline__ int kperm8(int r) { return 2 * ((r >> 1) & 1) + 4 * (
 __device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(src) : "memory");
 }
+// The same with a wave-uniform base address in scalar registers and the
+// lane's 32-bit byte offset from it (no 64-bit address per lane and load).
+__device__ __forceinline__ void lds_dma16s(const void* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(off), "s"(base) : "memory");
+}
 
 __device__ __forceinline__ void wgrad_adam_w4_tile(const GemmDesc& g, const EpiParams& e, int bx, int by,
                                                    char* smem) {
@@ -1982,16 +1987,21 @@ static hipError_t launch_wgrad_w8(const GemmDesc& g0, const EpiParams& e, const 
 // computes 256 positions x 256 vocabulary rows, each wave 64 x 128, so a
 // wave reads 24 KB of MFMA fragments from LDS per 64 x 128 x 64 slab (the
 // GEMM core's 2 x 2 waves of 32 x 64 read 12 KB per slab of a quarter of
-// that work), and the operands cross L2 once per 256 x 256 tile.  Measured
-// at 16384 x 32768 x 512 (kernel alone, same box): 818-821 us, against
-// 857-881 us for a 128 x 256 form (four waves, 32-wide k-steps in three 24
-// KB stages, two workgroups per CU: each operand line fetched in two halves)
-// and about 1 ms for the GEMM core's 64 x 128 tiles.  The
+// that work), and the operands cross L2 once per 256 x 256 tile.  The
 // operand rows of a 64-wide k-step (one 128-byte line per row) go straight
 // from global memory into one of two 64 KB LDS stages
 // (global_load_lds_dwordx4; chunk c of row r at slot c ^ (r & 7):
 // conflict-free 16-byte fragment reads), the next k-step in flight, one
-// barrier per k-step; two waves per SIMD.  The MFMA computes the transposed
+// barrier per k-step; two waves per SIMD.  The workgroups are persistent
+// (one per CU: the stages leave no room for a second), and each loads the
+// first k-step of its next tile during the last k-step of the current one.
+// Measured at 16384 x 32768 x 512 (kernel alone, same box): 761-766 us
+// against 834 us for one workgroup per tile (whose first k-step waited for
+// its loads) and 807 us for that form in groups of two M-tiles; on another
+// box the one-tile form took 818-821 us against 857-881 us for a 128 x 256
+// form (four waves, 32-wide k-steps in three 24 KB stages, two workgroups
+// per CU: each operand line fetched in two halves) and about 1 ms for the
+// GEMM core's 64 x 128 tiles.  The MFMA computes the transposed
 // tile (vocabulary rows as the A operand): a lane holds 4 consecutive
 // vocabulary columns of one position, stored as 8 bytes; a row's sum over a
 // 128-column tile adds the lane's 32 values, then the 4 lane groups, in a
@@ -2004,131 +2014,195 @@ constexpr int NST = 2;                      // LDS stages
 constexpr int STAGE = (BM + BN) * BK * 2;   // 64 KB: rows of 128 bytes
 constexpr int LOADS = (BM + BN) / 8 / NW;   // loads of 8 rows per wave and k-step
 // M-tiles per group of the tile order (each group walks every vocabulary
-// tile): one, 256 positions, the group size that measured best for the
-// 128 x 256 form (two of its tiles)
-constexpr int GROUP = 1;
+// tile): two, so the 32 tiles an XCD runs at once read 2 position blocks
+// and 16 vocabulary blocks (persistent form, same box: groups of 1, 2, 4,
+// 8, 16 took 795-798, 761-766, 772-779, 790, 783 us)
+constexpr int GROUP = 2;
 }  // namespace lgw
 
 __global__ __launch_bounds__(lgw::NT) void erase_fwd_logits_wide(GemmDesc g, EpiParams e) {
   using namespace lgw;
-  __shared__ __attribute__((aligned(16))) char smem[NST * STAGE];
+  // two operand stages, then two 1 KB slots of reference logits (one tile's
+  // 256 positions each, alternating between consecutive tiles)
+  __shared__ __attribute__((aligned(16))) char smem[NST * STAGE + 2 * BM * 4];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wv & 3, wn = wv >> 2;  // the wave's 64 positions and 128 vocabulary rows
-  const int gm = g.M / BM, gn = g.N / BN;
-  const TileIdx ti = tile_from(xcd_linear((int)blockIdx.x, (int)gridDim.x), gm, gn, GROUP);
-  const int m0 = ti.m * BM, n0 = ti.n * BN;
+  const int gm = g.M / BM, gn = g.N / BN, ntiles = gm * gn;
   const int nk = g.K / BK;
   const int fr = lane & 15, fg = lane >> 4;
   constexpr float kL2e = 1.4426950408889634f;
 
-  // the reference logits of the lane's 4 positions (log2 units), loaded
-  // before the operand loads so the first wait covers them
-  float xl[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) xl[j] = e.xref[m0 + 64 * wm + 16 * j + fr] * kL2e;
-
+  // Kernel arguments in registers: the loads' asm statements clobber memory,
+  // so values read from the arguments inside the loops would be loaded
+  // again (scalar loads and a full wait) before every load.  Row strides of
+  // 8 rows for the direct-to-LDS loads.
+  const int64_t lda = g.lda, ldb = g.ldb, sa = 8 * lda, sw = 8 * ldb, ldy = e.ldy, ldls = e.ldlstat;
+  uint16_t* Y = static_cast<uint16_t*>(e.y);
+  float* lstat = e.lstat;
   // direct-to-LDS loads: load u of wave wv fills stage rows 8 ui .. 8 ui + 7,
   // ui = LOADS wv + u (rows [0, BM) positions, then vocabulary rows); lane l
-  // writes row 8 ui + (l >> 3), slot l & 7, which holds chunk (l & 7) ^ (l >> 3)
+  // writes row 8 ui + (l >> 3), slot l & 7, which holds chunk (l & 7) ^ (l >> 3).
+  // A wave's loads all read one operand: the first BM / (8 LOADS) waves the
+  // positions, the others the vocabulary rows.  The addresses are a
+  // wave-uniform base (scalar registers) plus the lane's fixed byte offset.
+  static_assert((BM / 8) % LOADS == 0, "a wave's loads read one operand");
+  const bool wa = wv < BM / (8 * LOADS);
   const int ch = (lane & 7) ^ (lane >> 3);
-  const uint16_t* pa = static_cast<const uint16_t*>(g.A) + (int64_t)(m0 + (lane >> 3)) * g.lda + ch * 8;
-  const uint16_t* pw = static_cast<const uint16_t*>(g.B) + (int64_t)(n0 + (lane >> 3)) * g.ldb + ch * 8;
+  const uint32_t voff = (uint32_t)((lane >> 3) * (wa ? lda : ldb) * 2 + ch * 16);
+  const int64_t rstride = (wa ? sa : sw) * 2;  // bytes between a wave's 8-row groups
+  const int r0 = 8 * (wa ? LOADS * wv : LOADS * wv - BM / 8);  // the wave's first row of its operand
+  const char* Ab = static_cast<const char*>(g.A) + (int64_t)r0 * lda * 2;
+  const char* Wb = static_cast<const char*>(g.B) + (int64_t)r0 * ldb * 2;
+  const char* Xb = reinterpret_cast<const char*>(e.xref);
   const uint32_t lbase = (uint32_t)(uintptr_t)((__attribute__((address_space(3))) char*)smem);
-  // row strides of 8 rows, in registers: the loads' asm statements clobber
-  // memory, so values read from the kernel arguments inside the loop would
-  // be loaded again (scalar loads and a full wait) before every load
-  const int64_t sa = 8 * g.lda, sw = 8 * g.ldb;
-  auto dma = [&](int ks, int st) {
-    const uint32_t l0 = lbase + st * STAGE;
+  const uint32_t lwave = lbase + LOADS * wv * 1024;
+  const float* sxr = reinterpret_cast<const float*>(smem + NST * STAGE);
+  auto dma = [&](int64_t oa, int64_t ow, int ks, int st) {
+    const char* b = (wa ? Ab + oa * 2 : Wb + ow * 2) + ks * BK * 2;
+    const uint32_t l0 = lwave + st * STAGE;
 #pragma unroll
-    for (int u = 0; u < LOADS; ++u) {
-      const int ui = LOADS * wv + u;
-      const uint16_t* src = ui < BM / 8 ? pa + ui * sa : pw + (ui - BM / 8) * sw;
-      lds_dma16(src + ks * BK, l0 + ui * 1024);
-    }
+    for (int u = 0; u < LOADS; ++u) lds_dma16s(b + u * rstride, voff, l0 + u * 1024);
+  };
+  // a tile's 256 reference logits into its slot: one load by wave 0
+  auto dma_xref = [&](int m0, int slot) {
+    if (wv == 0) lds_dma16s(Xb + (int64_t)m0 * 4, 16 * lane, lbase + NST * STAGE + slot * BM * 4);
   };
 
   // fragment reads: row block at stage row R0 (a multiple of 16), k half h:
   // lane reads row R0 + (l & 15), chunk 4 h + (l >> 4), at slot chunk ^ (l & 7)
   const int fo0 = fr * 128 + ((0 + fg) ^ (lane & 7)) * 16, fo1 = fr * 128 + ((4 + fg) ^ (lane & 7)) * 16;
-  f32x4_t acc[8][4];
-#pragma unroll
-  for (int i = 0; i < 8; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  if (nk > 0) dma(0, 0);
-  for (int ks = 0; ks < nk; ++ks) {
-    // this wave's loads of k-step ks have landed; after the barrier every
-    // wave's have, and every wave is done reading k-step ks - 1, whose stage
-    // the loads of ks + 1 overwrite
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    if (ks + 1 < nk) dma(ks + 1, (ks + 1) % NST);
-    const char* st = smem + (ks % NST) * STAGE;
+  // Persistent workgroups: workgroup b runs tiles b, b + G, b + 2G, ... (G
+  // the grid, a multiple of the XCD count, so every tile of a workgroup lies
+  // in its own XCD's range).  The first k-step of the next tile and its
+  // reference logits are loaded during the last k-step of the current one,
+  // so their latency hides behind that k-step's MFMAs and the epilogue.
+  const int G = (int)gridDim.x;
+  int t = (int)blockIdx.x;
+  if (t >= ntiles || nk <= 0) return;
+  TileIdx ti = tile_from(xcd_linear(t, ntiles), gm, gn, GROUP);
+  int64_t oa = (int64_t)(ti.m * BM) * lda, ow = (int64_t)(ti.n * BN) * ldb;
+  dma_xref(ti.m * BM, 0);
+  dma(oa, ow, 0, 0);
+  int st0 = 0, slot = 0;  // the stage of the tile's first k-step; its reference-logit slot
+  bool first = true;
+  for (;;) {
+    const int m0 = ti.m * BM, n0 = ti.n * BN;
+    const int tn = t + G;
+    const bool more = tn < ntiles;
+    TileIdx tin = ti;
+    if (more) tin = tile_from(xcd_linear(tn, ntiles), gm, gn, GROUP);
+    const int64_t oan = (int64_t)(tin.m * BM) * lda, own = (int64_t)(tin.n * BN) * ldb;
+
+    f32x4_t acc[8][4];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int fo = h ? fo1 : fo0;
-      u32x4_t fw[8], fh[4];
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int i = 0; i < 8; ++i) fw[i] = *reinterpret_cast<const u32x4_t*>(st + (BM + 128 * wn + 16 * i) * 128 + fo);
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    for (int ks = 0; ks < nk; ++ks) {
+      // this wave's loads of k-step ks have landed; after the barrier every
+      // wave's have, and every wave is done reading k-step ks - 1, whose
+      // stage the next loads overwrite.  The first k-step of a later tile
+      // was loaded before the previous tile's epilogue, whose 36 stores (32
+      // of the exponentials, 4 of the row sums) were issued after it: the
+      // counter at 32 means it has landed.
+      if (ks == 0 && !first)
+        asm volatile("s_waitcnt vmcnt(32)" ::: "memory");
+      else
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+      if (ks + 1 < nk) {
+        dma(oa, ow, ks + 1, (st0 + ks + 1) % NST);
+      } else if (more) {
+        dma_xref(tin.m * BM, slot ^ 1);
+        dma(oan, own, 0, (st0 + nk) % NST);
+      }
+      const char* st = smem + ((st0 + ks) % NST) * STAGE;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) fh[j] = *reinterpret_cast<const u32x4_t*>(st + (64 * wm + 16 * j) * 128 + fo);
+      for (int h = 0; h < 2; ++h) {
+        const int fo = h ? fo1 : fo0;
+        u32x4_t fw[8], fh[4];
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
+        for (int i = 0; i < 8; ++i)
+          fw[i] = *reinterpret_cast<const u32x4_t*>(st + (BM + 128 * wn + 16 * i) * 128 + fo);
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, fw[i]),
-                                                              __builtin_bit_cast(bf16x8_t, fh[j]), acc[i][j], 0, 0, 0);
+        for (int j = 0; j < 4; ++j) fh[j] = *reinterpret_cast<const u32x4_t*>(st + (64 * wm + 16 * j) * 128 + fo);
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, fw[i]),
+                                                                __builtin_bit_cast(bf16x8_t, fh[j]), acc[i][j], 0, 0, 0);
+      }
     }
-  }
 
-  // The reference logits are needed from here on: taken now, the compiler's
-  // wait for them lies before the first store (stores count in the same
-  // counter, and a wait between stores would wait for them too)
-  asm volatile("" ::"v"(xl[0]), "v"(xl[1]), "v"(xl[2]), "v"(xl[3]));
-
-  // acc[i][j][q]: vocabulary row n0 + 128 wn + 16 i + 4 (l >> 4) + q of
-  // position m0 + 64 wm + 16 j + (l & 15)
-  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-  typedef float f32x2_t __attribute__((ext_vector_type(2)));
-  uint16_t* Y = static_cast<uint16_t*>(e.y);
-  const int64_t ldy = e.ldy;
-  const int tcol = (n0 + 128 * wn) / 128;  // the row-sum tile
+    // acc[i][j][q]: vocabulary row n0 + 128 wn + 16 i + 4 (l >> 4) + q of
+    // position m0 + 64 wm + 16 j + (l & 15)
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    typedef float f32x2_t __attribute__((ext_vector_type(2)));
+    const int tcol = (n0 + 128 * wn) / 128;  // the row-sum tile
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int p = m0 + 64 * wm + 16 * j + fr;
-    float se = 0.f;
+    for (int j = 0; j < 4; ++j) {
+      const int pl = 64 * wm + 16 * j + fr, p = m0 + pl;
+      const float xl = sxr[slot * BM + pl] * kL2e;
+      float se = 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      float ev[4];
+      for (int i = 0; i < 8; ++i) {
+        float ev[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) ev[q] = __builtin_amdgcn_exp2f(fmaf(acc[i][j][q], kL2e, -xl[j]));
-      const uint32_t o0 = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{ev[0], ev[1]}), bf16x2_t));
-      const uint32_t o1 = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{ev[2], ev[3]}), bf16x2_t));
-      se += __uint_as_float(o0 << 16);
-      se += __uint_as_float(o0 & 0xffff0000u);
-      se += __uint_as_float(o1 << 16);
-      se += __uint_as_float(o1 & 0xffff0000u);
-      *reinterpret_cast<uint2*>(Y + (int64_t)p * ldy + n0 + 128 * wn + 16 * i + 4 * fg) = uint2{o0, o1};
+        for (int q = 0; q < 4; ++q) ev[q] = __builtin_amdgcn_exp2f(fmaf(acc[i][j][q], kL2e, -xl));
+        const uint32_t o0 = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{ev[0], ev[1]}), bf16x2_t));
+        const uint32_t o1 = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{ev[2], ev[3]}), bf16x2_t));
+        se += __uint_as_float(o0 << 16);
+        se += __uint_as_float(o0 & 0xffff0000u);
+        se += __uint_as_float(o1 << 16);
+        se += __uint_as_float(o1 & 0xffff0000u);
+        *reinterpret_cast<uint2*>(Y + (int64_t)p * ldy + n0 + 128 * wn + 16 * i + 4 * fg) = uint2{o0, o1};
+      }
+      se += __shfl_xor(se, 16, 64);
+      se += __shfl_xor(se, 32, 64);
+      if (fg == 0) lstat[(int64_t)p * ldls + tcol] = se;
     }
-    se += __shfl_xor(se, 16, 64);
-    se += __shfl_xor(se, 32, 64);
-    if (fg == 0) e.lstat[(int64_t)p * e.ldlstat + tcol] = se;
+    if (!more) break;
+    t = tn;
+    ti = tin;
+    oa = oan;
+    ow = own;
+    st0 = (st0 + nk) % NST;
+    slot ^= 1;
+    first = false;
   }
 }
 
 static bool logits_wide_fits(const GemmDesc& g, const EpiParams& e) {
   // whole 256 x 256 tiles and 64-wide k-steps within both operand rows;
-  // 8-byte output stores
+  // 8-byte output stores; reference logits in 16-byte chunks
   return g.split == 1 && g.M > 0 && g.M % lgw::BM == 0 && g.N % lgw::BN == 0 && g.K % lgw::BK == 0 && g.K > 0 &&
-         g.K <= g.lda && g.K <= g.ldb && e.ldy % 4 == 0 && (reinterpret_cast<uintptr_t>(e.y) & 7) == 0;
+         g.K <= g.lda && g.K <= g.ldb && e.ldy % 4 == 0 && (reinterpret_cast<uintptr_t>(e.y) & 7) == 0 &&
+         (reinterpret_cast<uintptr_t>(e.xref) & 15) == 0;
+}
+
+// Compute units of the current device (cached per device).
+static int device_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+  if (dev < 64 && cached[dev] > 0) return cached[dev];
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+  if (dev < 64) cached[dev] = n;
+  return n;
 }
 
 static hipError_t launch_logits_wide(const GemmDesc& g, const EpiParams& e, hipStream_t s, const LaunchEv& ev) {
+  // one persistent workgroup per compute unit (the 128 KB of stages allow
+  // no second), a multiple of the XCD count
   const int tiles = (g.M / lgw::BM) * (g.N / lgw::BN);
-  ERASE_LAUNCH(erase_fwd_logits_wide, dim3((unsigned)tiles), dim3(lgw::NT), 0, s, ev, g, e);
+  int grid = std::max(kXcds, device_cus() / kXcds * kXcds);
+  if (grid > tiles) grid = tiles;
+  ERASE_LAUNCH(erase_fwd_logits_wide, dim3((unsigned)grid), dim3(lgw::NT), 0, s, ev, g, e);
   return hipGetLastError();
 }
 
