@@ -327,6 +327,33 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
     if constexpr (KIND == GK_FWD_RELU || KIND == GK_FWD_CROSS || KIND == GK_FWD_HEAD) bnv[j] = (n < g.N) ? e.bias[n] : 0.f;
   }
 
+  // input gradient below a ReLU (bf16, tiles of at most 64 x 64): the
+  // thread's mask values are loaded now, their latency hidden behind the
+  // main loop (the contraction of these launches is short), two per register
+  constexpr bool PFM = KIND == GK_DGRAD && sizeof(T) == 2 && TM * TN <= 4;
+  const bool pfm = PFM && e.mask != nullptr && !e.below_cross && kg == 0;
+  uint32_t mkp[PFM ? TM * TN * 2 : 1] = {};
+  if constexpr (PFM) {
+    const uint16_t* mk = static_cast<const uint16_t*>(e.mask);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          uint32_t w = 0;
+          if (pfm) {
+            const int n = n0 + wn * WN + j * 16 + (lane & 15);
+#pragma unroll
+            for (int q2 = 0; q2 < 2; ++q2) {
+              const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + 2 * h + q2;
+              if (m < g.M && n < g.N) w |= (uint32_t)mk[(int64_t)m * e.ldmask + n] << (16 * q2);
+            }
+          }
+          mkp[(i * TN + j) * 2 + h] = w;
+        }
+  }
+
   // logits: the epilogue's store pass gives each row LTPR threads of 8
   // consecutive columns; the reference
   // logit of each of the thread's rows (in units of log2) is loaded now,
@@ -677,7 +704,15 @@ __device__ __forceinline__ void gemm_body(const GemmDesc& g, const EpiParams& e,
         if constexpr (KIND == GK_WGRAD) {
           v = acc[i][j][q];
         } else {
-          v = (m < M && n < N) ? epi_value<T, KIND>(e, m, n, acc[i][j][q], bn) : OT(0);
+          if (PFM && pfm) {
+            // epi_value's masked input gradient with the prefetched mask
+            float a = acc[i][j][q];
+            if (e.res && m < M && n < N) a += ldf(static_cast<const T*>(e.res) + (int64_t)m * e.ldres + n);
+            const uint32_t mb = (mkp[PFM ? (i * TN + j) * 2 + (q >> 1) : 0] >> (16 * (q & 1))) & 0xffffu;
+            v = (m < M && n < N) ? cvt<T>(__uint_as_float(mb << 16) > 0.f ? a : 0.f) : OT(0);
+          } else {
+            v = (m < M && n < N) ? epi_value<T, KIND>(e, m, n, acc[i][j][q], bn) : OT(0);
+          }
           if constexpr (KIND != GK_FWD_GELU) acc[i][j][q] = asf(v);  // GELU keeps the pre-activation
         }
         sc[ml * OPITCH + nl] = v;
