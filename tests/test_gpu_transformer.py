@@ -285,6 +285,23 @@ def test_tf_c5_kernel_classes_full_step_vs_oracle():
     _check_bf16(cfg, gpu, params, batches)
 
 
+def test_tf_logits_tiles_uneven_over_the_persistent_grid():
+    """The 256x256 logits kernel runs one persistent workgroup per CU over
+    its tiles: here 9 x 37 = 333 tiles for 256 workgroups, so some walk two
+    tiles and the rest one (the next tile's first k-step and reference
+    logits are loaded during the current tile's last k-step).  The step
+    matches the oracles, and OVERLAP gives the same bits as SERIAL."""
+    cfg = synth_tf.tf_config("tf_tiny", vocab=37 * 256, d=128, heads=2, layers=1, seq=1152, batch=2)
+    params, batches = synth_tf.make_workload(cfg, seed=12, n_batches=1)
+    plan = _plan(cfg, params, batches[0])
+    print(f"[tf] N 2304, V 9472, d 128: launch plan {sorted(plan)}", flush=True)
+    assert ("fwd_gemm", 4, 256, 256, 1) in plan
+    _, a = _gpu_run(cfg, params, batches, "serial")
+    _, b = _gpu_run(cfg, params, batches, "overlap")
+    _bits_equal(a, b)
+    _check_bf16(cfg, a, params, batches)
+
+
 @pytest.mark.timeout(900)
 def test_tf_c5_full_size_block1_vs_oracle():
     """The full model (V 32768, d 512, 8 heads, 8 layers, 16 x 1024 tokens)
