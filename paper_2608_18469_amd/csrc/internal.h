@@ -166,7 +166,7 @@ hipError_t launch_head(int bf16, const HeadArgs& a, hipStream_t s, const LaunchE
 // tiles of ADAM_TR rows x ADAM_TC columns, one workgroup per tile (a
 // thread owns 4 columns of one row of a matrix tile, one element of a
 // vector).
-constexpr int ADAM_TR = 4, ADAM_TC = 256;
+constexpr int ADAM_TR = 16, ADAM_TC = 64;
 struct AdamSeg {
   float* p; float* m; float* v; float* g;   // flat [rows*cols] fp32 (g nullable)
   const float* part;                        // partial sums [nsplit][rows][ldpart]

@@ -1535,9 +1535,10 @@ __device__ __forceinline__ int find_seg(const AdamArgs& a, int64_t chunk) {
   return s;
 }
 
-// Thread = one column of an ADAM_TR-row tile: rows are read and written
-// coalesced across the workgroup, and the transposed GEMM copy gets the
-// tile's ADAM_TR consecutive values of one column as 16-byte stores.
+// A matrix tile is ADAM_TR rows of ADAM_TC columns: rows are read and
+// written coalesced across the workgroup, and the transposed GEMM copy gets
+// the tile's ADAM_TR consecutive values of each column from one thread
+// (32 contiguous bytes in bf16).
 // 16-byte access at 4-byte alignment (rows of the flat parameter arrays
 // start anywhere; gfx950 serves unaligned vector accesses)
 typedef float f32x4u_t __attribute__((ext_vector_type(4), aligned(4)));
@@ -1572,7 +1573,7 @@ __device__ __forceinline__ void adam_chunk(const AdamArgs& a, int64_t chunk, int
     // many partials (one per head workgroup), 32 loads in flight per batch,
     // added in slice order
     const int c = tile * ADAM_TC + tid;
-    const bool ok = c < sg.cols;
+    const bool ok = tid < ADAM_TC && c < sg.cols;
     const int cc = ok ? c : 0;  // clamped: loads stay in bounds
     float p = P[cc], m = Mo[cc], v = V[cc], g = 0.f;
     constexpr int ZV = 32;
@@ -1593,12 +1594,12 @@ __device__ __forceinline__ void adam_chunk(const AdamArgs& a, int64_t chunk, int
       if (sg.sh) gmem(static_cast<T*>(sg.sh))[c] = cvt<T>(p);
     }
   } else {
-    // a matrix: a workgroup covers ADAM_TR (4) rows x ADAM_TC (256) columns,
+    // a matrix: a workgroup covers ADAM_TR (16) rows x ADAM_TC (64) columns,
     // a thread 4 consecutive columns of one row (16-byte loads and stores)
-    static_assert(ADAM_TR == 4 && ADAM_TC == 256, "matrix tile is 4 rows x 64 threads x 4 columns");
+    static_assert(ADAM_TR == 16 && ADAM_TC == 64, "matrix tile is 16 rows x 16 threads x 4 columns");
     r0 = (tile / sg.tcols) * ADAM_TR;
-    const int r = r0 + (tid >> 6);
-    const int c0 = (tile % sg.tcols) * ADAM_TC + (tid & 63) * 4;
+    const int r = r0 + (tid >> 4);
+    const int c0 = (tile % sg.tcols) * ADAM_TC + (tid & 15) * 4;
     const bool any = r < sg.rows && c0 < sg.cols;
     const bool full = c0 + 4 <= sg.cols;
     const int rr = any ? r : 0, cc = any ? c0 : 0;  // clamped: loads stay in bounds
@@ -1683,28 +1684,29 @@ __device__ __forceinline__ void adam_chunk(const AdamArgs& a, int64_t chunk, int
         }
       }
     }
-    // transposed GEMM copy [cols][ldsht]: the 4 rows of each column, through
-    // LDS (one 8- or 16-byte store per column)
+    // transposed GEMM copy [cols][ldsht]: the 16 rows of each column, through
+    // LDS (one thread per column, four 4-element stores)
     if (sg.sht) {
-      const int cl = (tid & 63) * 4, rl = tid >> 6;
+      const int cl = (tid & 15) * 4, rl = tid >> 4;
 #pragma unroll
       for (int k = 0; k < 4; ++k) s_o[rl][cl + k] = o[k];
       trans = true;
     }
   }
   __syncthreads();
-  if (trans) {
-    {
-      const int c = (tile % sg.tcols) * ADAM_TC + tid;
-      if (c < sg.cols && r0 < sg.rows) {
-        T t4[4] = {s_o[0][tid], s_o[1][tid], s_o[2][tid], s_o[3][tid]};
-        T* D = static_cast<T*>(sg.sht) + (int64_t)c * sg.ldsht + r0;
-        if (r0 + 4 <= sg.rows) {
-          st4(D, t4);
+  if (trans && tid < ADAM_TC) {
+    const int c = (tile % sg.tcols) * ADAM_TC + tid;
+    if (c < sg.cols && r0 < sg.rows) {
+      T* D = static_cast<T*>(sg.sht) + (int64_t)c * sg.ldsht + r0;
+#pragma unroll
+      for (int q4 = 0; q4 < ADAM_TR; q4 += 4) {
+        T t4[4] = {s_o[q4][tid], s_o[q4 + 1][tid], s_o[q4 + 2][tid], s_o[q4 + 3][tid]};
+        if (r0 + q4 + 4 <= sg.rows) {
+          st4(D + q4, t4);
         } else {
 #pragma unroll
           for (int i = 0; i < 4; ++i)
-            if (r0 + i < sg.rows) D[i] = t4[i];
+            if (r0 + q4 + i < sg.rows) D[q4 + i] = t4[i];
         }
       }
     }
@@ -2259,7 +2261,7 @@ __global__ __launch_bounds__(256) void erase_refresh(AdamArgs a) {
   const int tile = (int)(chunk - sg.chunk0);
   const int r0 = (tile / sg.tcols) * ADAM_TR;
   const int c = (tile % sg.tcols) * ADAM_TC + (int)threadIdx.x;
-  if (c >= sg.cols) return;
+  if ((int)threadIdx.x >= ADAM_TC || c >= sg.cols) return;
   for (int q = 0; q < ADAM_TR && r0 + q < sg.rows; ++q) {
     const int r = r0 + q;
     const float p = gmem(sg.p)[(int64_t)r * sg.cols + c];
