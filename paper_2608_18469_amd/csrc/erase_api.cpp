@@ -316,7 +316,7 @@ size_t build_plan(const erase_config& c, uintptr_t base, Plan* P) {
         if (R.grouped && R.wgrad.split > 1) {
           // the input-gradient tiles of the same launch fill the chip: the
           // weight gradient keeps slices of >= 512 batch rows, so Adam reads
-          // fewer fp32 partial slices.  CTR layers 2 and 3, same-box A/B of
+          // fewer fp32 partial slices.  CTR layers 2 and 3, A/B on one MI355X of
           // 4, 8 and 16 slices: the launch 10.9, 9.2, 9.2 us; SERIAL 9.36M,
           // 9.78M, 9.51M samples/s; PIPELINE+worker 12.85M, 12.94M, 12.38M
           // (16 slices: the first layer's launch, whose extra workgroups run

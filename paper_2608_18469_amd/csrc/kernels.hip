@@ -2032,10 +2032,10 @@ static hipError_t launch_wgrad_w8(const GemmDesc& g0, const EpiParams& e, const 
 // barrier per k-step; two waves per SIMD.  The workgroups are persistent
 // (one per CU: the stages leave no room for a second), and each loads the
 // first k-step of its next tile during the last k-step of the current one.
-// Measured at 16384 x 32768 x 512 (kernel alone, same box): 761-766 us
+// Measured at 16384 x 32768 x 512 (kernel alone, one MI355X): 761-766 us
 // against 834 us for one workgroup per tile (whose first k-step waited for
 // its loads) and 807 us for that form in groups of two M-tiles; on another
-// box the one-tile form took 818-821 us against 857-881 us for a 128 x 256
+// MI355X the one-tile form took 818-821 us against 857-881 us for a 128 x 256
 // form (four waves, 32-wide k-steps in three 24 KB stages, two workgroups
 // per CU: each operand line fetched in two halves) and about 1 ms for the
 // GEMM core's 64 x 128 tiles.  The MFMA computes the transposed
@@ -2052,7 +2052,7 @@ constexpr int STAGE = (BM + BN) * BK * 2;   // 64 KB: rows of 128 bytes
 constexpr int LOADS = (BM + BN) / 8 / NW;   // loads of 8 rows per wave and k-step
 // M-tiles per group of the tile order (each group walks every vocabulary
 // tile): two, so the 32 tiles an XCD runs at once read 2 position blocks
-// and 16 vocabulary blocks (persistent form, same box: groups of 1, 2, 4,
+// and 16 vocabulary blocks (persistent form, one MI355X: groups of 1, 2, 4,
 // 8, 16 took 795-798, 761-766, 772-779, 790, 783 us)
 constexpr int GROUP = 2;
 }  // namespace lgw
